@@ -1,0 +1,262 @@
+"""Oracle: dense pre-norm decoder layer, forward and backward, fp64.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+The layer is the decoder block of App. B ("Model Architectures"): grouped-query
+attention, SwiGLU feed-forward, pre-normalisation RMSNorm, RoPE. Attention is
+causal (App. C, the causal factor of the attention-core count). The backward
+is written out by hand (the paper's engines use a static hand-written
+backward, App. J, and count the backward of every GEMM as one data-gradient
+and one weight-gradient product, App. C).
+
+Readings where the paper is silent:
+  * RMSNorm: y = x * (mean(x^2) + eps)^(-1/2) * g, per token over the hidden dim.
+  * RoPE: rotate-half pairs (i, i + d/2), angle pos * base^(-2i/d), i < d/2;
+    positions restart at 0 in every batch row; q and k rotated, v not.
+  * GQA: contiguous groups, query head n reads key/value head n // (n_h / n_kv).
+  * Attention scale 1/sqrt(d); key j visible to query i iff j <= i, same row.
+  * Fused weight order: w_qkv rows [q heads; k heads; v heads], head-major;
+    w_gate_up rows [gate; up]; nn.Linear convention y = x W^T.
+  * Layer order (Llama): a = RMSNorm(x); h1 = x + Attn(a) W_o^T;
+    b = RMSNorm(h1); out = h1 + (silu(b W_g^T) * (b W_u^T)) W_d^T.
+
+Shapes: x is [T, h] with T = batch * seq, batch-row major.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# RMSNorm
+# --------------------------------------------------------------------------
+
+def rmsnorm_fwd(x, g, eps):
+    """y = x * r * g with r = (mean_j x_j^2 + eps)^(-1/2). Returns (y, r)."""
+    r = 1.0 / np.sqrt(np.mean(x * x, axis=-1) + eps)
+    return x * r[:, None] * g[None, :], r
+
+
+def rmsnorm_bwd(x, g, r, dy):
+    """Gradients of y = x r g.
+
+    With dr/dx_k = -r^3 x_k / h:
+      dx_k = r (g dy)_k - r^3 x_k / h * sum_j (g dy)_j x_j
+      dg_j = sum_t dy_tj x_tj r_t
+    """
+    h = x.shape[-1]
+    gd = dy * g[None, :]
+    proj = np.sum(gd * x, axis=-1)
+    dx = gd * r[:, None] - x * (r ** 3 * proj / h)[:, None]
+    dg = np.sum(dy * x * r[:, None], axis=0)
+    return dx, dg
+
+
+# --------------------------------------------------------------------------
+# RoPE
+# --------------------------------------------------------------------------
+
+def rope_angles(seq, head_dim, base):
+    """phi[s, i] = s * base^(-2i/d) for s < seq, i < d/2 (fp64)."""
+    i = np.arange(head_dim // 2, dtype=np.float64)
+    inv_freq = base ** (-2.0 * i / head_dim)
+    return np.arange(seq, dtype=np.float64)[:, None] * inv_freq[None, :]
+
+
+def _positions(batch, seq):
+    return np.tile(np.arange(seq), batch)
+
+
+def rope_fwd(x, batch, seq, base):
+    """Rotate each head of x [T, n, d] by its token's angles (rotate-half).
+
+    y_i = x_i cos - x_{i+d/2} sin,  y_{i+d/2} = x_{i+d/2} cos + x_i sin.
+    """
+    d = x.shape[-1]
+    phi = rope_angles(seq, d, base)[_positions(batch, seq)]      # [T, d/2]
+    c, s = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
+    x1, x2 = x[..., : d // 2], x[..., d // 2:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def rope_bwd(dy, batch, seq, base):
+    """Transpose of the rotation (rotation by -phi)."""
+    d = dy.shape[-1]
+    phi = rope_angles(seq, d, base)[_positions(batch, seq)]
+    c, s = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
+    d1, d2 = dy[..., : d // 2], dy[..., d // 2:]
+    return np.concatenate([d1 * c + d2 * s, d2 * c - d1 * s], axis=-1)
+
+
+# --------------------------------------------------------------------------
+# Causal grouped-query attention (naive, full score matrix per head)
+# --------------------------------------------------------------------------
+
+def attention_probs(q, k, scale):
+    """Causal row-softmax of q k^T * scale for one (row, head): [S, S]."""
+    S = q.shape[0]
+    s = (q @ k.T) * scale
+    s = np.where(np.tril(np.ones((S, S), dtype=bool)), s, -np.inf)
+    m = np.max(s, axis=1, keepdims=True)
+    e = np.exp(s - m)
+    l = np.sum(e, axis=1, keepdims=True)
+    return e / l, (m + np.log(l))[:, 0]
+
+
+def attention_fwd(q, k, v, batch, seq):
+    """o_i = sum_{j<=i} softmax_j(q_i.k_j / sqrt(d)) v_j per head.
+
+    q [T, n_h, d], k/v [T, n_kv, d]. Returns o [T, n_h, d] and the row
+    log-sum-exp lse [batch, n_h, seq].
+    """
+    T, nh, d = q.shape
+    nkv = k.shape[1]
+    grp = nh // nkv
+    scale = 1.0 / np.sqrt(d)
+    o = np.zeros_like(q)
+    lse = np.zeros((batch, nh, seq))
+    for b in range(batch):
+        rows = slice(b * seq, (b + 1) * seq)
+        for n in range(nh):
+            m = n // grp
+            P, lse[b, n] = attention_probs(q[rows, n], k[rows, m], scale)
+            o[rows, n] = P @ v[rows, m]
+    return o, lse
+
+
+def attention_bwd(q, k, v, do, batch, seq):
+    """Softmax-attention backward, per head, summed over each GQA group.
+
+      dv_j = sum_i P_ij do_i
+      dP_ij = do_i . v_j
+      ds_ij = P_ij (dP_ij - sum_l P_il dP_il)
+      dq_i = scale sum_j ds_ij k_j,   dk_j = scale sum_i ds_ij q_i
+    """
+    T, nh, d = q.shape
+    nkv = k.shape[1]
+    grp = nh // nkv
+    scale = 1.0 / np.sqrt(d)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for b in range(batch):
+        rows = slice(b * seq, (b + 1) * seq)
+        for n in range(nh):
+            m = n // grp
+            P, _ = attention_probs(q[rows, n], k[rows, m], scale)
+            dO = do[rows, n]
+            dv[rows, m] += P.T @ dO
+            dP = dO @ v[rows, m].T
+            ds = P * (dP - np.sum(P * dP, axis=1, keepdims=True))
+            dq[rows, n] = scale * (ds @ k[rows, m])
+            dk[rows, m] += scale * (ds.T @ q[rows, n])
+    return dq, dk, dv
+
+
+# --------------------------------------------------------------------------
+# SwiGLU
+# --------------------------------------------------------------------------
+
+def sigmoid(x):
+    return 0.5 * (1.0 + np.tanh(0.5 * x))
+
+
+def silu(x):
+    return x * sigmoid(x)
+
+
+def swiglu_fwd(G, U):
+    """A = silu(G) * U."""
+    return silu(G) * U
+
+
+def swiglu_bwd(G, U, dA):
+    """dG = dA U silu'(G) with silu'(G) = s (1 + G (1 - s)), s = sigmoid(G);
+    dU = dA silu(G)."""
+    s = sigmoid(G)
+    return dA * U * s * (1.0 + G * (1.0 - s)), dA * G * s
+
+
+# --------------------------------------------------------------------------
+# Dense layer
+# --------------------------------------------------------------------------
+
+def _dims(cfg):
+    d = cfg["head_dim"]
+    return cfg["hidden"], cfg["n_heads"], cfg["n_kv_heads"], d, \
+        cfg["n_heads"] * d, cfg["n_kv_heads"] * d
+
+
+def attention_block_fwd(x, W, cfg):
+    """a = RMSNorm(x; g1); qkv = a W_qkv^T; RoPE; attention; h1 = x + o W_o^T."""
+    h, nh, nkv, d, hq, hkv = _dims(cfg)
+    B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    T = x.shape[0]
+    a, r1 = rmsnorm_fwd(x, W["attn_norm"], cfg["rms_eps"])
+    qkv = a @ W["w_qkv"].T
+    q = qkv[:, :hq].reshape(T, nh, d)
+    k = qkv[:, hq:hq + hkv].reshape(T, nkv, d)
+    v = qkv[:, hq + hkv:].reshape(T, nkv, d)
+    qr = rope_fwd(q, B, S, base)
+    kr = rope_fwd(k, B, S, base)
+    o, lse = attention_fwd(qr, kr, v, B, S)
+    o = o.reshape(T, hq)
+    h1 = x + o @ W["w_o"].T
+    cache = dict(x=x, a=a, r1=r1, qr=qr, kr=kr, v=v, o=o, lse=lse)
+    return h1, cache
+
+
+def attention_block_bwd(c, W, cfg, dh1):
+    """Backward of attention_block_fwd; dh1 flows through the residual."""
+    h, nh, nkv, d, hq, hkv = _dims(cfg)
+    B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    T = dh1.shape[0]
+    g = {}
+    g["w_o"] = dh1.T @ c["o"]
+    do = (dh1 @ W["w_o"]).reshape(T, nh, d)
+    dqr, dkr, dv = attention_bwd(c["qr"], c["kr"], c["v"], do, B, S)
+    dq = rope_bwd(dqr, B, S, base).reshape(T, hq)
+    dk = rope_bwd(dkr, B, S, base).reshape(T, hkv)
+    dqkv = np.concatenate([dq, dk, dv.reshape(T, hkv)], axis=1)
+    g["w_qkv"] = dqkv.T @ c["a"]
+    da = dqkv @ W["w_qkv"]
+    dxn, g["attn_norm"] = rmsnorm_bwd(c["x"], W["attn_norm"], c["r1"], da)
+    return dh1 + dxn, g
+
+
+def ffn_fwd(h1, W, cfg):
+    """b = RMSNorm(h1; g2); [G|U] = b W_gu^T; out = h1 + (silu(G) U) W_d^T."""
+    f = cfg["ffn"]
+    b, r2 = rmsnorm_fwd(h1, W["ffn_norm"], cfg["rms_eps"])
+    gu = b @ W["w_gate_up"].T
+    G, U = gu[:, :f], gu[:, f:]
+    A = swiglu_fwd(G, U)
+    out = h1 + A @ W["w_down"].T
+    return out, dict(h1=h1, b=b, r2=r2, G=G, U=U, A=A)
+
+
+def ffn_bwd(c, W, cfg, dout):
+    g = {}
+    g["w_down"] = dout.T @ c["A"]
+    dA = dout @ W["w_down"]
+    dG, dU = swiglu_bwd(c["G"], c["U"], dA)
+    dgu = np.concatenate([dG, dU], axis=1)
+    g["w_gate_up"] = dgu.T @ c["b"]
+    db = dgu @ W["w_gate_up"]
+    dh1n, g["ffn_norm"] = rmsnorm_bwd(c["h1"], W["ffn_norm"], c["r2"], db)
+    return dout + dh1n, g
+
+
+def layer_fwd(x, W, cfg):
+    """Dense decoder layer forward. Returns (out [T, h], cache)."""
+    h1, ca = attention_block_fwd(x, W, cfg)
+    out, cf = ffn_fwd(h1, W, cfg)
+    return out, dict(attn=ca, ffn=cf)
+
+
+def layer_bwd(cache, W, cfg, dout):
+    """Dense decoder layer backward. Returns (dx [T, h], grads by weight name)."""
+    dh1, gf = ffn_bwd(cache["ffn"], W, cfg, dout)
+    dx, ga = attention_block_bwd(cache["attn"], W, cfg, dh1)
+    ga.update(gf)
+    return dx, ga

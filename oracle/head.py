@@ -1,0 +1,98 @@
+"""Oracle: embedding, final norm + LM head + softmax cross-entropy, model step.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+The output head is the fp32 softmax cross-entropy the engines fuse
+(Sec. 4.2 / App. E, "Fused cross-entropy"; App. H, "Fused NPU cross-entropy
+(FP32)"), after a final RMSNorm, optionally with the LM head tied to the input
+embedding (App. B, "Tied input/output embeddings").
+
+Readings where the paper is silent:
+  * loss = (1/T) sum_t (logsumexp(z_t) - z_t[y_t]) over all T tokens, no
+    ignore index; the targets are given (not derived by shifting the ids).
+  * Tied head: the LM head matrix is the embedding matrix, and its gradient is
+    the sum of the head's weight gradient and the embedding scatter-add.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import dense, moe
+
+
+def embed_fwd(ids, E):
+    """x0[t] = E[ids[t]]."""
+    return E[np.asarray(ids)]
+
+
+def embed_bwd(ids, dx0, vocab):
+    """dE[v] = sum over t with ids[t] = v of dx0[t]."""
+    dE = np.zeros((vocab, dx0.shape[1]))
+    np.add.at(dE, np.asarray(ids), dx0)
+    return dE
+
+
+def logsumexp(z):
+    m = np.max(z, axis=1)
+    return m + np.log(np.sum(np.exp(z - m[:, None]), axis=1))
+
+
+def cross_entropy(z, targets):
+    """Mean over tokens of logsumexp(z_t) - z_t[y_t], and dloss/dz."""
+    T = z.shape[0]
+    lse = logsumexp(z)
+    t = np.asarray(targets)
+    loss = np.mean(lse - z[np.arange(T), t])
+    dz = np.exp(z - lse[:, None])
+    dz[np.arange(T), t] -= 1.0
+    return loss, dz / T
+
+
+def head_fwd_bwd(xL, gf, w_lm, targets, eps):
+    """Final RMSNorm, logits z = RMSNorm(xL) W_lm^T, mean CE, and all grads.
+
+    Returns (loss, dxL, dgf, dW_lm).
+    """
+    xn, r = dense.rmsnorm_fwd(xL, gf, eps)
+    z = xn @ w_lm.T
+    loss, dz = cross_entropy(z, targets)
+    dw = dz.T @ xn
+    dxn = dz @ w_lm
+    dxL, dgf = dense.rmsnorm_bwd(xL, gf, r, dxn)
+    return loss, dxL, dgf, dw
+
+
+def model_fwd_bwd(P, ids, targets, cfg):
+    """Whole model: embedding, layers, final norm, head, CE; then backward.
+
+    P holds 'embedding' [V, h], 'layers' (list of weight dicts),
+    'final_norm' [h] and 'w_lm' [V, h] (None when tied). Returns
+    (loss, grads) with grads mirroring P. For MoE layers the loss includes
+    the per-layer aux losses.
+    """
+    V = cfg["vocab"]
+    tied = P["w_lm"] is None
+    w_lm = P["embedding"] if tied else P["w_lm"]
+    x = embed_fwd(ids, P["embedding"])
+    caches, aux_total = [], 0.0
+    for W in P["layers"]:
+        if cfg["n_experts"]:
+            x, aux, c = moe.layer_fwd(x, W, cfg)
+            aux_total += aux
+        else:
+            x, c = dense.layer_fwd(x, W, cfg)
+        caches.append(c)
+    loss, dx, dgf, dw_lm = head_fwd_bwd(x, P["final_norm"], w_lm, targets,
+                                        cfg["rms_eps"])
+    grads = {"layers": [None] * len(P["layers"]), "final_norm": dgf}
+    for i in reversed(range(len(P["layers"]))):
+        mod = moe if cfg["n_experts"] else dense
+        dx, grads["layers"][i] = mod.layer_bwd(caches[i], P["layers"][i], cfg, dx)
+    dE = embed_bwd(ids, dx, V)
+    if tied:
+        grads["embedding"] = dE + dw_lm
+        grads["w_lm"] = None
+    else:
+        grads["embedding"] = dE
+        grads["w_lm"] = dw_lm
+    return loss + aux_total, grads

@@ -1,0 +1,103 @@
+"""Pins for the MoE oracle: routing brute force, aux loss, grouped vs per token, FD."""
+import numpy as np
+
+from oracle import moe
+from fdcheck import central_diff, sample_indices, rel_err
+from test_oracle_dense import MICRO, micro_weights
+
+MOE = dict(MICRO, ffn=0, n_experts=8, top_k=2, expert_ffn=12, aux_coef=1e-2)
+
+
+def moe_weights(cfg, rng, std=0.3):
+    W = micro_weights(dict(cfg, ffn=4), rng, std)
+    del W["w_gate_up"], W["w_down"]
+    E, h, fe = cfg["n_experts"], cfg["hidden"], cfg["expert_ffn"]
+    W["w_router"] = std * rng.standard_normal((E, h))
+    W["w_gate_up_e"] = std * rng.standard_normal((E, 2 * fe, h))
+    W["w_down_e"] = std * rng.standard_normal((E, h, fe))
+    return W
+
+
+def test_topk_brute_force_with_ties():
+    l = np.array([[0.5, 2.0, 2.0, -1.0, 2.0],
+                  [1.0, 1.0, 1.0, 1.0, 1.0],
+                  [-3.0, 0.0, 4.0, 0.0, 1.0]], np.float32)
+    assert np.array_equal(moe.topk(l, 3), [[1, 2, 4], [0, 1, 2], [2, 4, 1]])
+    rng = np.random.default_rng(1)
+    l = rng.standard_normal((50, 16)).astype(np.float32)
+    l[:, 5] = l[:, 9]                      # force exact ties
+    idx = moe.topk(l, 4)
+    for t in range(50):
+        want = sorted(range(16), key=lambda e: (-float(l[t, e]), e))[:4]
+        assert list(idx[t]) == want
+
+
+def test_route_counts_offsets_perm():
+    rng = np.random.default_rng(2)
+    T, E, k = 37, 8, 3
+    l = rng.standard_normal((T, E)).astype(np.float32)
+    idx, gates, p, counts, offsets, perm = moe.route(l, k)
+    assert counts.sum() == T * k and offsets[-1] == T * k
+    assert np.all(np.diff(offsets) == counts)
+    assert np.array_equal(np.sort(perm), np.arange(T * k))
+    flat = idx.reshape(-1)
+    for e in range(E):
+        seg = perm[offsets[e]:offsets[e + 1]]
+        assert np.all(flat[seg] == e) and np.all(np.diff(seg) > 0)
+    assert np.allclose(p.sum(1), 1.0, atol=1e-15)
+    assert np.allclose(gates, np.take_along_axis(p, idx, 1))
+
+
+def test_aux_loss_balanced_routing_equals_alpha():
+    T, E, k, alpha = 16, 8, 2, 1e-2
+    p = np.full((T, E), 1.0 / E)
+    counts = np.full(E, T * k // E)
+    assert np.isclose(moe.aux_loss(p, counts, k, alpha), alpha, rtol=1e-15)
+
+
+def test_grouped_equals_per_token():
+    rng = np.random.default_rng(3)
+    cfg = MOE
+    W = moe_weights(cfg, rng)
+    b = rng.standard_normal((10, cfg["hidden"]))
+    y, aux, _ = moe.moe_fwd(b, W, cfg)
+    assert np.allclose(y, moe.moe_fwd_per_token(b, W, cfg), rtol=1e-12, atol=1e-14)
+
+
+def test_moe_layer_backward_finite_differences():
+    rng = np.random.default_rng(4)
+    cfg = MOE
+    T = cfg["batch"] * cfg["seq"]
+    W = moe_weights(cfg, rng)
+    x = rng.standard_normal((T, cfg["hidden"]))
+    R = rng.standard_normal((T, cfg["hidden"]))
+    out, aux, cache = moe.layer_fwd(x, W, cfg)
+    idx0 = cache["moe"]["idx"].copy()
+
+    def objective():
+        o, a, c = moe.layer_fwd(x, W, cfg)
+        assert np.array_equal(c["moe"]["idx"], idx0)   # no routing flips under FD
+        return float(np.sum(o * R) + a)
+
+    dx, grads = moe.layer_bwd(cache, W, cfg, R)
+    srng = np.random.default_rng(0)
+    idx = sample_indices(x.size, 64, srng)
+    assert rel_err(dx.ravel()[idx], central_diff(objective, x, idx)) <= 1e-6
+    for name in ("w_router", "w_gate_up_e", "w_down_e", "ffn_norm", "w_qkv"):
+        idx = sample_indices(W[name].size, 96, srng)
+        fd = central_diff(objective, W[name], idx)
+        assert rel_err(grads[name].ravel()[idx], fd) <= 1e-6, name
+
+
+def test_aux_loss_gradient_reaches_router():
+    # with dy = 0 the only gradient is the aux loss's, through softmax
+    rng = np.random.default_rng(5)
+    cfg = dict(MOE, aux_coef=0.7)
+    W = moe_weights(cfg, rng)
+    b = rng.standard_normal((9, cfg["hidden"]))
+    _, aux, c = moe.moe_fwd(b, W, cfg)
+    db, g = moe.moe_bwd(c, W, cfg, np.zeros_like(b))
+    f = lambda: moe.moe_fwd(b, W, cfg)[1]
+    idx = np.arange(W["w_router"].size)
+    assert rel_err(g["w_router"].ravel(), central_diff(f, W["w_router"], idx)) <= 1e-6
+    assert np.all(g["w_down_e"] == 0)
