@@ -1,0 +1,332 @@
+/*
+ * forge.h — C ABI of libforge: one decoder-layer training step on MI355X.
+ *
+ * The library runs one training step of a decoder-only transformer of the
+ * kind the paper's engines train (App. B "Model Architectures": grouped-query
+ * attention, SwiGLU feed-forward, pre-normalisation RMSNorm, RoPE), in bf16
+ * with fp32 weight-gradient accumulation (Sec. 4.2, Table "Forged-kernel
+ * throughput", caption), as hand-written HIP kernels for gfx950. Calls follow
+ * the paper's direct-dispatch model: raw device pointers plus a stream, no
+ * framework types (App. J, "Direct dispatch").
+ *
+ * Conventions (every entry point):
+ *   - Pointers are device memory owned by the caller unless a parameter says
+ *     "host". The library allocates no device memory and keeps no state
+ *     beyond a per-device property cache.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
+ *     default stream). Nothing synchronises with the host.
+ *   - Arguments are validated on the host before anything is launched; a
+ *     failed check returns a status and launches nothing. A failed launch
+ *     returns FORGE_ERR_HIP. forge_last_error() gives a message for the last
+ *     failing call on the calling thread.
+ *   - Base pointers of tensors must be 16-byte aligned (FORGE_ERR_ALIGNMENT).
+ *   - bf16 is carried as its 16-bit pattern (forge_bf16).
+ *   - Matrices are row-major. Weights follow the nn.Linear convention
+ *     [out_features, in_features], y = x W^T.
+ *   - Gradient outputs documented as "+=" are accumulated into; the caller
+ *     zeroes them before the first accumulation.
+ *   - Results are deterministic (bit-identical across runs on one device)
+ *     except where a function says otherwise.
+ *   - Calls on one stream are ordered; concurrent calls on different streams
+ *     must not share workspace, saved or output buffers.
+ */
+#ifndef FORGE_H
+#define FORGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t forge_bf16;
+typedef void* forge_stream;
+
+typedef enum {
+  FORGE_OK = 0,
+  FORGE_ERR_INVALID_ARG = 1,   /* null pointer, bad size, aliasing          */
+  FORGE_ERR_UNSUPPORTED = 2,   /* valid request this build does not handle  */
+  FORGE_ERR_ALIGNMENT = 3,     /* base pointer not 16-byte aligned          */
+  FORGE_ERR_HIP = 4            /* a HIP runtime call or launch failed       */
+} forge_status;
+
+/* Static string naming a status. Never NULL. */
+const char* forge_status_string(forge_status s);
+
+/* Message describing the last non-OK status returned on this thread
+ * (empty string if none). Valid until the next call on this thread. */
+const char* forge_last_error(void);
+
+/* Library version string, e.g. "forge 0.1 gfx950". */
+const char* forge_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Layer configuration                                                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Shape and hyperparameters of one decoder layer (App. B). T = batch * seq
+ * tokens, stored batch-row major. hq = n_heads * head_dim,
+ * hkv = n_kv_heads * head_dim; query head n uses key/value head
+ * n / (n_heads / n_kv_heads) (contiguous GQA groups).
+ *
+ * n_experts == 0 selects the dense SwiGLU FFN of width `ffn`. n_experts > 0
+ * selects the routed MoE FFN (top_k experts of width expert_ffn per token,
+ * softmax router, load-balance aux loss with coefficient aux_coef); the MoE
+ * path is not in this build and returns FORGE_ERR_UNSUPPORTED.
+ *
+ * recompute_attn != 0: the forward does not keep the attention output and
+ * its row statistics; the backward re-runs the attention forward (a
+ * recomputation policy, Sec. 3.3, "Surpass" stage).
+ *
+ * Supported: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ * hidden, ffn, hq multiples of 8; seq >= 1; batch >= 1.
+ */
+typedef struct {
+  int32_t batch, seq, hidden, n_heads, n_kv_heads, head_dim, ffn;
+  float rope_base, rms_eps;
+  int32_t n_experts, top_k, expert_ffn;
+  float aux_coef;
+  int32_t recompute_attn;
+} forge_layer_cfg;
+
+/*
+ * Layer weights (bf16, caller-owned, read only).
+ *   attn_norm [h]            RMSNorm gain before attention
+ *   w_qkv     [hq+2hkv, h]   rows: q heads, then k heads, then v heads;
+ *                            each head's head_dim rows contiguous
+ *   w_o       [h, hq]
+ *   ffn_norm  [h]
+ *   w_gate_up [2f, h]        rows: gate (f rows), then up (f rows)
+ *   w_down    [h, f]
+ *   rope_cos, rope_sin [seq, head_dim/2] fp32 tables from forge_rope_table
+ *   MoE only (unused when n_experts == 0):
+ *   w_router [E, h], w_gate_up_e [E, 2fe, h], w_down_e [E, h, fe]
+ */
+typedef struct {
+  const forge_bf16* attn_norm;
+  const forge_bf16* w_qkv;
+  const forge_bf16* w_o;
+  const forge_bf16* ffn_norm;
+  const forge_bf16* w_gate_up;
+  const forge_bf16* w_down;
+  const float* rope_cos;
+  const float* rope_sin;
+  const forge_bf16* w_router;
+  const forge_bf16* w_gate_up_e;
+  const forge_bf16* w_down_e;
+} forge_layer_weights;
+
+/* Weight gradients, fp32, same shapes as the weights, accumulated (+=). */
+typedef struct {
+  float* d_attn_norm;
+  float* d_w_qkv;
+  float* d_w_o;
+  float* d_ffn_norm;
+  float* d_w_gate_up;
+  float* d_w_down;
+  float* d_w_router;
+  float* d_w_gate_up_e;
+  float* d_w_down_e;
+} forge_layer_grads;
+
+/* Bytes of the `saved` buffer that forge_layer_fwd fills and
+ * forge_layer_bwd reads (activations kept for the backward). Host only. */
+forge_status forge_layer_saved_bytes(const forge_layer_cfg* cfg, size_t* bytes);
+
+/* Bytes of the scratch `workspace` of forge_layer_fwd / forge_layer_bwd.
+ * Host only. The contents need not be preserved between calls. */
+forge_status forge_layer_workspace_bytes(const forge_layer_cfg* cfg, size_t* bytes);
+
+/*
+ * RoPE tables: for position s < seq and pair index i < head_dim/2,
+ * angle = s * base^(-2i/head_dim) (rotate-half pairing (i, i + head_dim/2)),
+ * cos_out[s*head_dim/2 + i] = cos(angle), sin_out[...] = sin(angle), computed
+ * in fp64 on the device and stored as fp32. Position restarts at 0 in every
+ * batch row. Fill once per (seq, head_dim, base).
+ */
+forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base,
+                              float* cos_out, float* sin_out, forge_stream stream);
+
+/*
+ * One decoder layer forward (App. B):
+ *   a  = RMSNorm(x; attn_norm)        qkv = a w_qkv^T, RoPE on q and k
+ *   o  = causal GQA attention(q,k,v)  h1  = x + o w_o^T
+ *   b  = RMSNorm(h1; ffn_norm)        x_out = h1 + (silu(b Wg^T) * (b Wu^T)) w_down^T
+ * x_in, x_out: [T, h] bf16; x_out must not overlap x_in.
+ * saved: forge_layer_saved_bytes bytes, written here, read by the backward.
+ * workspace: forge_layer_workspace_bytes bytes of scratch.
+ * aux_loss: MoE only (device fp32 scalar, +=); may be NULL for dense layers.
+ */
+forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                             const forge_bf16* x_in, forge_bf16* x_out,
+                             void* saved, void* workspace, float* aux_loss,
+                             forge_stream stream);
+
+/*
+ * Backward of forge_layer_fwd for upstream gradient d_out [T, h] (bf16):
+ * writes d_in [T, h] (bf16, may alias d_out) and accumulates every weight
+ * gradient into `grads` (fp32 +=). x_in and saved must be those of the
+ * matching forward. Weight gradients are the data-gradient / weight-gradient
+ * product pair of every projection (App. C).
+ */
+forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                             const void* saved, const forge_bf16* x_in,
+                             const forge_bf16* d_out, forge_bf16* d_in,
+                             const forge_layer_grads* grads, void* workspace,
+                             forge_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Output head: final RMSNorm + LM head + softmax cross-entropy            */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t tokens, hidden, vocab;
+  float rms_eps;
+} forge_head_cfg;
+
+/* Scratch bytes for forge_loss_fwd_bwd (holds the [T, V] bf16 logits). */
+forge_status forge_loss_workspace_bytes(const forge_head_cfg* cfg, size_t* bytes);
+
+/*
+ * Fused output head, forward and backward in one call (the fused fp32
+ * cross-entropy of Sec. 4.2 / App. E):
+ *   xn = RMSNorm(x_L; final_norm), z = xn w_lm^T (bf16 logits, [T, V]),
+ *   loss = (1/T) sum_t (logsumexp(z_t) - z_t[targets_t]), softmax in fp32,
+ *   then dz = (softmax(z) - onehot) / T and the gradients.
+ * x_L [T, h] bf16; final_norm [h] bf16; w_lm [V, h] bf16 (the embedding
+ * matrix when the head is tied); targets [T] int32 in [0, V) (checked on the
+ * device: an out-of-range target contributes nothing and sets loss to NaN).
+ * Outputs: loss_out device fp32 scalar (=); d_x_L [T, h] bf16 (=);
+ * d_final_norm [h] fp32 (+=); d_w_lm [V, h] fp32 (+=).
+ */
+forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L,
+                                const forge_bf16* final_norm, const forge_bf16* w_lm,
+                                const int32_t* targets, float* loss_out,
+                                forge_bf16* d_x_L, float* d_final_norm, float* d_w_lm,
+                                void* workspace, forge_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Embedding                                                                */
+/* ------------------------------------------------------------------------ */
+
+/* x0[t, :] = emb[ids[t], :]. ids [T] int32, emb [V, h] bf16, x0 [T, h] bf16.
+ * An id outside [0, V) yields a zero row. */
+forge_status forge_embed_fwd(const int32_t* ids, const forge_bf16* emb, forge_bf16* x0,
+                             int32_t tokens, int32_t hidden, int32_t vocab,
+                             forge_stream stream);
+
+/* d_emb[ids[t], :] += dx0[t, :] (fp32 +=). Ids outside [0, V) are skipped.
+ * Uses fp32 atomics: the summation order over repeated ids varies between
+ * runs (not bit-deterministic). */
+forge_status forge_embed_bwd(const int32_t* ids, const forge_bf16* dx0, float* d_emb,
+                             int32_t tokens, int32_t hidden, int32_t vocab,
+                             forge_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Optimizer                                                                */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  float beta1, beta2, eps, weight_decay;
+} forge_adamw_hparams;
+
+/*
+ * Fused clip + AdamW + bf16 write-back over n elements of flat fp32 buffers
+ * (App. F, "Vertical integration"):
+ *   g = grad * clip; m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2
+ *   master -= lr * ((m / bc1) / (sqrt(v / bc2) + eps) + wd * master)
+ *   param = bf16(master), round to nearest even
+ * dev_scalars: device fp32 [4] = {lr, bc1, bc2, clip}, read in the kernel so
+ * the host refreshes them once per step without a sync (App. F, "Deep
+ * customization"); bc1 = 1 - b1^t, bc2 = 1 - b2^t.
+ * master, m, v: updated in place; param: written; grad: read only.
+ * n may be 0 (no launch).
+ */
+forge_status forge_adamw_step(float* master, forge_bf16* param, const float* grad,
+                              float* m, float* v, int64_t n,
+                              const forge_adamw_hparams* hp, const float* dev_scalars,
+                              forge_stream stream);
+
+/* Floats of scratch that forge_grad_norm_sq needs. */
+#define FORGE_GRAD_NORM_WORKSPACE_FLOATS 1024
+
+/* accum[0] += sum_i g[i]^2 over n fp32 elements (device scalar), the first
+ * half of the device-side gradient-norm / clip pipeline (App. F, "Deep
+ * customization"). workspace: FORGE_GRAD_NORM_WORKSPACE_FLOATS device
+ * floats of scratch. The summation order is fixed (deterministic). */
+forge_status forge_grad_norm_sq(const float* g, int64_t n, float* accum,
+                                float* workspace, forge_stream stream);
+
+/* dev_scalars[3] = min(1, max_norm / (sqrt(max(norm_sq[0], 0)) + eps)), on
+ * the device (App. F, "Deep customization"). */
+forge_status forge_clip_coeff(const float* norm_sq, float max_norm, float eps,
+                              float* dev_scalars, forge_stream stream);
+
+/* ------------------------------------------------------------------------ */
+/* Building blocks, exposed for per-kernel measurement and tests            */
+/* ------------------------------------------------------------------------ */
+
+/* Operand layouts and epilogues of forge_gemm. */
+#define FORGE_GEMM_KC 0            /* contiguous along the reduction dim K  */
+#define FORGE_GEMM_MC 1            /* contiguous along the M (or N) dim     */
+#define FORGE_EPI_STORE_BF16 0     /* C bf16 = acc                          */
+#define FORGE_EPI_RESID_BF16 1     /* C bf16 = acc + R (bf16), one rounding */
+#define FORGE_EPI_ACC_F32 2        /* C fp32 += acc                         */
+#define FORGE_EPI_STORE_F32 3      /* C fp32 = acc                          */
+
+/*
+ * C[m][n] (op)= sum_k A(m,k) B(k,n): bf16 operands, fp32 accumulation, on the
+ * MFMA units. These are the three products of every projection of the step:
+ * the forward and, in the backward, one data-gradient and one
+ * weight-gradient product (App. C).
+ *   layout_a KC: A(m,k) = A[m*lda + k]    MC: A(m,k) = A[k*lda + m]
+ *   layout_b KC: B(k,n) = B[n*ldb + k]    MC: B(k,n) = B[k*ldb + n]
+ * so y = x W^T is (KC, KC), dX = dY W is (KC, MC), dW += dY^T X is (MC, MC).
+ * Supported: (KC, KC) with every epilogue; (KC, MC) with STORE_BF16 and
+ * RESID_BF16; (MC, MC) with ACC_F32 and STORE_F32 (else UNSUPPORTED).
+ * Shape rules (else INVALID_ARG): M, N, K >= 0; a KC operand needs K % 8 == 0,
+ * an MC operand needs M % 8 == 0 (A) or N % 8 == 0 (B); every leading
+ * dimension is a multiple of 8 and at least the operand's contiguous extent;
+ * R (RESID_BF16 only, leading dim ldr) must not overlap C.
+ */
+forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
+                        const forge_bf16* A, const forge_bf16* B, void* C,
+                        const forge_bf16* R, int32_t M, int32_t N, int32_t K,
+                        int64_t lda, int64_t ldb, int64_t ldc, int64_t ldr,
+                        forge_stream stream);
+
+typedef struct {
+  int32_t batch, seq, n_heads, n_kv_heads, head_dim;
+} forge_attn_cfg;
+
+/*
+ * Causal grouped-query attention forward (App. B; causal as in App. C's
+ * attention-core count): q, k, v are the column blocks [0, hq), [hq, hq+hkv),
+ * [hq+hkv, hq+2hkv) of the fused qkv buffer [T, hq+2hkv] bf16 (after RoPE);
+ * o [T, hq] bf16 = softmax(q k^T / sqrt(d) + causal mask) v per head;
+ * lse [batch, n_heads, seq] fp32 = natural-log row log-sum-exp of the scaled
+ * scores. head_dim in {64, 128}.
+ */
+forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qkv,
+                                 forge_bf16* o, float* lse, forge_stream stream);
+
+/* Scratch bytes of forge_attention_bwd. Host only. */
+forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes);
+
+/*
+ * Attention backward: from d_o [T, hq] bf16 and the forward's qkv, o, lse,
+ * writes d_qkv [T, hq+2hkv] bf16 (=): dq for every query head, dk and dv
+ * summed over each kv head's query group.
+ */
+forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qkv,
+                                 const forge_bf16* o, const float* lse,
+                                 const forge_bf16* d_o, forge_bf16* d_qkv,
+                                 void* workspace, forge_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FORGE_H */

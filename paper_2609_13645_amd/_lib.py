@@ -1,0 +1,275 @@
+"""ctypes binding of libforge (include/forge.h): same names, argument marshalling only.
+
+Every function takes device pointers as ints or as objects with a
+``data_ptr()`` method (torch tensors), and a stream handle (an int, a
+``torch.cuda.Stream``, or None for torch's current stream). A non-OK status
+raises ForgeError with the library's message. Nothing here computes: every
+step of the path runs in the HIP kernels of libforge.so, and importing this
+module fails loudly when that library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libforge.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "forge.h")
+
+FORGE_OK = 0
+FORGE_ERR_INVALID_ARG = 1
+FORGE_ERR_UNSUPPORTED = 2
+FORGE_ERR_ALIGNMENT = 3
+FORGE_ERR_HIP = 4
+GRAD_NORM_WORKSPACE_FLOATS = 1024
+
+# GEMM operand layouts and epilogues (forge_gemm)
+GEMM_KC, GEMM_MC = 0, 1
+EPI_STORE_BF16, EPI_RESID_BF16, EPI_ACC_F32, EPI_STORE_F32 = 0, 1, 2, 3
+
+
+class ForgeError(RuntimeError):
+    def __init__(self, status, message):
+        self.status = status
+        super().__init__(f"{status_name(status)}: {message}")
+
+
+class LayerCfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("batch", "seq", "hidden", "n_heads", "n_kv_heads", "head_dim", "ffn")] + [
+        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
+        ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+        ("expert_ffn", ctypes.c_int32), ("aux_coef", ctypes.c_float),
+        ("recompute_attn", ctypes.c_int32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down",
+                 "rope_cos", "rope_sin", "w_router", "w_gate_up_e", "w_down_e")]
+
+
+class LayerGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("d_attn_norm", "d_w_qkv", "d_w_o", "d_ffn_norm", "d_w_gate_up",
+                 "d_w_down", "d_w_router", "d_w_gate_up_e", "d_w_down_e")]
+
+
+class HeadCfg(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+
+
+class AdamwHparams(ctypes.Structure):
+    _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
+
+
+class AttnCfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("batch", "seq", "n_heads", "n_kv_heads", "head_dim")]
+
+
+_lib = None
+
+
+def load():
+    """Load libforge.so; raises ImportError if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"libforge.so not found at {LIB_PATH}: build it first "
+            "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, F32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    SZ = ctypes.POINTER(ctypes.c_size_t)
+    sigs = {
+        "forge_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "forge_last_error": (ctypes.c_char_p, []),
+        "forge_version": (ctypes.c_char_p, []),
+        "forge_layer_saved_bytes": (ctypes.c_int, [ctypes.POINTER(LayerCfg), SZ]),
+        "forge_layer_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(LayerCfg), SZ]),
+        "forge_rope_table": (ctypes.c_int, [I32, I32, F32, P, P, P]),
+        "forge_layer_fwd": (ctypes.c_int, [ctypes.POINTER(LayerCfg),
+                                           ctypes.POINTER(LayerWeights), P, P, P, P, P, P]),
+        "forge_layer_bwd": (ctypes.c_int, [ctypes.POINTER(LayerCfg),
+                                           ctypes.POINTER(LayerWeights), P, P, P, P,
+                                           ctypes.POINTER(LayerGrads), P, P]),
+        "forge_loss_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(HeadCfg), SZ]),
+        "forge_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(HeadCfg), P, P, P, P, P, P,
+                                              P, P, P, P]),
+        "forge_embed_fwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
+        "forge_embed_bwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
+        "forge_adamw_step": (ctypes.c_int, [P, P, P, P, P, I64,
+                                            ctypes.POINTER(AdamwHparams), P, P]),
+        "forge_grad_norm_sq": (ctypes.c_int, [P, I64, P, P, P]),
+        "forge_clip_coeff": (ctypes.c_int, [P, F32, F32, P, P]),
+        "forge_gemm": (ctypes.c_int, [I32, I32, I32, P, P, P, P, I32, I32, I32,
+                                      I64, I64, I64, I64, P]),
+        "forge_attention_fwd": (ctypes.c_int, [ctypes.POINTER(AttnCfg), P, P, P, P]),
+        "forge_attention_bwd_workspace_bytes": (ctypes.c_int,
+                                                [ctypes.POINTER(AttnCfg), SZ]),
+        "forge_attention_bwd": (ctypes.c_int, [ctypes.POINTER(AttnCfg), P, P, P, P, P,
+                                               P, P]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def header_functions(path: str = HEADER_PATH):
+    """Names of the functions include/forge.h declares."""
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(forge_[a-z0-9_]+)\s*\(", src)))
+
+
+def status_name(status: int) -> str:
+    return load().forge_status_string(status).decode()
+
+
+def _check(status: int):
+    if status != FORGE_OK:
+        raise ForgeError(status, load().forge_last_error().decode())
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if hasattr(s, "cuda_stream"):
+        return s.cuda_stream
+    return int(s)
+
+
+def layer_cfg(c: dict) -> LayerCfg:
+    return LayerCfg(c["batch"], c["seq"], c["hidden"], c["n_heads"], c["n_kv_heads"],
+                    c["head_dim"], c.get("ffn", 0), c["rope_base"], c["rms_eps"],
+                    c.get("n_experts", 0), c.get("top_k", 0), c.get("expert_ffn", 0),
+                    c.get("aux_coef", 0.0), c.get("recompute_attn", 0))
+
+
+def layer_weights(w: dict) -> LayerWeights:
+    return LayerWeights(*[_ptr(w.get(n)) for n, _ in LayerWeights._fields_])
+
+
+def layer_grads(g: dict) -> LayerGrads:
+    return LayerGrads(*[_ptr(g.get(n)) for n, _ in LayerGrads._fields_])
+
+
+def attn_cfg(c: dict) -> AttnCfg:
+    return AttnCfg(c["batch"], c["seq"], c["n_heads"], c["n_kv_heads"], c["head_dim"])
+
+
+# ---------------------------------------------------------------- calls ----
+
+def forge_version() -> str:
+    return load().forge_version().decode()
+
+
+def forge_layer_saved_bytes(cfg: LayerCfg) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_layer_saved_bytes(ctypes.byref(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def forge_layer_workspace_bytes(cfg: LayerCfg) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_layer_workspace_bytes(ctypes.byref(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def forge_rope_table(seq, head_dim, base, cos_out, sin_out, stream=None):
+    _check(load().forge_rope_table(seq, head_dim, base, _ptr(cos_out), _ptr(sin_out),
+                                   _stream(stream)))
+
+
+def forge_layer_fwd(cfg, weights, x_in, x_out, saved, workspace, aux_loss=None,
+                    stream=None):
+    _check(load().forge_layer_fwd(ctypes.byref(cfg), ctypes.byref(weights), _ptr(x_in),
+                                  _ptr(x_out), _ptr(saved), _ptr(workspace),
+                                  _ptr(aux_loss), _stream(stream)))
+
+
+def forge_layer_bwd(cfg, weights, saved, x_in, d_out, d_in, grads, workspace, stream=None):
+    _check(load().forge_layer_bwd(ctypes.byref(cfg), ctypes.byref(weights), _ptr(saved),
+                                  _ptr(x_in), _ptr(d_out), _ptr(d_in), ctypes.byref(grads),
+                                  _ptr(workspace), _stream(stream)))
+
+
+def forge_loss_workspace_bytes(cfg: HeadCfg) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_loss_workspace_bytes(ctypes.byref(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def forge_loss_fwd_bwd(cfg, x_L, final_norm, w_lm, targets, loss_out, d_x_L, d_final_norm,
+                       d_w_lm, workspace, stream=None):
+    _check(load().forge_loss_fwd_bwd(ctypes.byref(cfg), _ptr(x_L), _ptr(final_norm),
+                                     _ptr(w_lm), _ptr(targets), _ptr(loss_out), _ptr(d_x_L),
+                                     _ptr(d_final_norm), _ptr(d_w_lm), _ptr(workspace),
+                                     _stream(stream)))
+
+
+def forge_embed_fwd(ids, emb, x0, tokens, hidden, vocab, stream=None):
+    _check(load().forge_embed_fwd(_ptr(ids), _ptr(emb), _ptr(x0), tokens, hidden, vocab,
+                                  _stream(stream)))
+
+
+def forge_embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, stream=None):
+    _check(load().forge_embed_bwd(_ptr(ids), _ptr(dx0), _ptr(d_emb), tokens, hidden, vocab,
+                                  _stream(stream)))
+
+
+def forge_adamw_step(master, param, grad, m, v, n, hparams: AdamwHparams, dev_scalars,
+                     stream=None):
+    _check(load().forge_adamw_step(_ptr(master), _ptr(param), _ptr(grad), _ptr(m), _ptr(v),
+                                   int(n), ctypes.byref(hparams), _ptr(dev_scalars),
+                                   _stream(stream)))
+
+
+def forge_grad_norm_sq(g, n, accum, workspace, stream=None):
+    _check(load().forge_grad_norm_sq(_ptr(g), int(n), _ptr(accum), _ptr(workspace),
+                                     _stream(stream)))
+
+
+def forge_clip_coeff(norm_sq, max_norm, eps, dev_scalars, stream=None):
+    _check(load().forge_clip_coeff(_ptr(norm_sq), max_norm, eps, _ptr(dev_scalars),
+                                   _stream(stream)))
+
+
+def forge_gemm(layout_a, layout_b, epilogue, A, B, C, R, M, N, K, lda, ldb, ldc, ldr=0,
+               stream=None):
+    _check(load().forge_gemm(layout_a, layout_b, epilogue, _ptr(A), _ptr(B), _ptr(C),
+                             _ptr(R), M, N, K, lda, ldb, ldc, ldr, _stream(stream)))
+
+
+def forge_attention_fwd(cfg: AttnCfg, qkv, o, lse, stream=None):
+    _check(load().forge_attention_fwd(ctypes.byref(cfg), _ptr(qkv), _ptr(o), _ptr(lse),
+                                      _stream(stream)))
+
+
+def forge_attention_bwd_workspace_bytes(cfg: AttnCfg) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_attention_bwd_workspace_bytes(ctypes.byref(cfg), ctypes.byref(n)))
+    return n.value
+
+
+def forge_attention_bwd(cfg: AttnCfg, qkv, o, lse, d_o, d_qkv, workspace, stream=None):
+    _check(load().forge_attention_bwd(ctypes.byref(cfg), _ptr(qkv), _ptr(o), _ptr(lse),
+                                      _ptr(d_o), _ptr(d_qkv), _ptr(workspace),
+                                      _stream(stream)))

@@ -1,0 +1,647 @@
+// C ABI of libforge (include/forge.h): argument validation, the layout of
+// the caller-owned saved / workspace buffers, and the launch order of one
+// decoder layer's forward and backward, the fused output head, embedding,
+// optimizer and gradient-norm calls. Every call only enqueues kernels on the
+// caller's stream.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/forge.h"
+#include "kernels.h"
+
+namespace {
+
+using forge::GemmArgs;
+
+thread_local std::string g_last_error;
+
+forge_status fail(forge_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+forge_status fail(forge_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+forge_status ok() {
+  return FORGE_OK;
+}
+
+#define FORGE_HIP(call)                                                            \
+  do {                                                                             \
+    hipError_t e_ = (call);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return fail(FORGE_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_));   \
+  } while (0)
+
+#define FORGE_CHECK(cond, status, ...)             \
+  do {                                             \
+    if (!(cond)) return fail(status, __VA_ARGS__); \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define FORGE_PTR(p)                                                                     \
+  do {                                                                                   \
+    FORGE_CHECK((p) != nullptr, FORGE_ERR_INVALID_ARG, "%s is NULL", #p);                \
+    FORGE_CHECK(aligned16(p), FORGE_ERR_ALIGNMENT, "%s is not 16-byte aligned", #p);     \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// ---- derived sizes --------------------------------------------------------
+struct Dims {
+  long T, h, hq, hkv, qkv, f, nh, nkv, d, B, S;
+};
+
+Dims dims(const forge_layer_cfg& c) {
+  Dims d;
+  d.B = c.batch;
+  d.S = c.seq;
+  d.T = (long)c.batch * c.seq;
+  d.h = c.hidden;
+  d.d = c.head_dim;
+  d.nh = c.n_heads;
+  d.nkv = c.n_kv_heads;
+  d.hq = d.nh * d.d;
+  d.hkv = d.nkv * d.d;
+  d.qkv = d.hq + 2 * d.hkv;
+  d.f = c.ffn;
+  return d;
+}
+
+forge_status check_cfg(const forge_layer_cfg* c) {
+  FORGE_CHECK(c != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");
+  FORGE_CHECK(c->batch >= 1 && c->seq >= 1, FORGE_ERR_INVALID_ARG,
+              "batch and seq must be >= 1 (got %d, %d)", c->batch, c->seq);
+  FORGE_CHECK(c->hidden >= 8 && c->hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "hidden must be a positive multiple of 8 (got %d)", c->hidden);
+  FORGE_CHECK(c->hidden <= 8192, FORGE_ERR_UNSUPPORTED, "hidden > 8192 (got %d)", c->hidden);
+  FORGE_CHECK(c->n_heads >= 1 && c->n_kv_heads >= 1 && c->n_heads % c->n_kv_heads == 0,
+              FORGE_ERR_INVALID_ARG, "n_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+              c->n_heads, c->n_kv_heads);
+  FORGE_CHECK(c->head_dim == 64 || c->head_dim == 128, FORGE_ERR_UNSUPPORTED,
+              "head_dim must be 64 or 128 (got %d)", c->head_dim);
+  FORGE_CHECK(c->n_experts == 0, FORGE_ERR_UNSUPPORTED,
+              "the routed MoE FFN (n_experts = %d) is not in this build", c->n_experts);
+  FORGE_CHECK(c->ffn >= 8 && c->ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "ffn must be a positive multiple of 8 (got %d)", c->ffn);
+  FORGE_CHECK(c->rms_eps >= 0.0f && std::isfinite(c->rms_eps), FORGE_ERR_INVALID_ARG,
+              "rms_eps must be finite and >= 0");
+  FORGE_CHECK(c->rope_base > 0.0f && std::isfinite(c->rope_base), FORGE_ERR_INVALID_ARG,
+              "rope_base must be finite and > 0");
+  const Dims d = dims(*c);
+  const long widest = std::max(std::max(d.qkv, 2 * d.f), d.h);
+  FORGE_CHECK(d.T * widest < (1L << 31), FORGE_ERR_UNSUPPORTED,
+              "a [T, width] activation exceeds 2^31 elements");
+  return FORGE_OK;
+}
+
+// ---- saved buffer ----------------------------------------------------------
+struct Saved {
+  size_t a, rstd1, qkv, o, lse, h1, rstd2, b, gu, act, total;
+};
+
+Saved saved_layout(const forge_layer_cfg& c) {
+  const Dims d = dims(c);
+  Saved s;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
+  s.a = take(d.T * d.h * 2);
+  s.rstd1 = take(d.T * 4);
+  s.qkv = take(d.T * d.qkv * 2);
+  const bool keep = c.recompute_attn == 0;
+  s.o = keep ? take(d.T * d.hq * 2) : 0;
+  s.lse = keep ? take(d.B * d.nh * d.S * 4) : 0;
+  s.h1 = take(d.T * d.h * 2);
+  s.rstd2 = take(d.T * 4);
+  s.b = take(d.T * d.h * 2);
+  s.gu = take(d.T * 2 * d.f * 2);
+  s.act = take(d.T * d.f * 2);
+  s.total = off;
+  return s;
+}
+
+// ---- backward workspace ---------------------------------------------------
+struct Work {
+  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, total;
+};
+
+Work work_layout(const forge_layer_cfg& c) {
+  const Dims d = dims(c);
+  Work w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
+  w.dA = take(d.T * d.f * 2);
+  w.dgu = take(d.T * 2 * d.f * 2);
+  w.db = take(d.T * d.h * 2);
+  w.dh1 = take(d.T * d.h * 2);
+  w.dO = take(d.T * d.hq * 2);
+  w.delta = take(d.B * d.nh * d.S * 4);
+  w.dqkv = take(d.T * d.qkv * 2);
+  w.da = take(d.T * d.h * 2);
+  w.dg = take((size_t)forge::rmsnorm_bwd_blocks((int)d.T) * d.h * 4);
+  const bool rec = c.recompute_attn != 0;
+  w.o = rec ? take(d.T * d.hq * 2) : 0;
+  w.lse = rec ? take(d.B * d.nh * d.S * 4) : 0;
+  w.total = off;
+  return w;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+const T* at(const void* base, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+GemmArgs gargs(const void* A, long lda, const void* B, long ldb, void* C, long ldc, long M,
+               long N, long K, const void* R = nullptr, long ldr = 0) {
+  GemmArgs g;
+  g.A = static_cast<const uint16_t*>(A);
+  g.B = static_cast<const uint16_t*>(B);
+  g.C = C;
+  g.R = static_cast<const uint16_t*>(R);
+  g.M = (int)M;
+  g.N = (int)N;
+  g.K = (int)K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.ldr = ldr;
+  return g;
+}
+
+forge::AttnArgs attn_args(const Dims& d, const uint16_t* qkv) {
+  forge::AttnArgs a;
+  a.q = qkv;
+  a.k = qkv + d.hq;
+  a.v = qkv + d.hq + d.hkv;
+  a.ld_qkv = d.qkv;
+  a.batch = (int)d.B;
+  a.seq = (int)d.S;
+  a.n_heads = (int)d.nh;
+  a.n_kv_heads = (int)d.nkv;
+  a.d = (int)d.d;
+  a.scale = (float)(1.0 / std::sqrt((double)d.d));
+  return a;
+}
+
+forge_status check_weights(const forge_layer_weights* w) {
+  FORGE_CHECK(w != nullptr, FORGE_ERR_INVALID_ARG, "weights is NULL");
+  FORGE_PTR(w->attn_norm);
+  FORGE_PTR(w->w_qkv);
+  FORGE_PTR(w->w_o);
+  FORGE_PTR(w->ffn_norm);
+  FORGE_PTR(w->w_gate_up);
+  FORGE_PTR(w->w_down);
+  FORGE_PTR(w->rope_cos);
+  FORGE_PTR(w->rope_sin);
+  return FORGE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* forge_status_string(forge_status s) {
+  switch (s) {
+    case FORGE_OK: return "FORGE_OK";
+    case FORGE_ERR_INVALID_ARG: return "FORGE_ERR_INVALID_ARG";
+    case FORGE_ERR_UNSUPPORTED: return "FORGE_ERR_UNSUPPORTED";
+    case FORGE_ERR_ALIGNMENT: return "FORGE_ERR_ALIGNMENT";
+    case FORGE_ERR_HIP: return "FORGE_ERR_HIP";
+  }
+  return "FORGE_ERR_UNKNOWN";
+}
+
+const char* forge_last_error(void) { return g_last_error.c_str(); }
+
+const char* forge_version(void) { return "forge 0.1 gfx950"; }
+
+forge_status forge_layer_saved_bytes(const forge_layer_cfg* cfg, size_t* bytes) {
+  if (forge_status s = check_cfg(cfg)) return s;
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = saved_layout(*cfg).total;
+  return ok();
+}
+
+forge_status forge_layer_workspace_bytes(const forge_layer_cfg* cfg, size_t* bytes) {
+  if (forge_status s = check_cfg(cfg)) return s;
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = work_layout(*cfg).total;
+  return ok();
+}
+
+forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base, float* cos_out,
+                              float* sin_out, forge_stream stream) {
+  FORGE_CHECK(seq >= 1, FORGE_ERR_INVALID_ARG, "seq must be >= 1");
+  FORGE_CHECK(head_dim >= 16 && head_dim % 16 == 0, FORGE_ERR_INVALID_ARG,
+              "head_dim must be a positive multiple of 16");
+  FORGE_CHECK(base > 0.0f && std::isfinite(base), FORGE_ERR_INVALID_ARG, "base must be > 0");
+  FORGE_PTR(cos_out);
+  FORGE_PTR(sin_out);
+  FORGE_HIP(forge::rope_table(seq, head_dim, base, cos_out, sin_out, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                             const forge_bf16* x_in, forge_bf16* x_out, void* saved,
+                             void* workspace, float* aux_loss, forge_stream stream) {
+  (void)workspace;
+  (void)aux_loss;
+  if (forge_status s = check_cfg(cfg)) return s;
+  if (forge_status s = check_weights(w)) return s;
+  FORGE_PTR(x_in);
+  FORGE_PTR(x_out);
+  FORGE_PTR(saved);
+  const Dims d = dims(*cfg);
+  FORGE_CHECK(x_out + d.T * d.h <= x_in || x_in + d.T * d.h <= x_out, FORGE_ERR_INVALID_ARG,
+              "x_out overlaps x_in");
+  const Saved sv = saved_layout(*cfg);
+  hipStream_t s = (hipStream_t)stream;
+  uint16_t* a = at<uint16_t>(saved, sv.a);
+  float* rstd1 = at<float>(saved, sv.rstd1);
+  uint16_t* qkv = at<uint16_t>(saved, sv.qkv);
+  uint16_t* h1 = at<uint16_t>(saved, sv.h1);
+  float* rstd2 = at<float>(saved, sv.rstd2);
+  uint16_t* bn = at<uint16_t>(saved, sv.b);
+  uint16_t* gu = at<uint16_t>(saved, sv.gu);
+  uint16_t* act = at<uint16_t>(saved, sv.act);
+  FORGE_CHECK(cfg->recompute_attn == 0 || workspace != nullptr, FORGE_ERR_INVALID_ARG,
+              "workspace is NULL (needed when recompute_attn is set)");
+  const Work wk = work_layout(*cfg);
+  uint16_t* o = cfg->recompute_attn ? at<uint16_t>(workspace, wk.o) : at<uint16_t>(saved, sv.o);
+  float* lse = cfg->recompute_attn ? at<float>(workspace, wk.lse) : at<float>(saved, sv.lse);
+
+  FORGE_HIP(forge::rmsnorm_fwd(x_in, w->attn_norm, a, rstd1, (int)d.T, (int)d.h, cfg->rms_eps, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                        gargs(a, d.h, w->w_qkv, d.h, qkv, d.qkv, d.T, d.qkv, d.h), s));
+  FORGE_HIP(forge::rope_apply(qkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
+                              (int)(d.nh + d.nkv), (int)d.d, false, s));
+  FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o, lse, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
+                        gargs(o, d.hq, w->w_o, d.hq, h1, d.h, d.T, d.h, d.hq, x_in, d.h), s));
+  FORGE_HIP(forge::rmsnorm_fwd(h1, w->ffn_norm, bn, rstd2, (int)d.T, (int)d.h, cfg->rms_eps, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                        gargs(bn, d.h, w->w_gate_up, d.h, gu, 2 * d.f, d.T, 2 * d.f, d.h), s));
+  FORGE_HIP(forge::swiglu_fwd(gu, act, (int)d.T, (int)d.f, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
+                        gargs(act, d.f, w->w_down, d.f, x_out, d.h, d.T, d.h, d.f, h1, d.h), s));
+  return ok();
+}
+
+forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                             const void* saved, const forge_bf16* x_in,
+                             const forge_bf16* d_out, forge_bf16* d_in,
+                             const forge_layer_grads* g, void* workspace,
+                             forge_stream stream) {
+  if (forge_status s = check_cfg(cfg)) return s;
+  if (forge_status s = check_weights(w)) return s;
+  FORGE_PTR(saved);
+  FORGE_PTR(x_in);
+  FORGE_PTR(d_out);
+  FORGE_PTR(d_in);
+  FORGE_PTR(workspace);
+  FORGE_CHECK(g != nullptr, FORGE_ERR_INVALID_ARG, "grads is NULL");
+  FORGE_PTR(g->d_attn_norm);
+  FORGE_PTR(g->d_w_qkv);
+  FORGE_PTR(g->d_w_o);
+  FORGE_PTR(g->d_ffn_norm);
+  FORGE_PTR(g->d_w_gate_up);
+  FORGE_PTR(g->d_w_down);
+  const Dims d = dims(*cfg);
+  const Saved sv = saved_layout(*cfg);
+  const Work wk = work_layout(*cfg);
+  hipStream_t s = (hipStream_t)stream;
+  const uint16_t* a = at<uint16_t>(saved, sv.a);
+  const float* rstd1 = at<float>(saved, sv.rstd1);
+  const uint16_t* qkv = at<uint16_t>(saved, sv.qkv);
+  const uint16_t* h1 = at<uint16_t>(saved, sv.h1);
+  const float* rstd2 = at<float>(saved, sv.rstd2);
+  const uint16_t* bn = at<uint16_t>(saved, sv.b);
+  const uint16_t* gu = at<uint16_t>(saved, sv.gu);
+  const uint16_t* act = at<uint16_t>(saved, sv.act);
+  uint16_t* dA = at<uint16_t>(workspace, wk.dA);
+  uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
+  uint16_t* db = at<uint16_t>(workspace, wk.db);
+  uint16_t* dh1 = at<uint16_t>(workspace, wk.dh1);
+  uint16_t* dO = at<uint16_t>(workspace, wk.dO);
+  float* delta = at<float>(workspace, wk.delta);
+  uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
+  uint16_t* da = at<uint16_t>(workspace, wk.da);
+  float* dgp = at<float>(workspace, wk.dg);
+  const int nblk = forge::rmsnorm_bwd_blocks((int)d.T);
+  const forge::AttnArgs aa = attn_args(d, qkv);
+
+  const uint16_t* o;
+  const float* lse;
+  if (cfg->recompute_attn) {
+    uint16_t* o_w = at<uint16_t>(workspace, wk.o);
+    float* lse_w = at<float>(workspace, wk.lse);
+    FORGE_HIP(forge::attn_fwd(aa, o_w, lse_w, s));
+    o = o_w;
+    lse = lse_w;
+  } else {
+    o = at<uint16_t>(saved, sv.o);
+    lse = at<float>(saved, sv.lse);
+  }
+
+  // FFN: down projection, SwiGLU, gate/up projection, RMSNorm (+ residual)
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), s));
+  FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), s));
+  FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, s));
+
+  // attention: output projection, flash-attention backward, RoPE, QKV projection
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
+  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, dqkv + d.hq, dqkv + d.hq + d.hkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, dO, lse, delta, dqkv, d.qkv, s));
+  FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
+                              (int)(d.nh + d.nkv), (int)d.d, true, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), s));
+  FORGE_HIP(forge::rmsnorm_bwd(x_in, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, s));
+  return ok();
+}
+
+// ---- output head ----------------------------------------------------------
+namespace {
+struct HeadWork {
+  size_t xn, rstd, z, row_loss, dxn, dg, total;
+};
+forge_status check_head(const forge_head_cfg* c) {
+  FORGE_CHECK(c != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");
+  FORGE_CHECK(c->tokens >= 1, FORGE_ERR_INVALID_ARG, "tokens must be >= 1");
+  FORGE_CHECK(c->hidden >= 8 && c->hidden % 8 == 0 && c->hidden <= 8192, FORGE_ERR_INVALID_ARG,
+              "hidden must be a multiple of 8 in [8, 8192] (got %d)", c->hidden);
+  FORGE_CHECK(c->vocab >= 8 && c->vocab % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "vocab must be a positive multiple of 8 (got %d)", c->vocab);
+  FORGE_CHECK((long)c->tokens * c->vocab < (1L << 31), FORGE_ERR_UNSUPPORTED,
+              "tokens * vocab exceeds 2^31");
+  return FORGE_OK;
+}
+HeadWork head_layout(const forge_head_cfg& c) {
+  HeadWork w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
+  const long T = c.tokens, h = c.hidden, V = c.vocab;
+  w.xn = take(T * h * 2);
+  w.rstd = take(T * 4);
+  w.z = take(T * V * 2);
+  w.row_loss = take(T * 4);
+  w.dxn = take(T * h * 2);
+  w.dg = take((size_t)forge::rmsnorm_bwd_blocks((int)T) * h * 4);
+  w.total = off;
+  return w;
+}
+}  // namespace
+
+forge_status forge_loss_workspace_bytes(const forge_head_cfg* cfg, size_t* bytes) {
+  if (forge_status s = check_head(cfg)) return s;
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = head_layout(*cfg).total;
+  return ok();
+}
+
+forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L,
+                                const forge_bf16* final_norm, const forge_bf16* w_lm,
+                                const int32_t* targets, float* loss_out, forge_bf16* d_x_L,
+                                float* d_final_norm, float* d_w_lm, void* workspace,
+                                forge_stream stream) {
+  if (forge_status s = check_head(cfg)) return s;
+  FORGE_PTR(x_L);
+  FORGE_PTR(final_norm);
+  FORGE_PTR(w_lm);
+  FORGE_PTR(targets);
+  FORGE_CHECK(loss_out != nullptr, FORGE_ERR_INVALID_ARG, "loss_out is NULL");
+  FORGE_PTR(d_x_L);
+  FORGE_PTR(d_final_norm);
+  FORGE_PTR(d_w_lm);
+  FORGE_PTR(workspace);
+  const long T = cfg->tokens, h = cfg->hidden, V = cfg->vocab;
+  const HeadWork hw = head_layout(*cfg);
+  hipStream_t s = (hipStream_t)stream;
+  uint16_t* xn = at<uint16_t>(workspace, hw.xn);
+  float* rstd = at<float>(workspace, hw.rstd);
+  uint16_t* z = at<uint16_t>(workspace, hw.z);
+  float* rl = at<float>(workspace, hw.row_loss);
+  uint16_t* dxn = at<uint16_t>(workspace, hw.dxn);
+  float* dgp = at<float>(workspace, hw.dg);
+  const int nblk = forge::rmsnorm_bwd_blocks((int)T);
+
+  FORGE_HIP(forge::rmsnorm_fwd(x_L, final_norm, xn, rstd, (int)T, (int)h, cfg->rms_eps, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                        gargs(xn, h, w_lm, h, z, V, T, V, h), s));
+  FORGE_HIP(forge::ce_fwd_bwd(z, targets, rl, (int)T, (int)V, (float)(1.0 / (double)T), s));
+  FORGE_HIP(forge::mean_reduce(rl, (int)T, (float)(1.0 / (double)T), loss_out, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(z, V, w_lm, h, dxn, h, T, h, V), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(z, V, xn, h, d_w_lm, h, V, h, T), s));
+  FORGE_HIP(forge::rmsnorm_bwd(x_L, final_norm, rstd, dxn, nullptr, d_x_L, dgp, (int)T, (int)h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, d_final_norm, (int)h, s));
+  return ok();
+}
+
+// ---- embedding --------------------------------------------------------------
+forge_status forge_embed_fwd(const int32_t* ids, const forge_bf16* emb, forge_bf16* x0,
+                             int32_t tokens, int32_t hidden, int32_t vocab, forge_stream stream) {
+  FORGE_CHECK(tokens >= 0 && vocab >= 1, FORGE_ERR_INVALID_ARG, "bad tokens/vocab");
+  FORGE_CHECK(hidden >= 8 && hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "hidden must be a positive multiple of 8");
+  if (tokens == 0) return ok();
+  FORGE_PTR(ids);
+  FORGE_PTR(emb);
+  FORGE_PTR(x0);
+  FORGE_HIP(forge::embed_fwd(ids, emb, x0, tokens, hidden, vocab, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_embed_bwd(const int32_t* ids, const forge_bf16* dx0, float* d_emb,
+                             int32_t tokens, int32_t hidden, int32_t vocab, forge_stream stream) {
+  FORGE_CHECK(tokens >= 0 && vocab >= 1, FORGE_ERR_INVALID_ARG, "bad tokens/vocab");
+  FORGE_CHECK(hidden >= 8 && hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "hidden must be a positive multiple of 8");
+  if (tokens == 0) return ok();
+  FORGE_PTR(ids);
+  FORGE_PTR(dx0);
+  FORGE_PTR(d_emb);
+  FORGE_HIP(forge::embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, (hipStream_t)stream));
+  return ok();
+}
+
+// ---- optimizer ---------------------------------------------------------------
+forge_status forge_adamw_step(float* master, forge_bf16* param, const float* grad, float* m,
+                              float* v, int64_t n, const forge_adamw_hparams* hp,
+                              const float* dev_scalars, forge_stream stream) {
+  FORGE_CHECK(n >= 0, FORGE_ERR_INVALID_ARG, "n must be >= 0");
+  FORGE_CHECK(hp != nullptr, FORGE_ERR_INVALID_ARG, "hparams is NULL");
+  FORGE_CHECK(hp->beta1 >= 0.0f && hp->beta1 < 1.0f && hp->beta2 >= 0.0f && hp->beta2 < 1.0f,
+              FORGE_ERR_INVALID_ARG, "betas must be in [0, 1)");
+  FORGE_CHECK(hp->eps >= 0.0f && std::isfinite(hp->eps), FORGE_ERR_INVALID_ARG, "bad eps");
+  FORGE_CHECK(std::isfinite(hp->weight_decay), FORGE_ERR_INVALID_ARG, "bad weight_decay");
+  if (n == 0) return ok();
+  FORGE_PTR(master);
+  FORGE_PTR(param);
+  FORGE_PTR(grad);
+  FORGE_PTR(m);
+  FORGE_PTR(v);
+  FORGE_PTR(dev_scalars);
+  FORGE_HIP(forge::adamw(master, param, grad, m, v, n, hp->beta1, hp->beta2, hp->eps,
+                         hp->weight_decay, dev_scalars, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_grad_norm_sq(const float* g, int64_t n, float* accum, float* workspace,
+                                forge_stream stream) {
+  FORGE_CHECK(n >= 0, FORGE_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return ok();
+  FORGE_PTR(g);
+  FORGE_CHECK(accum != nullptr, FORGE_ERR_INVALID_ARG, "accum is NULL");
+  FORGE_PTR(workspace);
+  hipStream_t s = (hipStream_t)stream;
+  FORGE_HIP(forge::sumsq_partials(g, n, workspace, s));
+  FORGE_HIP(forge::sumsq_finish(workspace, accum, s));
+  return ok();
+}
+
+forge_status forge_clip_coeff(const float* norm_sq, float max_norm, float eps,
+                              float* dev_scalars, forge_stream stream) {
+  FORGE_CHECK(norm_sq != nullptr && dev_scalars != nullptr, FORGE_ERR_INVALID_ARG,
+              "NULL pointer");
+  FORGE_CHECK(max_norm > 0.0f && eps >= 0.0f, FORGE_ERR_INVALID_ARG,
+              "max_norm must be > 0 and eps >= 0");
+  FORGE_HIP(forge::clip_coeff(norm_sq, max_norm, eps, dev_scalars, (hipStream_t)stream));
+  return ok();
+}
+
+// ---- building blocks --------------------------------------------------------
+forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
+                        const forge_bf16* A, const forge_bf16* B, void* C, const forge_bf16* R,
+                        int32_t M, int32_t N, int32_t K, int64_t lda, int64_t ldb, int64_t ldc,
+                        int64_t ldr, forge_stream stream) {
+  FORGE_CHECK((layout_a == 0 || layout_a == 1) && (layout_b == 0 || layout_b == 1) &&
+                  epilogue >= 0 && epilogue <= 3,
+              FORGE_ERR_INVALID_ARG, "bad layout or epilogue code");
+  const bool bf16_out = epilogue == FORGE_EPI_STORE_BF16 || epilogue == FORGE_EPI_RESID_BF16;
+  const bool supported = (layout_a == 0 && layout_b == 0) ||
+                         (layout_a == 0 && layout_b == 1 && bf16_out) ||
+                         (layout_a == 1 && layout_b == 1 && !bf16_out);
+  FORGE_CHECK(supported, FORGE_ERR_UNSUPPORTED, "layout/epilogue combination (%d,%d,%d)",
+              layout_a, layout_b, epilogue);
+  FORGE_CHECK(M >= 0 && N >= 0 && K >= 0, FORGE_ERR_INVALID_ARG, "negative size");
+  if (M == 0 || N == 0) return ok();
+  FORGE_PTR(C);
+  if (K > 0) {
+    FORGE_PTR(A);
+    FORGE_PTR(B);
+  }
+  FORGE_CHECK(layout_a == 1 || K % 8 == 0, FORGE_ERR_INVALID_ARG, "K-contiguous A needs K %% 8 == 0");
+  FORGE_CHECK(layout_b == 1 || K % 8 == 0, FORGE_ERR_INVALID_ARG, "K-contiguous B needs K %% 8 == 0");
+  FORGE_CHECK(layout_a == 0 || M % 8 == 0, FORGE_ERR_INVALID_ARG, "M-contiguous A needs M %% 8 == 0");
+  FORGE_CHECK(layout_b == 0 || N % 8 == 0, FORGE_ERR_INVALID_ARG, "N-contiguous B needs N %% 8 == 0");
+  FORGE_CHECK(lda % 8 == 0 && ldb % 8 == 0 && ldc % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "leading dimensions must be multiples of 8");
+  FORGE_CHECK(lda >= (layout_a == 0 ? K : M) && ldb >= (layout_b == 0 ? K : N) && ldc >= N,
+              FORGE_ERR_INVALID_ARG, "leading dimension smaller than the contiguous extent");
+  if (epilogue == FORGE_EPI_RESID_BF16) {
+    FORGE_PTR(R);
+    FORGE_CHECK(ldr % 8 == 0 && ldr >= N, FORGE_ERR_INVALID_ARG, "bad ldr");
+    const char* c0 = static_cast<const char*>(C);
+    const char* c1 = c0 + ((M - 1) * ldc + N) * 2;
+    const char* r0 = reinterpret_cast<const char*>(R);
+    const char* r1 = r0 + ((M - 1) * ldr + N) * 2;
+    FORGE_CHECK(c1 <= r0 || r1 <= c0, FORGE_ERR_INVALID_ARG, "R overlaps C");
+  }
+  FORGE_CHECK((int64_t)M * ldc < (1LL << 40), FORGE_ERR_INVALID_ARG, "C too large");
+  GemmArgs g = gargs(A, lda, B, ldb, C, ldc, M, N, K, R, ldr);
+  FORGE_HIP(forge::gemm((forge::GemmLayout)layout_a, (forge::GemmLayout)layout_b,
+                        (forge::GemmEpilogue)epilogue, g, (hipStream_t)stream));
+  return ok();
+}
+
+namespace {
+forge_status check_attn(const forge_attn_cfg* c) {
+  FORGE_CHECK(c != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");
+  FORGE_CHECK(c->batch >= 1 && c->seq >= 1, FORGE_ERR_INVALID_ARG, "batch, seq must be >= 1");
+  FORGE_CHECK(c->n_heads >= 1 && c->n_kv_heads >= 1 && c->n_heads % c->n_kv_heads == 0,
+              FORGE_ERR_INVALID_ARG, "n_heads must be a positive multiple of n_kv_heads");
+  FORGE_CHECK(c->head_dim == 64 || c->head_dim == 128, FORGE_ERR_UNSUPPORTED,
+              "head_dim must be 64 or 128");
+  return FORGE_OK;
+}
+Dims attn_dims(const forge_attn_cfg& c) {
+  forge_layer_cfg l{};
+  l.batch = c.batch;
+  l.seq = c.seq;
+  l.n_heads = c.n_heads;
+  l.n_kv_heads = c.n_kv_heads;
+  l.head_dim = c.head_dim;
+  return dims(l);
+}
+}  // namespace
+
+forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qkv, forge_bf16* o,
+                                 float* lse, forge_stream stream) {
+  if (forge_status s = check_attn(cfg)) return s;
+  FORGE_PTR(qkv);
+  FORGE_PTR(o);
+  FORGE_PTR(lse);
+  const Dims d = attn_dims(*cfg);
+  FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o, lse, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes) {
+  if (forge_status s = check_attn(cfg)) return s;
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
+  return ok();
+}
+
+forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qkv,
+                                 const forge_bf16* o, const float* lse, const forge_bf16* d_o,
+                                 forge_bf16* d_qkv, void* workspace, forge_stream stream) {
+  if (forge_status s = check_attn(cfg)) return s;
+  FORGE_PTR(qkv);
+  FORGE_PTR(o);
+  FORGE_PTR(lse);
+  FORGE_PTR(d_o);
+  FORGE_PTR(d_qkv);
+  FORGE_PTR(workspace);
+  const Dims d = attn_dims(*cfg);
+  const forge::AttnArgs aa = attn_args(d, qkv);
+  hipStream_t s = (hipStream_t)stream;
+  float* delta = static_cast<float*>(workspace);
+  FORGE_HIP(forge::attn_bwd_pre(aa, o, d_o, delta, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, lse, delta, d_qkv + d.hq, d_qkv + d.hq + d.hkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, d_o, lse, delta, d_qkv, d.qkv, s));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,294 @@
+// bf16 GEMM on gfx950 MFMA (v_mfma_f32_32x32x16_bf16), fp32 accumulation.
+//
+// Every projection of the layer is one of three products (App. C: the
+// backward of each GEMM is one data-gradient and one weight-gradient
+// product): y = x W^T (both operands K-contiguous), dX = dY W (W is
+// N-contiguous) and dW += dY^T X (both operands M/N-contiguous, reduction
+// over tokens). One kernel template covers all three:
+//
+//  * A block tile BM x BN x 64 is staged through LDS, double-buffered, with
+//    one barrier per k-step. Both LDS tiles are kept K-contiguous, so every
+//    MFMA operand is one 16-byte LDS read per lane. Operands that are not
+//    K-contiguous in HBM are loaded as coalesced 16-byte rows and transposed
+//    8x8 in registers before the LDS store.
+//  * LDS rows are 128 bytes (eight 16-byte chunks); chunk c of row r lives at
+//    c ^ ((r ^ (r >> 3)) & 7), which keeps both the MFMA reads (32 rows, one
+//    chunk) and the transposed stores (rows 8 apart) spread over the banks.
+//  * The MFMA computes D = Btile * Atile^T, i.e. C transposed, so each lane's
+//    four consecutive accumulator rows are four consecutive n of one row m of
+//    C: the epilogue writes 8-byte (bf16) or 16-byte (fp32) vectors.
+//  * Workgroups are dispatched round-robin over the 8 XCDs; the tile order is
+//    remapped so each XCD works on a contiguous, M-grouped band of tiles and
+//    reuses operands in its own L2.
+#include "common.h"
+#include "kernels.h"
+
+namespace forge {
+namespace {
+
+constexpr int BK = 64;
+constexpr int CHUNKS = BK / 8;  // 16-byte chunks per LDS tile row
+constexpr int GROUP_M = 8;
+constexpr int NUM_XCD = 8;
+
+__device__ __forceinline__ int swz(int row, int c) {
+  return row * CHUNKS + (c ^ ((row ^ (row >> 3)) & 7));
+}
+
+// ---- global -> registers -> LDS, K-contiguous source ----------------------
+template <int ROWS, int NT>
+struct KcLoader {
+  static constexpr int PER = ROWS * CHUNKS / NT;
+  static_assert(PER * NT == ROWS * CHUNKS, "tile rows must split over threads");
+  uint4 r[PER];
+  __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
+                                       int rows_lim, int k0, int K) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int id = i * NT + t;
+      const int row = id / CHUNKS, c = id % CHUNKS;
+      const int gr = row0 + row, gk = k0 + c * 8;
+      if (gr < rows_lim && gk < K)
+        r[i] = *reinterpret_cast<const uint4*>(src + (long)gr * ld + gk);
+      else
+        r[i] = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void store(uint4* lds) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int id = i * NT + t;
+      lds[swz(id / CHUNKS, id % CHUNKS)] = r[i];
+    }
+  }
+};
+
+// ---- global -> registers -> LDS, source contiguous along the row dim -----
+// The tile is 64 k-rows of ROWS contiguous elements in HBM. Each thread owns
+// 8x8 blocks (8 k by 8 rows), loads them as eight 16-byte rows and
+// transposes them in registers.
+template <int ROWS, int NT>
+struct McLoader {
+  static constexpr int NBLK = ROWS;  // (ROWS/8 row chunks) x (8 k groups)
+  static constexpr int PER = (NBLK + NT - 1) / NT;
+  uint4 r[PER][8];
+  __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
+                                       int rows_lim, int k0, int K) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int b = j * NT + t;
+      const int mc = b % (ROWS / 8), kg = b / (ROWS / 8);
+      const int gm = row0 + mc * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int gk = k0 + kg * 8 + i;
+        if (b < NBLK && gm < rows_lim && gk < K)
+          r[j][i] = *reinterpret_cast<const uint4*>(src + (long)gk * ld + gm);
+        else
+          r[j][i] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(uint4* lds) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int b = j * NT + t;
+      if (b < NBLK) {
+        const int mc = b % (ROWS / 8), kg = b / (ROWS / 8);
+        uint4 tr[8];
+        transpose8x8(r[j], tr);
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr) lds[swz(mc * 8 + rr, kg)] = tr[rr];
+      }
+    }
+  }
+};
+
+template <int ROWS, int NT, int LAYOUT>
+using Loader = typename std::conditional<LAYOUT == kKC, KcLoader<ROWS, NT>,
+                                         McLoader<ROWS, NT>>::type;
+
+// ---- epilogue: four consecutive n of row m ---------------------------------
+template <int EPI>
+__device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const float* v) {
+  if (m >= p.M) return;
+  const bool full = (n + 3 < p.N);
+  if (EPI == kStoreBF16 || EPI == kResidBF16) {
+    bf16_t* C = reinterpret_cast<bf16_t*>(p.C) + (long)m * p.ldc + n;
+    float x[4] = {v[0], v[1], v[2], v[3]};
+    if (EPI == kResidBF16) {
+      const bf16_t* R = p.R + (long)m * p.ldr + n;
+      if (full) {
+        const uint2 r = *reinterpret_cast<const uint2*>(R);
+        x[0] += lo_f(r.x); x[1] += hi_f(r.x); x[2] += lo_f(r.y); x[3] += hi_f(r.y);
+      } else {
+        for (int e = 0; e < 4; ++e)
+          if (n + e < p.N) x[e] += bf2f(R[e]);
+      }
+    }
+    if (full) {
+      *reinterpret_cast<uint2*>(C) = make_uint2(pack2(x[0], x[1]), pack2(x[2], x[3]));
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < p.N) C[e] = f2bf(x[e]);
+    }
+  } else {
+    float* C = reinterpret_cast<float*>(p.C) + (long)m * p.ldc + n;
+    if (full) {
+      float4 o = make_float4(v[0], v[1], v[2], v[3]);
+      if (EPI == kAccF32) {
+        const float4 c = *reinterpret_cast<const float4*>(C);
+        o.x += c.x; o.y += c.y; o.z += c.z; o.w += c.w;
+      }
+      *reinterpret_cast<float4*>(C) = o;
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (n + e < p.N) C[e] = (EPI == kAccF32 ? C[e] : 0.0f) + v[e];
+    }
+  }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
+  constexpr int NT = WAVES_M * WAVES_N * 64;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
+  constexpr int A_ELEMS = BM * CHUNKS, B_ELEMS = BN * CHUNKS;
+  __shared__ uint4 lds[2][A_ELEMS + B_ELEMS];
+
+  // ---- tile order: XCD-contiguous bands, GROUP_M rows of tiles per band ----
+  const int tiles_m = (p.M + BM - 1) / BM;
+  const int tiles_n = (p.N + BN - 1) / BN;
+  const int nb = gridDim.x;
+  const int bid = blockIdx.x;
+  const int nb8 = nb - nb % NUM_XCD;
+  const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
+  const int in_group = GROUP_M * tiles_n;
+  const int first_m = (pid / in_group) * GROUP_M;
+  const int gsize = min(tiles_m - first_m, GROUP_M);
+  const int tm = first_m + (pid % in_group) % gsize;
+  const int tn = (pid % in_group) / gsize;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+
+  Loader<BM, NT, LA> la;
+  Loader<BN, NT, LB> lb;
+
+  f32x16_t acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  const int nk = (p.K + BK - 1) / BK;
+  la.load(p.A, p.lda, m0, p.M, 0, p.K);
+  lb.load(p.B, p.ldb, n0, p.N, 0, p.K);
+  la.store(lds[0]);
+  lb.store(lds[0] + A_ELEMS);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K);
+      lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K);
+    }
+    const uint4* At = lds[cur];
+    const uint4* Bt = lds[cur] + A_ELEMS;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int c = kk * 2 + (lane >> 5);
+      bf16x8_t fa[FN], fb[FM];
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+        fa[i] = __builtin_bit_cast(bf16x8_t, Bt[swz(wn * WN + i * 32 + (lane & 31), c)]);
+#pragma unroll
+      for (int j = 0; j < FM; ++j)
+        fb[j] = __builtin_bit_cast(bf16x8_t, At[swz(wm * WM + j * 32 + (lane & 31), c)]);
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      la.store(lds[cur ^ 1]);
+      lb.store(lds[cur ^ 1] + A_ELEMS);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block ------
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const int m = m0 + wm * WM + j * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * WN + i * 32 + g * 8 + (lane >> 5) * 4;
+        float v[4] = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
+                      acc[i][j][g * 4 + 3]};
+        store4<EPI>(p, m, n, v);
+      }
+    }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI>
+hipError_t launch(const GemmArgs& a, hipStream_t s) {
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI>), dim3(tiles),
+                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int LA, int LB, int EPI>
+hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
+  // Large tiles once they fill the chip, smaller ones for small problems.
+  const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
+  const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
+  if (big >= 256) return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
+  if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
+  return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
+}
+
+}  // namespace
+
+hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,
+                hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (la == kKC && lb == kKC) {
+    switch (epi) {
+      case kStoreBF16: return dispatch_tiles<kKC, kKC, kStoreBF16>(a, s);
+      case kResidBF16: return dispatch_tiles<kKC, kKC, kResidBF16>(a, s);
+      case kAccF32: return dispatch_tiles<kKC, kKC, kAccF32>(a, s);
+      case kStoreF32: return dispatch_tiles<kKC, kKC, kStoreF32>(a, s);
+    }
+  } else if (la == kKC && lb == kMC) {
+    switch (epi) {
+      case kStoreBF16: return dispatch_tiles<kKC, kMC, kStoreBF16>(a, s);
+      case kResidBF16: return dispatch_tiles<kKC, kMC, kResidBF16>(a, s);
+      default: break;
+    }
+  } else if (la == kMC && lb == kMC) {
+    switch (epi) {
+      case kAccF32: return dispatch_tiles<kMC, kMC, kAccF32>(a, s);
+      case kStoreF32: return dispatch_tiles<kMC, kMC, kStoreF32>(a, s);
+      default: break;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace forge

@@ -1,0 +1,94 @@
+// Internal launchers of libforge's gfx950 kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace forge {
+
+// ---------------------------------------------------------------- GEMM ----
+// C[m][n] (op)= sum_k A(m,k) B(k,n), bf16 operands, fp32 accumulation.
+//   A layout KC: A(m,k) = A[m*lda + k]     MC: A(m,k) = A[k*lda + m]
+//   B layout KC: B(k,n) = B[n*ldb + k]     MC: B(k,n) = B[k*ldb + n]
+// so y = x W^T is (KC, KC), dX = dY W is (KC, MC), dW = dY^T X is (MC, MC).
+enum GemmLayout { kKC = 0, kMC = 1 };
+enum GemmEpilogue {
+  kStoreBF16 = 0,     // C bf16 = acc
+  kResidBF16 = 1,     // C bf16 = acc + R (bf16), one rounding
+  kAccF32 = 2,        // C fp32 += acc
+  kStoreF32 = 3,      // C fp32 = acc
+};
+
+struct GemmArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  void* C;
+  const uint16_t* R;
+  int M, N, K;
+  long lda, ldb, ldc, ldr;
+};
+
+// Host-side shape rules (checked by the caller): K-contiguous operands need
+// K % 8 == 0; M/N-contiguous operands need that dimension % 8 == 0; leading
+// dimensions % 8 == 0; base pointers 16-byte aligned.
+hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,
+                hipStream_t stream);
+
+// --------------------------------------------------------- elementwise ----
+hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* g, uint16_t* y, float* rstd,
+                       int T, int h, float eps, hipStream_t s);
+// dx = RMSNorm backward (+ resid if non-null); dg_partial [nblk, h] per-block
+// partial sums of dy*x*rstd, reduced into dg (+=) by rmsnorm_dg_reduce.
+int rmsnorm_bwd_blocks(int T);
+hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
+                       const uint16_t* dy, const uint16_t* resid, uint16_t* dx,
+                       float* dg_partial, int T, int h, hipStream_t s);
+hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h,
+                             hipStream_t s);
+hipError_t rope_table(int seq, int d, float base, float* cos_t, float* sin_t,
+                      hipStream_t s);
+hipError_t rope_apply(uint16_t* qkv, long row_stride, const float* cos_t,
+                      const float* sin_t, int T, int seq, int n_heads_rot, int d,
+                      bool inverse, hipStream_t s);
+hipError_t swiglu_fwd(const uint16_t* gu, uint16_t* a, int T, int f, hipStream_t s);
+hipError_t swiglu_bwd(const uint16_t* gu, const uint16_t* da, uint16_t* dgu, int T,
+                      int f, hipStream_t s);
+hipError_t embed_fwd(const int32_t* ids, const uint16_t* emb, uint16_t* x, int T,
+                     int h, int V, hipStream_t s);
+hipError_t embed_bwd(const int32_t* ids, const uint16_t* dx, float* demb, int T,
+                     int h, int V, hipStream_t s);
+// In place: z [T, V] bf16 logits -> dz = (softmax - onehot) * inv_T; row_loss[t].
+hipError_t ce_fwd_bwd(uint16_t* z, const int32_t* targets, float* row_loss, int T,
+                      int V, float inv_T, hipStream_t s);
+hipError_t mean_reduce(const float* v, int n, float scale, float* out, hipStream_t s);
+hipError_t adamw(float* master, uint16_t* param, const float* grad, float* m, float* v,
+                 int64_t n, float b1, float b2, float eps, float wd,
+                 const float* scalars, hipStream_t s);
+constexpr int kNormPartials = 1024;
+hipError_t sumsq_partials(const float* g, int64_t n, float* partials, hipStream_t s);
+hipError_t sumsq_finish(const float* partials, float* accum, hipStream_t s);
+hipError_t clip_coeff(const float* norm_sq, float max_norm, float eps, float* scalars,
+                      hipStream_t s);
+
+// ----------------------------------------------------------- attention ----
+struct AttnArgs {
+  const uint16_t* q;    // [T, *] rows, head n at column n*d, row stride ld_qkv
+  const uint16_t* k;
+  const uint16_t* v;
+  long ld_qkv;
+  int batch, seq, n_heads, n_kv_heads, d;
+  float scale;          // 1/sqrt(d)
+};
+// o [T, n_heads*d] bf16; lse [batch, n_heads, seq] fp32 (natural log).
+hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s);
+// delta[b,n,i] = sum_d dO*O (fp32).
+hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
+                        float* delta, hipStream_t s);
+// dk, dv [T, n_kv*d] columns of the dqkv buffer (row stride ld_dqkv).
+hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* lse,
+                         const float* delta, uint16_t* dk, uint16_t* dv, long ld_dqkv,
+                         hipStream_t s);
+hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* lse,
+                       const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
+
+}  // namespace forge

@@ -1,0 +1,98 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol,
+answers size queries, and rejects bad arguments before touching the device."""
+import ctypes
+
+import pytest
+
+import forge_inputs as fi
+from paper_2609_13645_amd import _lib
+
+
+def test_library_exports_every_header_function():
+    L = _lib.load()
+    names = _lib.header_functions()
+    assert len(names) >= 15
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, missing
+    for n in ("forge_layer_fwd", "forge_layer_bwd", "forge_loss_fwd_bwd", "forge_adamw_step"):
+        assert n in names
+
+
+def test_status_strings_and_version():
+    assert _lib.status_name(0) == "FORGE_OK"
+    assert _lib.status_name(3) == "FORGE_ERR_ALIGNMENT"
+    assert _lib.status_name(99) == "FORGE_ERR_UNKNOWN"
+    assert "gfx950" in _lib.forge_version()
+
+
+def test_size_queries_are_consistent():
+    c2 = _lib.layer_cfg(fi.config("llama8b_layer"))
+    T, h, f = 4096, 4096, 14336
+    saved = _lib.forge_layer_saved_bytes(c2)
+    # a, qkv, o, h1, b, gu, act (bf16) + rstd x2, lse (fp32), 256-byte aligned pieces
+    lower = 2 * T * (h + 6144 + 4096 + h + h + 2 * f + f) + 4 * (2 * T + 32 * T)
+    assert lower <= saved <= lower + 256 * 12
+    rec = _lib.layer_cfg(fi.config("llama8b_layer_16k"))
+    rec_nokeep = _lib.layer_cfg(dict(fi.config("llama8b_layer_16k"), recompute_attn=0))
+    assert _lib.forge_layer_saved_bytes(rec) < _lib.forge_layer_saved_bytes(rec_nokeep)
+    assert _lib.forge_layer_workspace_bytes(rec) > _lib.forge_layer_workspace_bytes(rec_nokeep)
+    hc = _lib.HeadCfg(8192, 2048, 32000, 1e-5)
+    assert _lib.forge_loss_workspace_bytes(hc) >= 8192 * 32000 * 2
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(head_dim=96), _lib.FORGE_ERR_UNSUPPORTED),
+    (dict(n_heads=6, n_kv_heads=4), _lib.FORGE_ERR_INVALID_ARG),
+    (dict(hidden=260), _lib.FORGE_ERR_INVALID_ARG),
+    (dict(ffn=690), _lib.FORGE_ERR_INVALID_ARG),
+    (dict(seq=0), _lib.FORGE_ERR_INVALID_ARG),
+    (dict(n_experts=64, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
+])
+def test_bad_configs_rejected(change, status):
+    c = _lib.layer_cfg(dict(fi.config("tiny"), **change))
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_layer_saved_bytes(c)
+    assert e.value.status == status
+
+
+def test_null_and_misaligned_pointers_rejected_before_launch():
+    c = _lib.layer_cfg(fi.config("tiny"))
+    w = _lib.LayerWeights(*([0x1000] * 8 + [0, 0, 0]))
+    with pytest.raises(_lib.ForgeError) as e:      # x_in NULL
+        _lib.forge_layer_fwd(c, w, None, 0x2000, 0x3000, 0x4000, None, 0)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+    with pytest.raises(_lib.ForgeError) as e:      # misaligned x_out
+        _lib.forge_layer_fwd(c, w, 0x2000, 0x2008, 0x3000, 0x4000, None, 0)
+    assert e.value.status == _lib.FORGE_ERR_ALIGNMENT
+    with pytest.raises(_lib.ForgeError) as e:      # x_out overlaps x_in
+        _lib.forge_layer_fwd(c, w, 0x200000, 0x200000 + 4096, 0x3000, 0x4000, None, 0)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+    w_bad = _lib.LayerWeights(*([0x1000] * 7 + [0, 0, 0, 0]))   # rope_sin NULL
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_layer_fwd(c, w_bad, 0x2000, 0x900000, 0x3000, 0x4000, None, 0)
+    assert "rope_sin" in str(e.value)
+
+
+def test_gemm_argument_rules():
+    with pytest.raises(_lib.ForgeError) as e:      # (MC, KC) is not a supported combination
+        _lib.forge_gemm(1, 0, 0, 0x1000, 0x2000, 0x3000, None, 8, 8, 8, 8, 8, 8, 0, 0)
+    assert e.value.status == _lib.FORGE_ERR_UNSUPPORTED
+    with pytest.raises(_lib.ForgeError) as e:      # K-contiguous A with K % 8 != 0
+        _lib.forge_gemm(0, 0, 0, 0x1000, 0x2000, 0x3000, None, 8, 8, 12, 16, 16, 8, 0, 0)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+    with pytest.raises(_lib.ForgeError) as e:      # residual epilogue without R
+        _lib.forge_gemm(0, 0, 1, 0x1000, 0x2000, 0x3000, None, 8, 8, 8, 8, 8, 8, 8, 0)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+    # empty problems return OK without launching
+    _lib.forge_gemm(0, 0, 0, None, None, None, None, 0, 8, 8, 8, 8, 8, 0, 0)
+
+
+def test_optimizer_argument_rules():
+    hp = _lib.AdamwHparams(0.9, 1.5, 1e-8, 0.1)
+    with pytest.raises(_lib.ForgeError):
+        _lib.forge_adamw_step(0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 10, hp, 0x6000, 0)
+    ok = _lib.AdamwHparams(0.9, 0.95, 1e-8, 0.1)
+    _lib.forge_adamw_step(None, None, None, None, None, 0, ok, None, 0)   # n = 0: no-op
+    with pytest.raises(_lib.ForgeError):
+        _lib.forge_loss_workspace_bytes(_lib.HeadCfg(16, 64, 1001, 1e-5))  # vocab % 8
+    assert ctypes.sizeof(_lib.LayerCfg) == 14 * 4

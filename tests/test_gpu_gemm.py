@@ -1,0 +1,93 @@
+"""GPU parity of forge_gemm: every supported layout / epilogue, ragged shapes.
+
+Integer-valued inputs in [-4, 4] are exact in bf16 and every partial sum stays
+below 2^24, so fp32 accumulation is exact: fp32 outputs must match the exact
+product bit for bit, bf16 outputs must equal its round-to-nearest-even.
+Random-normal inputs check the large-tile paths against an fp64 product.
+"""
+import numpy as np
+import pytest
+
+import forge_inputs as fi
+from gpu_util import rel_fro, dev_bf16, host_f64, banner
+
+pytestmark = pytest.mark.gpu
+
+KC, MC = 0, 1
+STORE_BF16, RESID_BF16, ACC_F32, STORE_F32 = 0, 1, 2, 3
+COMBOS = [(KC, KC, STORE_BF16), (KC, KC, RESID_BF16), (KC, KC, ACC_F32), (KC, KC, STORE_F32),
+          (KC, MC, STORE_BF16), (KC, MC, RESID_BF16), (MC, MC, ACC_F32), (MC, MC, STORE_F32)]
+
+
+def _operands(la, lb, M, N, K, rng, integer):
+    def draw(shape):
+        if integer:
+            return rng.integers(-4, 5, size=shape).astype(np.float32)
+        return rng.standard_normal(shape, dtype=np.float32)
+    A = draw((M, K) if la == KC else (K, M))
+    B = draw((N, K) if lb == KC else (K, N))
+    return A, B
+
+
+def run_gemm(la, lb, epi, M, N, K, seed=0, integer=True):
+    import torch
+    from paper_2609_13645_amd import _lib
+    rng = np.random.default_rng(seed)
+    A, B = _operands(la, lb, M, N, K, rng, integer)
+    Ab, Bb = fi.to_bf16_bits(A), fi.to_bf16_bits(B)
+    Al64 = fi.bf16_bits_to_f64(Ab).reshape(A.shape)
+    Bl64 = fi.bf16_bits_to_f64(Bb).reshape(B.shape)
+    Al64 = Al64 if la == KC else Al64.T
+    Bl64 = Bl64.T if lb == KC else Bl64
+    prod = Al64 @ Bl64
+    dA, dB = dev_bf16(Ab), dev_bf16(Bb)
+    R = None
+    ref = prod.copy()
+    if epi in (STORE_BF16, RESID_BF16):
+        C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        if epi == RESID_BF16:
+            rb = fi.to_bf16_bits(rng.integers(-8, 9, size=(M, N)).astype(np.float32) if integer
+                                 else rng.standard_normal((M, N), dtype=np.float32))
+            R = dev_bf16(rb)
+            ref = ref + fi.bf16_bits_to_f64(rb)
+    else:
+        init = (rng.integers(-8, 9, size=(M, N)).astype(np.float32) if epi == ACC_F32
+                else np.full((M, N), np.nan, np.float32))
+        C = torch.from_numpy(init).cuda()
+        if epi == ACC_F32:
+            ref = ref + init
+    _lib.forge_gemm(la, lb, epi, dA, dB, C, R, M, N, K, A.shape[1], B.shape[1], N,
+                    N if R is not None else 0)
+    torch.cuda.synchronize()
+    return host_f64(C), ref
+
+
+@pytest.mark.parametrize("la,lb,epi", COMBOS)
+@pytest.mark.parametrize("M,N,K", [(64, 64, 64), (136, 200, 688), (264, 392, 40),
+                                   (8, 8, 8), (520, 136, 1000)])
+def test_gemm_integer_exact(la, lb, epi, M, N, K):
+    banner(f"gemm int la={la} lb={lb} epi={epi} M={M} N={N} K={K}")
+    got, ref = run_gemm(la, lb, epi, M, N, K, seed=M + N + K)
+    if epi in (STORE_BF16, RESID_BF16):
+        want = fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
+    else:
+        want = ref
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("la,lb,epi", [(KC, KC, STORE_BF16), (KC, MC, STORE_BF16),
+                                       (MC, MC, ACC_F32)])
+@pytest.mark.parametrize("M,N,K", [(4096, 4096, 64), (4096, 2048, 72), (1024, 1536, 256)])
+def test_gemm_tile_paths_random(la, lb, epi, M, N, K):
+    banner(f"gemm rand la={la} lb={lb} epi={epi} M={M} N={N} K={K}")
+    got, ref = run_gemm(la, lb, epi, M, N, K, seed=7, integer=False)
+    tol = 1e-2 if epi == STORE_BF16 else 1e-5
+    assert rel_fro(got, ref) <= tol
+
+
+def test_gemm_zero_k_and_empty():
+    banner("gemm K=0 / empty")
+    got, ref = run_gemm(KC, KC, ACC_F32, 64, 64, 0)
+    assert np.array_equal(got, ref)
+    got, ref = run_gemm(MC, MC, STORE_F32, 16, 24, 0)
+    assert np.array_equal(got, np.zeros_like(ref))
