@@ -4,7 +4,7 @@
  * The library runs one training step of a decoder-only transformer of the
  * kind the paper's engines train (App. B "Model Architectures": grouped-query
  * attention, SwiGLU feed-forward, pre-normalisation RMSNorm, RoPE), in bf16
- * with fp32 weight-gradient accumulation (Sec. 4.2, Table "Forged-kernel
+ * with fp32 weight-gradient accumulation (Sec. 4.2.2, Table "Forged-kernel
  * throughput", caption), as hand-written HIP kernels for gfx950. Calls follow
  * the paper's direct-dispatch model: raw device pointers plus a stream, no
  * framework types (App. J, "Direct dispatch").
@@ -191,7 +191,8 @@ forge_status forge_loss_workspace_bytes(const forge_head_cfg* cfg, size_t* bytes
 
 /*
  * Fused output head, forward and backward in one call (the fused fp32
- * cross-entropy of Sec. 4.2 / App. E):
+ * cross-entropy of App. A (framework-level trajectory) and App. G (fused
+ * FP32 cross-entropy)):
  *   xn = RMSNorm(x_L; final_norm), z = xn w_lm^T (bf16 logits, [T, V]),
  *   loss = (1/T) sum_t (logsumexp(z_t) - z_t[targets_t]), softmax in fp32,
  *   then dz = (softmax(z) - onehot) / T and the gradients.

@@ -9,7 +9,7 @@ input generator, which holds none of the method's arithmetic.
 What it computes is the plain definition of the training step of a
 decoder-only transformer with grouped-query attention, SwiGLU feed-forward
 blocks, pre-normalisation RMSNorm and RoPE (App. B "Model Architectures"),
-trained in bf16 with fp32 weight-gradient accumulation (Sec. 4.2, Table
+trained in bf16 with fp32 weight-gradient accumulation (Sec. 4.2.2, Table
 "Forged-kernel throughput", caption), with the fused clip + AdamW + bf16
 write-back update of App. F ("Vertical integration") and the device-side clip
 coefficient of App. F ("Deep customization"). The method only reaches this

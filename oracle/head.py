@@ -3,8 +3,8 @@
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 The output head is the fp32 softmax cross-entropy the engines fuse
-(Sec. 4.2 / App. E, "Fused cross-entropy"; App. H, "Fused NPU cross-entropy
-(FP32)"), after a final RMSNorm, optionally with the LM head tied to the input
+(App. A, framework-level trajectory, fused cross-entropy steps; App. G,
+fused NPU cross-entropy in FP32), after a final RMSNorm, optionally with the LM head tied to the input
 embedding (App. B, "Tied input/output embeddings").
 
 Readings where the paper is silent:
