@@ -35,60 +35,70 @@ __device__ __forceinline__ int swz(int row, int c) {
   return row * CHUNKS + (c ^ ((row ^ (row >> 3)) & 7));
 }
 
-// ---- global -> registers -> LDS, K-contiguous source ----------------------
-template <int ROWS, int NT>
+// ---- buffer resources ------------------------------------------------------
+// Raw buffer loads return zero for an offset past num_records, so every
+// out-of-range chunk (ragged M/N edge, K tail) is fetched as zeros without a
+// branch: the address of a chunk that is out of range is set to kOOB.
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr uint32_t kRecords = 0x7FFFFFF0u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)kRecords,
+                                           0x00020000);
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// ---- K-contiguous source: global -> LDS directly (no register staging) ----
+// Each wave-wide buffer_load_dwordx4 ... lds writes 1 KB of LDS: 8 tile rows
+// of 128 bytes, lane l landing at byte 16*l. Lane l therefore fetches the
+// logical chunk that the swizzle places at physical slot l % 8 of row l / 8.
+template <int ROWS, int NW>
 struct KcLoader {
-  static constexpr int PER = ROWS * CHUNKS / NT;
-  static_assert(PER * NT == ROWS * CHUNKS, "tile rows must split over threads");
-  uint4 r[PER];
+  static constexpr int PER = ROWS / 8 / NW;
+  static_assert(PER * 8 * NW == ROWS, "tile rows must split over waves");
   __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
-                                       int rows_lim, int k0, int K) {
-    const int t = threadIdx.x;
+                                       int rows_lim, int k0, int K, uint4* lds, int wave,
+                                       int lane) const {
+    const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)row0 * ld + k0);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int id = i * NT + t;
-      const int row = id / CHUNKS, c = id % CHUNKS;
-      const int gr = row0 + row, gk = k0 + c * 8;
-      if (gr < rows_lim && gk < K)
-        r[i] = *reinterpret_cast<const uint4*>(src + (long)gr * ld + gk);
-      else
-        r[i] = make_uint4(0, 0, 0, 0);
+      const int blk = i * NW + wave;
+      const int row = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+      const bool ok = (row0 + row < rows_lim) && (k0 + c * 8 < K);
+      const uint32_t off = ok ? (uint32_t)(((long)row * ld + c * 8) * 2) : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + blk * 64), 16, off, 0, 0, 0);
     }
   }
-  __device__ __forceinline__ void store(uint4* lds) const {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int id = i * NT + t;
-      lds[swz(id / CHUNKS, id % CHUNKS)] = r[i];
-    }
-  }
+  __device__ __forceinline__ void store(uint4*) const {}
 };
 
-// ---- global -> registers -> LDS, source contiguous along the row dim -----
+// ---- source contiguous along the row dim: registers, 8x8 transpose -------
 // The tile is 64 k-rows of ROWS contiguous elements in HBM. Each thread owns
 // 8x8 blocks (8 k by 8 rows), loads them as eight 16-byte rows and
-// transposes them in registers.
-template <int ROWS, int NT>
+// transposes them in registers before the LDS store.
+template <int ROWS, int NW>
 struct McLoader {
+  static constexpr int NT = NW * 64;
   static constexpr int NBLK = ROWS;  // (ROWS/8 row chunks) x (8 k groups)
   static constexpr int PER = (NBLK + NT - 1) / NT;
   uint4 r[PER][8];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
-                                       int rows_lim, int k0, int K) {
+                                       int rows_lim, int k0, int K, uint4*, int, int) {
+    const __amdgpu_buffer_rsrc_t rs = rsrc(src + (long)k0 * ld + row0);
     const int t = threadIdx.x;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       const int b = j * NT + t;
       const int mc = b % (ROWS / 8), kg = b / (ROWS / 8);
-      const int gm = row0 + mc * 8;
+      const bool okr = (b < NBLK) && (row0 + mc * 8 < rows_lim);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const int gk = k0 + kg * 8 + i;
-        if (b < NBLK && gm < rows_lim && gk < K)
-          r[j][i] = *reinterpret_cast<const uint4*>(src + (long)gk * ld + gm);
-        else
-          r[j][i] = make_uint4(0, 0, 0, 0);
+        const int k = kg * 8 + i;
+        const bool ok = okr && (k0 + k < K);
+        const uint32_t off = ok ? (uint32_t)(((long)k * ld + mc * 8) * 2) : kOOB;
+        r[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
       }
     }
   }
@@ -108,9 +118,9 @@ struct McLoader {
   }
 };
 
-template <int ROWS, int NT, int LAYOUT>
-using Loader = typename std::conditional<LAYOUT == kKC, KcLoader<ROWS, NT>,
-                                         McLoader<ROWS, NT>>::type;
+template <int ROWS, int NW, int LAYOUT>
+using Loader = typename std::conditional<LAYOUT == kKC, KcLoader<ROWS, NW>,
+                                         McLoader<ROWS, NW>>::type;
 
 // ---- epilogue: four consecutive n of row m ---------------------------------
 template <int EPI>
@@ -176,11 +186,12 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  constexpr int NW = WAVES_M * WAVES_N;
 
-  Loader<BM, NT, LA> la;
-  Loader<BN, NT, LB> lb;
+  Loader<BM, NW, LA> la;
+  Loader<BN, NW, LB> lb;
 
   f32x16_t acc[FN][FM];
 #pragma unroll
@@ -191,36 +202,48 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
   const int nk = (p.K + BK - 1) / BK;
-  la.load(p.A, p.lda, m0, p.M, 0, p.K);
-  lb.load(p.B, p.ldb, n0, p.N, 0, p.K);
+  la.load(p.A, p.lda, m0, p.M, 0, p.K, lds[0], wave, lane);
+  lb.load(p.B, p.ldb, n0, p.N, 0, p.K, lds[0] + A_ELEMS, wave, lane);
   la.store(lds[0]);
   lb.store(lds[0] + A_ELEMS);
   __syncthreads();
 
+  const int ra = wn * WN + (lane & 31);  // first B-tile row of this lane
+  const int rb = wm * WM + (lane & 31);  // first A-tile row of this lane
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {
-      la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K);
-      lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K);
+      la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K, lds[cur ^ 1], wave, lane);
+      lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K, lds[cur ^ 1] + A_ELEMS, wave, lane);
     }
     const uint4* At = lds[cur];
     const uint4* Bt = lds[cur] + A_ELEMS;
+    // fragments double-buffered across the four 16-deep k-slices
+    bf16x8_t fa[2][FN], fb[2][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+      fa[0][i] = __builtin_bit_cast(bf16x8_t, Bt[swz(ra + i * 32, lane >> 5)]);
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+      fb[0][j] = __builtin_bit_cast(bf16x8_t, At[swz(rb + j * 32, lane >> 5)]);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = kk * 2 + (lane >> 5);
-      bf16x8_t fa[FN], fb[FM];
+      const int cb = kk & 1, nb = cb ^ 1;
+      if (kk + 1 < BK / 16) {
+        const int c = (kk + 1) * 2 + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
-        fa[i] = __builtin_bit_cast(bf16x8_t, Bt[swz(wn * WN + i * 32 + (lane & 31), c)]);
+        for (int i = 0; i < FN; ++i)
+          fa[nb][i] = __builtin_bit_cast(bf16x8_t, Bt[swz(ra + i * 32, c)]);
 #pragma unroll
-      for (int j = 0; j < FM; ++j)
-        fb[j] = __builtin_bit_cast(bf16x8_t, At[swz(wm * WM + j * 32 + (lane & 31), c)]);
+        for (int j = 0; j < FM; ++j)
+          fb[nb][j] = __builtin_bit_cast(bf16x8_t, At[swz(rb + j * 32, c)]);
+      }
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
         for (int j = 0; j < FM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fb[cb][j], acc[i][j], 0, 0, 0);
     }
     if (more) {
       la.store(lds[cur ^ 1]);
@@ -256,9 +279,14 @@ hipError_t launch(const GemmArgs& a, hipStream_t s) {
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
+  // With both operands K-contiguous (LDS filled by DMA) 8 waves of 64x128
+  // hide LDS latency better; the transposing loaders keep 4 waves.
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
-  if (big >= 256) return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
+  if (big >= 256) {
+    if (LA == kKC && LB == kKC) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
+    return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
+  }
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
 }
