@@ -136,7 +136,7 @@ def gpu_step_bench(cfg, steps, warmup, kernel_reps):
     torch.cuda.synchronize()
     k_ms = e0.elapsed_time(e1) / kernel_reps
     k_flop = 2.0 * T * (2 * f) * h
-    kernel = {"name": "gemm_kernel<256,256,2,2,KC,KC,StoreBF16> (gate/up fwd)",
+    kernel = {"name": "gemm_kernel<256,256,4,2,KC,KC,StoreBF16> (gate/up fwd)",
               "shape": f"M={T} N={2 * f} K={h}", "avg_us": k_ms * 1e3,
               "flop_per_launch": k_flop}
     return ms, phases, kernel, flat.n

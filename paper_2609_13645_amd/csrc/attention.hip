@@ -1,30 +1,30 @@
 // Causal grouped-query flash attention on gfx950 MFMA: forward, and the
-// backward as a pre-pass (delta = rowsum(dO * O)) plus two kernels, one that
-// owns a key tile and accumulates dK, dV over the queries of its whole GQA
-// group, and one that owns a query tile and accumulates dQ over keys. The
-// paper's H100 kernel accumulates dQ through a flat global buffer (App. D,
-// "Anatomy of a Forged Kernel"); on MI355X the separate dQ kernel costs two
-// recomputed products but no fp32 atomics and keeps every output
-// deterministic.
+// backward as a pre-pass (delta = rowsum(dO * O)), key-owned kernels that
+// accumulate dV and dK, a query-owned kernel that accumulates dQ, and a
+// small reduction of the dK, dV partials over each GQA group. The paper's H100
+// kernel accumulates dQ through a flat global buffer (App. D, "Anatomy of a
+// Forged Kernel"); here the dQ kernel recomputes two products instead, with no
+// fp32 atomics, so every output is deterministic.
 //
 // Operand layout. The 32x32x16 MFMA gives each lane one column of its 32x32
 // result and sixteen rows. Scores are formed with the lane-owned index on the
 // column:
 //   * forward / dQ: S^T = K Q^T (lane owns a query), so the softmax row
-//     statistics, the LSE and delta are lane-local and O^T = V^T P^T,
+//     statistics, the LSE and delta are lane-local, and O^T = V^T P^T,
 //     dQ^T = K^T dS^T take P^T / dS^T straight from the accumulators;
 //   * dK/dV: S = Q K^T (lane owns a key), so dV^T = dO^T P and dK^T = Q^T dS
 //     take P / dS straight from the accumulators.
 // Accumulator rows come in groups of four, so the reduction index of those
-// register-sourced operands is permuted; the LDS copies of V^T, K^T, Q^T and
-// dO^T are stored with the same permutation of their key / query index (each
-// 16-byte LDS chunk holds keys {4h..4h+3, 8+4h..8+4h+3} of a 16-key group), so
-// every MFMA operand is one 16-byte LDS read. Transposed copies are made in
-// registers (8x8 blocks) from the same coalesced loads as the natural copies.
+// register-sourced operands is permuted (keys {4h..4h+3, 8+4h..8+4h+3} of a
+// 16-group for lane half h); the matching transposed operand (V^T, K^T, Q^T,
+// dO^T) is read with two ds_read_b64_tr_b16 of four consecutive rows each
+// from the natural [rows][d] tile, which gives exactly that order.
 //
-// Online softmax runs in the log2 domain (scale * log2 e folded into one
-// multiply); the causal mask is only evaluated on tiles that straddle the
-// diagonal, and waves whose rows are fully masked skip their MFMAs.
+// Every tile is loaded global -> LDS by buffer_load ... lds (no register
+// staging); rows past the sequence end read as zeros. The online softmax runs
+// in the log2 domain (scale * log2 e folded into one multiply); the causal
+// mask is evaluated only on tiles that straddle the diagonal, and waves whose
+// rows are fully masked skip their MFMAs.
 #include "common.h"
 #include "kernels.h"
 
@@ -33,60 +33,78 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr uint32_t kOOB = 0x80000000u;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// [64 rows][D] tile, row-contiguous along D, chunk-swizzled.
-template <int D>
-__device__ __forceinline__ int nat_idx(int row, int c) {
-  constexpr int CPR = D / 8;
-  return row * CPR + (c ^ (row & (CPR - 1)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7FFFFFF0,
+                                           0x00020000);
 }
-// [D rows][64] tile of a transposed operand: 8 chunks per row, permuted
-// 4+4 index order inside each 16-group, chunk-swizzled.
-__device__ __forceinline__ int tr_idx(int row, int pc) {
-  return row * 8 + (pc ^ ((row ^ (row >> 3)) & 7));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
+
+// Natural [64 rows][D] bf16 tile in LDS, 16-byte chunk c of row r at slot
+// c ^ fsw(r). For D = 128 the swizzle keeps both read patterns on distinct
+// banks: 32 rows of one chunk (row-fragment reads) and 4 consecutive rows of
+// 4 consecutive chunks (transposed reads).
+template <int D>
+__device__ __forceinline__ int fsw(int r) {
+  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : (r & 7);
+}
+template <int D>
+__device__ __forceinline__ int slot(int r, int c) {
+  return r * (D / 8) + (c ^ fsw<D>(r));
 }
 
-__device__ __forceinline__ void load_blk(const bf16_t* __restrict__ base, long ld, int row0,
-                                         int lim, int cg, uint4* r) {
+// DMA 64 rows [row0, row0 + 64) of a [*, ld] bf16 matrix (column block at
+// base) into a natural tile; rows >= lim read as zeros.
+template <int D, int NW>
+__device__ __forceinline__ void dma_tile(const bf16_t* base, long ld, int row0, int lim,
+                                         uint4* lds, int wave, int lane) {
+  constexpr int LPR = D / 8;            // 16-byte chunks per row
+  constexpr int RPI = 64 / LPR;         // rows per 1 KB instruction
+  constexpr int PER = 64 / RPI / NW;    // instructions per wave
+  static_assert(PER * RPI * NW == 64, "tile rows must split over waves");
+  const __amdgpu_buffer_rsrc_t r = rsrc(base + (long)row0 * ld);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int row = row0 + i;
-    r[i] = row < lim ? *reinterpret_cast<const uint4*>(base + (long)row * ld + cg * 8)
-                     : make_uint4(0, 0, 0, 0);
+  for (int i = 0; i < PER; ++i) {
+    const int q = i * NW + wave;
+    const int row = q * RPI + lane / LPR;
+    const int c = (lane % LPR) ^ fsw<D>(row);
+    const uint32_t off = row0 + row < lim ? (uint32_t)(((long)row * ld + c * 8) * 2) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + q * 64), 16, off, 0, 0, 0);
   }
 }
 
+// Row fragment: rows rb..rb+31 (lane row rb + lane % 32), d = kk*16 + 8*(lane/32) .. +7.
 template <int D>
-__device__ __forceinline__ void store_nat(uint4* lds, int rg, int cg, const uint4* r) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) lds[nat_idx<D>(rg * 8 + i, cg)] = r[i];
+__device__ __forceinline__ bf16x8_t row_frag(const uint4* t, int rb, int kk, int lane) {
+  return __builtin_bit_cast(bf16x8_t, t[slot<D>(rb + (lane & 31), kk * 2 + (lane >> 5))]);
 }
 
-// Block (rg, cg) of a [64][D] tile -> rows cg*8..+7 of the [D][64] permuted copy.
-__device__ __forceinline__ void store_tr(uint4* lds, int rg, int cg, const uint4* r) {
-  uint4 t[8];
-  transpose8x8(r, t);
-  const int a = rg >> 1, odd = rg & 1;
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    const int row = cg * 8 + c;
-    uint2* p0 = reinterpret_cast<uint2*>(lds + tr_idx(row, 2 * a)) + odd;
-    uint2* p1 = reinterpret_cast<uint2*>(lds + tr_idx(row, 2 * a + 1)) + odd;
-    *p0 = make_uint2(t[c].x, t[c].y);
-    *p1 = make_uint2(t[c].z, t[c].w);
-  }
+// Transposed fragment: column d = db*32 + lane % 32 of the tile, rows
+// (the reduction index) r16 + 4h + {0..3} and r16 + 8 + 4h + {0..3}, h = lane/32.
+template <int D>
+__device__ __forceinline__ bf16x8_t tr_frag(const uint4* t, int r16, int db, int lane) {
+  const uint16_t* e = reinterpret_cast<const uint16_t*>(t);
+  const int g = lane >> 4, i = lane & 15;
+  const int d = db * 32 + (g & 1) * 16 + 4 * (i & 3);
+  const int r = r16 + (g >> 1) * 4 + (i >> 2);
+  const int c = d >> 3, w = d & 7;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16_ptr)(e + (long)slot<D>(r, c) * 8 + w));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16_ptr)(e + (long)slot<D>(r + 8, c) * 8 + w));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
 }
 
 __device__ __forceinline__ bf16x8_t pack_frag(const f32x16_t& v, int s) {
   uint4 u = make_uint4(pack2(v[8 * s + 0], v[8 * s + 1]), pack2(v[8 * s + 2], v[8 * s + 3]),
                        pack2(v[8 * s + 4], v[8 * s + 5]), pack2(v[8 * s + 6], v[8 * s + 7]));
   return __builtin_bit_cast(bf16x8_t, u);
-}
-
-__device__ __forceinline__ bf16x8_t ld_frag(const uint4* p) {
-  return __builtin_bit_cast(bf16x8_t, *p);
 }
 
 __device__ __forceinline__ bf16x8_t gload_frag(const bf16_t* p, bool ok) {
@@ -99,14 +117,15 @@ __device__ __forceinline__ void zero(f32x16_t& a) {
   for (int e = 0; e < 16; ++e) a[e] = 0.0f;
 }
 
+#define MFMA(a, b, c) __builtin_amdgcn_mfma_f32_32x32x16_bf16((a), (b), (c), 0, 0, 0)
+
 // ------------------------------------------------------------- forward ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_fwd_k(AttnArgs a, bf16_t* __restrict__ o,
+__global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restrict__ o,
                                                      float* __restrict__ lse) {
-  constexpr int BQ = 128, BKV = 64, CPR = D / 8;
-  constexpr int NAT = BKV * CPR, TRN = D * 8, NBLK = 8 * CPR;
-  __shared__ uint4 smem[2][NAT + TRN];
+  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8;
+  __shared__ uint4 smem[2][2 * NAT];  // K tile, V tile
 
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
@@ -117,7 +136,8 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
   const bf16_t* Kg = a.k + rb * a.ld_qkv + (long)m * D;
   const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
   const int q0w = qt * BQ + wave * 32;
   const int q = q0w + l32;
@@ -135,42 +155,28 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
 
-  // staging: block t < NBLK -> K block (natural), NBLK <= t < 2 NBLK -> V block (transposed)
-  const int tb = threadIdx.x;
-  const bool has_blk = tb < 2 * NBLK;
-  const bool is_v = tb >= NBLK;
-  const int blk = tb % NBLK, rg = blk / CPR, cg = blk % CPR;
-  uint4 st[8];
-  auto load_tile = [&](int kt) {
-    if (has_blk) load_blk(is_v ? Vg : Kg, a.ld_qkv, kt * BKV + rg * 8, S, cg, st);
-  };
-  auto store_tile = [&](int buf) {
-    if (has_blk) {
-      if (is_v) store_tr(smem[buf] + NAT, rg, cg, st);
-      else store_nat<D>(smem[buf], rg, cg, st);
-    }
-  };
-
-  load_tile(0);
-  store_tile(0);
+  dma_tile<D, 4>(Kg, a.ld_qkv, 0, S, smem[0], wave, lane);
+  dma_tile<D, 4>(Vg, a.ld_qkv, 0, S, smem[0] + NAT, wave, lane);
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < nkt;
-    if (more) load_tile(kt + 1);
+    if (kt + 1 < nkt) {
+      dma_tile<D, 4>(Kg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1], wave, lane);
+      dma_tile<D, 4>(Vg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1] + NAT, wave, lane);
+    }
     const int k0 = kt * BKV;
     if (k0 <= q0w + 31) {
+      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
+      asm volatile("" : "+v"(ln));
       const uint4* Ks = smem[cur];
-      const uint4* Vt = smem[cur] + NAT;
+      const uint4* Vs = smem[cur] + NAT;
       f32x16_t s[2];
       zero(s[0]);
       zero(s[1]);
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              ld_frag(Ks + nat_idx<D>(kb * 32 + l32, kk * 2 + hh)), qf[kk], s[kb], 0, 0, 0);
+        for (int kb = 0; kb < 2; ++kb) s[kb] = MFMA(row_frag<D>(Ks, kb * 32, kk, ln), qf[kk], s[kb]);
       const bool diag = (k0 + BKV - 1 > q0w);
       float mt = -INFINITY;
 #pragma unroll
@@ -209,11 +215,9 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_k(AttnArgs a, bf16_t* __restr
           const bf16x8_t pf = pack_frag(s[kb], ss);
 #pragma unroll
           for (int db = 0; db < D / 32; ++db)
-            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                ld_frag(Vt + tr_idx(db * 32 + l32, kb * 4 + ss * 2 + hh)), pf, oacc[db], 0, 0, 0);
+            oacc[db] = MFMA(tr_frag<D>(Vs, kb * 32 + ss * 16, db, ln), pf, oacc[db]);
         }
     }
-    if (more) store_tile(cur ^ 1);
     __syncthreads();
   }
 
@@ -235,198 +239,208 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_k(AttnArgs a, bf16_t* __restr
 }
 
 // -------------------------------------------------- backward pre-pass ----
-// delta[b, n, s] = sum_d dO[t, n, d] O[t, n, d]; one thread per (token, head).
+// delta[b, n, s] = sum_d dO[t, n, d] O[t, n, d]; 8 lanes per (token, head).
 template <int D>
-__global__ void attn_bwd_pre_k(AttnArgs a, const bf16_t* __restrict__ o,
-                               const bf16_t* __restrict__ dout, float* __restrict__ delta) {
-  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
+__global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* __restrict__ o,
+                                                      const bf16_t* __restrict__ dout,
+                                                      float* __restrict__ delta) {
+  const long id = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
+  const int sub = threadIdx.x & 7;
   const long T = (long)a.batch * a.seq;
-  if (id >= T * a.n_heads) return;
-  const long t = id / a.n_heads;
-  const int n = (int)(id % a.n_heads);
+  const bool ok = id < T * a.n_heads;
+  const long t = ok ? id / a.n_heads : 0;
+  const int n = ok ? (int)(id % a.n_heads) : 0;
   const long off = t * (long)(a.n_heads * D) + (long)n * D;
-  const uint4* op = reinterpret_cast<const uint4*>(o + off);
-  const uint4* dp = reinterpret_cast<const uint4*>(dout + off);
   float s = 0.0f;
+  if (ok) {
 #pragma unroll
-  for (int c = 0; c < D / 8; ++c) {
-    float x[8], y[8];
-    unpack8(op[c], x);
-    unpack8(dp[c], y);
+    for (int c = sub; c < D / 8; c += 8) {
+      float x[8], y[8];
+      unpack8(reinterpret_cast<const uint4*>(o + off)[c], x);
+      unpack8(reinterpret_cast<const uint4*>(dout + off)[c], y);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s += x[e] * y[e];
+      for (int e = 0; e < 8; ++e) s += x[e] * y[e];
+    }
   }
-  const long b = t / a.seq, i = t % a.seq;
-  delta[(b * a.n_heads + n) * a.seq + i] = s;
+  s += __shfl_xor(s, 1, 64);
+  s += __shfl_xor(s, 2, 64);
+  s += __shfl_xor(s, 4, 64);
+  if (ok && sub == 0) {
+    const long bb = t / a.seq, i = t % a.seq;
+    delta[(bb * a.n_heads + n) * a.seq + i] = s;
+  }
 }
 
 // ------------------------------------------------------ backward dK, dV ----
-// Block: 128 keys (32 per wave) of one (batch, kv head); loops over the GQA
-// group's query heads and the 64-query tiles at or after its first key.
-template <int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_k(
+// Block: 128 keys (32 per wave) of one (batch, query head); loops over the
+// 64-query tiles at or after its first key and writes fp32 partials of its
+// query head; attn_bwd_reduce_k sums the GQA group's partials. The work is
+// split into two passes so each keeps one d x 32 accumulator per wave and
+// the kernel runs two blocks per CU:
+//   PASS 0: S = Q K^T, P = exp(S - LSE), dV^T += dO^T P
+//   PASS 1: S, dP = dO V^T, dS = P (dP - delta), dK^T += Q^T dS
+// (S is formed twice, 5 products instead of 4, for twice the occupancy.)
+template <int D, int PASS>
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ lse,
-    const float* __restrict__ delta, bf16_t* __restrict__ dk, bf16_t* __restrict__ dv,
-    long ld_d) {
-  constexpr int BKEY = 128, BQ = 64, CPR = D / 8;
-  constexpr int NAT = BQ * CPR, TRN = D * 8, NBLK = 8 * CPR;
-  // per stage: Q nat, dO nat, Q^T, dO^T, then lse2[64], delta[64] as floats
-  constexpr int STAGE = 2 * NAT + 2 * TRN + 32;
+    const float* __restrict__ delta, float* __restrict__ pk, float* __restrict__ pv) {
+  constexpr int BKEY = 128, BQ = 64, NAT = BQ * D / 8;
+  constexpr int STAGE = 2 * NAT + 32;  // Q tile, dO tile, lse[64], delta[64]
   __shared__ uint4 smem[2][STAGE];
 
   const int S = a.seq;
-  const int kt = blockIdx.x, m = blockIdx.y, b = blockIdx.z;
+  const int kt = blockIdx.x;  // low key tiles have the most work: dispatched first
+  const int n = blockIdx.y, b = blockIdx.z;
   const int grp = a.n_heads / a.n_kv_heads;
+  const int m = n / grp;
   const long rb = (long)b * S;
   const long ldo = (long)a.n_heads * D;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
   const int kw0 = kt * BKEY + wave * 32;
   const int key = kw0 + l32;
 
   const bf16_t* Kg = a.k + rb * a.ld_qkv + (long)m * D;
   const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
-  bf16x8_t kf[D / 16], vf[D / 16];
+  const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
+  const bf16_t* dOg = dout + rb * ldo + (long)n * D;
+  const float* Lg = lse + ((long)b * a.n_heads + n) * S;
+  const float* Dg = delta + ((long)b * a.n_heads + n) * S;
+  // K (and, for PASS 1, V) rows of this lane's key: the B operands of S, dP
+  bf16x8_t kf[D / 16], vf[PASS ? D / 16 : 1];
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
     kf[kk] = gload_frag(Kg + (long)key * a.ld_qkv + kk * 16 + hh * 8, key < S);
-    vf[kk] = gload_frag(Vg + (long)key * a.ld_qkv + kk * 16 + hh * 8, key < S);
+    if (PASS) vf[kk] = gload_frag(Vg + (long)key * a.ld_qkv + kk * 16 + hh * 8, key < S);
   }
-  f32x16_t dka[D / 32], dva[D / 32];
+  f32x16_t acc[D / 32];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) {
-    zero(dka[db]);
-    zero(dva[db]);
-  }
+  for (int db = 0; db < D / 32; ++db) zero(acc[db]);
   const float c = a.scale * kLog2e;
   const int nqt = (S + BQ - 1) / BQ;
   const int qt0 = (kt * BKEY) / BQ;
-  const int per_head = nqt - qt0;
-  const int iters = grp * per_head;
+  const int iters = nqt - qt0;
 
-  const int tb = threadIdx.x;
-  const bool has_blk = tb < 2 * NBLK;
-  const bool is_do = tb >= NBLK;
-  const int blk = tb % NBLK, rg = blk / CPR, cg = blk % CPR;
-  uint4 st[8];
-  float st_l = 0.0f, st_d = 0.0f;
-  auto load_tile = [&](int it) {
-    const int n = m * grp + it / per_head;
-    const int q0 = (qt0 + it % per_head) * BQ;
-    if (has_blk) {
-      if (is_do) load_blk(dout + rb * ldo + (long)n * D, ldo, q0 + rg * 8, S, cg, st);
-      else load_blk(a.q + rb * a.ld_qkv + (long)n * D, a.ld_qkv, q0 + rg * 8, S, cg, st);
-    }
-    if (tb < BQ) {
-      const int qq = q0 + tb;
-      const long li = ((long)b * a.n_heads + n) * S + qq;
-      st_l = qq < S ? lse[li] * kLog2e : INFINITY;
-      st_d = qq < S ? delta[li] : 0.0f;
-    }
-  };
-  auto store_tile = [&](int buf) {
+  auto load_tile = [&](int it, int buf) {
+    const int q0 = (qt0 + it) * BQ;
     uint4* base = smem[buf];
-    if (has_blk) {
-      store_nat<D>(base + (is_do ? NAT : 0), rg, cg, st);
-      store_tr(base + 2 * NAT + (is_do ? TRN : 0), rg, cg, st);
-    }
-    float* stats = reinterpret_cast<float*>(base + 2 * NAT + 2 * TRN);
-    if (tb < BQ) {
-      stats[tb] = st_l;
-      stats[BQ + tb] = st_d;
+    dma_tile<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, lane);
+    dma_tile<D, 4>(dOg, ldo, q0, S, base + NAT, wave, lane);
+    if (wave == 0) {
+      const uint32_t off = q0 + lane < S ? (uint32_t)((q0 + lane) * 4) : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Lg), (lds_ptr_t)(base + 2 * NAT), 4, off, 0, 0, 0);
+      if (PASS)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Dg), (lds_ptr_t)(base + 2 * NAT + 16), 4, off, 0, 0, 0);
     }
   };
 
-  if (iters > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
+  load_tile(0, 0);
   __syncthreads();
   for (int it = 0; it < iters; ++it) {
     const int cur = it & 1;
-    const bool more = it + 1 < iters;
-    if (more) load_tile(it + 1);
-    const int q0 = (qt0 + it % per_head) * BQ;
+    if (it + 1 < iters) load_tile(it + 1, cur ^ 1);
+    const int q0 = (qt0 + it) * BQ;
     if (q0 + BQ - 1 >= kw0) {
-      const uint4* base = smem[cur];
-      const uint4* Qs = base;
-      const uint4* dOs = base + NAT;
-      const uint4* Qt = base + 2 * NAT;
-      const uint4* dOt = base + 2 * NAT + TRN;
-      const float* L2 = reinterpret_cast<const float*>(base + 2 * NAT + 2 * TRN);
-      const float* Dl = L2 + BQ;
+      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
+      asm volatile("" : "+v"(ln));
+      const uint4* Qs = smem[cur];
+      const uint4* dOs = smem[cur] + NAT;
+      const float* L = reinterpret_cast<const float*>(smem[cur] + 2 * NAT);
+      const float* Dl = L + BQ;
       f32x16_t s[2], dp[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         zero(s[qb]);
-        zero(dp[qb]);
+        if (PASS) zero(dp[qb]);
       }
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-          s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              ld_frag(Qs + nat_idx<D>(qb * 32 + l32, kk * 2 + hh)), kf[kk], s[qb], 0, 0, 0);
-          dp[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              ld_frag(dOs + nat_idx<D>(qb * 32 + l32, kk * 2 + hh)), vf[kk], dp[qb], 0, 0, 0);
+          s[qb] = MFMA(row_frag<D>(Qs, qb * 32, kk, ln), kf[kk], s[qb]);
+          if (PASS) dp[qb] = MFMA(row_frag<D>(dOs, qb * 32, kk, ln), vf[kk], dp[qb]);
         }
       const bool diag = (q0 < kw0 + 31);
+      const bool tail = (q0 + BQ > S);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          float p = fast_exp2(s[qb][i] * c - L2[qi]);
-          if (diag && key > q0 + qi) p = 0.0f;
-          s[qb][i] = p;
-          dp[qb][i] = p * (dp[qb][i] - Dl[qi]);
+          float p = fast_exp2(s[qb][i] * c - L[qi] * kLog2e);
+          if ((diag && key > q0 + qi) || (tail && q0 + qi >= S)) p = 0.0f;
+          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
         }
+      // PASS 0: dV^T += dO^T P;  PASS 1: dK^T += Q^T dS
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int ss = 0; ss < 2; ++ss) {
-          const bf16x8_t pf = pack_frag(s[qb], ss);
-          const bf16x8_t df = pack_frag(dp[qb], ss);
+          const bf16x8_t f = pack_frag(s[qb], ss);
 #pragma unroll
-          for (int db = 0; db < D / 32; ++db) {
-            const int ti = tr_idx(db * 32 + l32, qb * 4 + ss * 2 + hh);
-            dva[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(dOt + ti), pf, dva[db], 0, 0, 0);
-            dka[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld_frag(Qt + ti), df, dka[db], 0, 0, 0);
-          }
+          for (int db = 0; db < D / 32; ++db)
+            acc[db] = MFMA(tr_frag<D>(PASS ? Qs : dOs, qb * 32 + ss * 16, db, ln), f, acc[db]);
         }
     }
-    if (more) store_tile(cur ^ 1);
     __syncthreads();
   }
 
+  // partials: [grp][T][hkv] fp32, this block's query head is slot n % grp
   if (key < S) {
-    bf16_t* dkr = dk + (rb + key) * ld_d + (long)m * D;
-    bf16_t* dvr = dv + (rb + key) * ld_d + (long)m * D;
+    const long hkv = (long)a.n_kv_heads * D;
+    const long base = ((long)(n % grp) * a.batch * S + rb + key) * hkv + (long)m * D;
+    float* dst = PASS ? pk : pv;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = db * 32 + g * 8 + hh * 4;
-        *reinterpret_cast<uint2*>(dkr + d) =
-            make_uint2(pack2(dka[db][g * 4 + 0] * a.scale, dka[db][g * 4 + 1] * a.scale),
-                       pack2(dka[db][g * 4 + 2] * a.scale, dka[db][g * 4 + 3] * a.scale));
-        *reinterpret_cast<uint2*>(dvr + d) =
-            make_uint2(pack2(dva[db][g * 4 + 0], dva[db][g * 4 + 1]),
-                       pack2(dva[db][g * 4 + 2], dva[db][g * 4 + 3]));
+        *reinterpret_cast<float4*>(dst + base + d) =
+            make_float4(acc[db][g * 4], acc[db][g * 4 + 1], acc[db][g * 4 + 2], acc[db][g * 4 + 3]);
       }
   }
+}
+
+// dk = scale * sum_g pk[g], dv = sum_g pv[g] (fixed order) -> bf16 into the
+// dk / dv columns of the dqkv buffer. One thread per 8 elements.
+__global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict__ pk,
+                                                         const float* __restrict__ pv, int grp,
+                                                         long T, int hkv, float scale,
+                                                         bf16_t* __restrict__ dk,
+                                                         bf16_t* __restrict__ dv, long ld_d) {
+  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = hkv / 8;
+  if (id >= T * cpr) return;
+  const long t = id / cpr;
+  const int c = (int)(id % cpr);
+  float k8[8] = {}, v8[8] = {};
+  for (int g = 0; g < grp; ++g) {
+    const long off = ((long)g * T + t) * hkv + c * 8;
+    const float4 k0 = *reinterpret_cast<const float4*>(pk + off);
+    const float4 k1 = *reinterpret_cast<const float4*>(pk + off + 4);
+    const float4 v0 = *reinterpret_cast<const float4*>(pv + off);
+    const float4 v1 = *reinterpret_cast<const float4*>(pv + off + 4);
+    k8[0] += k0.x; k8[1] += k0.y; k8[2] += k0.z; k8[3] += k0.w;
+    k8[4] += k1.x; k8[5] += k1.y; k8[6] += k1.z; k8[7] += k1.w;
+    v8[0] += v0.x; v8[1] += v0.y; v8[2] += v0.z; v8[3] += v0.w;
+    v8[4] += v1.x; v8[5] += v1.y; v8[6] += v1.z; v8[7] += v1.w;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) k8[e] *= scale;
+  *reinterpret_cast<uint4*>(dk + t * ld_d + c * 8) = pack8(k8);
+  *reinterpret_cast<uint4*>(dv + t * ld_d + c * 8) = pack8(v8);
 }
 
 // ---------------------------------------------------------- backward dQ ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
                                                         const float* __restrict__ lse,
                                                         const float* __restrict__ delta,
                                                         bf16_t* __restrict__ dq, long ld_d) {
-  constexpr int BQ = 128, BKV = 64, CPR = D / 8;
-  constexpr int NAT = BKV * CPR, TRN = D * 8, NBLK = 8 * CPR;
-  __shared__ uint4 smem[2][2 * NAT + TRN];  // K nat, V nat, K^T
+  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8;
+  __shared__ uint4 smem[2][2 * NAT];  // K tile, V tile
 
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
@@ -439,7 +453,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   const bf16_t* Kg = a.k + rb * a.ld_qkv + (long)m * D;
   const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
   const bf16_t* dOg = dout + rb * ldo + (long)n * D;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
   const int q0w = qt * BQ + wave * 32;
   const int q = q0w + l32;
@@ -460,37 +475,21 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
 
-  const int tb = threadIdx.x;
-  const bool has_blk = tb < 2 * NBLK;
-  const bool is_v = tb >= NBLK;
-  const int blk = tb % NBLK, rg = blk / CPR, cg = blk % CPR;
-  uint4 st[8];
-  auto load_tile = [&](int kt) {
-    if (has_blk) load_blk(is_v ? Vg : Kg, a.ld_qkv, kt * BKV + rg * 8, S, cg, st);
-  };
-  auto store_tile = [&](int buf) {
-    if (has_blk) {
-      if (is_v) {
-        store_nat<D>(smem[buf] + NAT, rg, cg, st);
-      } else {
-        store_nat<D>(smem[buf], rg, cg, st);
-        store_tr(smem[buf] + 2 * NAT, rg, cg, st);
-      }
-    }
-  };
-
-  load_tile(0);
-  store_tile(0);
+  dma_tile<D, 4>(Kg, a.ld_qkv, 0, S, smem[0], wave, lane);
+  dma_tile<D, 4>(Vg, a.ld_qkv, 0, S, smem[0] + NAT, wave, lane);
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < nkt;
-    if (more) load_tile(kt + 1);
+    if (kt + 1 < nkt) {
+      dma_tile<D, 4>(Kg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1], wave, lane);
+      dma_tile<D, 4>(Vg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1] + NAT, wave, lane);
+    }
     const int k0 = kt * BKV;
     if (k0 <= q0w + 31) {
+      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
+      asm volatile("" : "+v"(ln));
       const uint4* Ks = smem[cur];
       const uint4* Vs = smem[cur] + NAT;
-      const uint4* Kt = smem[cur] + 2 * NAT;
       f32x16_t s[2], dp[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -501,10 +500,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
       for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              ld_frag(Ks + nat_idx<D>(kb * 32 + l32, kk * 2 + hh)), qf[kk], s[kb], 0, 0, 0);
-          dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              ld_frag(Vs + nat_idx<D>(kb * 32 + l32, kk * 2 + hh)), of[kk], dp[kb], 0, 0, 0);
+          s[kb] = MFMA(row_frag<D>(Ks, kb * 32, kk, ln), qf[kk], s[kb]);
+          dp[kb] = MFMA(row_frag<D>(Vs, kb * 32, kk, ln), of[kk], dp[kb]);
         }
       const bool diag = (k0 + BKV - 1 > q0w);
 #pragma unroll
@@ -525,11 +522,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
           const bf16x8_t df = pack_frag(dp[kb], ss);
 #pragma unroll
           for (int db = 0; db < D / 32; ++db)
-            dqa[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                ld_frag(Kt + tr_idx(db * 32 + l32, kb * 4 + ss * 2 + hh)), df, dqa[db], 0, 0, 0);
+            dqa[db] = MFMA(tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln), df, dqa[db]);
         }
     }
-    if (more) store_tile(cur ^ 1);
     __syncthreads();
   }
 
@@ -559,7 +554,7 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
 
 hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout, float* delta,
                         hipStream_t s) {
-  const long n = (long)a.batch * a.seq * a.n_heads;
+  const long n = (long)a.batch * a.seq * a.n_heads * 8;
   const dim3 grid((unsigned)((n + 255) / 256)), block(256);
   if (a.d == 128) hipLaunchKernelGGL(attn_bwd_pre_k<128>, grid, block, 0, s, a, o, dout, delta);
   else if (a.d == 64) hipLaunchKernelGGL(attn_bwd_pre_k<64>, grid, block, 0, s, a, o, dout, delta);
@@ -567,15 +562,30 @@ hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* do
   return hipGetLastError();
 }
 
+size_t attn_bwd_partial_floats(const AttnArgs& a) {
+  return (size_t)(a.n_heads / a.n_kv_heads) * a.batch * a.seq * a.n_kv_heads * a.d;
+}
+
 hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* lse,
-                         const float* delta, uint16_t* dk, uint16_t* dv, long ld_d,
-                         hipStream_t s) {
-  const dim3 grid((a.seq + 127) / 128, a.n_kv_heads, a.batch), block(256);
-  if (a.d == 128)
-    hipLaunchKernelGGL(attn_bwd_dkdv_k<128>, grid, block, 0, s, a, dout, lse, delta, dk, dv, ld_d);
-  else if (a.d == 64)
-    hipLaunchKernelGGL(attn_bwd_dkdv_k<64>, grid, block, 0, s, a, dout, lse, delta, dk, dv, ld_d);
-  else return hipErrorInvalidValue;
+                         const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
+                         long ld_d, hipStream_t s) {
+  const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
+  if (a.d == 128) {
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 0>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 1>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+  } else if (a.d == 64) {
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 0>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 1>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long T = (long)a.batch * a.seq;
+  const int hkv = a.n_kv_heads * a.d;
+  const long work = T * (hkv / 8);
+  hipLaunchKernelGGL(attn_bwd_reduce_k, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s,
+                     pk, pv, a.n_heads / a.n_kv_heads, T, hkv, a.scale, dk, dv, ld_d);
   return hipGetLastError();
 }
 

@@ -13,7 +13,9 @@
 namespace forge {
 namespace {
 
-constexpr int kRowsPerBlock = 4;  // one wave per row, 4 waves per block
+constexpr int kRowsPerBlock = 4;  // forward: one wave per row, 4 waves per block
+constexpr int kBwdWaves = 8;      // backward: 8 waves per block, rows strided over the grid
+constexpr int kBwdMaxBlocks = 512;
 
 // ------------------------------------------------------------- RMSNorm ----
 // y = x * rstd * g with rstd = (mean(x^2) + eps)^(-1/2), fp32 math, one
@@ -64,12 +66,12 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_k(const bf16_t* __restrict__ 
 // dx = r (g dy) - r^3 x sum(g dy x) / h  (+ resid);  per-block partial of
 // dg = sum_rows dy x r, reduced across the block's waves through LDS.
 template <int MAXCH>
-__global__ __launch_bounds__(256) void rmsnorm_bwd_k(
+__global__ __launch_bounds__(512) void rmsnorm_bwd_k(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ g,
     const float* __restrict__ rstd, const bf16_t* __restrict__ dy,
     const bf16_t* __restrict__ resid, bf16_t* __restrict__ dx,
     float* __restrict__ dg_partial, int T, int h) {
-  __shared__ float red[kRowsPerBlock][512];
+  __shared__ float red[kBwdWaves][512];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = h / 8;
   const uint4* gr = reinterpret_cast<const uint4*>(g);
@@ -79,8 +81,8 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_k(
 #pragma unroll
     for (int e = 0; e < 8; ++e) dga[i][e] = 0.0f;
 
-  for (long row = (long)blockIdx.x * kRowsPerBlock + wave; row < T;
-       row += (long)gridDim.x * kRowsPerBlock) {
+  for (long row = (long)blockIdx.x * kBwdWaves + wave; row < T;
+       row += (long)gridDim.x * kBwdWaves) {
     const uint4* xr = reinterpret_cast<const uint4*>(x + row * h);
     const uint4* dyr = reinterpret_cast<const uint4*>(dy + row * h);
     const float r = rstd[row];
@@ -138,7 +140,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_k(
       if (col < h) {
         float s = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kRowsPerBlock; ++w) s += red[w][j];
+        for (int w = 0; w < kBwdWaves; ++w) s += red[w][j];
         dg_partial[(long)blockIdx.x * h + col] = s;
       }
     }
@@ -146,13 +148,25 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_k(
   }
 }
 
-__global__ void dg_reduce_k(const float* __restrict__ part, int nblk, float* __restrict__ dg,
-                            int h) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= h) return;
+// dg[c] += sum_b part[b][c]: a block covers 32 columns; 8 groups of 32
+// threads each sum a fixed stripe of partial rows, then the 8 stripe sums
+// are added in a fixed order (deterministic).
+__global__ __launch_bounds__(256) void dg_reduce_k(const float* __restrict__ part, int nblk,
+                                                   float* __restrict__ dg, int h) {
+  __shared__ float red[8][32];
+  const int col = blockIdx.x * 32 + (threadIdx.x & 31);
+  const int stripe = threadIdx.x >> 5;
   float s = 0.0f;
-  for (int b = 0; b < nblk; ++b) s += part[(long)b * h + c];
-  dg[c] += s;
+  if (col < h)
+    for (int b = stripe; b < nblk; b += 8) s += part[(long)b * h + col];
+  red[stripe][threadIdx.x & 31] = s;
+  __syncthreads();
+  if (threadIdx.x < 32 && col < h) {
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) t += red[w][threadIdx.x];
+    dg[col] += t;
+  }
 }
 
 // ---------------------------------------------------------------- RoPE ----
@@ -371,6 +385,9 @@ __device__ __forceinline__ void adam1(float& p, float& m, float& v, float g, flo
   p = p - lr * upd;
 }
 
+// One float4 of parameters per thread and no grid-stride loop: with seven
+// streams (read g, p, m, v; write p, m, v and bf16 p) this keeps the most
+// independent 16-byte requests in flight and runs at plain-copy bandwidth.
 __global__ __launch_bounds__(256) void adamw_k(float* __restrict__ master,
                                                bf16_t* __restrict__ param,
                                                const float* __restrict__ grad,
@@ -380,8 +397,8 @@ __global__ __launch_bounds__(256) void adamw_k(float* __restrict__ master,
                                                const float* __restrict__ sc) {
   const float lr = sc[0], ibc1 = 1.0f / sc[1], ibc2 = 1.0f / sc[2], clip = sc[3];
   const int64_t n4 = n / 4;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n4) {
     float4 p = reinterpret_cast<float4*>(master)[i];
     float4 m = reinterpret_cast<float4*>(mom1)[i];
     float4 v = reinterpret_cast<float4*>(mom2)[i];
@@ -394,16 +411,15 @@ __global__ __launch_bounds__(256) void adamw_k(float* __restrict__ master,
     reinterpret_cast<float4*>(mom1)[i] = m;
     reinterpret_cast<float4*>(mom2)[i] = v;
     reinterpret_cast<uint2*>(param)[i] = make_uint2(pack2(p.x, p.y), pack2(p.z, p.w));
-  }
-  // tail (n % 4 elements) by the first threads of block 0
-  if (blockIdx.x == 0 && threadIdx.x < (n - n4 * 4)) {
-    const int64_t i = n4 * 4 + threadIdx.x;
-    float p = master[i], m = mom1[i], v = mom2[i];
-    adam1(p, m, v, grad[i], b1, b2, eps, wd, lr, ibc1, ibc2, clip);
-    master[i] = p;
-    mom1[i] = m;
-    mom2[i] = v;
-    param[i] = f2bf(p);
+  } else if (i < n4 + (n - n4 * 4)) {
+    // tail: the last n % 4 elements, one per thread
+    const int64_t e = n4 * 4 + (i - n4);
+    float p = master[e], m = mom1[e], v = mom2[e];
+    adam1(p, m, v, grad[e], b1, b2, eps, wd, lr, ibc1, ibc2, clip);
+    master[e] = p;
+    mom1[e] = m;
+    mom2[e] = v;
+    param[e] = f2bf(p);
   }
 }
 
@@ -474,14 +490,14 @@ hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* g, uint16_t* y, float*
 }
 
 int rmsnorm_bwd_blocks(int T) {
-  const int need = (T + kRowsPerBlock - 1) / kRowsPerBlock;
-  return need < 256 ? (need > 0 ? need : 1) : 256;
+  const int need = (T + kBwdWaves - 1) / kBwdWaves;
+  return need < kBwdMaxBlocks ? (need > 0 ? need : 1) : kBwdMaxBlocks;
 }
 
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
                        const uint16_t* dy, const uint16_t* resid, uint16_t* dx, float* dg_partial,
                        int T, int h, hipStream_t s) {
-  const dim3 grid(rmsnorm_bwd_blocks(T)), block(256);
+  const dim3 grid(rmsnorm_bwd_blocks(T)), block(64 * kBwdWaves);
   const int ch = (h / 8 + 63) / 64;
 #define FORGE_RMSB(N) hipLaunchKernelGGL(rmsnorm_bwd_k<N>, grid, block, 0, s, x, g, rstd, dy, resid, dx, dg_partial, T, h)
   if (ch <= 1) FORGE_RMSB(1);
@@ -495,7 +511,7 @@ hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
 }
 
 hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h, hipStream_t s) {
-  hipLaunchKernelGGL(dg_reduce_k, dim3(blocks_for(h, 256)), dim3(256), 0, s, dg_partial, nblk, dg, h);
+  hipLaunchKernelGGL(dg_reduce_k, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
   return hipGetLastError();
 }
 
@@ -563,9 +579,8 @@ hipError_t adamw(float* master, uint16_t* param, const float* grad, float* m, fl
                  int64_t n, float b1, float b2, float eps, float wd, const float* sc,
                  hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  long blocks = (n / 4 + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 8192) blocks = 8192;
+  const int64_t work = n / 4 + (n % 4);
+  const int64_t blocks = (work + 255) / 256;
   hipLaunchKernelGGL(adamw_k, dim3((unsigned)blocks), dim3(256), 0, s, master, param, grad, m, v,
                      n, b1, b2, eps, wd, sc);
   return hipGetLastError();

@@ -132,7 +132,7 @@ Saved saved_layout(const forge_layer_cfg& c) {
 
 // ---- backward workspace ---------------------------------------------------
 struct Work {
-  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, total;
+  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv, total;
 };
 
 Work work_layout(const forge_layer_cfg& c) {
@@ -152,6 +152,9 @@ Work work_layout(const forge_layer_cfg& c) {
   const bool rec = c.recompute_attn != 0;
   w.o = rec ? take(d.T * d.hq * 2) : 0;
   w.lse = rec ? take(d.B * d.nh * d.S * 4) : 0;
+  const size_t part = (size_t)(d.nh / d.nkv) * d.T * d.hkv * 4;
+  w.pk = take(part);
+  w.pv = take(part);
   w.total = off;
   return w;
 }
@@ -376,7 +379,9 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
                         gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
   FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, dqkv + d.hq, dqkv + d.hq + d.hkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, at<float>(workspace, wk.pk),
+                                 at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
+                                 d.qkv, s));
   FORGE_HIP(forge::attn_bwd_dq(aa, dO, lse, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
                               (int)(d.nh + d.nkv), (int)d.d, true, s));
@@ -620,7 +625,9 @@ forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qk
 forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes) {
   if (forge_status s = check_attn(cfg)) return s;
   FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
-  *bytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
+  const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
+                      cfg->n_kv_heads * cfg->head_dim * 4;
+  *bytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4) + 2 * up(part);
   return ok();
 }
 
@@ -638,8 +645,14 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
   const forge::AttnArgs aa = attn_args(d, qkv);
   hipStream_t s = (hipStream_t)stream;
   float* delta = static_cast<float*>(workspace);
+  const size_t dbytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
+  const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
+                      cfg->n_kv_heads * cfg->head_dim * 4;
+  float* pk = at<float>(workspace, dbytes);
+  float* pv = at<float>(workspace, dbytes + up(part));
   FORGE_HIP(forge::attn_bwd_pre(aa, o, d_o, delta, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, lse, delta, d_qkv + d.hq, d_qkv + d.hq + d.hkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, lse, delta, pk, pv, d_qkv + d.hq,
+                                 d_qkv + d.hq + d.hkv, d.qkv, s));
   FORGE_HIP(forge::attn_bwd_dq(aa, d_o, lse, delta, d_qkv, d.qkv, s));
   return ok();
 }

@@ -7,13 +7,14 @@
 // over tokens). One kernel template covers all three:
 //
 //  * A block tile BM x BN x 64 is staged through LDS, double-buffered, with
-//    one barrier per k-step. Both LDS tiles are kept K-contiguous, so every
-//    MFMA operand is one 16-byte LDS read per lane. Operands that are not
-//    K-contiguous in HBM are loaded as coalesced 16-byte rows and transposed
-//    8x8 in registers before the LDS store.
-//  * LDS rows are 128 bytes (eight 16-byte chunks); chunk c of row r lives at
-//    c ^ ((r ^ (r >> 3)) & 7), which keeps both the MFMA reads (32 rows, one
-//    chunk) and the transposed stores (rows 8 apart) spread over the banks.
+//    one barrier per k-step. Tiles are filled by buffer_load ... lds (global
+//    to LDS without registers); out-of-range chunks read as zeros through the
+//    buffer descriptor's range check, so ragged edges need no branches.
+//  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
+//    chunk c of row r at c ^ ((r ^ (r >> 3)) & 7)); each MFMA operand is one
+//    16-byte LDS read. An operand contiguous along M / N is stored as it lies
+//    in HBM and read with gfx950's ds_read_b64_tr_b16 transpose reads, so
+//    dgrad and wgrad need no transpose pass.
 //  * The MFMA computes D = Btile * Atile^T, i.e. C transposed, so each lane's
 //    four consecutive accumulator rows are four consecutive n of one row m of
 //    C: the epilogue writes 8-byte (bf16) or 16-byte (fp32) vectors.
@@ -71,52 +72,63 @@ struct KcLoader {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + blk * 64), 16, off, 0, 0, 0);
     }
   }
-  __device__ __forceinline__ void store(uint4*) const {}
 };
 
-// ---- source contiguous along the row dim: registers, 8x8 transpose -------
-// The tile is 64 k-rows of ROWS contiguous elements in HBM. Each thread owns
-// 8x8 blocks (8 k by 8 rows), loads them as eight 16-byte rows and
-// transposes them in registers before the LDS store.
+// ---- source contiguous along the row dim (M or N): LDS-DMA, read transposed --
+// The tile is stored as it lies in HBM: 64 k-rows of ROWS contiguous
+// elements, 16-byte chunk c of row k at slot c ^ (4 (k & 3)). MFMA fragments
+// are read with ds_read_b64_tr_b16: within each 16-lane group, lane 4r + j
+// points at row r, columns 4j..4j+3 of a 4 x 16 block and receives column
+// (lane % 16) of rows 0..3, i.e. four consecutive k of one m. Two such reads
+// give a lane its eight k values. The XOR keeps the 32 lanes of a half-wave
+// (4 rows x 4 chunks) on distinct banks.
 template <int ROWS, int NW>
 struct McLoader {
-  static constexpr int NT = NW * 64;
-  static constexpr int NBLK = ROWS;  // (ROWS/8 row chunks) x (8 k groups)
-  static constexpr int PER = (NBLK + NT - 1) / NT;
-  uint4 r[PER][8];
+  static constexpr int LPR = ROWS / 8;          // lanes (16-byte chunks) per tile row
+  static constexpr int RPI = 64 / LPR;          // tile rows per wave instruction
+  static constexpr int PER = 64 / RPI / NW;     // instructions per wave per tile
+  static_assert(PER * RPI * NW == 64, "tile k-rows must split over waves");
   __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
-                                       int rows_lim, int k0, int K, uint4*, int, int) {
-    const __amdgpu_buffer_rsrc_t rs = rsrc(src + (long)k0 * ld + row0);
-    const int t = threadIdx.x;
+                                       int rows_lim, int k0, int K, uint4* lds, int wave,
+                                       int lane) const {
+    const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)k0 * ld + row0);
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int b = j * NT + t;
-      const int mc = b % (ROWS / 8), kg = b / (ROWS / 8);
-      const bool okr = (b < NBLK) && (row0 + mc * 8 < rows_lim);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int k = kg * 8 + i;
-        const bool ok = okr && (k0 + k < K);
-        const uint32_t off = ok ? (uint32_t)(((long)k * ld + mc * 8) * 2) : kOOB;
-        r[j][i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-      }
-    }
-  }
-  __device__ __forceinline__ void store(uint4* lds) const {
-    const int t = threadIdx.x;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int b = j * NT + t;
-      if (b < NBLK) {
-        const int mc = b % (ROWS / 8), kg = b / (ROWS / 8);
-        uint4 tr[8];
-        transpose8x8(r[j], tr);
-#pragma unroll
-        for (int rr = 0; rr < 8; ++rr) lds[swz(mc * 8 + rr, kg)] = tr[rr];
-      }
+    for (int i = 0; i < PER; ++i) {
+      const int q = i * NW + wave;
+      const int k = q * RPI + lane / LPR;
+      const int c = (lane % LPR) ^ ((k & 3) << 2);
+      const bool ok = (k0 + k < K) && (row0 + c * 8 < rows_lim);
+      const uint32_t off = ok ? (uint32_t)(((long)k * ld + c * 8) * 2) : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + q * 64), 16, off, 0, 0, 0);
     }
   }
 };
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
+
+template <int ROWS>
+__device__ __forceinline__ int mc_elem(int k, int m) {
+  return k * ROWS + ((((m >> 3) ^ ((k & 3) << 2))) << 3) + (m & 7);
+}
+
+// Fragment of rows base..base+31 (the lane's row is base + lane % 32) over
+// k-slice kk: eight consecutive k starting at kk*16 + 8*(lane / 32).
+template <int LAYOUT, int ROWS>
+__device__ __forceinline__ bf16x8_t frag(const uint4* tile, int base, int kk, int lane) {
+  if (LAYOUT == kKC) {
+    return __builtin_bit_cast(bf16x8_t, tile[swz(base + (lane & 31), kk * 2 + (lane >> 5))]);
+  } else {
+    const uint16_t* t = reinterpret_cast<const uint16_t*>(tile);
+    const int g = lane >> 4, i = lane & 15;
+    const int m = base + (g & 1) * 16 + 4 * (i & 3);
+    const int k = kk * 16 + (g >> 1) * 8 + (i >> 2);
+    const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(t + mc_elem<ROWS>(k, m)));
+    const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(t + mc_elem<ROWS>(k + 4, m)));
+    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
+  }
+}
 
 template <int ROWS, int NW, int LAYOUT>
 using Loader = typename std::conditional<LAYOUT == kKC, KcLoader<ROWS, NW>,
@@ -164,7 +176,6 @@ __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const fl
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
-  constexpr int NT = WAVES_M * WAVES_N * 64;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 32, FN = WN / 32;
   static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
@@ -204,12 +215,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   const int nk = (p.K + BK - 1) / BK;
   la.load(p.A, p.lda, m0, p.M, 0, p.K, lds[0], wave, lane);
   lb.load(p.B, p.ldb, n0, p.N, 0, p.K, lds[0] + A_ELEMS, wave, lane);
-  la.store(lds[0]);
-  lb.store(lds[0] + A_ELEMS);
   __syncthreads();
 
-  const int ra = wn * WN + (lane & 31);  // first B-tile row of this lane
-  const int rb = wm * WM + (lane & 31);  // first A-tile row of this lane
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
@@ -222,32 +229,23 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     // fragments double-buffered across the four 16-deep k-slices
     bf16x8_t fa[2][FN], fb[2][FM];
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
-      fa[0][i] = __builtin_bit_cast(bf16x8_t, Bt[swz(ra + i * 32, lane >> 5)]);
+    for (int i = 0; i < FN; ++i) fa[0][i] = frag<LB, BN>(Bt, wn * WN + i * 32, 0, lane);
 #pragma unroll
-    for (int j = 0; j < FM; ++j)
-      fb[0][j] = __builtin_bit_cast(bf16x8_t, At[swz(rb + j * 32, lane >> 5)]);
+    for (int j = 0; j < FM; ++j) fb[0][j] = frag<LA, BM>(At, wm * WM + j * 32, 0, lane);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       const int cb = kk & 1, nb = cb ^ 1;
       if (kk + 1 < BK / 16) {
-        const int c = (kk + 1) * 2 + (lane >> 5);
 #pragma unroll
-        for (int i = 0; i < FN; ++i)
-          fa[nb][i] = __builtin_bit_cast(bf16x8_t, Bt[swz(ra + i * 32, c)]);
+        for (int i = 0; i < FN; ++i) fa[nb][i] = frag<LB, BN>(Bt, wn * WN + i * 32, kk + 1, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j)
-          fb[nb][j] = __builtin_bit_cast(bf16x8_t, At[swz(rb + j * 32, c)]);
+        for (int j = 0; j < FM; ++j) fb[nb][j] = frag<LA, BM>(At, wm * WM + j * 32, kk + 1, lane);
       }
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
         for (int j = 0; j < FM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fb[cb][j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      la.store(lds[cur ^ 1]);
-      lb.store(lds[cur ^ 1] + A_ELEMS);
     }
     __syncthreads();
   }
@@ -279,14 +277,11 @@ hipError_t launch(const GemmArgs& a, hipStream_t s) {
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
-  // With both operands K-contiguous (LDS filled by DMA) 8 waves of 64x128
-  // hide LDS latency better; the transposing loaders keep 4 waves.
+  // 8 waves of 64x128 (two per SIMD) hide LDS latency better than 4 waves
+  // of 128x128 for every layout.
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
-  if (big >= 256) {
-    if (LA == kKC && LB == kKC) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
-    return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
-  }
+  if (big >= 256) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
 }
