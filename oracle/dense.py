@@ -260,3 +260,38 @@ def layer_bwd(cache, W, cfg, dout):
     dx, ga = attention_block_bwd(cache["attn"], W, cfg, dh1)
     ga.update(gf)
     return dx, ga
+
+
+def layer_fwd_rows(x, W, cfg, rows):
+    """The layer output at selected token rows only (the same definition).
+
+    Keys and values need every token, so RMSNorm and the k/v projections run
+    over all rows; the query projection, attention, output projection and FFN
+    run only for `rows`. Used to check very long sequences one row at a time.
+    """
+    h, nh, nkv, d, hq, hkv = _dims(cfg)
+    B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    rows = np.asarray(rows)
+    T = x.shape[0]
+    a, _ = rmsnorm_fwd(x, W["attn_norm"], cfg["rms_eps"])
+    wq, wk, wv = W["w_qkv"][:hq], W["w_qkv"][hq:hq + hkv], W["w_qkv"][hq + hkv:]
+    k = rope_fwd((a @ wk.T).reshape(T, nkv, d), B, S, base)
+    v = (a @ wv.T).reshape(T, nkv, d)
+    pos = rows % S
+    phi = rope_angles(S, d, base)[pos]
+    cs, sn = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
+    q = (a[rows] @ wq.T).reshape(len(rows), nh, d)
+    q1, q2 = q[..., : d // 2], q[..., d // 2:]
+    q = np.concatenate([q1 * cs - q2 * sn, q2 * cs + q1 * sn], axis=-1)
+    grp = nh // nkv
+    o = np.zeros((len(rows), nh, d))
+    for r, t in enumerate(rows):
+        b0 = (t // S) * S
+        keys = slice(b0, t + 1)
+        for n in range(nh):
+            s = (k[keys, n // grp] @ q[r, n]) / np.sqrt(d)
+            p = np.exp(s - s.max())
+            o[r, n] = (p / p.sum()) @ v[keys, n // grp]
+    h1 = x[rows] + o.reshape(len(rows), hq) @ W["w_o"].T
+    out, _ = ffn_fwd(h1, W, cfg)
+    return out

@@ -131,3 +131,110 @@ class Layer:
         _lib.forge_layer_bwd(self.c, self.weights, self.saved if saved is None else saved,
                              x_in, d_out, d_in, self.grads,
                              self.workspace if workspace is None else workspace, self.stream)
+
+
+class Model:
+    """A whole decoder stack's training step through the C ABI.
+
+    Embedding -> n_layers decoder layers -> final RMSNorm + LM head + CE
+    (tied to the embedding when w_lm is None) -> backward -> embedding
+    backward -> one fused AdamW over every parameter (flat buffers).
+    Every step of the computation runs in libforge's kernels; this class only
+    owns the buffers and issues the calls in order on one stream.
+    """
+
+    def __init__(self, cfg: dict, inputs: dict, device="cuda", stream=None):
+        torch = _torch()
+        self.cfg = dict(cfg)
+        self.stream = stream
+        L, V, h = cfg["n_layers"], cfg["vocab"], cfg["hidden"]
+        self.T = cfg["batch"] * cfg["seq"]
+        self.tied = inputs["w_lm"] is None
+        shapes = {"embedding": (V, h), "final_norm": (h,)}
+        if not self.tied:
+            shapes["w_lm"] = (V, h)
+        for i in range(L):
+            for n, s in layer_shapes(cfg).items():
+                shapes[f"{i}.{n}"] = s
+        self.flat = FlatParams(shapes, device)
+        self.flat.load_bits("embedding", inputs["embedding"])
+        self.flat.load_bits("final_norm", inputs["final_norm"])
+        if not self.tied:
+            self.flat.load_bits("w_lm", inputs["w_lm"])
+        self.layers = []
+        for i in range(L):
+            view = _PrefixedFlat(self.flat, f"{i}.")
+            self.layers.append(Layer(cfg, inputs["layers"][i], device, stream, flat=view))
+        ws = max(_lib.forge_layer_workspace_bytes(self.layers[0].c), 1)
+        self.workspace = empty_bytes(ws, device)
+        for ly in self.layers:               # one shared scratch buffer
+            ly.workspace = self.workspace
+        self.head = _lib.HeadCfg(self.T, h, V, cfg["rms_eps"])
+        self.head_ws = empty_bytes(_lib.forge_loss_workspace_bytes(self.head), device)
+        self.ids = torch.from_numpy(inputs["ids"].astype(np.int32)).to(device)
+        self.targets = torch.from_numpy(inputs["targets"].astype(np.int32)).to(device)
+        self.acts = [torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
+                     for _ in range(L + 1)]
+        self.grad_a = torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
+        self.grad_b = torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=device)
+        self.scalars = torch.zeros(4, dtype=torch.float32, device=device)
+        self.hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"],
+                                    cfg["weight_decay"])
+        self.step_count = 0
+
+    def w_lm(self, buf):
+        return self.flat.view(buf, "embedding" if self.tied else "w_lm")
+
+    def forward_backward(self):
+        """Loss (device scalar) and every gradient accumulated into flat.grad."""
+        c, s = self.cfg, self.stream
+        T, h, V = self.T, c["hidden"], c["vocab"]
+        emb = self.flat.view(self.flat.param, "embedding")
+        _lib.forge_embed_fwd(self.ids, emb, self.acts[0], T, h, V, s)
+        for i, ly in enumerate(self.layers):
+            ly.fwd(self.acts[i], self.acts[i + 1])
+        _lib.forge_loss_fwd_bwd(self.head, self.acts[-1],
+                                self.flat.view(self.flat.param, "final_norm"),
+                                self.w_lm(self.flat.param), self.targets, self.loss,
+                                self.grad_a, self.flat.view(self.flat.grad, "final_norm"),
+                                self.w_lm(self.flat.grad), self.head_ws, s)
+        g_in, g_out = self.grad_a, self.grad_b
+        for i in reversed(range(len(self.layers))):
+            self.layers[i].bwd(self.acts[i], g_in, g_out)
+            g_in, g_out = g_out, g_in
+        _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
+                             T, h, V, s)
+        return self.loss
+
+    def optimizer_step(self, lr=None, clip=1.0):
+        """One fused AdamW over all parameters; bias corrections for the next step."""
+        torch = _torch()
+        self.step_count += 1
+        c, t = self.cfg, self.step_count
+        lr = c["lr"] if lr is None else lr
+        self.scalars.copy_(torch.tensor([lr, 1 - c["beta1"] ** t, 1 - c["beta2"] ** t, clip],
+                                        dtype=torch.float32))
+        f = self.flat
+        _lib.forge_adamw_step(f.master, f.param, f.grad, f.m, f.v, f.n, self.hp,
+                              self.scalars, self.stream)
+
+    def train_step(self):
+        self.flat.grad.zero_()
+        loss = self.forward_backward()
+        self.optimizer_step()
+        return loss
+
+
+class _PrefixedFlat:
+    """View of a FlatParams under a name prefix (one layer's tensors)."""
+
+    def __init__(self, flat: FlatParams, prefix: str):
+        self._f, self._p = flat, prefix
+        self.param, self.grad = flat.param, flat.grad
+
+    def view(self, buf, name):
+        return self._f.view(buf, self._p + name)
+
+    def load_bits(self, name, bits):
+        self._f.load_bits(self._p + name, bits)

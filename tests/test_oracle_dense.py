@@ -219,3 +219,13 @@ def test_swiglu_backward_finite_differences():
     idx = np.arange(20)
     assert rel_err(dG, central_diff(f, G, idx)) <= 1e-8
     assert rel_err(dU, central_diff(f, U, idx)) <= 1e-8
+
+
+def test_layer_rows_equals_full_layer():
+    rng = np.random.default_rng(14)
+    cfg = dict(MICRO, batch=2, seq=5)
+    W = micro_weights(cfg, rng)
+    x = rng.standard_normal((10, cfg["hidden"]))
+    out, _ = dense.layer_fwd(x, W, cfg)
+    rows = [0, 3, 4, 5, 9]
+    assert np.allclose(dense.layer_fwd_rows(x, W, cfg, rows), out[rows], rtol=1e-12, atol=1e-13)
