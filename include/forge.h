@@ -72,9 +72,16 @@ const char* forge_version(void);
  * n / (n_heads / n_kv_heads) (contiguous GQA groups).
  *
  * n_experts == 0 selects the dense SwiGLU FFN of width `ffn`. n_experts > 0
- * selects the routed MoE FFN (top_k experts of width expert_ffn per token,
- * softmax router, load-balance aux loss with coefficient aux_coef); the MoE
- * path is not in this build and returns FORGE_ERR_UNSUPPORTED.
+ * selects the routed MoE FFN of the paper's sparse model (App. B, Table "H100
+ * architecture configurations": routed experts, top-k): every token goes to
+ * its top_k experts (dropless, no capacity), each a SwiGLU FFN of width
+ * expert_ffn; the router is a softmax over all experts of fp32 logits
+ * b w_router^T, a token's experts are its top_k logits (ties to the lower
+ * expert id), each weighted by its softmax probability (no renormalisation);
+ * the load-balance loss aux_coef * E * sum_e f_e P_e (f_e = share of routed
+ * slots, a constant; P_e = mean router probability) is added to aux_loss.
+ * MoE limits: n_experts a multiple of 8 and <= 64, 1 <= top_k <= min(E, 16),
+ * expert_ffn a multiple of 8.
  *
  * recompute_attn != 0: the forward does not keep the attention output and
  * its row statistics; the backward re-runs the attention forward (a
@@ -155,9 +162,13 @@ forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base,
  *   o  = causal GQA attention(q,k,v)  h1  = x + o w_o^T
  *   b  = RMSNorm(h1; ffn_norm)        x_out = h1 + (silu(b Wg^T) * (b Wu^T)) w_down^T
  * x_in, x_out: [T, h] bf16; x_out must not overlap x_in.
+ * For a MoE layer the FFN branch is h1 + sum_j gate_j FFN_{e_j}(b) instead.
  * saved: forge_layer_saved_bytes bytes, written here, read by the backward.
- * workspace: forge_layer_workspace_bytes bytes of scratch.
- * aux_loss: MoE only (device fp32 scalar, +=); may be NULL for dense layers.
+ * workspace: forge_layer_workspace_bytes bytes of scratch (may be NULL for a
+ * dense layer without recompute_attn).
+ * aux_loss: device fp32 scalar, MoE only: += the layer's load-balance loss;
+ * may be NULL (the loss is then not reported; the backward still includes
+ * its gradient).
  */
 forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
                              const forge_bf16* x_in, forge_bf16* x_out,
@@ -169,7 +180,11 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
  * writes d_in [T, h] (bf16, may alias d_out) and accumulates every weight
  * gradient into `grads` (fp32 +=). x_in and saved must be those of the
  * matching forward. Weight gradients are the data-gradient / weight-gradient
- * product pair of every projection (App. C).
+ * product pair of every projection (App. C). For a MoE layer the objective
+ * is <x_out, d_out> + aux: the router gradient includes the load-balance
+ * term, and expert weights that received no tokens get no contribution.
+ * MoE results are deterministic; d_w_router goes through a bf16 rounding of
+ * the router logit gradient.
  */
 forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
                              const void* saved, const forge_bf16* x_in,
@@ -325,6 +340,25 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
                                  const forge_bf16* o, const float* lse,
                                  const forge_bf16* d_o, forge_bf16* d_qkv,
                                  void* workspace, forge_stream stream);
+
+/* Scratch bytes of forge_moe_route. Host only. */
+forge_status forge_moe_route_workspace_bytes(int32_t tokens, int32_t n_experts, int32_t top_k,
+                                             size_t* bytes);
+
+/*
+ * Token routing of the MoE layer on given fp32 logits [tokens, n_experts]
+ * (n_experts <= 64): probs [tokens, E] = softmax over all experts; idx
+ * [tokens, top_k] = the top_k experts by descending logit, ties to the lower
+ * expert id; gates [tokens, top_k] = their probabilities; counts [E] slots
+ * per expert; offsets [E + 1] = exclusive scan of counts; perm [tokens *
+ * top_k] = the flat (token * top_k + slot) entries in expert-major order,
+ * tokens ascending within an expert, then slots ascending. Integer outputs
+ * are bit-exact and deterministic. All pointers device, 4-byte aligned.
+ */
+forge_status forge_moe_route(const float* logits, int32_t tokens, int32_t n_experts,
+                             int32_t top_k, int32_t* idx, float* gates, float* probs,
+                             int32_t* counts, int32_t* offsets, int32_t* perm,
+                             void* workspace, forge_stream stream);
 
 #ifdef __cplusplus
 }

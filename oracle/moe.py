@@ -38,6 +38,18 @@ def topk(l32, k):
     return order[:, :k].astype(np.int32)
 
 
+def topk_margin(l32, k):
+    """Per row, how far the k-th largest logit lies above the (k+1)-th (fp64
+    difference of the fp32 values). A perturbation of the logits smaller than
+    half of it in every entry cannot change the top-k set; when k equals the
+    number of experts the set is fixed and the margin is infinite.
+    """
+    v = -np.sort(-np.asarray(l32, dtype=np.float32).astype(np.float64), axis=1)
+    if k >= v.shape[1]:
+        return np.full(v.shape[0], np.inf)
+    return v[:, k - 1] - v[:, k]
+
+
 def route(l, k):
     """Routing decision for logits l [T, E].
 
@@ -165,3 +177,39 @@ def layer_bwd(cache, W, cfg, dout):
     dx, ga = attention_block_bwd(cache["attn"], W, cfg, dout + dh1n)
     g.update(ga)
     return dx, g
+
+
+def layer_fwd_rows(x, W, cfg, rows, with_logits=False):
+    """MoE layer output at selected token rows only (the same definition).
+
+    Attention needs every key, so it runs through dense.layer_fwd_rows'
+    pieces; the routed FFN of a token depends on that token alone. With
+    with_logits, also returns the router logits of those rows.
+    """
+    from . import dense
+    h, nh, nkv, d, hq, hkv = dense._dims(cfg)
+    rows = np.asarray(rows)
+    # h1 at the selected rows: attention block only (FFN of the dense helper unused)
+    B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    T = x.shape[0]
+    a, _ = dense.rmsnorm_fwd(x, W["attn_norm"], cfg["rms_eps"])
+    wq, wk, wv = W["w_qkv"][:hq], W["w_qkv"][hq:hq + hkv], W["w_qkv"][hq + hkv:]
+    k_ = dense.rope_fwd((a @ wk.T).reshape(T, nkv, d), B, S, base)
+    v_ = (a @ wv.T).reshape(T, nkv, d)
+    phi = dense.rope_angles(S, d, base)[rows % S]
+    cs, sn = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
+    q = (a[rows] @ wq.T).reshape(len(rows), nh, d)
+    q1, q2 = q[..., : d // 2], q[..., d // 2:]
+    q = np.concatenate([q1 * cs - q2 * sn, q2 * cs + q1 * sn], axis=-1)
+    grp = nh // nkv
+    o = np.zeros((len(rows), nh, d))
+    for r, t in enumerate(rows):
+        keys = slice((t // S) * S, t + 1)
+        for n in range(nh):
+            s = (k_[keys, n // grp] @ q[r, n]) / np.sqrt(d)
+            p = np.exp(s - s.max())
+            o[r, n] = (p / p.sum()) @ v_[keys, n // grp]
+    h1 = x[rows] + o.reshape(len(rows), hq) @ W["w_o"].T
+    bn, _ = dense.rmsnorm_fwd(h1, W["ffn_norm"], cfg["rms_eps"])
+    out = h1 + moe_fwd_per_token(bn, W, cfg)
+    return (out, bn @ W["w_router"].T) if with_logits else out

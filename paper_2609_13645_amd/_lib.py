@@ -114,6 +114,8 @@ def load():
                                                 [ctypes.POINTER(AttnCfg), SZ]),
         "forge_attention_bwd": (ctypes.c_int, [ctypes.POINTER(AttnCfg), P, P, P, P, P,
                                                P, P]),
+        "forge_moe_route_workspace_bytes": (ctypes.c_int, [I32, I32, I32, SZ]),
+        "forge_moe_route": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P, P, P, P, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -273,3 +275,16 @@ def forge_attention_bwd(cfg: AttnCfg, qkv, o, lse, d_o, d_qkv, workspace, stream
     _check(load().forge_attention_bwd(ctypes.byref(cfg), _ptr(qkv), _ptr(o), _ptr(lse),
                                       _ptr(d_o), _ptr(d_qkv), _ptr(workspace),
                                       _stream(stream)))
+
+
+def forge_moe_route_workspace_bytes(tokens, n_experts, top_k) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_moe_route_workspace_bytes(tokens, n_experts, top_k, ctypes.byref(n)))
+    return n.value
+
+
+def forge_moe_route(logits, tokens, n_experts, top_k, idx, gates, probs, counts, offsets, perm,
+                    workspace, stream=None):
+    _check(load().forge_moe_route(_ptr(logits), tokens, n_experts, top_k, _ptr(idx), _ptr(gates),
+                                  _ptr(probs), _ptr(counts), _ptr(offsets), _ptr(perm),
+                                  _ptr(workspace), _stream(stream)))

@@ -60,6 +60,7 @@ size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // ---- derived sizes --------------------------------------------------------
 struct Dims {
   long T, h, hq, hkv, qkv, f, nh, nkv, d, B, S;
+  long E, k, fe, R;  // MoE: experts, top-k, expert FFN width, routed rows T*k
 };
 
 Dims dims(const forge_layer_cfg& c) {
@@ -75,8 +76,15 @@ Dims dims(const forge_layer_cfg& c) {
   d.hkv = d.nkv * d.d;
   d.qkv = d.hq + 2 * d.hkv;
   d.f = c.ffn;
+  d.E = c.n_experts;
+  d.k = c.top_k;
+  d.fe = c.expert_ffn;
+  d.R = d.T * d.k;
   return d;
 }
+
+constexpr int kMaxExperts = 64;
+constexpr int kMaxTopK = 16;
 
 forge_status check_cfg(const forge_layer_cfg* c) {
   FORGE_CHECK(c != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");
@@ -90,10 +98,21 @@ forge_status check_cfg(const forge_layer_cfg* c) {
               c->n_heads, c->n_kv_heads);
   FORGE_CHECK(c->head_dim == 64 || c->head_dim == 128, FORGE_ERR_UNSUPPORTED,
               "head_dim must be 64 or 128 (got %d)", c->head_dim);
-  FORGE_CHECK(c->n_experts == 0, FORGE_ERR_UNSUPPORTED,
-              "the routed MoE FFN (n_experts = %d) is not in this build", c->n_experts);
-  FORGE_CHECK(c->ffn >= 8 && c->ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
-              "ffn must be a positive multiple of 8 (got %d)", c->ffn);
+  FORGE_CHECK(c->n_experts >= 0, FORGE_ERR_INVALID_ARG, "n_experts must be >= 0");
+  if (c->n_experts == 0) {
+    FORGE_CHECK(c->ffn >= 8 && c->ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+                "ffn must be a positive multiple of 8 (got %d)", c->ffn);
+  } else {
+    FORGE_CHECK(c->n_experts % 8 == 0 && c->n_experts <= kMaxExperts, FORGE_ERR_UNSUPPORTED,
+                "n_experts must be a multiple of 8 and <= %d (got %d)", kMaxExperts,
+                c->n_experts);
+    FORGE_CHECK(c->top_k >= 1 && c->top_k <= c->n_experts && c->top_k <= kMaxTopK,
+                FORGE_ERR_INVALID_ARG, "top_k must be in [1, min(n_experts, %d)] (got %d)",
+                kMaxTopK, c->top_k);
+    FORGE_CHECK(c->expert_ffn >= 8 && c->expert_ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+                "expert_ffn must be a positive multiple of 8 (got %d)", c->expert_ffn);
+    FORGE_CHECK(std::isfinite(c->aux_coef), FORGE_ERR_INVALID_ARG, "aux_coef must be finite");
+  }
   FORGE_CHECK(c->rms_eps >= 0.0f && std::isfinite(c->rms_eps), FORGE_ERR_INVALID_ARG,
               "rms_eps must be finite and >= 0");
   FORGE_CHECK(c->rope_base > 0.0f && std::isfinite(c->rope_base), FORGE_ERR_INVALID_ARG,
@@ -102,17 +121,24 @@ forge_status check_cfg(const forge_layer_cfg* c) {
   const long widest = std::max(std::max(d.qkv, 2 * d.f), d.h);
   FORGE_CHECK(d.T * widest < (1L << 31), FORGE_ERR_UNSUPPORTED,
               "a [T, width] activation exceeds 2^31 elements");
+  FORGE_CHECK(d.E == 0 || d.R * std::max(2 * d.fe, d.h) < (1L << 31), FORGE_ERR_UNSUPPORTED,
+              "a [T * top_k, width] routed activation exceeds 2^31 elements");
   return FORGE_OK;
 }
 
 // ---- saved buffer ----------------------------------------------------------
+// Everything the backward reads. Dense FFN: b, G|U, A. MoE FFN: b, router
+// probabilities, routing (idx, gates, counts, offsets, perm, pos_of), the
+// routed rows xs, G|U, A and the expert outputs ys.
 struct Saved {
-  size_t a, rstd1, qkv, o, lse, h1, rstd2, b, gu, act, total;
+  size_t a, rstd1, qkv, o, lse, h1, rstd2, b, gu, act;
+  size_t probs, idx, gates, counts, offsets, perm, pos_of, xs, ys;
+  size_t total;
 };
 
 Saved saved_layout(const forge_layer_cfg& c) {
   const Dims d = dims(c);
-  Saved s;
+  Saved s{};
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
   s.a = take(d.T * d.h * 2);
@@ -124,24 +150,53 @@ Saved saved_layout(const forge_layer_cfg& c) {
   s.h1 = take(d.T * d.h * 2);
   s.rstd2 = take(d.T * 4);
   s.b = take(d.T * d.h * 2);
-  s.gu = take(d.T * 2 * d.f * 2);
-  s.act = take(d.T * d.f * 2);
+  if (d.E == 0) {
+    s.gu = take(d.T * 2 * d.f * 2);
+    s.act = take(d.T * d.f * 2);
+  } else {
+    s.probs = take(d.T * d.E * 4);
+    s.idx = take(d.R * 4);
+    s.gates = take(d.R * 4);
+    s.counts = take(d.E * 4);
+    s.offsets = take((d.E + 1) * 4);
+    s.perm = take(d.R * 4);
+    s.pos_of = take(d.R * 4);
+    s.xs = take(d.R * d.h * 2);
+    s.gu = take(d.R * 2 * d.fe * 2);
+    s.act = take(d.R * d.fe * 2);
+    s.ys = take(d.R * d.h * 2);
+  }
   s.total = off;
   return s;
 }
 
-// ---- backward workspace ---------------------------------------------------
+// ---- workspace -------------------------------------------------------------
 struct Work {
-  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv, total;
+  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv;
+  size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs;  // MoE
+  size_t total;
 };
 
 Work work_layout(const forge_layer_cfg& c) {
   const Dims d = dims(c);
-  Work w;
+  Work w{};
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
-  w.dA = take(d.T * d.f * 2);
-  w.dgu = take(d.T * 2 * d.f * 2);
+  if (d.E == 0) {
+    w.dA = take(d.T * d.f * 2);
+    w.dgu = take(d.T * 2 * d.f * 2);
+  } else {
+    w.dA = take(d.R * d.fe * 2);
+    w.dgu = take(d.R * 2 * d.fe * 2);
+    w.logits = take(d.T * d.E * 4);
+    w.blk = take((size_t)forge::moe_sort_blocks((int)d.T) * d.E * 4);
+    w.colsum = take(d.E * 4);
+    w.dys = take(d.R * d.h * 2);
+    w.dxs = take(d.R * d.h * 2);
+    w.dgate = take(d.R * 4);
+    w.dl = take(d.T * d.E * 2);
+    w.dbs = take(d.T * d.h * 2);
+  }
   w.db = take(d.T * d.h * 2);
   w.dh1 = take(d.T * d.h * 2);
   w.dO = take(d.T * d.hq * 2);
@@ -185,6 +240,14 @@ GemmArgs gargs(const void* A, long lda, const void* B, long ldb, void* C, long l
   return g;
 }
 
+GemmArgs grouped(GemmArgs g, const int32_t* off, long E, long strideB, long strideC) {
+  g.g_off = off;
+  g.groups = (int)E;
+  g.strideB = strideB;
+  g.strideC = strideC;
+  return g;
+}
+
 forge::AttnArgs attn_args(const Dims& d, const uint16_t* qkv) {
   forge::AttnArgs a;
   a.q = qkv;
@@ -200,16 +263,187 @@ forge::AttnArgs attn_args(const Dims& d, const uint16_t* qkv) {
   return a;
 }
 
-forge_status check_weights(const forge_layer_weights* w) {
+forge_status check_weights(const forge_layer_cfg& c, const forge_layer_weights* w) {
   FORGE_CHECK(w != nullptr, FORGE_ERR_INVALID_ARG, "weights is NULL");
   FORGE_PTR(w->attn_norm);
   FORGE_PTR(w->w_qkv);
   FORGE_PTR(w->w_o);
   FORGE_PTR(w->ffn_norm);
-  FORGE_PTR(w->w_gate_up);
-  FORGE_PTR(w->w_down);
   FORGE_PTR(w->rope_cos);
   FORGE_PTR(w->rope_sin);
+  if (c.n_experts == 0) {
+    FORGE_PTR(w->w_gate_up);
+    FORGE_PTR(w->w_down);
+  } else {
+    FORGE_PTR(w->w_router);
+    FORGE_PTR(w->w_gate_up_e);
+    FORGE_PTR(w->w_down_e);
+  }
+  return FORGE_OK;
+}
+
+forge_status check_grads(const forge_layer_cfg& c, const forge_layer_grads* g) {
+  FORGE_CHECK(g != nullptr, FORGE_ERR_INVALID_ARG, "grads is NULL");
+  FORGE_PTR(g->d_attn_norm);
+  FORGE_PTR(g->d_w_qkv);
+  FORGE_PTR(g->d_w_o);
+  FORGE_PTR(g->d_ffn_norm);
+  if (c.n_experts == 0) {
+    FORGE_PTR(g->d_w_gate_up);
+    FORGE_PTR(g->d_w_down);
+  } else {
+    FORGE_PTR(g->d_w_router);
+    FORGE_PTR(g->d_w_gate_up_e);
+    FORGE_PTR(g->d_w_down_e);
+  }
+  return FORGE_OK;
+}
+
+// ---- attention block (shared by the dense and MoE layers) -----------------
+// a = RMSNorm(x), qkv = a W_qkv^T, RoPE, attention, h1 = x + O W_o^T.
+forge_status attn_block_fwd(const forge_layer_cfg& c, const Dims& d,
+                            const forge_layer_weights* w, const uint16_t* x, uint16_t* a,
+                            float* rstd1, uint16_t* qkv, uint16_t* o, float* lse, uint16_t* h1,
+                            hipStream_t s) {
+  FORGE_HIP(forge::rmsnorm_fwd(x, w->attn_norm, a, rstd1, (int)d.T, (int)d.h, c.rms_eps, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                        gargs(a, d.h, w->w_qkv, d.h, qkv, d.qkv, d.T, d.qkv, d.h), s));
+  FORGE_HIP(forge::rope_apply(qkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
+                              (int)(d.nh + d.nkv), (int)d.d, false, s));
+  FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o, lse, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
+                        gargs(o, d.hq, w->w_o, d.hq, h1, d.h, d.T, d.h, d.hq, x, d.h), s));
+  return FORGE_OK;
+}
+
+// Backward of attn_block_fwd from dh1 (the full gradient at h1, residual
+// path included) to d_in.
+forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
+                            const forge_layer_weights* w, const forge_layer_grads* g,
+                            const uint16_t* x, const uint16_t* a, const float* rstd1,
+                            const uint16_t* qkv, const uint16_t* o, const float* lse,
+                            const uint16_t* dh1, uint16_t* d_in, void* workspace, const Work& wk,
+                            hipStream_t s) {
+  uint16_t* dO = at<uint16_t>(workspace, wk.dO);
+  float* delta = at<float>(workspace, wk.delta);
+  uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
+  uint16_t* da = at<uint16_t>(workspace, wk.da);
+  float* dgp = at<float>(workspace, wk.dg);
+  const int nblk = forge::rmsnorm_bwd_blocks((int)d.T);
+  const forge::AttnArgs aa = attn_args(d, qkv);
+  (void)c;
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
+  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, at<float>(workspace, wk.pk),
+                                 at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
+                                 d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, dO, lse, delta, dqkv, d.qkv, s));
+  FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
+                              (int)(d.nh + d.nkv), (int)d.d, true, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                        gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), s));
+  FORGE_HIP(forge::rmsnorm_bwd(x, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, s));
+  return FORGE_OK;
+}
+
+// ---- MoE FFN ------------------------------------------------------------------
+// out = h1 + sum_j gate_j FFN_{e_j}(b), b = RMSNorm(h1) already in saved.b;
+// aux (if non-null) += alpha E sum_e f_e P_e.
+forge_status moe_ffn_fwd(const forge_layer_cfg& c, const Dims& d, const forge_layer_weights* w,
+                         void* saved, const Saved& sv, void* workspace, const Work& wk,
+                         const uint16_t* h1, uint16_t* out, float* aux, hipStream_t s) {
+  const uint16_t* bn = at<uint16_t>(saved, sv.b);
+  float* logits = at<float>(workspace, wk.logits);
+  float* probs = at<float>(saved, sv.probs);
+  int32_t* idx = at<int32_t>(saved, sv.idx);
+  float* gates = at<float>(saved, sv.gates);
+  int32_t* counts = at<int32_t>(saved, sv.counts);
+  int32_t* offsets = at<int32_t>(saved, sv.offsets);
+  int32_t* perm = at<int32_t>(saved, sv.perm);
+  int32_t* pos_of = at<int32_t>(saved, sv.pos_of);
+  uint16_t* xs = at<uint16_t>(saved, sv.xs);
+  uint16_t* gu = at<uint16_t>(saved, sv.gu);
+  uint16_t* act = at<uint16_t>(saved, sv.act);
+  uint16_t* ys = at<uint16_t>(saved, sv.ys);
+  const int T = (int)d.T, E = (int)d.E, k = (int)d.k;
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreF32,
+                        gargs(bn, d.h, w->w_router, d.h, logits, d.E, d.T, d.E, d.h), s));
+  FORGE_HIP(forge::moe_route(logits, T, E, k, idx, gates, probs, s));
+  FORGE_HIP(forge::moe_sort(idx, T, E, k, at<int32_t>(workspace, wk.blk), counts, offsets, perm,
+                            pos_of, s));
+  FORGE_HIP(forge::moe_gather(bn, perm, d.R, (int)d.h, k, xs, s));
+  FORGE_HIP(forge::gemm_grouped_m(
+      forge::kKC, forge::kStoreBF16,
+      grouped(gargs(xs, d.h, w->w_gate_up_e, d.h, gu, 2 * d.fe, d.R, 2 * d.fe, d.h), offsets, E,
+              2 * d.fe * d.h, 0), s));
+  FORGE_HIP(forge::swiglu_fwd(gu, act, (int)d.R, (int)d.fe, s));
+  FORGE_HIP(forge::gemm_grouped_m(
+      forge::kKC, forge::kStoreBF16,
+      grouped(gargs(act, d.fe, w->w_down_e, d.fe, ys, d.h, d.R, d.h, d.fe), offsets, E,
+              d.h * d.fe, 0), s));
+  FORGE_HIP(forge::moe_combine(ys, gates, pos_of, h1, d.T, (int)d.h, k, out, s));
+  FORGE_HIP(forge::moe_aux_loss(probs, counts, T, E, k, c.aux_coef,
+                                at<float>(workspace, wk.colsum), aux, s));
+  return FORGE_OK;
+}
+
+// Backward of moe_ffn_fwd for upstream d_out (objective <out, d_out> + aux):
+// writes db (the gradient at b) into the workspace.
+forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_layer_weights* w,
+                         const forge_layer_grads* g, const void* saved, const Saved& sv,
+                         void* workspace, const Work& wk, const uint16_t* d_out, uint16_t* db,
+                         hipStream_t s) {
+  const uint16_t* bn = at<uint16_t>(saved, sv.b);
+  const float* probs = at<float>(saved, sv.probs);
+  const int32_t* idx = at<int32_t>(saved, sv.idx);
+  const float* gates = at<float>(saved, sv.gates);
+  const int32_t* counts = at<int32_t>(saved, sv.counts);
+  const int32_t* offsets = at<int32_t>(saved, sv.offsets);
+  const int32_t* pos_of = at<int32_t>(saved, sv.pos_of);
+  const uint16_t* xs = at<uint16_t>(saved, sv.xs);
+  const uint16_t* gu = at<uint16_t>(saved, sv.gu);
+  const uint16_t* act = at<uint16_t>(saved, sv.act);
+  const uint16_t* ys = at<uint16_t>(saved, sv.ys);
+  uint16_t* dys = at<uint16_t>(workspace, wk.dys);
+  uint16_t* dact = at<uint16_t>(workspace, wk.dA);
+  uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
+  uint16_t* dxs = at<uint16_t>(workspace, wk.dxs);
+  float* dgate = at<float>(workspace, wk.dgate);
+  uint16_t* dl = at<uint16_t>(workspace, wk.dl);
+  uint16_t* dbs = at<uint16_t>(workspace, wk.dbs);
+  const int T = (int)d.T, E = (int)d.E, k = (int)d.k;
+  FORGE_HIP(forge::moe_combine_bwd(ys, gates, pos_of, d_out, d.T, (int)d.h, k, dgate, dys, s));
+  // down projection: dgrad into the routed rows, wgrad per expert
+  FORGE_HIP(forge::gemm_grouped_m(
+      forge::kMC, forge::kStoreBF16,
+      grouped(gargs(dys, d.h, w->w_down_e, d.fe, dact, d.fe, d.R, d.fe, d.h), offsets, E,
+              d.h * d.fe, 0), s));
+  FORGE_HIP(forge::gemm_grouped_k(
+      forge::kAccF32,
+      grouped(gargs(dys, d.h, act, d.fe, g->d_w_down_e, d.fe, d.h, d.fe, 0), offsets, E, 0,
+              d.h * d.fe), s));
+  FORGE_HIP(forge::swiglu_bwd(gu, dact, dgu, (int)d.R, (int)d.fe, s));
+  FORGE_HIP(forge::gemm_grouped_m(
+      forge::kMC, forge::kStoreBF16,
+      grouped(gargs(dgu, 2 * d.fe, w->w_gate_up_e, d.h, dxs, d.h, d.R, d.h, 2 * d.fe), offsets,
+              E, 2 * d.fe * d.h, 0), s));
+  FORGE_HIP(forge::gemm_grouped_k(
+      forge::kAccF32,
+      grouped(gargs(dgu, 2 * d.fe, xs, d.h, g->d_w_gate_up_e, d.h, 2 * d.fe, d.h, 0), offsets,
+              E, 0, 2 * d.fe * d.h), s));
+  FORGE_HIP(forge::moe_scatter_back(dxs, pos_of, d.T, (int)d.h, k, dbs, s));
+  // router: dl through the softmax (gates and aux loss), then its two products
+  FORGE_HIP(forge::moe_router_bwd(probs, idx, dgate, counts, T, E, k, c.aux_coef, dl, s));
+  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kResidBF16,
+                        gargs(dl, d.E, w->w_router, d.h, db, d.h, d.T, d.h, d.E, dbs, d.h), s));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                        gargs(dl, d.E, bn, d.h, g->d_w_router, d.h, d.E, d.h, d.T), s));
   return FORGE_OK;
 }
 
@@ -230,7 +464,7 @@ const char* forge_status_string(forge_status s) {
 
 const char* forge_last_error(void) { return g_last_error.c_str(); }
 
-const char* forge_version(void) { return "forge 0.1 gfx950"; }
+const char* forge_version(void) { return "forge 0.2 gfx950"; }
 
 forge_status forge_layer_saved_bytes(const forge_layer_cfg* cfg, size_t* bytes) {
   if (forge_status s = check_cfg(cfg)) return s;
@@ -261,17 +495,21 @@ forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base, float* 
 forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
                              const forge_bf16* x_in, forge_bf16* x_out, void* saved,
                              void* workspace, float* aux_loss, forge_stream stream) {
-  (void)workspace;
-  (void)aux_loss;
   if (forge_status s = check_cfg(cfg)) return s;
-  if (forge_status s = check_weights(w)) return s;
+  if (forge_status s = check_weights(*cfg, w)) return s;
   FORGE_PTR(x_in);
   FORGE_PTR(x_out);
   FORGE_PTR(saved);
   const Dims d = dims(*cfg);
   FORGE_CHECK(x_out + d.T * d.h <= x_in || x_in + d.T * d.h <= x_out, FORGE_ERR_INVALID_ARG,
               "x_out overlaps x_in");
+  const bool moe = d.E > 0;
+  FORGE_CHECK(!(cfg->recompute_attn || moe) || workspace != nullptr, FORGE_ERR_INVALID_ARG,
+              "workspace is NULL (needed for recompute_attn and for MoE layers)");
+  FORGE_CHECK(aux_loss == nullptr || (reinterpret_cast<uintptr_t>(aux_loss) & 3u) == 0,
+              FORGE_ERR_ALIGNMENT, "aux_loss is not 4-byte aligned");
   const Saved sv = saved_layout(*cfg);
+  const Work wk = work_layout(*cfg);
   hipStream_t s = (hipStream_t)stream;
   uint16_t* a = at<uint16_t>(saved, sv.a);
   float* rstd1 = at<float>(saved, sv.rstd1);
@@ -279,23 +517,14 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   uint16_t* h1 = at<uint16_t>(saved, sv.h1);
   float* rstd2 = at<float>(saved, sv.rstd2);
   uint16_t* bn = at<uint16_t>(saved, sv.b);
-  uint16_t* gu = at<uint16_t>(saved, sv.gu);
-  uint16_t* act = at<uint16_t>(saved, sv.act);
-  FORGE_CHECK(cfg->recompute_attn == 0 || workspace != nullptr, FORGE_ERR_INVALID_ARG,
-              "workspace is NULL (needed when recompute_attn is set)");
-  const Work wk = work_layout(*cfg);
   uint16_t* o = cfg->recompute_attn ? at<uint16_t>(workspace, wk.o) : at<uint16_t>(saved, sv.o);
   float* lse = cfg->recompute_attn ? at<float>(workspace, wk.lse) : at<float>(saved, sv.lse);
 
-  FORGE_HIP(forge::rmsnorm_fwd(x_in, w->attn_norm, a, rstd1, (int)d.T, (int)d.h, cfg->rms_eps, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
-                        gargs(a, d.h, w->w_qkv, d.h, qkv, d.qkv, d.T, d.qkv, d.h), s));
-  FORGE_HIP(forge::rope_apply(qkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
-                              (int)(d.nh + d.nkv), (int)d.d, false, s));
-  FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o, lse, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
-                        gargs(o, d.hq, w->w_o, d.hq, h1, d.h, d.T, d.h, d.hq, x_in, d.h), s));
+  if (forge_status e = attn_block_fwd(*cfg, d, w, x_in, a, rstd1, qkv, o, lse, h1, s)) return e;
   FORGE_HIP(forge::rmsnorm_fwd(h1, w->ffn_norm, bn, rstd2, (int)d.T, (int)d.h, cfg->rms_eps, s));
+  if (moe) return moe_ffn_fwd(*cfg, d, w, saved, sv, workspace, wk, h1, x_out, aux_loss, s);
+  uint16_t* gu = at<uint16_t>(saved, sv.gu);
+  uint16_t* act = at<uint16_t>(saved, sv.act);
   FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
                         gargs(bn, d.h, w->w_gate_up, d.h, gu, 2 * d.f, d.T, 2 * d.f, d.h), s));
   FORGE_HIP(forge::swiglu_fwd(gu, act, (int)d.T, (int)d.f, s));
@@ -310,19 +539,13 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
                              const forge_layer_grads* g, void* workspace,
                              forge_stream stream) {
   if (forge_status s = check_cfg(cfg)) return s;
-  if (forge_status s = check_weights(w)) return s;
+  if (forge_status s = check_weights(*cfg, w)) return s;
   FORGE_PTR(saved);
   FORGE_PTR(x_in);
   FORGE_PTR(d_out);
   FORGE_PTR(d_in);
   FORGE_PTR(workspace);
-  FORGE_CHECK(g != nullptr, FORGE_ERR_INVALID_ARG, "grads is NULL");
-  FORGE_PTR(g->d_attn_norm);
-  FORGE_PTR(g->d_w_qkv);
-  FORGE_PTR(g->d_w_o);
-  FORGE_PTR(g->d_ffn_norm);
-  FORGE_PTR(g->d_w_gate_up);
-  FORGE_PTR(g->d_w_down);
+  if (forge_status s = check_grads(*cfg, g)) return s;
   const Dims d = dims(*cfg);
   const Saved sv = saved_layout(*cfg);
   const Work wk = work_layout(*cfg);
@@ -333,26 +556,17 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   const uint16_t* h1 = at<uint16_t>(saved, sv.h1);
   const float* rstd2 = at<float>(saved, sv.rstd2);
   const uint16_t* bn = at<uint16_t>(saved, sv.b);
-  const uint16_t* gu = at<uint16_t>(saved, sv.gu);
-  const uint16_t* act = at<uint16_t>(saved, sv.act);
-  uint16_t* dA = at<uint16_t>(workspace, wk.dA);
-  uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
   uint16_t* db = at<uint16_t>(workspace, wk.db);
   uint16_t* dh1 = at<uint16_t>(workspace, wk.dh1);
-  uint16_t* dO = at<uint16_t>(workspace, wk.dO);
-  float* delta = at<float>(workspace, wk.delta);
-  uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
-  uint16_t* da = at<uint16_t>(workspace, wk.da);
   float* dgp = at<float>(workspace, wk.dg);
   const int nblk = forge::rmsnorm_bwd_blocks((int)d.T);
-  const forge::AttnArgs aa = attn_args(d, qkv);
 
   const uint16_t* o;
   const float* lse;
   if (cfg->recompute_attn) {
     uint16_t* o_w = at<uint16_t>(workspace, wk.o);
     float* lse_w = at<float>(workspace, wk.lse);
-    FORGE_HIP(forge::attn_fwd(aa, o_w, lse_w, s));
+    FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o_w, lse_w, s));
     o = o_w;
     lse = lse_w;
   } else {
@@ -360,37 +574,72 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
     lse = at<float>(saved, sv.lse);
   }
 
-  // FFN: down projection, SwiGLU, gate/up projection, RMSNorm (+ residual)
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), s));
-  FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), s));
+  // FFN branch: gradient at b, then RMSNorm backward plus the residual path
+  if (d.E > 0) {
+    if (forge_status e = moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s))
+      return e;
+  } else {
+    const uint16_t* gu = at<uint16_t>(saved, sv.gu);
+    const uint16_t* act = at<uint16_t>(saved, sv.act);
+    uint16_t* dA = at<uint16_t>(workspace, wk.dA);
+    uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                          gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                          gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), s));
+    FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                          gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                          gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), s));
+  }
   FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, s));
+  return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s);
+}
 
-  // attention: output projection, flash-attention backward, RoPE, QKV projection
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
-  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, at<float>(workspace, wk.pk),
-                                 at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
-                                 d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dq(aa, dO, lse, delta, dqkv, d.qkv, s));
-  FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
-                              (int)(d.nh + d.nkv), (int)d.d, true, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), s));
-  FORGE_HIP(forge::rmsnorm_bwd(x_in, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
-  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, s));
+// ---- MoE routing building block -----------------------------------------------
+namespace {
+size_t route_ws_bytes(int32_t tokens, int32_t n_experts, int32_t top_k, size_t* pos_of_off) {
+  const size_t hist = up((size_t)forge::moe_sort_blocks(tokens) * n_experts * 4);
+  if (pos_of_off) *pos_of_off = hist;
+  return hist + up((size_t)tokens * top_k * 4);
+}
+}  // namespace
+
+forge_status forge_moe_route_workspace_bytes(int32_t tokens, int32_t n_experts, int32_t top_k,
+                                             size_t* bytes) {
+  FORGE_CHECK(tokens >= 1, FORGE_ERR_INVALID_ARG, "tokens must be >= 1");
+  FORGE_CHECK(n_experts >= 1 && n_experts <= kMaxExperts, FORGE_ERR_UNSUPPORTED,
+              "n_experts must be in [1, %d]", kMaxExperts);
+  FORGE_CHECK(top_k >= 1 && top_k <= n_experts, FORGE_ERR_INVALID_ARG,
+              "top_k must be in [1, n_experts]");
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = route_ws_bytes(tokens, n_experts, top_k, nullptr);
+  return ok();
+}
+
+forge_status forge_moe_route(const float* logits, int32_t tokens, int32_t n_experts,
+                             int32_t top_k, int32_t* idx, float* gates, float* probs,
+                             int32_t* counts, int32_t* offsets, int32_t* perm, void* workspace,
+                             forge_stream stream) {
+  FORGE_CHECK(tokens >= 1, FORGE_ERR_INVALID_ARG, "tokens must be >= 1");
+  FORGE_CHECK(n_experts >= 1 && n_experts <= kMaxExperts, FORGE_ERR_UNSUPPORTED,
+              "n_experts must be in [1, %d]", kMaxExperts);
+  FORGE_CHECK(top_k >= 1 && top_k <= n_experts, FORGE_ERR_INVALID_ARG,
+              "top_k must be in [1, n_experts]");
+  FORGE_CHECK((long)tokens * top_k < (1L << 31), FORGE_ERR_UNSUPPORTED, "tokens * top_k too large");
+  for (const void* p : {(const void*)logits, (const void*)idx, (const void*)gates,
+                        (const void*)probs, (const void*)counts, (const void*)offsets,
+                        (const void*)perm, (const void*)workspace})
+    FORGE_CHECK(p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3u) == 0,
+                FORGE_ERR_INVALID_ARG, "a pointer argument is NULL or not 4-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  size_t pos_off = 0;
+  route_ws_bytes(tokens, n_experts, top_k, &pos_off);
+  FORGE_HIP(forge::moe_route(logits, tokens, n_experts, top_k, idx, gates, probs, s));
+  FORGE_HIP(forge::moe_sort(idx, tokens, n_experts, top_k, static_cast<int32_t*>(workspace),
+                            counts, offsets, perm, at<int32_t>(workspace, pos_off), s));
   return ok();
 }
 

@@ -174,7 +174,7 @@ __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const fl
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -182,18 +182,55 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   constexpr int A_ELEMS = BM * CHUNKS, B_ELEMS = BN * CHUNKS;
   __shared__ uint4 lds[2][A_ELEMS + B_ELEMS];
 
-  // ---- tile order: XCD-contiguous bands, GROUP_M rows of tiles per band ----
-  const int tiles_m = (p.M + BM - 1) / BM;
-  const int tiles_n = (p.N + BN - 1) / BN;
-  const int nb = gridDim.x;
-  const int bid = blockIdx.x;
-  const int nb8 = nb - nb % NUM_XCD;
-  const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
-  const int in_group = GROUP_M * tiles_n;
-  const int first_m = (pid / in_group) * GROUP_M;
-  const int gsize = min(tiles_m - first_m, GROUP_M);
-  const int tm = first_m + (pid % in_group) % gsize;
-  const int tn = (pid % in_group) / gsize;
+  int tm, tn;
+  if (GROUP == 0) {
+    // ---- tile order: XCD-contiguous bands, GROUP_M rows of tiles per band ----
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int nb = gridDim.x;
+    const int bid = blockIdx.x;
+    const int nb8 = nb - nb % NUM_XCD;
+    const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
+    const int in_group = GROUP_M * tiles_n;
+    const int first_m = (pid / in_group) * GROUP_M;
+    const int gsize = min(tiles_m - first_m, GROUP_M);
+    tm = first_m + (pid % in_group) % gsize;
+    tn = (pid % in_group) / gsize;
+  } else if (GROUP == 1) {
+    // M-grouped: global m-tile index -> (group, local m-tile); groups whose
+    // rows are exhausted leave the surplus blocks of the upper-bound grid idle
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int gt = blockIdx.x / tiles_n;
+    tn = blockIdx.x % tiles_n;
+    int e = 0, acc = 0, rows = 0;
+    for (; e < p.groups; ++e) {
+      rows = p.g_off[e + 1] - p.g_off[e];
+      const int te = (rows + BM - 1) / BM;
+      if (gt < acc + te) break;
+      acc += te;
+    }
+    if (e >= p.groups) return;
+    tm = gt - acc;
+    const long r0 = p.g_off[e];
+    p.M = rows;
+    p.A += r0 * p.lda;  // K-contiguous A: group rows are row blocks
+    p.B += (long)e * p.strideB;
+    p.C = (char*)p.C + r0 * p.ldc * (EPI == kStoreBF16 || EPI == kResidBF16 ? 2 : 4);
+    if (EPI == kResidBF16) p.R += r0 * p.ldr;
+  } else {
+    // K-grouped: one (m, n) tile grid per group, reduction over the group's rows
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int e = blockIdx.x / (tiles_m * tiles_n);
+    const int t = blockIdx.x % (tiles_m * tiles_n);
+    tm = t / tiles_n;
+    tn = t % tiles_n;
+    const long r0 = p.g_off[e];
+    p.K = p.g_off[e + 1] - p.g_off[e];
+    p.A += r0 * p.lda;  // both operands M/N-contiguous: group rows are k rows
+    p.B += r0 * p.ldb;
+    p.C = (char*)p.C + (long)e * p.strideC * 4;
+  }
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int lane = threadIdx.x & 63;
@@ -274,6 +311,24 @@ hipError_t launch(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// M-grouped: at most M / BM + groups m-tiles exist, whatever the group sizes.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LB, int EPI>
+hipError_t launch_grouped_m(const GemmArgs& a, hipStream_t s) {
+  const long mt = a.M / BM + a.groups;
+  const long tiles = mt * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, kKC, LB, EPI, 1>), dim3((unsigned)tiles),
+                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
+hipError_t launch_grouped_k(const GemmArgs& a, hipStream_t s) {
+  const long tiles = (long)a.groups * ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, kMC, kMC, EPI, 2>), dim3((unsigned)tiles),
+                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
@@ -287,6 +342,19 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
+  if (lb == kKC && epi == kStoreBF16) return launch_grouped_m<256, 256, 4, 2, kKC, kStoreBF16>(a, s);
+  if (lb == kMC && epi == kStoreBF16) return launch_grouped_m<256, 256, 4, 2, kMC, kStoreBF16>(a, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
+  if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
+  return hipErrorInvalidValue;
+}
 
 hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,
                 hipStream_t s) {

@@ -26,6 +26,11 @@ struct GemmArgs {
   const uint16_t* R;
   int M, N, K;
   long lda, ldb, ldc, ldr;
+  // grouped products (MoE experts): g_off[E + 1] device row offsets of the
+  // groups; strideB / strideC elements between consecutive groups' B / C.
+  const int* g_off = nullptr;
+  int groups = 0;
+  long strideB = 0, strideC = 0;
 };
 
 // Host-side shape rules (checked by the caller): K-contiguous operands need
@@ -33,6 +38,12 @@ struct GemmArgs {
 // dimensions % 8 == 0; base pointers 16-byte aligned.
 hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,
                 hipStream_t stream);
+// Grouped forms, one product per group e with rows [g_off[e], g_off[e+1]):
+//   M-grouped (KC or MC B): C rows g_off[e].. = A rows g_off[e].. x B_e, where
+//     B_e = B + e * strideB; M is an upper bound of the total rows (T * k).
+//   K-grouped (MC, MC): C_e (+)= sum over rows g_off[e].. of A^T B, C_e = C + e * strideC.
+hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
+hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
 
 // --------------------------------------------------------- elementwise ----
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* g, uint16_t* y, float* rstd,
@@ -94,5 +105,30 @@ hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* l
                          long ld_dqkv, hipStream_t s);
 hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* lse,
                        const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
+
+// ----------------------------------------------------------------- MoE ----
+// Routing of fp32 logits [T, E] (E <= 64): idx / gates [T, k], probs [T, E].
+hipError_t moe_route(const float* logits, int T, int E, int k, int32_t* idx, float* gates,
+                     float* probs, hipStream_t s);
+// Blocks of the counting sort; block_counts needs moe_sort_blocks(T) * E ints.
+int moe_sort_blocks(int T);
+// counts [E], offsets [E + 1], perm / pos_of [T k] (canonical order).
+hipError_t moe_sort(const int32_t* idx, int T, int E, int k, int32_t* block_counts,
+                    int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* pos_of,
+                    hipStream_t s);
+hipError_t moe_gather(const uint16_t* b, const int32_t* perm, long rows, int h, int k,
+                      uint16_t* xs, hipStream_t s);
+hipError_t moe_combine(const uint16_t* ys, const float* gates, const int32_t* pos_of,
+                       const uint16_t* h1, long T, int h, int k, uint16_t* out, hipStream_t s);
+hipError_t moe_combine_bwd(const uint16_t* ys, const float* gates, const int32_t* pos_of,
+                           const uint16_t* dy, long T, int h, int k, float* dgate,
+                           uint16_t* dys, hipStream_t s);
+hipError_t moe_scatter_back(const uint16_t* dxs, const int32_t* pos_of, long T, int h, int k,
+                            uint16_t* db, hipStream_t s);
+hipError_t moe_aux_loss(const float* probs, const int32_t* counts, int T, int E, int k,
+                        float alpha, float* colsum, float* aux, hipStream_t s);
+hipError_t moe_router_bwd(const float* probs, const int32_t* idx, const float* dgate,
+                          const int32_t* counts, int T, int E, int k, float alpha, uint16_t* dl,
+                          hipStream_t s);
 
 }  // namespace forge

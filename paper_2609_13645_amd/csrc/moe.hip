@@ -1,0 +1,347 @@
+// Routed mixture-of-experts pieces of the layer (the sparse model of App. B,
+// Table "H100 architecture configurations": routed experts with top-k
+// selection), dropless: every token goes to its top_k experts.
+//
+//  * route: one wave per token, lane e holds expert e's fp32 logit: softmax
+//    over all experts, then top_k rounds of wave argmax (largest logit, ties
+//    to the lower expert id). Gates are the softmax probabilities of the
+//    chosen experts (no renormalisation).
+//  * permutation: a counting sort that is deterministic by construction —
+//    per-block expert histograms, a fixed-order scan over blocks, then each
+//    block assigns ranks in flat (token, slot) order with wave ballots, so
+//    the order is expert-major, token ascending, slot ascending.
+//  * gather / combine / their backward move whole bf16 rows with 16-byte
+//    vectors; every sum over the k slots of a token runs in slot order.
+//  * the load-balance auxiliary loss alpha * E * sum_e f_e P_e and its
+//    gradient through the softmax (f_e = count_e / (T k) is a constant).
+#include "common.h"
+#include "kernels.h"
+
+namespace forge {
+namespace {
+
+constexpr int kSortTokens = 128;  // tokens per counting-sort block
+
+// ------------------------------------------------------------- routing ----
+__global__ __launch_bounds__(256) void route_k(const float* __restrict__ logits, int T, int E,
+                                               int k, int32_t* __restrict__ idx,
+                                               float* __restrict__ gates,
+                                               float* __restrict__ probs) {
+  const int lane = threadIdx.x & 63;
+  const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const float l = lane < E ? logits[t * E + lane] : -INFINITY;
+  const float mx = wave_max(l);
+  const float ex = lane < E ? __expf(l - mx) : 0.0f;
+  const float p = ex / wave_sum(ex);
+  if (lane < E) probs[t * E + lane] = p;
+  float cand = l;
+  for (int j = 0; j < k; ++j) {
+    const float best = wave_max(cand);
+    const uint64_t hit = __ballot(cand == best && lane < E);
+    const int e = __ffsll((unsigned long long)hit) - 1;  // lowest lane among ties
+    const float g = __shfl(p, e, 64);
+    if (lane == 0) {
+      idx[t * k + j] = e;
+      gates[t * k + j] = g;
+    }
+    if (lane == e) cand = -INFINITY;
+  }
+}
+
+// Per-block expert histogram of the flat (token, slot) entries.
+__global__ __launch_bounds__(256) void sort_count_k(const int32_t* __restrict__ idx, int T, int E,
+                                                    int k, int32_t* __restrict__ block_counts) {
+  __shared__ int hist[64];
+  if (threadIdx.x < 64) hist[threadIdx.x] = 0;
+  __syncthreads();
+  const long f0 = (long)blockIdx.x * kSortTokens * k;
+  const long f1 = min((long)T * k, f0 + (long)kSortTokens * k);
+  for (long f = f0 + threadIdx.x; f < f1; f += blockDim.x) atomicAdd(&hist[idx[f]], 1);
+  __syncthreads();
+  if (threadIdx.x < E) block_counts[(long)blockIdx.x * E + threadIdx.x] = hist[threadIdx.x];
+}
+
+// Fixed-order scan: offsets[e] (exclusive over experts), per-block bases.
+__global__ void sort_scan_k(int32_t* __restrict__ block_counts, int nblk, int E,
+                            int32_t* __restrict__ counts, int32_t* __restrict__ offsets) {
+  __shared__ int tot[64];
+  const int e = threadIdx.x;
+  if (e < E) {
+    int run = 0;
+    for (int b = 0; b < nblk; ++b) {
+      const int c = block_counts[(long)b * E + e];
+      block_counts[(long)b * E + e] = run;  // becomes the in-expert base of block b
+      run += c;
+    }
+    tot[e] = run;
+    counts[e] = run;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int i = 0; i < E; ++i) {
+      offsets[i] = acc;
+      acc += tot[i];
+    }
+    offsets[E] = acc;
+  }
+}
+
+// Ranks within each expert in flat order: one wave per block, 64 entries per
+// round; for each expert present in the round, a ballot gives the lanes'
+// ranks. perm[pos] = flat entry, pos_of[flat entry] = pos.
+__global__ __launch_bounds__(64) void sort_scatter_k(const int32_t* __restrict__ idx, int T, int E,
+                                                     int k, const int32_t* __restrict__ block_base,
+                                                     const int32_t* __restrict__ offsets,
+                                                     int32_t* __restrict__ perm,
+                                                     int32_t* __restrict__ pos_of) {
+  __shared__ int run[64];
+  const int lane = threadIdx.x;
+  if (lane < E) run[lane] = offsets[lane] + block_base[(long)blockIdx.x * E + lane];
+  __syncthreads();
+  const long f0 = (long)blockIdx.x * kSortTokens * k;
+  const long f1 = min((long)T * k, f0 + (long)kSortTokens * k);
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (long base = f0; base < f1; base += 64) {
+    const long f = base + lane;
+    const bool ok = f < f1;
+    const int e = ok ? idx[f] : -1;
+    uint64_t todo = __ballot(ok);
+    while (todo) {
+      const int leader = __ffsll((unsigned long long)todo) - 1;
+      const int ex = __shfl(e, leader, 64);
+      const uint64_t same = __ballot(ok && e == ex);
+      if (ok && e == ex) {
+        const int pos = run[ex] + __popcll(same & below);
+        perm[pos] = (int32_t)f;
+        pos_of[f] = pos;
+      }
+      __syncthreads();  // all lanes read run[ex] before it advances
+      if (lane == 0) run[ex] += __popcll(same);
+      __syncthreads();
+      todo &= ~same;
+    }
+  }
+}
+
+// xs[pos] = b[perm[pos] / k]; one thread per 8 elements.
+__global__ __launch_bounds__(256) void gather_k(const bf16_t* __restrict__ b,
+                                                const int32_t* __restrict__ perm, long rows, int h,
+                                                int k, bf16_t* __restrict__ xs) {
+  const int cpr = h / 8;
+  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= rows * cpr) return;
+  const long r = id / cpr;
+  const int c = (int)(id % cpr);
+  const long t = perm[r] / k;
+  reinterpret_cast<uint4*>(xs + r * h)[c] = reinterpret_cast<const uint4*>(b + t * h)[c];
+}
+
+// out[t] = h1[t] + sum_j gate[t, j] * ys[pos_of[t k + j]] (fp32, slot order).
+__global__ __launch_bounds__(256) void combine_k(const bf16_t* __restrict__ ys,
+                                                 const float* __restrict__ gates,
+                                                 const int32_t* __restrict__ pos_of,
+                                                 const bf16_t* __restrict__ h1, long T, int h,
+                                                 int k, bf16_t* __restrict__ out) {
+  const int cpr = h / 8;
+  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= T * cpr) return;
+  const long t = id / cpr;
+  const int c = (int)(id % cpr);
+  float acc[8] = {};
+  for (int j = 0; j < k; ++j) {
+    const float g = gates[t * k + j];
+    float y[8];
+    unpack8(reinterpret_cast<const uint4*>(ys + (long)pos_of[t * k + j] * h)[c], y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += g * y[e];
+  }
+  float r[8];
+  unpack8(reinterpret_cast<const uint4*>(h1 + t * h)[c], r);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] += acc[e];
+  reinterpret_cast<uint4*>(out + t * h)[c] = pack8(r);
+}
+
+// Backward of combine for one token per block: dgate[t, j] = dy_t . ys_row and
+// dys_row = gate[t, j] * dy_t. k <= 16.
+__global__ __launch_bounds__(256) void combine_bwd_k(const bf16_t* __restrict__ ys,
+                                                     const float* __restrict__ gates,
+                                                     const int32_t* __restrict__ pos_of,
+                                                     const bf16_t* __restrict__ dy, int h, int k,
+                                                     float* __restrict__ dgate,
+                                                     bf16_t* __restrict__ dys) {
+  __shared__ float red[4][16];
+  const long t = blockIdx.x;
+  const int cpr = h / 8;
+  float dot[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) dot[j] = 0.0f;
+  for (int c = threadIdx.x; c < cpr; c += blockDim.x) {
+    float d[8];
+    unpack8(reinterpret_cast<const uint4*>(dy + t * h)[c], d);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (j < k) {
+        const long row = pos_of[t * k + j];
+        float y[8], o[8];
+        unpack8(reinterpret_cast<const uint4*>(ys + row * h)[c], y);
+        const float g = gates[t * k + j];
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          s += d[e] * y[e];
+          o[e] = g * d[e];
+        }
+        dot[j] += s;
+        reinterpret_cast<uint4*>(dys + row * h)[c] = pack8(o);
+      }
+    }
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    if (j < k) {
+      const float s = wave_sum(dot[j]);
+      if (lane == 0) red[wave][j] = s;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < k) {
+    const int j = threadIdx.x;
+    dgate[t * k + j] = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+  }
+}
+
+// db_s[t] = sum_j dxs[pos_of[t k + j]] (fp32 in slot order, one rounding).
+__global__ __launch_bounds__(256) void scatter_back_k(const bf16_t* __restrict__ dxs,
+                                                      const int32_t* __restrict__ pos_of, long T,
+                                                      int h, int k, bf16_t* __restrict__ db) {
+  const int cpr = h / 8;
+  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= T * cpr) return;
+  const long t = id / cpr;
+  const int c = (int)(id % cpr);
+  float acc[8] = {};
+  for (int j = 0; j < k; ++j) {
+    float y[8];
+    unpack8(reinterpret_cast<const uint4*>(dxs + (long)pos_of[t * k + j] * h)[c], y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += y[e];
+  }
+  reinterpret_cast<uint4*>(db + t * h)[c] = pack8(acc);
+}
+
+// P_e = sum_t p[t, e] (fixed order) and aux += alpha E sum_e f_e P_e / T.
+// One block; wave w sums the token stripe t = w mod 16 for each expert lane.
+__global__ __launch_bounds__(1024) void aux_loss_k(const float* __restrict__ probs,
+                                                   const int32_t* __restrict__ counts, int T,
+                                                   int E, int k, float alpha,
+                                                   float* __restrict__ colsum,
+                                                   float* __restrict__ aux) {
+  __shared__ float part[16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float s = 0.0f;
+  if (lane < E)
+    for (int t = wave; t < T; t += 16) s += probs[(long)t * E + lane];
+  part[wave][lane] = s;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    float c = 0.0f;
+    for (int w = 0; w < 16; ++w) c += part[w][threadIdx.x];
+    if (threadIdx.x < E) colsum[threadIdx.x] = c;
+    const float fe = threadIdx.x < E ? (float)counts[threadIdx.x] / ((float)T * k) : 0.0f;
+    const float term = wave_sum(fe * (threadIdx.x < E ? c : 0.0f));
+    if (threadIdx.x == 0 && aux) aux[0] += alpha * (float)E * term / (float)T;
+  }
+}
+
+// dl[t, e] = p (dp - sum_e p dp) with dp = dgate on chosen experts plus the
+// aux term alpha E f_e / T on every expert; written as bf16 for the router
+// data / weight gradient products. One wave per token.
+__global__ __launch_bounds__(256) void router_bwd_k(const float* __restrict__ probs,
+                                                    const int32_t* __restrict__ idx,
+                                                    const float* __restrict__ dgate,
+                                                    const int32_t* __restrict__ counts, int T,
+                                                    int E, int k, float alpha,
+                                                    bf16_t* __restrict__ dl) {
+  const int lane = threadIdx.x & 63;
+  const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const float p = lane < E ? probs[t * E + lane] : 0.0f;
+  float dp = lane < E ? alpha * (float)E * ((float)counts[lane] / ((float)T * k)) / (float)T : 0.0f;
+  for (int j = 0; j < k; ++j)
+    if (idx[t * k + j] == lane) dp += dgate[t * k + j];
+  const float dot = wave_sum(p * dp);
+  if (lane < E) dl[t * E + lane] = f2bf(p * (dp - dot));
+}
+
+inline unsigned nblocks(long work, int threads) { return (unsigned)((work + threads - 1) / threads); }
+
+}  // namespace
+
+int moe_sort_blocks(int T) { return (T + kSortTokens - 1) / kSortTokens; }
+
+hipError_t moe_route(const float* logits, int T, int E, int k, int32_t* idx, float* gates,
+                     float* probs, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(route_k, dim3(nblocks(T, 4)), dim3(256), 0, s, logits, T, E, k, idx, gates, probs);
+  return hipGetLastError();
+}
+
+hipError_t moe_sort(const int32_t* idx, int T, int E, int k, int32_t* block_counts,
+                    int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* pos_of,
+                    hipStream_t s) {
+  const int nb = moe_sort_blocks(T);
+  hipLaunchKernelGGL(sort_count_k, dim3(nb), dim3(256), 0, s, idx, T, E, k, block_counts);
+  hipLaunchKernelGGL(sort_scan_k, dim3(1), dim3(64), 0, s, block_counts, nb, E, counts, offsets);
+  hipLaunchKernelGGL(sort_scatter_k, dim3(nb), dim3(64), 0, s, idx, T, E, k, block_counts, offsets,
+                     perm, pos_of);
+  return hipGetLastError();
+}
+
+hipError_t moe_gather(const uint16_t* b, const int32_t* perm, long rows, int h, int k,
+                      uint16_t* xs, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_k, dim3(nblocks(rows * (h / 8), 256)), dim3(256), 0, s, b, perm, rows, h, k, xs);
+  return hipGetLastError();
+}
+
+hipError_t moe_combine(const uint16_t* ys, const float* gates, const int32_t* pos_of,
+                       const uint16_t* h1, long T, int h, int k, uint16_t* out, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_k, dim3(nblocks(T * (h / 8), 256)), dim3(256), 0, s, ys, gates, pos_of, h1, T, h, k, out);
+  return hipGetLastError();
+}
+
+hipError_t moe_combine_bwd(const uint16_t* ys, const float* gates, const int32_t* pos_of,
+                           const uint16_t* dy, long T, int h, int k, float* dgate, uint16_t* dys,
+                           hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_bwd_k, dim3((unsigned)T), dim3(256), 0, s, ys, gates, pos_of, dy, h, k, dgate, dys);
+  return hipGetLastError();
+}
+
+hipError_t moe_scatter_back(const uint16_t* dxs, const int32_t* pos_of, long T, int h, int k,
+                            uint16_t* db, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(scatter_back_k, dim3(nblocks(T * (h / 8), 256)), dim3(256), 0, s, dxs, pos_of, T, h, k, db);
+  return hipGetLastError();
+}
+
+hipError_t moe_aux_loss(const float* probs, const int32_t* counts, int T, int E, int k, float alpha,
+                        float* colsum, float* aux, hipStream_t s) {
+  hipLaunchKernelGGL(aux_loss_k, dim3(1), dim3(1024), 0, s, probs, counts, T, E, k, alpha, colsum, aux);
+  return hipGetLastError();
+}
+
+hipError_t moe_router_bwd(const float* probs, const int32_t* idx, const float* dgate,
+                          const int32_t* counts, int T, int E, int k, float alpha, uint16_t* dl,
+                          hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(router_bwd_k, dim3(nblocks(T, 4)), dim3(256), 0, s, probs, idx, dgate, counts, T, E, k, alpha, dl);
+  return hipGetLastError();
+}
+
+}  // namespace forge

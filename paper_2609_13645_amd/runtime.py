@@ -11,7 +11,6 @@ import numpy as np
 from . import _lib
 
 LAYER_WEIGHTS = ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")
-GRAD_NAMES = {n: "d_" + n for n in LAYER_WEIGHTS}
 
 
 def _torch():
@@ -39,12 +38,24 @@ def to_device(arr: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(arr).copy()).to(device)
 
 
+def layer_weight_names(cfg: dict):
+    if cfg.get("n_experts", 0):
+        return ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_router", "w_gate_up_e", "w_down_e")
+    return LAYER_WEIGHTS
+
+
 def layer_shapes(cfg: dict) -> dict:
-    """Shapes of one dense layer's weights."""
+    """Shapes of one layer's weights (dense or MoE)."""
     h, d = cfg["hidden"], cfg["head_dim"]
-    hq, hkv, f = cfg["n_heads"] * d, cfg["n_kv_heads"] * d, cfg["ffn"]
-    return {"attn_norm": (h,), "w_qkv": (hq + 2 * hkv, h), "w_o": (h, hq),
-            "ffn_norm": (h,), "w_gate_up": (2 * f, h), "w_down": (h, f)}
+    hq, hkv = cfg["n_heads"] * d, cfg["n_kv_heads"] * d
+    out = {"attn_norm": (h,), "w_qkv": (hq + 2 * hkv, h), "w_o": (h, hq), "ffn_norm": (h,)}
+    if cfg.get("n_experts", 0):
+        E, fe = cfg["n_experts"], cfg["expert_ffn"]
+        out.update({"w_router": (E, h), "w_gate_up_e": (E, 2 * fe, h), "w_down_e": (E, h, fe)})
+    else:
+        f = cfg["ffn"]
+        out.update({"w_gate_up": (2 * f, h), "w_down": (h, f)})
+    return out
 
 
 def empty_bytes(n: int, device="cuda"):
@@ -96,12 +107,14 @@ class Layer:
         self.cfg = dict(cfg)
         self.c = _lib.layer_cfg(cfg)
         self.stream = stream
+        names = layer_weight_names(cfg)
+        self.names = names
         if flat is None:
-            self.w = {n: to_device_bf16(weights_bits[n], device) for n in LAYER_WEIGHTS}
+            self.w = {n: to_device_bf16(weights_bits[n], device) for n in names}
         else:
-            for n in LAYER_WEIGHTS:
+            for n in names:
                 flat.load_bits(n, weights_bits[n])
-            self.w = {n: flat.view(flat.param, n) for n in LAYER_WEIGHTS}
+            self.w = {n: flat.view(flat.param, n) for n in names}
         half = cfg["head_dim"] // 2
         self.w["rope_cos"] = torch.empty((cfg["seq"], half), dtype=torch.float32, device=device)
         self.w["rope_sin"] = torch.empty((cfg["seq"], half), dtype=torch.float32, device=device)
@@ -109,10 +122,11 @@ class Layer:
                               self.w["rope_cos"], self.w["rope_sin"], stream)
         self.weights = _lib.layer_weights(self.w)
         if flat is None:
-            self.g = {GRAD_NAMES[n]: torch.zeros(self.w[n].shape, dtype=torch.float32,
-                                                 device=device) for n in LAYER_WEIGHTS}
+            self.g = {"d_" + n: torch.zeros(self.w[n].shape, dtype=torch.float32,
+                                            device=device) for n in names}
         else:
-            self.g = {GRAD_NAMES[n]: flat.view(flat.grad, n) for n in LAYER_WEIGHTS}
+            self.g = {"d_" + n: flat.view(flat.grad, n) for n in names}
+        self.aux = torch.zeros(1, dtype=torch.float32, device=device)
         self.grads = _lib.layer_grads(self.g)
         self.saved = empty_bytes(_lib.forge_layer_saved_bytes(self.c), device)
         self.workspace = empty_bytes(_lib.forge_layer_workspace_bytes(self.c), device)
@@ -121,11 +135,14 @@ class Layer:
         for t in self.g.values():
             t.zero_()
 
-    def fwd(self, x_in, x_out, saved=None, workspace=None):
+    def fwd(self, x_in, x_out, saved=None, workspace=None, aux=None):
+        """Forward; for a MoE layer the load-balance loss is added to `aux`
+        (a device fp32 scalar; self.aux when None)."""
         _lib.forge_layer_fwd(self.c, self.weights, x_in, x_out,
                              self.saved if saved is None else saved,
                              self.workspace if workspace is None else workspace,
-                             None, self.stream)
+                             (self.aux if aux is None else aux) if self.cfg.get("n_experts", 0)
+                             else None, self.stream)
 
     def bwd(self, x_in, d_out, d_in, saved=None, workspace=None):
         _lib.forge_layer_bwd(self.c, self.weights, self.saved if saved is None else saved,

@@ -46,7 +46,9 @@ def test_size_queries_are_consistent():
     (dict(hidden=260), _lib.FORGE_ERR_INVALID_ARG),
     (dict(ffn=690), _lib.FORGE_ERR_INVALID_ARG),
     (dict(seq=0), _lib.FORGE_ERR_INVALID_ARG),
-    (dict(n_experts=64, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
+    (dict(n_experts=96, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
+    (dict(n_experts=64, top_k=0, expert_ffn=1408), _lib.FORGE_ERR_INVALID_ARG),
+    (dict(n_experts=64, top_k=8, expert_ffn=1404), _lib.FORGE_ERR_INVALID_ARG),
 ])
 def test_bad_configs_rejected(change, status):
     c = _lib.layer_cfg(dict(fi.config("tiny"), **change))
@@ -96,3 +98,16 @@ def test_optimizer_argument_rules():
     with pytest.raises(_lib.ForgeError):
         _lib.forge_loss_workspace_bytes(_lib.HeadCfg(16, 64, 1001, 1e-5))  # vocab % 8
     assert ctypes.sizeof(_lib.LayerCfg) == 14 * 4
+
+
+def test_moe_layer_sizes():
+    c5 = fi.config("moe_layer")
+    cfg = _lib.layer_cfg(c5)
+    T, k, h, fe = 8192, 8, 2048, 1408
+    saved = _lib.forge_layer_saved_bytes(cfg)
+    # routed rows xs, G|U, A, ys dominate the saved activations
+    assert saved >= 2 * T * k * (h + 2 * fe + fe + h)
+    assert _lib.forge_layer_workspace_bytes(cfg) >= 2 * T * k * (2 * h + 3 * fe)
+    assert _lib.forge_moe_route_workspace_bytes(T, 64, 8) >= T * 8 * 4
+    with pytest.raises(_lib.ForgeError):
+        _lib.forge_moe_route_workspace_bytes(T, 65, 8)

@@ -101,3 +101,35 @@ def test_aux_loss_gradient_reaches_router():
     idx = np.arange(W["w_router"].size)
     assert rel_err(g["w_router"].ravel(), central_diff(f, W["w_router"], idx)) <= 1e-6
     assert np.all(g["w_down_e"] == 0)
+
+
+def test_moe_layer_rows_equals_full_layer():
+    rng = np.random.default_rng(6)
+    cfg = dict(MOE, batch=2, seq=5)
+    W = moe_weights(cfg, rng)
+    x = rng.standard_normal((10, cfg["hidden"]))
+    out, _, cache = moe.layer_fwd(x, W, cfg)
+    rows = [0, 4, 5, 9]
+    assert np.allclose(moe.layer_fwd_rows(x, W, cfg, rows), out[rows], rtol=1e-12, atol=1e-13)
+    o2, l2 = moe.layer_fwd_rows(x, W, cfg, rows, with_logits=True)
+    assert np.allclose(l2, cache["moe"]["l"][rows], rtol=1e-12, atol=1e-13)
+
+
+def test_topk_margin_brute_force():
+    rng = np.random.default_rng(7)
+    l = rng.standard_normal((40, 12)).astype(np.float32)
+    l[3, 4] = l[3, 9]                                   # a tie is a zero margin
+    for k in (1, 3, 11):
+        m = moe.topk_margin(l, k)
+        idx = moe.topk(l, k)
+        for t in range(40):
+            inside = float(min(l[t, e] for e in idx[t]))
+            outside = float(max(l[t, e] for e in range(12) if e not in idx[t]))
+            assert m[t] == inside - outside and m[t] >= 0
+    assert np.all(np.isinf(moe.topk_margin(l, 12)))
+    # a perturbation below half the margin leaves the top-k set unchanged
+    k = 3
+    m = moe.topk_margin(l, k)
+    d = (0.49 * m[:, None] * rng.uniform(-1, 1, l.shape)).astype(np.float32)
+    keep = m > 1e-3
+    assert np.array_equal(np.sort(moe.topk(l + d, k)[keep], 1), np.sort(moe.topk(l, k)[keep], 1))
