@@ -1,14 +1,18 @@
-"""Throughput of one decoder-layer training step on one MI355X.
+"""Throughput of one training step on one MI355X.
 
-Workload: the 8B-shape decoder layer (micro-batch 1 x seq 4096, hidden 4096,
-32 query / 8 kv heads of 128, SwiGLU FFN 14336, RoPE base 5e5), bf16 with
-fp32 gradient accumulation. One step = layer forward + layer backward + fused
-clip/AdamW/bf16 write-back over all 218 M parameters of the layer (flat fp32
-master, moments and gradient), on synthetic seeded inputs resident in HBM.
+Default workload: the 8B-shape decoder layer (micro-batch 1 x seq 4096,
+hidden 4096, 32 query / 8 kv heads of 128, SwiGLU FFN 14336, RoPE base 5e5),
+bf16 with fp32 gradient accumulation. One step = layer forward + layer
+backward + fused clip/AdamW/bf16 write-back over all 218 M parameters of the
+layer (flat fp32 master, moments and gradient), on synthetic seeded inputs
+resident in HBM. Other workloads (--workload): the same layer at seq 16384
+with attention recomputed in the backward, the 64-expert top-8 MoE layer,
+the 16-layer tied-head model (embedding, layers, LM head + cross-entropy)
+and the tiny one-layer model.
 
-Prints one JSON line: model TFLOP/s (App. C count of the layer fwd+bwd, the
+Prints one JSON line: model TFLOP/s (App. C count of the fwd+bwd; the
 optimizer adds time but no model FLOPs), MFU against the MI355X dense bf16
-peak, tokens/s, the roofline of the dominant kernel (measured here with HIP
+peak, tokens/s, the roofline of the dominant kernel (timed here with HIP
 events on the stream it runs on) and the fp64 CPU oracle's rate on a bounded
 sample of the same workload.
 """
@@ -35,9 +39,15 @@ from paper_2609_13645_amd import flops  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA (published)
 MFU_PEAK_TFLOPS = 2516.6           # 256 CU x 4096 FLOP/clk x 2.4 GHz
-PEAK_HBM_GBS = 8000.0
 METRIC = "model TFLOP/s and MFU (%) per fwd+bwd+AdamW step, tokens/s, 1×MI355X"
 WORKLOAD = "llama8b_layer"
+DESCRIPTION = {
+    "tiny": "tiny decoder layer + untied LM head + CE + AdamW (B1 S128 h256)",
+    "llama8b_layer": "Llama-8B-shape decoder layer fwd+bwd+AdamW (B1 S4096 h4096)",
+    "dense1b": "16-layer dense model, tied LM head + CE + AdamW (B4 S2048 h2048 V32000)",
+    "llama8b_layer_16k": "Llama-8B-shape layer at S16384, attention recomputed in bwd",
+    "moe_layer": "MoE decoder layer, 64 experts top-8, fe 1408 (B2 S4096 h2048)",
+}
 
 
 def parse():
@@ -45,44 +55,160 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seq", type=int, default=4096,
-                    help="tokens of the CPU-baseline sample")
+                    help="tokens of the CPU-baseline sample (layer workloads)")
     ap.add_argument("--kernel-reps", type=int, default=20)
     return ap.parse_args()
 
 
+def is_model(cfg):
+    return cfg["vocab"] > 0
+
+
+def tile_name(M, N):
+    """The tile the library's dispatch picks for a plain GEMM of this shape
+    (for labelling the roofline kernel only)."""
+    big = -(-M // 256) * -(-N // 256)
+    mid = -(-M // 256) * -(-N // 128)
+    return "256,256,4,2" if big >= 256 else ("256,128,2,2" if mid >= 256 else "128,128,2,2")
+
+
+class Step:
+    """Buffers and calls of one training step; every call goes to libforge."""
+
+    def __init__(self, cfg, stream):
+        import torch
+        from paper_2609_13645_amd import _lib, runtime
+        self.cfg, self.stream, self.lib = cfg, stream, _lib
+        if is_model(cfg):
+            inp = fi.model_inputs(cfg)
+            self.model = runtime.Model(cfg, inp, stream=stream)
+            self.flat = self.model.flat
+        else:
+            inp = fi.layer_inputs(cfg)
+            self.flat = runtime.FlatParams(runtime.layer_shapes(cfg))
+            self.layer = runtime.Layer(cfg, inp["weights"], flat=self.flat, stream=stream)
+            self.x = runtime.to_device_bf16(inp["x"])
+            self.dy = runtime.to_device_bf16(inp["dy"])
+            self.out = torch.empty_like(self.x)
+            self.dx = torch.empty_like(self.x)
+        self.hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"],
+                                    cfg["weight_decay"])
+        self.scal = torch.zeros(4, dtype=torch.float32, device="cuda")
+        self.host_scal = torch.zeros(4, dtype=torch.float32).pin_memory()
+        self.t = 0
+
+    def zero(self):
+        self.flat.grad.zero_()
+        if self.cfg["n_experts"] and not is_model(self.cfg):
+            self.layer.aux.zero_()
+
+    def fwd(self):
+        if is_model(self.cfg):
+            self.model.forward_backward()       # the head fuses loss fwd and bwd
+        else:
+            self.layer.fwd(self.x, self.out)
+
+    def bwd(self):
+        if not is_model(self.cfg):
+            self.layer.bwd(self.x, self.dy, self.dx)
+
+    def adamw(self):
+        import torch
+        self.t += 1
+        c = self.cfg
+        self.host_scal.copy_(torch.tensor([c["lr"], 1 - c["beta1"] ** self.t,
+                                           1 - c["beta2"] ** self.t, 1.0]))
+        self.scal.copy_(self.host_scal, non_blocking=True)
+        f = self.flat
+        self.lib.forge_adamw_step(f.master, f.param, f.grad, f.m, f.v, f.n, self.hp,
+                                  self.scal, self.stream)
+
+    def __call__(self):
+        self.zero()
+        self.fwd()
+        self.bwd()
+        self.adamw()
+
+    def finite(self):
+        import torch
+        ok = bool(torch.isfinite(self.flat.master).all())
+        if is_model(self.cfg):
+            return ok and bool(torch.isfinite(self.model.loss).all())
+        return ok and bool(torch.isfinite(self.out.float()).all())
+
+
+def dominant_kernel(cfg, stream, step, reps):
+    """The largest single launch of the step, run alone on the step's stream:
+    the gate/up projection GEMM of a dense layer, the grouped gate/up GEMM of
+    the MoE layer over the routed rows, the LM-head logits GEMM of a model."""
+    import torch
+    from paper_2609_13645_amd import _lib
+    T, h = fi.tokens(cfg), cfg["hidden"]
+    if cfg["n_experts"]:
+        E, k, fe = cfg["n_experts"], cfg["top_k"], cfg["expert_ffn"]
+        # routed row groups from the workload's N(0, 1) router logits
+        lg = torch.from_numpy(fi.router_logits(T, E, seed=cfg["seed"])).cuda()
+        d = lambda shape, dt: torch.empty(shape, dtype=dt, device="cuda")
+        idx, gates, probs = d((T, k), torch.int32), d((T, k), torch.float32), d((T, E), torch.float32)
+        counts, offsets, perm = d(E, torch.int32), d(E + 1, torch.int32), d(T * k, torch.int32)
+        ws = d(_lib.forge_moe_route_workspace_bytes(T, E, k), torch.uint8)
+        _lib.forge_moe_route(lg, T, E, k, idx, gates, probs, counts, offsets, perm, ws, stream)
+        rows = T * k
+        A = torch.randn((rows, h), device="cuda").to(torch.bfloat16)
+        C = torch.empty((rows, 2 * fe), dtype=torch.bfloat16, device="cuda")
+        W = step.layer.w["w_gate_up_e"]
+
+        def launch():
+            _lib.forge_gemm_grouped_rows(_lib.GEMM_KC, A, W, C, offsets, E, rows, 2 * fe, h,
+                                         h, h, 2 * fe, 2 * fe * h, stream)
+        flop = 2.0 * rows * 2 * fe * h
+        name = "gemm_kernel<256,256,4,2,KC,KC,StoreBF16,grouped rows> (expert gate/up fwd)"
+        shape = f"rows={rows} E={E} N={2 * fe} K={h}"
+    elif is_model(cfg):
+        V = cfg["vocab"]
+        A = torch.randn((T, h), device="cuda").to(torch.bfloat16)
+        C = torch.empty((T, V), dtype=torch.bfloat16, device="cuda")
+        W = step.model.w_lm(step.flat.param)
+
+        def launch():
+            _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
+                            T, V, h, h, h, V, 0, stream)
+        flop = 2.0 * T * V * h
+        name = f"gemm_kernel<{tile_name(T, V)},KC,KC,StoreBF16> (LM-head logits)"
+        shape = f"M={T} N={V} K={h}"
+    else:
+        f = cfg["ffn"]
+        A = torch.randn((T, h), device="cuda").to(torch.bfloat16)
+        C = torch.empty((T, 2 * f), dtype=torch.bfloat16, device="cuda")
+        W = step.layer.w["w_gate_up"]
+
+        def launch():
+            _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
+                            T, 2 * f, h, h, h, 2 * f, 0, stream)
+        flop = 2.0 * T * 2 * f * h
+        name = f"gemm_kernel<{tile_name(T, 2 * f)},KC,KC,StoreBF16> (gate/up fwd)"
+        shape = f"M={T} N={2 * f} K={h}"
+    for _ in range(3):
+        launch()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return {"name": name, "shape": shape, "avg_us": e0.elapsed_time(e1) / reps * 1e3,
+            "flop_per_launch": flop}
+
+
 def gpu_step_bench(cfg, steps, warmup, kernel_reps):
     import torch
-    from paper_2609_13645_amd import _lib, runtime
-
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-    inp = fi.layer_inputs(cfg)
-    flat = runtime.FlatParams(runtime.layer_shapes(cfg))
-    layer = runtime.Layer(cfg, inp["weights"], flat=flat, stream=stream)
-    x = runtime.to_device_bf16(inp["x"])
-    dy = runtime.to_device_bf16(inp["dy"])
-    out = torch.empty_like(x)
-    dx = torch.empty_like(x)
-    hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"])
-    scal = torch.zeros(4, dtype=torch.float32, device="cuda")
-    host_scal = torch.zeros(4, dtype=torch.float32).pin_memory()
-    step_no = [0]
-
-    def step():
-        step_no[0] += 1
-        t = step_no[0]
-        host_scal.copy_(torch.tensor([cfg["lr"], 1 - cfg["beta1"] ** t,
-                                      1 - cfg["beta2"] ** t, 1.0]))
-        scal.copy_(host_scal, non_blocking=True)
-        flat.grad.zero_()
-        layer.fwd(x, out)
-        layer.bwd(x, dy, dx)
-        _lib.forge_adamw_step(flat.master, flat.param, flat.grad, flat.m, flat.v, flat.n,
-                              hp, scal, stream)
-
+    step = Step(cfg, stream)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -94,90 +220,93 @@ def gpu_step_bench(cfg, steps, warmup, kernel_reps):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    assert torch.isfinite(out.float()).all() and torch.isfinite(flat.master).all()
+    assert step.finite(), "non-finite output or master weights"
 
-    # phase split (separate pass, not part of the headline number)
+    # phase split (separate pass, not part of the headline number); a model's
+    # forward and backward are one call (the loss head fuses them)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     phases = {"fwd": 0.0, "bwd": 0.0, "adamw": 0.0}
     reps = max(3, min(steps, 10))
     for _ in range(reps):
-        flat.grad.zero_()
+        step.zero()
         ev[0].record(stream)
-        layer.fwd(x, out)
+        step.fwd()
         ev[1].record(stream)
-        layer.bwd(x, dy, dx)
+        step.bwd()
         ev[2].record(stream)
-        _lib.forge_adamw_step(flat.master, flat.param, flat.grad, flat.m, flat.v, flat.n,
-                              hp, scal, stream)
+        step.adamw()
         ev[3].record(stream)
         torch.cuda.synchronize()
         phases["fwd"] += ev[0].elapsed_time(ev[1]) / reps
         phases["bwd"] += ev[1].elapsed_time(ev[2]) / reps
         phases["adamw"] += ev[2].elapsed_time(ev[3]) / reps
-
-    # dominant kernel: the gate/up projection GEMM (largest single launch of
-    # the step, y = b W_gu^T, M = T, N = 2f, K = h), run alone on the step's
-    # stream on buffers of its shape
-    T, h, f = fi.tokens(cfg), cfg["hidden"], cfg["ffn"]
-    A = torch.randn((T, h), device="cuda").to(torch.bfloat16)
-    C = torch.empty((T, 2 * f), dtype=torch.bfloat16, device="cuda")
-    Wgu = layer.w["w_gate_up"]
-
-    def gemm():
-        _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, Wgu, C, None,
-                        T, 2 * f, h, h, h, 2 * f, 0, stream)
-
-    for _ in range(3):
-        gemm()
-    e0.record(stream)
-    for _ in range(kernel_reps):
-        gemm()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    k_ms = e0.elapsed_time(e1) / kernel_reps
-    k_flop = 2.0 * T * (2 * f) * h
-    kernel = {"name": "gemm_kernel<256,256,4,2,KC,KC,StoreBF16> (gate/up fwd)",
-              "shape": f"M={T} N={2 * f} K={h}", "avg_us": k_ms * 1e3,
-              "flop_per_launch": k_flop}
-    return ms, phases, kernel, flat.n
+    if is_model(cfg):
+        phases = {"fwd_bwd": phases["fwd"] + phases["bwd"], "adamw": phases["adamw"]}
+    kernel = dominant_kernel(cfg, stream, step, kernel_reps)
+    return ms, phases, kernel, step.flat.n
 
 
 def cpu_baseline(cfg, seq):
     """The fp64 oracle (as it stands) on a bounded sample of the workload."""
-    from oracle import dense, adamw as oadam
+    from oracle import dense, moe, head, adamw as oadam
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
         threads = _CORES
-    c = dict(cfg, seq=seq)
-    inp = fi.layer_inputs(c)
-    W = {k: fi.bf16_bits_to_f64(v) for k, v in inp["weights"].items()}
-    x = fi.bf16_bits_to_f64(inp["x"])
-    dy = fi.bf16_bits_to_f64(inp["dy"])
-    frac = seq / cfg["seq"]
-    t0 = time.perf_counter()
-    out, cache = dense.layer_fwd(x, W, c)
-    _, grads = dense.layer_bwd(cache, W, c, dy)
-    # the optimizer over the same fraction of the parameters (a prefix of them)
-    budget = int(round(frac * sum(w.size for w in W.values())))
+    f64 = fi.bf16_bits_to_f64
+    if is_model(cfg):
+        # one layer of the model at one sequence of the batch (plus the full head)
+        c = dict(cfg, n_layers=1, batch=1)
+        inp = fi.model_inputs(c)
+        P = {"embedding": f64(inp["embedding"]), "final_norm": f64(inp["final_norm"]),
+             "w_lm": None if inp["w_lm"] is None else f64(inp["w_lm"]),
+             "layers": [{k: f64(v) for k, v in W.items()} for W in inp["layers"]]}
+        n_params = sum(v.size for v in P["layers"][0].values()) + P["embedding"].size
+        t0 = time.perf_counter()
+        _, grads = head.model_fwd_bwd(P, inp["ids"], inp["targets"], c)
+        flat_p = [P["embedding"]] + list(P["layers"][0].values())
+        flat_g = [grads["embedding"]] + [grads["layers"][0][k] for k in P["layers"][0]]
+        sample = (f"fp64 oracle: 1 of {cfg['n_layers']} layers, 1 of {cfg['batch']} "
+                  f"sequences ({c['seq']} tokens), full LM head and CE, AdamW over that "
+                  f"layer and the embedding")
+    else:
+        seq = min(seq, cfg["seq"])
+        c = dict(cfg, seq=seq, batch=1)
+        inp = fi.layer_inputs(c)
+        W = {k: f64(v) for k, v in inp["weights"].items()}
+        x, dy = f64(inp["x"]), f64(inp["dy"])
+        n_params = sum(w.size for w in W.values())
+        t0 = time.perf_counter()
+        if cfg["n_experts"]:
+            _, _, cache = moe.layer_fwd(x, W, c)
+            _, grads = moe.layer_bwd(cache, W, c, dy)
+        else:
+            _, cache = dense.layer_fwd(x, W, c)
+            _, grads = dense.layer_bwd(cache, W, c, dy)
+        flat_p = list(W.values())
+        flat_g = [grads[k] for k in W]
+        sample = (f"fp64 oracle: fwd+bwd of the same layer shapes over {seq} tokens "
+                  f"(one sequence; the workload has {cfg['batch']} x {cfg['seq']})")
+    # the optimizer over the same fraction of the parameters as the sample's
+    # share of the step's tokens
+    frac = fi.tokens(c) / fi.tokens(cfg)
+    budget = int(round(frac * n_params))
     n_opt = 0
-    for name, g in grads.items():
+    for p, g in zip(flat_p, flat_g):
         if budget <= 0:
             break
         k = min(budget, g.size)
-        p, gg = W[name].reshape(-1)[:k], g.reshape(-1)[:k]
-        oadam.adamw_step(p, gg, np.zeros_like(p), np.zeros_like(p), cfg["lr"], cfg["beta1"],
-                         cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"], 1)
+        pp, gg = p.reshape(-1)[:k], g.reshape(-1)[:k]
+        oadam.adamw_step(pp, gg, np.zeros_like(pp), np.zeros_like(pp), cfg["lr"],
+                         cfg["beta1"], cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"], 1)
         budget -= k
         n_opt += k
     dt = time.perf_counter() - t0
     model_flop = flops.step_flops(c)
     return {"value": model_flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": (f"fp64 oracle, {frac:.3f} of one step of the same 8B-shape layer: "
-                       f"fwd+bwd over the first {seq} of the 4096 tokens, AdamW over "
-                       f"{n_opt / 1e6:.1f}M of the 218.1M params; {dt:.1f} s for "
+            "sample": (f"{sample}; AdamW over {n_opt / 1e6:.1f}M params; {dt:.1f} s for "
                        f"{model_flop / 1e12:.3f} TFLOP of model work"),
             "seconds": dt}
 
@@ -212,19 +341,20 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build runs one decoder-layer step on one "
+        print("bench.py measures one GPU: this build runs the training step on one "
               "MI355X and has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
         sys.exit(2)
     cfg = fi.config(args.workload)
     T = fi.tokens(cfg)
     step_flop = flops.step_flops(cfg)
-    print(f"[bench] workload {args.workload}: T={T} h={cfg['hidden']} f={cfg['ffn']} "
+    print(f"[bench] workload {args.workload}: {DESCRIPTION[args.workload]}; "
           f"warmup={args.warmup} steps={args.steps}", file=sys.stderr, flush=True)
     ms, phases, kernel, nparams = gpu_step_bench(cfg, args.steps, args.warmup,
                                                  args.kernel_reps)
     tflops = step_flop / (ms * 1e-3) / 1e12
     print(f"[bench] {ms:.3f} ms/step, {tflops:.1f} TFLOP/s; phases {phases}",
           file=sys.stderr, flush=True)
+    fb_ms = sum(v for k, v in phases.items() if k != "adamw")
     k_tf = kernel["flop_per_launch"] / (kernel["avg_us"] * 1e-6) / 1e12
     res = {
         "metric": METRIC,
@@ -240,23 +370,30 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "mfu_pct": round(100.0 * tflops / MFU_PEAK_TFLOPS, 2),
-        "mfu_fwd_bwd_pct": round(100.0 * step_flop / ((phases["fwd"] + phases["bwd"]) * 1e-3)
-                                 / 1e12 / MFU_PEAK_TFLOPS, 2),
+        "mfu_fwd_bwd_pct": round(100.0 * step_flop / (fb_ms * 1e-3) / 1e12 / MFU_PEAK_TFLOPS, 2),
         "tokens_per_s": round(T / (ms * 1e-3), 1),
         "phases_ms": {k: round(v, 4) for k, v in phases.items()},
-        "config": {"workload": args.workload, "batch": cfg["batch"], "seq": cfg["seq"],
-                   "hidden": cfg["hidden"], "n_heads": cfg["n_heads"],
-                   "n_kv_heads": cfg["n_kv_heads"], "head_dim": cfg["head_dim"],
-                   "ffn": cfg["ffn"], "params": nparams,
+        "config": {"workload": args.workload, "description": DESCRIPTION[args.workload],
+                   "batch": cfg["batch"], "seq": cfg["seq"], "hidden": cfg["hidden"],
+                   "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"],
+                   "head_dim": cfg["head_dim"], "ffn": cfg["ffn"], "params": nparams,
                    "model_flop_per_step": step_flop},
         "roofline": {"bound": "mfma", "kernel": kernel["name"], "shape": kernel["shape"],
                      "achieved": round(k_tf, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(k_tf / PEAK_BF16_TFLOPS, 4),
                      "avg_us": round(kernel["avg_us"], 2), "traffic": None},
     }
+    if cfg["n_experts"]:
+        res["config"].update(n_experts=cfg["n_experts"], top_k=cfg["top_k"],
+                             expert_ffn=cfg["expert_ffn"], aux_coef=cfg["aux_coef"])
+    if is_model(cfg):
+        res["config"].update(n_layers=cfg["n_layers"], vocab=cfg["vocab"], tied=cfg["tied"])
+    if cfg["recompute_attn"]:
+        hw = step_flop + flops.recompute_flops(cfg)
+        res["hfu_pct"] = round(100.0 * hw / (ms * 1e-3) / 1e12 / MFU_PEAK_TFLOPS, 2)
+        res["config"]["recompute_attn"] = 1
     if not args.no_cpu_baseline:
-        print(f"[bench] cpu baseline: oracle on {args.cpu_seq} tokens ...", file=sys.stderr,
-              flush=True)
+        print(f"[bench] cpu baseline: oracle sample ...", file=sys.stderr, flush=True)
         cb = cpu_baseline(cfg, args.cpu_seq)
         res["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)
                                for k, v in cb.items() if k != "seconds"}

@@ -313,6 +313,43 @@ forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
                         int64_t lda, int64_t ldb, int64_t ldc, int64_t ldr,
                         forge_stream stream);
 
+/*
+ * Grouped products over row groups: the per-expert projections of a routed
+ * mixture-of-experts FFN (App. B, MoE configurations), whose routed rows are
+ * stored expert-major so that group e owns rows [offsets[e], offsets[e+1]).
+ * offsets: device int32 [groups + 1] with offsets[0] = 0, non-decreasing and
+ * offsets[groups] <= rows. The offsets are read on the device and not
+ * checked: rows beyond `rows` are not computed, and every operand must hold
+ * the rows the offsets name. An empty group contributes nothing.
+ *
+ * forge_gemm_grouped_rows: for r in group e,
+ *   C[r][n] = sum_k A[r][k] B_e(k, n)   (bf16 out, fp32 accumulation)
+ * with B_e = B + e * stride_b, layout_b KC: B_e(k,n) = B_e[n*ldb + k]
+ * (y = x W_e^T, W_e [N, K]) or MC: B_e(k,n) = B_e[k*ldb + n] (dX = dY W_e).
+ * Rules (else INVALID_ARG): K % 8 == 0 (K > 0 for KC); N % 8 == 0 for MC;
+ * lda >= K, ldb >= K (KC) or N (MC), ldc >= N; every leading dimension and
+ * stride_b a multiple of 8. Pointers 16-byte aligned (ALIGNMENT).
+ */
+forge_status forge_gemm_grouped_rows(int32_t layout_b, const forge_bf16* A, const forge_bf16* B,
+                                     forge_bf16* C, const int32_t* offsets, int32_t groups,
+                                     int32_t rows, int32_t N, int32_t K, int64_t lda,
+                                     int64_t ldb, int64_t ldc, int64_t stride_b,
+                                     forge_stream stream);
+
+/*
+ * forge_gemm_grouped_wgrad: the per-expert weight gradients, for each group e
+ *   C_e[m][n] += sum over rows r of group e of A[r][m] B[r][n]
+ * with A [rows, M] (lda), B [rows, N] (ldb) bf16 and C_e = C + e * stride_c
+ * fp32 [M, N] (ldc), accumulated (+=; the caller zeroes). Rules (else
+ * INVALID_ARG): M, N multiples of 8; lda >= M, ldb >= N, ldc >= N, all and
+ * stride_c multiples of 8; stride_c >= (M - 1) * ldc + N (groups do not
+ * overlap). Deterministic (one workgroup owns each output tile).
+ */
+forge_status forge_gemm_grouped_wgrad(const forge_bf16* A, const forge_bf16* B, float* C,
+                                      const int32_t* offsets, int32_t groups, int32_t M,
+                                      int32_t N, int64_t lda, int64_t ldb, int64_t ldc,
+                                      int64_t stride_c, forge_stream stream);
+
 typedef struct {
   int32_t batch, seq, n_heads, n_kv_heads, head_dim;
 } forge_attn_cfg;

@@ -109,6 +109,10 @@ def load():
         "forge_clip_coeff": (ctypes.c_int, [P, F32, F32, P, P]),
         "forge_gemm": (ctypes.c_int, [I32, I32, I32, P, P, P, P, I32, I32, I32,
                                       I64, I64, I64, I64, P]),
+        "forge_gemm_grouped_rows": (ctypes.c_int, [I32, P, P, P, P, I32, I32, I32, I32,
+                                                   I64, I64, I64, I64, P]),
+        "forge_gemm_grouped_wgrad": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I64, I64,
+                                                    I64, I64, P]),
         "forge_attention_fwd": (ctypes.c_int, [ctypes.POINTER(AttnCfg), P, P, P, P]),
         "forge_attention_bwd_workspace_bytes": (ctypes.c_int,
                                                 [ctypes.POINTER(AttnCfg), SZ]),
@@ -258,6 +262,19 @@ def forge_gemm(layout_a, layout_b, epilogue, A, B, C, R, M, N, K, lda, ldb, ldc,
                stream=None):
     _check(load().forge_gemm(layout_a, layout_b, epilogue, _ptr(A), _ptr(B), _ptr(C),
                              _ptr(R), M, N, K, lda, ldb, ldc, ldr, _stream(stream)))
+
+
+def forge_gemm_grouped_rows(layout_b, A, B, C, offsets, groups, rows, N, K, lda, ldb, ldc,
+                            stride_b, stream=None):
+    _check(load().forge_gemm_grouped_rows(layout_b, _ptr(A), _ptr(B), _ptr(C), _ptr(offsets),
+                                          groups, rows, N, K, lda, ldb, ldc, stride_b,
+                                          _stream(stream)))
+
+
+def forge_gemm_grouped_wgrad(A, B, C, offsets, groups, M, N, lda, ldb, ldc, stride_c,
+                             stream=None):
+    _check(load().forge_gemm_grouped_wgrad(_ptr(A), _ptr(B), _ptr(C), _ptr(offsets), groups,
+                                           M, N, lda, ldb, ldc, stride_c, _stream(stream)))
 
 
 def forge_attention_fwd(cfg: AttnCfg, qkv, o, lse, stream=None):

@@ -839,6 +839,60 @@ forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
   return ok();
 }
 
+forge_status forge_gemm_grouped_rows(int32_t layout_b, const forge_bf16* A, const forge_bf16* B,
+                                     forge_bf16* C, const int32_t* offsets, int32_t groups,
+                                     int32_t rows, int32_t N, int32_t K, int64_t lda,
+                                     int64_t ldb, int64_t ldc, int64_t stride_b,
+                                     forge_stream stream) {
+  FORGE_CHECK(layout_b == FORGE_GEMM_KC || layout_b == FORGE_GEMM_MC, FORGE_ERR_INVALID_ARG,
+              "bad layout_b");
+  FORGE_CHECK(groups >= 0 && rows >= 0 && N >= 0 && K >= 0, FORGE_ERR_INVALID_ARG,
+              "negative size");
+  if (groups == 0 || rows == 0 || N == 0) return ok();
+  FORGE_PTR(A);
+  FORGE_PTR(B);
+  FORGE_PTR(C);
+  FORGE_PTR(offsets);
+  FORGE_CHECK(K % 8 == 0, FORGE_ERR_INVALID_ARG, "K-contiguous A needs K %% 8 == 0");
+  FORGE_CHECK(layout_b == FORGE_GEMM_MC || K > 0, FORGE_ERR_INVALID_ARG, "K must be > 0");
+  FORGE_CHECK(layout_b == FORGE_GEMM_KC || N % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "N-contiguous B needs N %% 8 == 0");
+  FORGE_CHECK(lda % 8 == 0 && ldb % 8 == 0 && ldc % 8 == 0 && stride_b % 8 == 0,
+              FORGE_ERR_INVALID_ARG, "leading dimensions and stride_b must be multiples of 8");
+  FORGE_CHECK(lda >= K && ldb >= (layout_b == FORGE_GEMM_KC ? K : N) && ldc >= N,
+              FORGE_ERR_INVALID_ARG, "leading dimension smaller than the contiguous extent");
+  FORGE_CHECK(stride_b >= 0, FORGE_ERR_INVALID_ARG, "negative stride_b");
+  FORGE_CHECK((int64_t)rows * ldc < (1LL << 40) && (int64_t)rows * lda < (1LL << 40),
+              FORGE_ERR_INVALID_ARG, "operand too large");
+  GemmArgs g = grouped(gargs(A, lda, B, ldb, C, ldc, rows, N, K), offsets, groups, stride_b, 0);
+  FORGE_HIP(forge::gemm_grouped_m((forge::GemmLayout)layout_b, forge::kStoreBF16, g,
+                                  (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_gemm_grouped_wgrad(const forge_bf16* A, const forge_bf16* B, float* C,
+                                      const int32_t* offsets, int32_t groups, int32_t M,
+                                      int32_t N, int64_t lda, int64_t ldb, int64_t ldc,
+                                      int64_t stride_c, forge_stream stream) {
+  FORGE_CHECK(groups >= 0 && M >= 0 && N >= 0, FORGE_ERR_INVALID_ARG, "negative size");
+  if (groups == 0 || M == 0 || N == 0) return ok();
+  FORGE_PTR(A);
+  FORGE_PTR(B);
+  FORGE_PTR(C);
+  FORGE_PTR(offsets);
+  FORGE_CHECK(M % 8 == 0 && N % 8 == 0, FORGE_ERR_INVALID_ARG, "M and N must be multiples of 8");
+  FORGE_CHECK(lda % 8 == 0 && ldb % 8 == 0 && ldc % 8 == 0 && stride_c % 8 == 0,
+              FORGE_ERR_INVALID_ARG, "leading dimensions and stride_c must be multiples of 8");
+  FORGE_CHECK(lda >= M && ldb >= N && ldc >= N, FORGE_ERR_INVALID_ARG,
+              "leading dimension smaller than the contiguous extent");
+  FORGE_CHECK(stride_c >= (int64_t)(M - 1) * ldc + N, FORGE_ERR_INVALID_ARG,
+              "stride_c smaller than one group's output: groups would overlap");
+  FORGE_CHECK((int64_t)groups * stride_c < (1LL << 40), FORGE_ERR_INVALID_ARG, "C too large");
+  GemmArgs g = grouped(gargs(A, lda, B, ldb, C, ldc, M, N, 0), offsets, groups, 0, stride_c);
+  FORGE_HIP(forge::gemm_grouped_k(forge::kAccF32, g, (hipStream_t)stream));
+  return ok();
+}
+
 namespace {
 forge_status check_attn(const forge_attn_cfg* c) {
   FORGE_CHECK(c != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");

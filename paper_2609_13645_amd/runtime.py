@@ -195,6 +195,9 @@ class Model:
         self.grad_a = torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
         self.grad_b = torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
         self.loss = torch.zeros(1, dtype=torch.float32, device=device)
+        # MoE layers add their load-balance losses here (their gradients are
+        # part of each layer's backward); the reported loss is the CE alone
+        self.aux = torch.zeros(1, dtype=torch.float32, device=device)
         self.scalars = torch.zeros(4, dtype=torch.float32, device=device)
         self.hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"],
                                     cfg["weight_decay"])
@@ -204,13 +207,16 @@ class Model:
         return self.flat.view(buf, "embedding" if self.tied else "w_lm")
 
     def forward_backward(self):
-        """Loss (device scalar) and every gradient accumulated into flat.grad."""
+        """Cross-entropy loss (device scalar) and every gradient accumulated
+        into flat.grad; for MoE layers self.aux holds the summed aux losses."""
         c, s = self.cfg, self.stream
         T, h, V = self.T, c["hidden"], c["vocab"]
         emb = self.flat.view(self.flat.param, "embedding")
         _lib.forge_embed_fwd(self.ids, emb, self.acts[0], T, h, V, s)
+        if c.get("n_experts", 0):
+            self.aux.zero_()
         for i, ly in enumerate(self.layers):
-            ly.fwd(self.acts[i], self.acts[i + 1])
+            ly.fwd(self.acts[i], self.acts[i + 1], aux=self.aux)
         _lib.forge_loss_fwd_bwd(self.head, self.acts[-1],
                                 self.flat.view(self.flat.param, "final_norm"),
                                 self.w_lm(self.flat.param), self.targets, self.loss,

@@ -89,6 +89,29 @@ def test_gemm_argument_rules():
     _lib.forge_gemm(0, 0, 0, None, None, None, None, 0, 8, 8, 8, 8, 8, 0, 0)
 
 
+def test_grouped_gemm_argument_rules():
+    def status(fn, *a):
+        with pytest.raises(_lib.ForgeError) as e:
+            fn(*a)
+        return e.value.status
+    rows, wgrad = _lib.forge_gemm_grouped_rows, _lib.forge_gemm_grouped_wgrad
+    P = (0x1000, 0x2000, 0x3000, 0x4000)
+    assert status(rows, 2, *P, 4, 64, 16, 16, 16, 16, 16, 256, 0) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(rows, 0, *P, 4, 64, 16, 12, 12, 12, 16, 192, 0) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(rows, 1, *P, 4, 64, 12, 16, 16, 16, 16, 192, 0) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(rows, 0, 0x1000, 0x2008, 0x3000, 0x4000, 4, 64, 16, 16, 16, 16, 16, 256,
+                  0) == _lib.FORGE_ERR_ALIGNMENT
+    assert status(rows, 0, *P, 4, 64, 16, 16, 16, 16, 16, 252, 0) == _lib.FORGE_ERR_INVALID_ARG
+    # per-group outputs may not overlap
+    assert status(wgrad, *P, 4, 16, 16, 16, 16, 16, 128, 0) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(wgrad, *P, 4, 12, 16, 16, 16, 16, 256, 0) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(wgrad, 0x1000, None, 0x3000, 0x4000, 4, 16, 16, 16, 16, 16, 256,
+                  0) == _lib.FORGE_ERR_INVALID_ARG
+    # nothing to do: OK without launching
+    rows(0, None, None, None, None, 0, 64, 16, 16, 16, 16, 16, 256, 0)
+    wgrad(None, None, None, None, 4, 0, 16, 16, 16, 16, 256, 0)
+
+
 def test_optimizer_argument_rules():
     hp = _lib.AdamwHparams(0.9, 1.5, 1e-8, 0.1)
     with pytest.raises(_lib.ForgeError):

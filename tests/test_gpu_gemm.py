@@ -91,3 +91,56 @@ def test_gemm_zero_k_and_empty():
     assert np.array_equal(got, ref)
     got, ref = run_gemm(MC, MC, STORE_F32, 16, 24, 0)
     assert np.array_equal(got, np.zeros_like(ref))
+
+
+GROUP_SIZES = [0, 37, 256, 1, 300, 0, 129, 8, 513]
+
+
+@pytest.mark.parametrize("lb", [KC, MC])
+@pytest.mark.parametrize("N,K", [(136, 64), (264, 200)])
+def test_grouped_rows_integer_exact(lb, N, K):
+    """Per-group products over expert-major rows, ragged and empty groups;
+    rows past the last offset are never written."""
+    import torch
+    from paper_2609_13645_amd import _lib
+    banner(f"grouped rows lb={lb} N={N} K={K}")
+    rng = np.random.default_rng(N + K + lb)
+    off = np.concatenate([[0], np.cumsum(GROUP_SIZES)]).astype(np.int32)
+    G, rows = len(GROUP_SIZES), int(off[-1]) + 40          # a slack of unused rows
+    A = rng.integers(-4, 5, size=(rows, K)).astype(np.float32)
+    B = rng.integers(-4, 5, size=(G, N, K) if lb == KC else (G, K, N)).astype(np.float32)
+    C = torch.full((rows, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    _lib.forge_gemm_grouped_rows(lb, dev_bf16(fi.to_bf16_bits(A)), dev_bf16(fi.to_bf16_bits(B)),
+                                 C, torch.from_numpy(off).cuda(), G, rows, N, K, K,
+                                 K if lb == KC else N, N, N * K)
+    torch.cuda.synchronize()
+    got = host_f64(C)
+    for e in range(G):
+        r0, r1 = off[e], off[e + 1]
+        Be = B[e].T if lb == KC else B[e]
+        want = A[r0:r1].astype(np.float64) @ Be
+        assert np.array_equal(got[r0:r1], fi.bf16_bits_to_f64(fi.to_bf16_bits(want.astype(np.float32)))), e
+    assert np.all(np.isnan(got[off[-1]:]))
+
+
+@pytest.mark.parametrize("M,N", [(64, 136), (264, 128)])
+def test_grouped_wgrad_integer_exact(M, N):
+    """C_e += A_e^T B_e over each group's rows; empty groups leave C_e as is."""
+    import torch
+    from paper_2609_13645_amd import _lib
+    banner(f"grouped wgrad M={M} N={N}")
+    rng = np.random.default_rng(M * N)
+    off = np.concatenate([[0], np.cumsum(GROUP_SIZES)]).astype(np.int32)
+    G, rows = len(GROUP_SIZES), int(off[-1])
+    A = rng.integers(-4, 5, size=(rows, M)).astype(np.float32)
+    B = rng.integers(-4, 5, size=(rows, N)).astype(np.float32)
+    init = rng.integers(-8, 9, size=(G, M, N)).astype(np.float32)
+    C = torch.from_numpy(init).cuda()
+    _lib.forge_gemm_grouped_wgrad(dev_bf16(fi.to_bf16_bits(A)), dev_bf16(fi.to_bf16_bits(B)), C,
+                                  torch.from_numpy(off).cuda(), G, M, N, M, N, N, M * N)
+    torch.cuda.synchronize()
+    got = host_f64(C)
+    for e in range(G):
+        r0, r1 = off[e], off[e + 1]
+        want = init[e] + A[r0:r1].T.astype(np.float64) @ B[r0:r1]
+        assert np.array_equal(got[e], want), e
