@@ -173,7 +173,7 @@ Saved saved_layout(const forge_layer_cfg& c) {
 // ---- workspace -------------------------------------------------------------
 struct Work {
   size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv;
-  size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs;  // MoE
+  size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs, wpart;  // MoE
   size_t total;
 };
 
@@ -190,12 +190,14 @@ Work work_layout(const forge_layer_cfg& c) {
     w.dgu = take(d.R * 2 * d.fe * 2);
     w.logits = take(d.T * d.E * 4);
     w.blk = take((size_t)forge::moe_sort_blocks((int)d.T) * d.E * 4);
-    w.colsum = take(d.E * 4);
+    w.colsum = take((1 + (size_t)forge::moe_aux_blocks((int)d.T)) * d.E * 4);
     w.dys = take(d.R * d.h * 2);
     w.dxs = take(d.R * d.h * 2);
     w.dgate = take(d.R * 4);
     w.dl = take(d.T * d.E * 2);
     w.dbs = take(d.T * d.h * 2);
+    const int rs = forge::splitk_splits((int)d.E, (int)d.h, (int)d.T);
+    w.wpart = rs > 1 ? take((size_t)rs * d.E * d.h * 4) : 0;
   }
   w.db = take(d.T * d.h * 2);
   w.dh1 = take(d.T * d.h * 2);
@@ -442,8 +444,10 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
   FORGE_HIP(forge::moe_router_bwd(probs, idx, dgate, counts, T, E, k, c.aux_coef, dl, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kResidBF16,
                         gargs(dl, d.E, w->w_router, d.h, db, d.h, d.T, d.h, d.E, dbs, d.h), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(dl, d.E, bn, d.h, g->d_w_router, d.h, d.E, d.h, d.T), s));
+  // router weight gradient: 64 x h output tiles over T tokens, split over T
+  FORGE_HIP(forge::gemm_wgrad_splitk(gargs(dl, d.E, bn, d.h, g->d_w_router, d.h, d.E, d.h, d.T),
+                                     forge::splitk_splits((int)d.E, (int)d.h, (int)d.T),
+                                     at<float>(workspace, wk.wpart), s));
   return FORGE_OK;
 }
 

@@ -7,7 +7,8 @@
 // over tokens). One kernel template covers all three:
 //
 //  * A block tile BM x BN x 64 is staged through LDS, double-buffered, with
-//    one barrier per k-step. Tiles are filled by buffer_load ... lds (global
+//    one barrier per k-step, placed before the step's last 16-deep slice so
+//    that MFMAs are ready to issue as the waves leave it. Tiles are filled by buffer_load ... lds (global
 //    to LDS without registers); out-of-range chunks read as zeros through the
 //    buffer descriptor's range check, so ragged edges need no branches.
 //  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
@@ -217,6 +218,20 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     p.B += (long)e * p.strideB;
     p.C = (char*)p.C + r0 * p.ldc * (EPI == kStoreBF16 || EPI == kResidBF16 ? 2 : 4);
     if (EPI == kResidBF16) p.R += r0 * p.ldr;
+  } else if (GROUP == 3) {
+    // uniform split of the reduction: split e covers k rows [e * ks, e * ks + ks)
+    // (ks = p.strideB) and stores its partial product to C + e * strideC
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int e = blockIdx.x / (tiles_m * tiles_n);
+    const int t = blockIdx.x % (tiles_m * tiles_n);
+    tm = t / tiles_n;
+    tn = t % tiles_n;
+    const long k0 = (long)e * p.strideB;
+    p.K = (int)min((long)p.K - k0, p.strideB);
+    p.A += k0 * p.lda;  // both operands M/N-contiguous: k rows
+    p.B += k0 * p.ldb;
+    p.C = (char*)p.C + (long)e * p.strideC * 4;
   } else {
     // K-grouped: one (m, n) tile grid per group, reduction over the group's rows
     const int tiles_m = (p.M + BM - 1) / BM;
@@ -249,42 +264,55 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+  // ---- main loop: the barrier that publishes tile t+1 sits before the last
+  // 16-deep k-slice of tile t, so every wave leaves it with that slice's
+  // MFMAs to issue while the first fragments of tile t+1 are read.
   const int nk = (p.K + BK - 1) / BK;
+  constexpr int KS = BK / 16;
   la.load(p.A, p.lda, m0, p.M, 0, p.K, lds[0], wave, lane);
   lb.load(p.B, p.ldb, n0, p.N, 0, p.K, lds[0] + A_ELEMS, wave, lane);
   __syncthreads();
+  bf16x8_t fa[2][FN], fb[2][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i) fa[0][i] = frag<LB, BN>(lds[0] + A_ELEMS, wn * WN + i * 32, 0, lane);
+#pragma unroll
+  for (int j = 0; j < FM; ++j) fb[0][j] = frag<LA, BM>(lds[0], wm * WM + j * 32, 0, lane);
 
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K, lds[cur ^ 1], wave, lane);
-      lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K, lds[cur ^ 1] + A_ELEMS, wave, lane);
-    }
     const uint4* At = lds[cur];
     const uint4* Bt = lds[cur] + A_ELEMS;
-    // fragments double-buffered across the four 16-deep k-slices
-    bf16x8_t fa[2][FN], fb[2][FM];
+    // tile t+1 into the other buffer, whose last reads finished before the
+    // previous barrier; past the end it reads zeros into an unused buffer
+    la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K, lds[cur ^ 1], wave, lane);
+    lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K, lds[cur ^ 1] + A_ELEMS, wave, lane);
 #pragma unroll
-    for (int i = 0; i < FN; ++i) fa[0][i] = frag<LB, BN>(Bt, wn * WN + i * 32, 0, lane);
+    for (int kk = 0; kk < KS; ++kk) {
+      const int cb = kk & 1, nx = cb ^ 1;
+      if (kk + 1 < KS) {
 #pragma unroll
-    for (int j = 0; j < FM; ++j) fb[0][j] = frag<LA, BM>(At, wm * WM + j * 32, 0, lane);
+        for (int i = 0; i < FN; ++i) fa[nx][i] = frag<LB, BN>(Bt, wn * WN + i * 32, kk + 1, lane);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int cb = kk & 1, nb = cb ^ 1;
-      if (kk + 1 < BK / 16) {
+        for (int j = 0; j < FM; ++j) fb[nx][j] = frag<LA, BM>(At, wm * WM + j * 32, kk + 1, lane);
+      } else {
+        // publish tile t+1: this wave's DMA has landed and its reads of tile
+        // t are complete; after the barrier every wave's are
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+        const uint4* An = lds[cur ^ 1];
+        const uint4* Bn = lds[cur ^ 1] + A_ELEMS;
 #pragma unroll
-        for (int i = 0; i < FN; ++i) fa[nb][i] = frag<LB, BN>(Bt, wn * WN + i * 32, kk + 1, lane);
+        for (int i = 0; i < FN; ++i) fa[nx][i] = frag<LB, BN>(Bn, wn * WN + i * 32, 0, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) fb[nb][j] = frag<LA, BM>(At, wm * WM + j * 32, kk + 1, lane);
+        for (int j = 0; j < FM; ++j) fb[nx][j] = frag<LA, BM>(An, wm * WM + j * 32, 0, lane);
       }
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
         for (int j = 0; j < FM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fb[cb][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
   }
 
   // ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block ------
@@ -329,6 +357,26 @@ hipError_t launch_grouped_k(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void splitk_reduce_k(const float* __restrict__ part, int S,
+                                                      long stride, int M, int N,
+                                                      float* __restrict__ out, long ldo) {
+  // out[m][n..n+3] += sum over splits, in split order
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;
+  const int nq = N / 4;
+  if (q >= (long)M * nq) return;
+  const int m = (int)(q / nq), n = (int)(q % nq) * 4;
+  const float* src = part + (long)m * N + n;
+  float4 acc = *reinterpret_cast<const float4*>(src);
+  for (int e = 1; e < S; ++e) {
+    const float4 v = *reinterpret_cast<const float4*>(src + e * stride);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  float4* o = reinterpret_cast<float4*>(out + (long)m * ldo + n);
+  float4 c = *o;
+  c.x += acc.x; c.y += acc.y; c.z += acc.z; c.w += acc.w;
+  *o = c;
+}
+
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
@@ -354,6 +402,34 @@ hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
   if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
   return hipErrorInvalidValue;
+}
+
+int splitk_splits(int M, int N, int K) {
+  const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
+  if (tiles >= 128 || K < 1024) return 1;
+  int S = (int)((256 + tiles - 1) / tiles);
+  S = S > K / 512 ? K / 512 : S;
+  return S < 1 ? 1 : (S > 32 ? 32 : S);
+}
+
+hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (splits <= 1 || a.K <= 0) return gemm(kMC, kMC, kAccF32, a, s);
+  const long ks = ((a.K + splits - 1) / splits + BK - 1) / BK * BK;
+  const int S = (int)((a.K + ks - 1) / ks);
+  GemmArgs p = a;
+  p.C = partial;
+  p.ldc = a.N;
+  p.strideB = ks;
+  p.strideC = (long)a.M * a.N;
+  p.groups = S;
+  const long tiles = (long)S * ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  hipLaunchKernelGGL((gemm_kernel<128, 128, 2, 2, kMC, kMC, kStoreF32, 3>), dim3((unsigned)tiles),
+                     dim3(256), 0, s, p);
+  const long n4 = (long)a.M * (a.N / 4);
+  hipLaunchKernelGGL(splitk_reduce_k, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, partial, S,
+                     (long)a.M * a.N, a.M, a.N, reinterpret_cast<float*>(a.C), a.ldc);
+  return hipGetLastError();
 }
 
 hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,

@@ -44,6 +44,13 @@ hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& 
 //   K-grouped (MC, MC): C_e (+)= sum over rows g_off[e].. of A^T B, C_e = C + e * strideC.
 hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
 hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
+// Weight gradient C (+)= A^T B (both M/N-contiguous) with the reduction split
+// into `splits` uniform slices: fp32 partials [splits][M][N] in `partial`,
+// then summed in slice order into C. For products with few output tiles and
+// a long reduction (N % 4 == 0). splitk_splits picks the split count (1 =
+// plain GEMM, no partials needed).
+int splitk_splits(int M, int N, int K);
+hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, hipStream_t s);
 
 // --------------------------------------------------------- elementwise ----
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* g, uint16_t* y, float* rstd,
@@ -125,6 +132,8 @@ hipError_t moe_combine_bwd(const uint16_t* ys, const float* gates, const int32_t
                            uint16_t* dys, hipStream_t s);
 hipError_t moe_scatter_back(const uint16_t* dxs, const int32_t* pos_of, long T, int h, int k,
                             uint16_t* db, hipStream_t s);
+// colsum: E column sums followed by moe_aux_blocks(T) * E block partials.
+int moe_aux_blocks(int T);
 hipError_t moe_aux_loss(const float* probs, const int32_t* counts, int T, int E, int k,
                         float alpha, float* colsum, float* aux, hipStream_t s);
 hipError_t moe_router_bwd(const float* probs, const int32_t* idx, const float* dgate,

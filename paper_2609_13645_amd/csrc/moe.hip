@@ -13,7 +13,8 @@
 //  * gather / combine / their backward move whole bf16 rows with 16-byte
 //    vectors; every sum over the k slots of a token runs in slot order.
 //  * the load-balance auxiliary loss alpha * E * sum_e f_e P_e and its
-//    gradient through the softmax (f_e = count_e / (T k) is a constant).
+//    gradient through the softmax (f_e = count_e / (T k) is a constant);
+//    the column sums behind P_e are per-block partials summed in block order.
 #include "common.h"
 #include "kernels.h"
 
@@ -96,6 +97,11 @@ __global__ __launch_bounds__(64) void sort_scatter_k(const int32_t* __restrict__
                                                      const int32_t* __restrict__ offsets,
                                                      int32_t* __restrict__ perm,
                                                      int32_t* __restrict__ pos_of) {
+  // One wave walks the block's entries 64 at a time in flat order. The lanes
+  // holding the same expert are found with one ballot per bit of the expert
+  // id (E <= 64: six bits), so each lane's rank among the earlier lanes of
+  // its expert is a popcount, and the group's lowest lane advances the
+  // expert's running position.
   __shared__ int run[64];
   const int lane = threadIdx.x;
   if (lane < E) run[lane] = offsets[lane] + block_base[(long)blockIdx.x * E + lane];
@@ -106,22 +112,21 @@ __global__ __launch_bounds__(64) void sort_scatter_k(const int32_t* __restrict__
   for (long base = f0; base < f1; base += 64) {
     const long f = base + lane;
     const bool ok = f < f1;
-    const int e = ok ? idx[f] : -1;
-    uint64_t todo = __ballot(ok);
-    while (todo) {
-      const int leader = __ffsll((unsigned long long)todo) - 1;
-      const int ex = __shfl(e, leader, 64);
-      const uint64_t same = __ballot(ok && e == ex);
-      if (ok && e == ex) {
-        const int pos = run[ex] + __popcll(same & below);
-        perm[pos] = (int32_t)f;
-        pos_of[f] = pos;
-      }
-      __syncthreads();  // all lanes read run[ex] before it advances
-      if (lane == 0) run[ex] += __popcll(same);
-      __syncthreads();
-      todo &= ~same;
+    const int e = ok ? idx[f] : 0;
+    uint64_t same = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+      const uint64_t ones = __ballot(ok && ((e >> b) & 1));
+      same &= ((e >> b) & 1) ? ones : ~ones;
     }
+    const int pos = run[e] + __popcll(same & below);  // every lane reads before any update
+    __builtin_amdgcn_wave_barrier();
+    if (ok) {
+      perm[pos] = (int32_t)f;
+      pos_of[f] = pos;
+      if ((same & below) == 0) run[e] += __popcll(same);
+    }
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -235,26 +240,36 @@ __global__ __launch_bounds__(256) void scatter_back_k(const bf16_t* __restrict__
 
 // P_e = sum_t p[t, e] (fixed order) and aux += alpha E sum_e f_e P_e / T.
 // One block; wave w sums the token stripe t = w mod 16 for each expert lane.
-__global__ __launch_bounds__(1024) void aux_loss_k(const float* __restrict__ probs,
-                                                   const int32_t* __restrict__ counts, int T,
-                                                   int E, int k, float alpha,
-                                                   float* __restrict__ colsum,
-                                                   float* __restrict__ aux) {
-  __shared__ float part[16][64];
+// Column sums of the router probabilities over kAuxTokens-token blocks,
+// partial[block][e]; summed in block order by aux_loss_k.
+constexpr int kAuxTokens = 64;
+__global__ __launch_bounds__(256) void prob_colsum_k(const float* __restrict__ probs, int T, int E,
+                                                     float* __restrict__ partial) {
+  __shared__ float part[4][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float s = 0.0f;
+  const long t0 = (long)blockIdx.x * kAuxTokens;
+  float sum = 0.0f;
   if (lane < E)
-    for (int t = wave; t < T; t += 16) s += probs[(long)t * E + lane];
-  part[wave][lane] = s;
+    for (int i = wave; i < kAuxTokens && t0 + i < T; i += 4) sum += probs[(t0 + i) * E + lane];
+  part[wave][lane] = sum;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    float c = 0.0f;
-    for (int w = 0; w < 16; ++w) c += part[w][threadIdx.x];
-    if (threadIdx.x < E) colsum[threadIdx.x] = c;
-    const float fe = threadIdx.x < E ? (float)counts[threadIdx.x] / ((float)T * k) : 0.0f;
-    const float term = wave_sum(fe * (threadIdx.x < E ? c : 0.0f));
-    if (threadIdx.x == 0 && aux) aux[0] += alpha * (float)E * term / (float)T;
-  }
+  if (threadIdx.x < E)
+    partial[(long)blockIdx.x * E + threadIdx.x] =
+        ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
+}
+
+__global__ __launch_bounds__(64) void aux_loss_k(const float* __restrict__ partial, int nblk,
+                                                 const int32_t* __restrict__ counts, int T, int E,
+                                                 int k, float alpha, float* __restrict__ colsum,
+                                                 float* __restrict__ aux) {
+  const int e = threadIdx.x;
+  float c = 0.0f;
+  if (e < E)
+    for (int b = 0; b < nblk; ++b) c += partial[(long)b * E + e];
+  if (e < E) colsum[e] = c;
+  const float fe = e < E ? (float)counts[e] / ((float)T * k) : 0.0f;
+  const float term = wave_sum(fe * (e < E ? c : 0.0f));
+  if (e == 0 && aux) aux[0] += alpha * (float)E * term / (float)T;
 }
 
 // dl[t, e] = p (dp - sum_e p dp) with dp = dgate on chosen experts plus the
@@ -330,9 +345,15 @@ hipError_t moe_scatter_back(const uint16_t* dxs, const int32_t* pos_of, long T, 
   return hipGetLastError();
 }
 
+int moe_aux_blocks(int T) { return (T + kAuxTokens - 1) / kAuxTokens; }
 hipError_t moe_aux_loss(const float* probs, const int32_t* counts, int T, int E, int k, float alpha,
                         float* colsum, float* aux, hipStream_t s) {
-  hipLaunchKernelGGL(aux_loss_k, dim3(1), dim3(1024), 0, s, probs, counts, T, E, k, alpha, colsum, aux);
+  // colsum holds E sums followed by moe_aux_blocks(T) * E block partials
+  if (T <= 0) return hipSuccess;
+  const int nb = moe_aux_blocks(T);
+  float* partial = colsum + E;
+  hipLaunchKernelGGL(prob_colsum_k, dim3(nb), dim3(256), 0, s, probs, T, E, partial);
+  hipLaunchKernelGGL(aux_loss_k, dim3(1), dim3(64), 0, s, partial, nb, counts, T, E, k, alpha, colsum, aux);
   return hipGetLastError();
 }
 

@@ -143,6 +143,16 @@ def test_moe_layer_full_geometry_short_seq():
     check_moe(got, ref)
 
 
+def test_moe_layer_long_sequence_split_router_gradient():
+    # 2048 tokens: the router weight gradient (16 x 256 outputs) is reduced
+    # over the tokens in four slices whose partial sums are added in order
+    cfg = fi.config("tiny", batch=1, seq=2048, ffn=0, n_experts=16, top_k=2, expert_ffn=64,
+                    aux_coef=0.05, seed=61)
+    banner("moe layer seq 2048 (router gradient split over tokens)")
+    got, ref, _ = run_moe_layer(cfg)
+    check_moe(got, ref)
+
+
 def test_moe_layer_is_deterministic():
     cfg = fi.config("tiny", seq=128, ffn=0, n_experts=8, top_k=2, expert_ffn=64, aux_coef=0.01)
     banner("moe determinism")
