@@ -60,6 +60,9 @@ def parse():
     ap.add_argument("--cpu-seq", type=int, default=4096,
                     help="tokens of the CPU-baseline sample (layer workloads)")
     ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="run only the dominant kernel and a 1 GiB device copy (for "
+                         "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE passes), then exit")
     return ap.parse_args()
 
 
@@ -204,6 +207,77 @@ def dominant_kernel(cfg, stream, step, reps):
             "flop_per_launch": flop}
 
 
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dominant_kernel_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_13645_amd", "csrc", "gemm.hip")
+
+
+def source_digest():
+    import hashlib
+    with open(GEMM_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_run(cfg, reps):
+    """The dominant kernel alone, then a plain device-to-device copy of
+    COPY_BYTES, each a few times: the counter passes read both, and the copy
+    converts the counters' units into bytes."""
+    import torch
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    step = Step(cfg, stream)
+    kernel = dominant_kernel(cfg, stream, step, reps)
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"kernel": kernel["name"], "shape": kernel["shape"],
+                      "copy_bytes": COPY_BYTES}), flush=True)
+
+
+def traffic_from_counters(fetch_csv, write_csv, kernel_grid, out=TRAFFIC_FILE):
+    """Per-launch HBM bytes of the dominant kernel from the two counter
+    passes: each counter's average over the kernel's dispatches, scaled by
+    (bytes the copy moves) / (what the counter reads for the copy)."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {"kernel": [], "copy": []}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name, grid = r["Kernel_Name"], int(r["Grid_Size"])
+            if "gemm_kernel" in name and grid == kernel_grid:
+                vals["kernel"].append(float(r["Counter_Value"]))
+            elif "copyBuffer" in name or ("copy" in name.lower() and "gemm" not in name):
+                vals["copy"].append(float(r["Counter_Value"]))
+        return statistics.median(vals["kernel"]), max(vals["copy"])
+
+    kf, cf = per_kernel(fetch_csv, "FETCH_SIZE")
+    kw, cw = per_kernel(write_csv, "WRITE_SIZE")
+    res = {"source_sha256": source_digest(), "counters_kib": {"fetch": kf, "write": kw},
+           "copy_counters_kib": {"fetch": cf, "write": cw}, "copy_bytes": COPY_BYTES,
+           "bytes_per_fetch_kib": COPY_BYTES / cf, "bytes_per_write_kib": COPY_BYTES / cw,
+           "fetch_bytes": kf * COPY_BYTES / cf, "write_bytes": kw * COPY_BYTES / cw}
+    res["traffic_bytes"] = res["fetch_bytes"] + res["write_bytes"]
+    with open(out, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res, indent=1))
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the dominant kernel, if the recorded counter
+    runs were taken on the current GEMM source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return rec["traffic_bytes"] if rec.get("source_sha256") == source_digest() else None
+
+
 def gpu_step_bench(cfg, steps, warmup, kernel_reps):
     import torch
     torch.cuda.set_device(0)
@@ -338,6 +412,9 @@ def main():
     if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
         summarize_profile(sys.argv[2])
         return
+    if len(sys.argv) == 5 and sys.argv[1] == "--traffic-summarize":
+        traffic_from_counters(sys.argv[2], sys.argv[3], int(sys.argv[4]))
+        return
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -345,6 +422,9 @@ def main():
               "MI355X and has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
         sys.exit(2)
     cfg = fi.config(args.workload)
+    if args.traffic_run:
+        traffic_run(cfg, args.kernel_reps)
+        return
     T = fi.tokens(cfg)
     step_flop = flops.step_flops(cfg)
     print(f"[bench] workload {args.workload}: {DESCRIPTION[args.workload]}; "
@@ -381,7 +461,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": kernel["name"], "shape": kernel["shape"],
                      "achieved": round(k_tf, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(k_tf / PEAK_BF16_TFLOPS, 4),
-                     "avg_us": round(kernel["avg_us"], 2), "traffic": None},
+                     "avg_us": round(kernel["avg_us"], 2),
+                     "traffic": (recorded_traffic() if args.workload == WORKLOAD else None)},
     }
     if cfg["n_experts"]:
         res["config"].update(n_experts=cfg["n_experts"], top_k=cfg["top_k"],
