@@ -121,12 +121,24 @@ __device__ __forceinline__ void zero(f32x16_t& a) {
 
 // ------------------------------------------------------------- forward ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
+//  * K/V tiles alternate between two separately declared LDS arrays with the
+//    loop unrolled by two, so the compiler can see that the DMA filling one
+//    never aliases reads of the other (else it waits for the DMA before every
+//    read); each tile ends with an explicit wait + barrier.
+//  * All K fragments of a tile are read in one batch before its 16 score
+//    MFMAs; the V fragments are read into the same registers right after, so
+//    their latency hides under the softmax.
+//  * The softmax is VALU-bound on this chip (a wave64 VALU op takes 4 cycles,
+//    exp more), so it is trimmed: the scale is folded into the exponent's
+//    FMA, and the running max (log2 units) is raised only when a tile's max
+//    exceeds it by more than 8, so the output rescale runs on few tiles and
+//    probabilities stay below 2^8 (exact in the final normalisation).
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restrict__ o,
-                                                     float* __restrict__ lse) {
-  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8;
-  __shared__ uint4 smem[2][2 * NAT];  // K tile, V tile
-
+                                                    float* __restrict__ lse) {
+  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
+  __shared__ uint4 sm0[2 * NAT];
+  __shared__ uint4 sm1[2 * NAT];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
   const int qt = nqt - 1 - (int)blockIdx.x;
@@ -141,92 +153,123 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   const int hh = lane >> 5, l32 = lane & 31;
   const int q0w = qt * BQ + wave * 32;
   const int q = q0w + l32;
-
-  bf16x8_t qf[D / 16];
+  bf16x8_t qf[KK];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk)
+  for (int kk = 0; kk < KK; ++kk)
     qf[kk] = gload_frag(Qg + (long)q * a.ld_qkv + kk * 16 + hh * 8, q < S);
-
-  f32x16_t oacc[D / 32];
+  f32x16_t oacc[DB];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) zero(oacc[db]);
+  for (int db = 0; db < DB; ++db) zero(oacc[db]);
   float mrow = -INFINITY, lrow = 0.0f;
   const float c = a.scale * kLog2e;
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
 
-  dma_tile<D, 4>(Kg, a.ld_qkv, 0, S, smem[0], wave, lane);
-  dma_tile<D, 4>(Vg, a.ld_qkv, 0, S, smem[0] + NAT, wave, lane);
-  __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nkt) {
-      dma_tile<D, 4>(Kg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1], wave, lane);
-      dma_tile<D, 4>(Vg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1] + NAT, wave, lane);
-    }
+  auto dma = [&](int kt, uint4* sm) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, ln);
+    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, ln);
+  };
+  auto tile = [&](const uint4* Ks, const uint4* Vs, int kt) __attribute__((always_inline)) {
     const int k0 = kt * BKV;
-    if (k0 <= q0w + 31) {
-      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
-      asm volatile("" : "+v"(ln));
-      const uint4* Ks = smem[cur];
-      const uint4* Vs = smem[cur] + NAT;
-      f32x16_t s[2];
-      zero(s[0]);
-      zero(s[1]);
+    if (k0 > q0w + 31) return;   // every query of this wave is before the tile
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    bf16x8_t f[KK][2];           // K fragments, then V fragments
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
+    for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) s[kb] = MFMA(row_frag<D>(Ks, kb * 32, kk, ln), qf[kk], s[kb]);
-      const bool diag = (k0 + BKV - 1 > q0w);
-      float mt = -INFINITY;
+      for (int kb = 0; kb < 2; ++kb) f[kk][kb] = row_frag<D>(Ks, kb * 32, kk, ln);
+    f32x16_t s[2];
+    zero(s[0]);
+    zero(s[1]);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) s[kb] = MFMA(f[kk][kb], qf[kk], s[kb]);
+    // V fragments for the P V products: read now, consumed after the softmax
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          f[(kb * 2 + ss) * DB / 2 + db / 2][db & 1] = tr_frag<D>(Vs, kb * 32 + ss * 16, db, ln);
+    const bool diag = (k0 + BKV - 1 > q0w);
+    if (diag) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float t = s[kb][i] * c;
-          if (diag) {
-            const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-            if (key > q) t = -INFINITY;
-          }
-          s[kb][i] = t;
-          mt = fmaxf(mt, t);
+          const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+          if (key > q) s[kb][i] = -INFINITY;
         }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float mnew = fmaxf(mrow, mt);
+    }
+    float mx[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int kb = r >> 1, o8 = (r & 1) * 8;
+      mx[r] = fmaxf(fmaxf(fmaxf(s[kb][o8 + 0], s[kb][o8 + 1]), fmaxf(s[kb][o8 + 2], s[kb][o8 + 3])),
+                    fmaxf(fmaxf(s[kb][o8 + 4], s[kb][o8 + 5]), fmaxf(s[kb][o8 + 6], s[kb][o8 + 7])));
+    }
+    float mt = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * c;
+    const bool grow = mt > mrow + 8.0f;
+    if (__ballot(grow)) {
+      const float mnew = grow ? mt : mrow;
       const float alpha = fast_exp2(mrow - mnew);
       lrow *= alpha;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = fast_exp2(s[kb][i] - mnew);
-          s[kb][i] = p;
-          lrow += p;
-        }
       mrow = mnew;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss) {
-          const bf16x8_t pf = pack_frag(s[kb], ss);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db)
-            oacc[db] = MFMA(tr_frag<D>(Vs, kb * 32 + ss * 16, db, ln), pf, oacc[db]);
-        }
     }
-    __syncthreads();
-  }
+    const float nm = -mrow;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float pp = fast_exp2(__builtin_fmaf(s[kb][i], c, nm));
+        s[kb][i] = pp;
+        lrow += pp;
+      }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+        const bf16x8_t pf = pack_frag(s[kb], ss);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = MFMA(f[(kb * 2 + ss) * DB / 2 + db / 2][db & 1], pf, oacc[db]);
+      }
+  };
+  auto sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
+  dma(0, sm0);
+  sync();
+  for (int kt = 0; kt < nkt; kt += 2) {
+    if (kt + 1 < nkt) dma(kt + 1, sm1);
+    tile(sm0, sm0 + NAT, kt);
+    sync();
+    if (kt + 1 < nkt) {
+      if (kt + 2 < nkt) dma(kt + 2, sm0);
+      tile(sm1, sm1 + NAT, kt + 1);
+      sync();
+    }
+  }
   lrow += __shfl_xor(lrow, 32, 64);
   if (q < S) {
     const float inv = 1.0f / lrow;
     bf16_t* orow = o + (rb + q) * (long)(a.n_heads * D) + (long)n * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = db * 32 + g * 8 + hh * 4;
