@@ -323,13 +323,17 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* 
 //   PASS 0: S = Q K^T, P = exp(S - LSE), dV^T += dO^T P
 //   PASS 1: S, dP = dO V^T, dS = P (dP - delta), dK^T += Q^T dS
 // (S is formed twice, 5 products instead of 4, for twice the occupancy.)
+// LDS double buffering in two separate arrays with explicit waits, as in the
+// forward; pass 0 batches its fragment reads, pass 1 (K and V both held in
+// registers) reads them in place.
 template <int D, int PASS>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, float* __restrict__ pk, float* __restrict__ pv) {
   constexpr int BKEY = 128, BQ = 64, NAT = BQ * D / 8;
   constexpr int STAGE = 2 * NAT + 32;  // Q tile, dO tile, lse[64], delta[64]
-  __shared__ uint4 smem[2][STAGE];
+  __shared__ uint4 sm0[STAGE];
+  __shared__ uint4 sm1[STAGE];
 
   const int S = a.seq;
   const int kt = blockIdx.x;  // low key tiles have the most work: dispatched first
@@ -365,11 +369,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
   const int qt0 = (kt * BKEY) / BQ;
   const int iters = nqt - qt0;
 
-  auto load_tile = [&](int it, int buf) {
+  auto load_tile = [&](int it, uint4* base) __attribute__((always_inline)) {
     const int q0 = (qt0 + it) * BQ;
-    uint4* base = smem[buf];
-    dma_tile<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, lane);
-    dma_tile<D, 4>(dOg, ldo, q0, S, base + NAT, wave, lane);
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    dma_tile<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, ln);
+    dma_tile<D, 4>(dOg, ldo, q0, S, base + NAT, wave, ln);
     if (wave == 0) {
       const uint32_t off = q0 + lane < S ? (uint32_t)((q0 + lane) * 4) : kOOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Lg), (lds_ptr_t)(base + 2 * NAT), 4, off, 0, 0, 0);
@@ -378,55 +383,89 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     }
   };
 
-  load_tile(0, 0);
-  __syncthreads();
-  for (int it = 0; it < iters; ++it) {
-    const int cur = it & 1;
-    if (it + 1 < iters) load_tile(it + 1, cur ^ 1);
+  auto tile = [&](const uint4* base, int it) __attribute__((always_inline)) {
     const int q0 = (qt0 + it) * BQ;
-    if (q0 + BQ - 1 >= kw0) {
-      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
-      asm volatile("" : "+v"(ln));
-      const uint4* Qs = smem[cur];
-      const uint4* dOs = smem[cur] + NAT;
-      const float* L = reinterpret_cast<const float*>(smem[cur] + 2 * NAT);
-      const float* Dl = L + BQ;
-      f32x16_t s[2], dp[2];
+    if (q0 + BQ - 1 < kw0) return;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const uint4* Qs = base;
+    const uint4* dOs = base + NAT;
+    const float* L = reinterpret_cast<const float*>(base + 2 * NAT);
+    const float* Dl = L + BQ;
+    f32x16_t s[2], dp[2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        zero(s[qb]);
-        if (PASS) zero(dp[qb]);
+    for (int qb = 0; qb < 2; ++qb) {
+      zero(s[qb]);
+      if (PASS) zero(dp[qb]);
+    }
+    bf16x8_t fq[D / 16][2], fo[D / 16][2];
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      constexpr int BAT = PASS ? 1 : 4;   // pass 1 holds V too: no room to batch
+      if (kk % BAT == 0) {
+#pragma unroll
+        for (int u = kk; u < kk + BAT; ++u)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            fq[u][qb] = row_frag<D>(Qs, qb * 32, u, ln);
+            if (PASS) fo[u][qb] = row_frag<D>(dOs, qb * 32, u, ln);
+          }
       }
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          s[qb] = MFMA(row_frag<D>(Qs, qb * 32, kk, ln), kf[kk], s[qb]);
-          if (PASS) dp[qb] = MFMA(row_frag<D>(dOs, qb * 32, kk, ln), vf[kk], dp[qb]);
-        }
-      const bool diag = (q0 < kw0 + 31);
-      const bool tail = (q0 + BQ > S);
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          float p = fast_exp2(s[qb][i] * c - L[qi] * kLog2e);
-          if ((diag && key > q0 + qi) || (tail && q0 + qi >= S)) p = 0.0f;
-          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
-        }
-      // PASS 0: dV^T += dO^T P;  PASS 1: dK^T += Q^T dS
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss) {
-          const bf16x8_t f = pack_frag(s[qb], ss);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db)
-            acc[db] = MFMA(tr_frag<D>(PASS ? Qs : dOs, qb * 32 + ss * 16, db, ln), f, acc[db]);
-        }
+      for (int qb = 0; qb < 2; ++qb) {
+        s[qb] = MFMA(fq[kk][qb], kf[kk], s[qb]);
+        if (PASS) dp[qb] = MFMA(fo[kk][qb], vf[kk], dp[qb]);
+      }
     }
-    __syncthreads();
+    // transposed fragments of the second product: pass 0 reads them before
+    // the elementwise part; pass 1 (more live registers) reads them in place
+    bf16x8_t ft[2][2][D / 32];
+    if (!PASS) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) ft[qb][ss][db] = tr_frag<D>(dOs, qb * 32 + ss * 16, db, ln);
+    }
+    const bool diag = (q0 < kw0 + 31);
+    const bool tail = (q0 + BQ > S);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+        float p = fast_exp2(__builtin_fmaf(s[qb][i], c, -L[qi] * kLog2e));
+        if ((diag && key > q0 + qi) || (tail && q0 + qi >= S)) p = 0.0f;
+        s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
+      }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+        const bf16x8_t f = pack_frag(s[qb], ss);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+          acc[db] = MFMA(PASS ? tr_frag<D>(Qs, qb * 32 + ss * 16, db, ln) : ft[qb][ss][db], f, acc[db]);
+      }
+  };
+  auto sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  load_tile(0, sm0);
+  sync();
+  for (int it = 0; it < iters; it += 2) {
+    if (it + 1 < iters) load_tile(it + 1, sm1);
+    tile(sm0, it);
+    sync();
+    if (it + 1 < iters) {
+      if (it + 2 < iters) load_tile(it + 2, sm0);
+      tile(sm1, it + 1);
+      sync();
+    }
   }
 
   // partials: [grp][T][hkv] fp32, this block's query head is slot n % grp
@@ -477,14 +516,17 @@ __global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict
 
 // ---------------------------------------------------------- backward dQ ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
+// P is recomputed from the saved LSE (exponent argument as one FMA), then
+// dS = P (dP - delta) and dQ^T += K^T dS^T. LDS double buffering, batched
+// fragment reads and explicit waits as in the forward.
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
-                                                        const float* __restrict__ lse,
-                                                        const float* __restrict__ delta,
-                                                        bf16_t* __restrict__ dq, long ld_d) {
-  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8;
-  __shared__ uint4 smem[2][2 * NAT];  // K tile, V tile
-
+                                                const float* __restrict__ lse,
+                                                const float* __restrict__ delta,
+                                                bf16_t* __restrict__ dq, long ld_d) {
+  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
+  __shared__ uint4 sm0[2 * NAT];
+  __shared__ uint4 sm1[2 * NAT];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
   const int qt = nqt - 1 - (int)blockIdx.x;
@@ -501,80 +543,108 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   const int hh = lane >> 5, l32 = lane & 31;
   const int q0w = qt * BQ + wave * 32;
   const int q = q0w + l32;
-
-  bf16x8_t qf[D / 16], of[D / 16];
+  bf16x8_t qf[KK], of[KK];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
+  for (int kk = 0; kk < KK; ++kk) {
     qf[kk] = gload_frag(Qg + (long)q * a.ld_qkv + kk * 16 + hh * 8, q < S);
     of[kk] = gload_frag(dOg + (long)q * ldo + kk * 16 + hh * 8, q < S);
   }
   const long li = ((long)b * a.n_heads + n) * S + q;
-  const float l2 = q < S ? lse[li] * kLog2e : INFINITY;
+  const float nl2 = q < S ? -lse[li] * kLog2e : -INFINITY;
   const float dl = q < S ? delta[li] : 0.0f;
-  f32x16_t dqa[D / 32];
+  f32x16_t dqa[DB];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) zero(dqa[db]);
+  for (int db = 0; db < DB; ++db) zero(dqa[db]);
   const float c = a.scale * kLog2e;
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
-
-  dma_tile<D, 4>(Kg, a.ld_qkv, 0, S, smem[0], wave, lane);
-  dma_tile<D, 4>(Vg, a.ld_qkv, 0, S, smem[0] + NAT, wave, lane);
-  __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nkt) {
-      dma_tile<D, 4>(Kg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1], wave, lane);
-      dma_tile<D, 4>(Vg, a.ld_qkv, (kt + 1) * BKV, S, smem[cur ^ 1] + NAT, wave, lane);
-    }
+  auto dma = [&](int kt, uint4* sm) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, ln);
+    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, ln);
+  };
+  auto tile = [&](const uint4* Ks, const uint4* Vs, int kt) __attribute__((always_inline)) {
     const int k0 = kt * BKV;
-    if (k0 <= q0w + 31) {
-      int ln = lane;  // opaque: fragment addresses recomputed per tile, not hoisted
-      asm volatile("" : "+v"(ln));
-      const uint4* Ks = smem[cur];
-      const uint4* Vs = smem[cur] + NAT;
-      f32x16_t s[2], dp[2];
+    if (k0 > q0w + 31) return;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    f32x16_t s[2], dp[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        zero(s[kb]);
-        zero(dp[kb]);
+    for (int kb = 0; kb < 2; ++kb) {
+      zero(s[kb]);
+      zero(dp[kb]);
+    }
+    // scores and dP: K and V fragments read four 16-deep slices at a time
+    bf16x8_t fk[KK][2], fv[KK][2];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      if (kk % 4 == 0) {
+#pragma unroll
+        for (int u = kk; u < kk + 4; ++u)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb) {
+            fk[u][kb] = row_frag<D>(Ks, kb * 32, u, ln);
+            fv[u][kb] = row_frag<D>(Vs, kb * 32, u, ln);
+          }
       }
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          s[kb] = MFMA(row_frag<D>(Ks, kb * 32, kk, ln), qf[kk], s[kb]);
-          dp[kb] = MFMA(row_frag<D>(Vs, kb * 32, kk, ln), of[kk], dp[kb]);
-        }
-      const bool diag = (k0 + BKV - 1 > q0w);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float p = fast_exp2(s[kb][i] * c - l2);
-          if (diag) {
-            const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-            if (key > q) p = 0.0f;
-          }
-          dp[kb][i] = p * (dp[kb][i] - dl);
-        }
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss) {
-          const bf16x8_t df = pack_frag(dp[kb], ss);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db)
-            dqa[db] = MFMA(tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln), df, dqa[db]);
-        }
+      for (int kb = 0; kb < 2; ++kb) {
+        s[kb] = MFMA(fk[kk][kb], qf[kk], s[kb]);
+        dp[kb] = MFMA(fv[kk][kb], of[kk], dp[kb]);
+      }
     }
-    __syncthreads();
+    // K^T fragments for dQ^T = K^T dS^T: read before the elementwise part
+    bf16x8_t ft[2][2][DB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) ft[kb][ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
+    const bool diag = (k0 + BKV - 1 > q0w);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float p = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2));
+        if (diag) {
+          const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+          if (key > q) p = 0.0f;
+        }
+        dp[kb][i] = p * (dp[kb][i] - dl);
+      }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+        const bf16x8_t df = pack_frag(dp[kb], ss);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) dqa[db] = MFMA(ft[kb][ss][db], df, dqa[db]);
+      }
+  };
+  auto sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  dma(0, sm0);
+  sync();
+  for (int kt = 0; kt < nkt; kt += 2) {
+    if (kt + 1 < nkt) dma(kt + 1, sm1);
+    tile(sm0, sm0 + NAT, kt);
+    sync();
+    if (kt + 1 < nkt) {
+      if (kt + 2 < nkt) dma(kt + 2, sm0);
+      tile(sm1, sm1 + NAT, kt + 1);
+      sync();
+    }
   }
-
   if (q < S) {
     bf16_t* dqr = dq + (rb + q) * ld_d + (long)n * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = db * 32 + g * 8 + hh * 4;
