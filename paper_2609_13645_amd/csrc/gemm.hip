@@ -377,6 +377,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_k(const float* __restrict__
   *o = c;
 }
 
+constexpr int kCUs = 256;
+
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
@@ -384,6 +386,15 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // of 128x128 for every layout.
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
+  if (LB == kKC && big >= kCUs) {
+    // 256 x 192 tiles when 256 x 256 ones leave the last wave of workgroups
+    // partly empty: cost ~ waves x tile area, the narrower tile being ~11 %
+    // less efficient per FLOP
+    const long t192 = (long)((a.M + 255) / 256) * ((a.N + 191) / 192);
+    const double c256 = (double)((big + kCUs - 1) / kCUs) * 256.0;
+    const double c192 = (double)((t192 + kCUs - 1) / kCUs) * 192.0 / 0.89;
+    if (c192 < c256) return launch<256, 192, 4, 2, LA, LB, EPI>(a, s);
+  }
   if (big >= 256) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);

@@ -77,7 +77,8 @@ def test_gemm_integer_exact(la, lb, epi, M, N, K):
 
 @pytest.mark.parametrize("la,lb,epi", [(KC, KC, STORE_BF16), (KC, MC, STORE_BF16),
                                        (MC, MC, ACC_F32)])
-@pytest.mark.parametrize("M,N,K", [(4096, 4096, 64), (4096, 2048, 72), (1024, 1536, 256)])
+@pytest.mark.parametrize("M,N,K", [(4096, 4096, 64), (4096, 2048, 72), (1024, 1536, 256),
+                                   (4096, 6144, 64)])
 def test_gemm_tile_paths_random(la, lb, epi, M, N, K):
     banner(f"gemm rand la={la} lb={lb} epi={epi} M={M} N={N} K={K}")
     got, ref = run_gemm(la, lb, epi, M, N, K, seed=7, integer=False)
@@ -91,6 +92,19 @@ def test_gemm_zero_k_and_empty():
     assert np.array_equal(got, ref)
     got, ref = run_gemm(MC, MC, STORE_F32, 16, 24, 0)
     assert np.array_equal(got, np.zeros_like(ref))
+
+
+@pytest.mark.parametrize("epi", [STORE_BF16, RESID_BF16, ACC_F32, STORE_F32])
+def test_gemm_256x192_tiles_integer_exact(epi):
+    """A K-contiguous product whose 256 x 256 tiles would leave the last wave
+    of workgroups half empty runs on 256 x 192 tiles; N = 6136 also leaves a
+    ragged last tile column."""
+    M, N, K = 4096, 6136, 40
+    banner(f"gemm 256x192 tiles epi={epi}")
+    got, ref = run_gemm(KC, KC, epi, M, N, K, seed=epi + 11)
+    want = (fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
+            if epi in (STORE_BF16, RESID_BF16) else ref)
+    assert np.array_equal(got, want)
 
 
 GROUP_SIZES = [0, 37, 256, 1, 300, 0, 129, 8, 513]
