@@ -4,8 +4,9 @@ Default workload: the 8B-shape decoder layer (micro-batch 1 x seq 4096,
 hidden 4096, 32 query / 8 kv heads of 128, SwiGLU FFN 14336, RoPE base 5e5),
 bf16 with fp32 gradient accumulation. One step = layer forward + layer
 backward + fused clip/AdamW/bf16 write-back over all 218 M parameters of the
-layer (flat fp32 master, moments and gradient), on synthetic seeded inputs
-resident in HBM. Other workloads (--workload): the same layer at seq 16384
+layer (flat fp32 master, moments and gradient; the backward writes this
+step's gradients rather than accumulating into zeroed ones), on synthetic
+seeded inputs resident in HBM. Other workloads (--workload): the same layer at seq 16384
 with attention recomputed in the backward, the 64-expert top-8 MoE layer,
 the 16-layer tied-head model (embedding, layers, LM head + cross-entropy)
 and the tiny one-layer model.
@@ -104,19 +105,22 @@ class Step:
         self.t = 0
 
     def zero(self):
-        self.flat.grad.zero_()
+        # gradients are written, not accumulated, by the backward (one
+        # micro-batch per step): only the MoE aux scalar starts from zero
         if self.cfg["n_experts"] and not is_model(self.cfg):
             self.layer.aux.zero_()
 
     def fwd(self):
         if is_model(self.cfg):
-            self.model.forward_backward()       # the head fuses loss fwd and bwd
+            # the head fuses loss fwd and bwd; layers write their gradients,
+            # the head / embedding gradients are zeroed first
+            self.model.forward_backward(accumulate=False)
         else:
             self.layer.fwd(self.x, self.out)
 
     def bwd(self):
         if not is_model(self.cfg):
-            self.layer.bwd(self.x, self.dy, self.dx)
+            self.layer.bwd(self.x, self.dy, self.dx, overwrite=True)
 
     def adamw(self):
         import torch

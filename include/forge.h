@@ -125,7 +125,13 @@ typedef struct {
   const forge_bf16* w_down_e;
 } forge_layer_weights;
 
-/* Weight gradients, fp32, same shapes as the weights, accumulated (+=). */
+/*
+ * Weight gradients, fp32, same shapes as the weights. With overwrite == 0
+ * they are accumulated (+=, micro-batch accumulation: the caller zeroes them
+ * before the first micro-batch); with overwrite != 0 every one is written
+ * (=), the same values as accumulating into zeros, without the zeroing pass
+ * or the read of the old contents.
+ */
 typedef struct {
   float* d_attn_norm;
   float* d_w_qkv;
@@ -136,6 +142,7 @@ typedef struct {
   float* d_w_router;
   float* d_w_gate_up_e;
   float* d_w_down_e;
+  int32_t overwrite;
 } forge_layer_grads;
 
 /* Bytes of the `saved` buffer that forge_layer_fwd fills and
@@ -178,7 +185,7 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
 /*
  * Backward of forge_layer_fwd for upstream gradient d_out [T, h] (bf16):
  * writes d_in [T, h] (bf16, may alias d_out) and accumulates every weight
- * gradient into `grads` (fp32 +=). x_in and saved must be those of the
+ * gradient into `grads` (fp32 +=, or = when grads->overwrite is set). x_in and saved must be those of the
  * matching forward. Weight gradients are the data-gradient / weight-gradient
  * product pair of every projection (App. C). For a MoE layer the objective
  * is <x_out, d_out> + aux: the router gradient includes the load-balance

@@ -53,7 +53,8 @@ class LayerWeights(ctypes.Structure):
 class LayerGrads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("d_attn_norm", "d_w_qkv", "d_w_o", "d_ffn_norm", "d_w_gate_up",
-                 "d_w_down", "d_w_router", "d_w_gate_up_e", "d_w_down_e")]
+                 "d_w_down", "d_w_router", "d_w_gate_up_e", "d_w_down_e")] + \
+        [("overwrite", ctypes.c_int32)]
 
 
 class HeadCfg(ctypes.Structure):
@@ -173,8 +174,8 @@ def layer_weights(w: dict) -> LayerWeights:
     return LayerWeights(*[_ptr(w.get(n)) for n, _ in LayerWeights._fields_])
 
 
-def layer_grads(g: dict) -> LayerGrads:
-    return LayerGrads(*[_ptr(g.get(n)) for n, _ in LayerGrads._fields_])
+def layer_grads(g: dict, overwrite: bool = False) -> LayerGrads:
+    return LayerGrads(*[_ptr(g.get(n)) for n, _ in LayerGrads._fields_[:-1]], int(overwrite))
 
 
 def attn_cfg(c: dict) -> AttnCfg:

@@ -151,6 +151,7 @@ __global__ __launch_bounds__(512) void rmsnorm_bwd_k(
 // dg[c] += sum_b part[b][c]: a block covers 32 columns; 8 groups of 32
 // threads each sum a fixed stripe of partial rows, then the 8 stripe sums
 // are added in a fixed order (deterministic).
+template <bool ACC>
 __global__ __launch_bounds__(256) void dg_reduce_k(const float* __restrict__ part, int nblk,
                                                    float* __restrict__ dg, int h) {
   __shared__ float red[8][32];
@@ -165,7 +166,7 @@ __global__ __launch_bounds__(256) void dg_reduce_k(const float* __restrict__ par
     float t = 0.0f;
 #pragma unroll
     for (int w = 0; w < 8; ++w) t += red[w][threadIdx.x];
-    dg[col] += t;
+    dg[col] = ACC ? dg[col] + t : t;
   }
 }
 
@@ -510,8 +511,12 @@ hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
   return hipGetLastError();
 }
 
-hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h, hipStream_t s) {
-  hipLaunchKernelGGL(dg_reduce_k, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
+hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h, bool accumulate,
+                             hipStream_t s) {
+  if (accumulate)
+    hipLaunchKernelGGL(dg_reduce_k<true>, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
+  else
+    hipLaunchKernelGGL(dg_reduce_k<false>, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
   return hipGetLastError();
 }
 

@@ -242,6 +242,11 @@ GemmArgs gargs(const void* A, long lda, const void* B, long ldb, void* C, long l
   return g;
 }
 
+// weight-gradient epilogue: accumulate, or store when the caller asked for it
+forge::GemmEpilogue wgrad_epi(const forge_layer_grads* g) {
+  return g->overwrite ? forge::kStoreF32 : forge::kAccF32;
+}
+
 GemmArgs grouped(GemmArgs g, const int32_t* off, long E, long strideB, long strideC) {
   g.g_off = off;
   g.groups = (int)E;
@@ -336,7 +341,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   (void)c;
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                         gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
   FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, at<float>(workspace, wk.pk),
@@ -347,10 +352,10 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                               (int)(d.nh + d.nkv), (int)d.d, true, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                         gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), s));
   FORGE_HIP(forge::rmsnorm_bwd(x, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
-  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, !g->overwrite, s));
   return FORGE_OK;
 }
 
@@ -427,7 +432,7 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
       grouped(gargs(dys, d.h, w->w_down_e, d.fe, dact, d.fe, d.R, d.fe, d.h), offsets, E,
               d.h * d.fe, 0), s));
   FORGE_HIP(forge::gemm_grouped_k(
-      forge::kAccF32,
+      wgrad_epi(g),
       grouped(gargs(dys, d.h, act, d.fe, g->d_w_down_e, d.fe, d.h, d.fe, 0), offsets, E, 0,
               d.h * d.fe), s));
   FORGE_HIP(forge::swiglu_bwd(gu, dact, dgu, (int)d.R, (int)d.fe, s));
@@ -436,7 +441,7 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
       grouped(gargs(dgu, 2 * d.fe, w->w_gate_up_e, d.h, dxs, d.h, d.R, d.h, 2 * d.fe), offsets,
               E, 2 * d.fe * d.h, 0), s));
   FORGE_HIP(forge::gemm_grouped_k(
-      forge::kAccF32,
+      wgrad_epi(g),
       grouped(gargs(dgu, 2 * d.fe, xs, d.h, g->d_w_gate_up_e, d.h, 2 * d.fe, d.h, 0), offsets,
               E, 0, 2 * d.fe * d.h), s));
   FORGE_HIP(forge::moe_scatter_back(dxs, pos_of, d.T, (int)d.h, k, dbs, s));
@@ -447,7 +452,7 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
   // router weight gradient: 64 x h output tiles over T tokens, split over T
   FORGE_HIP(forge::gemm_wgrad_splitk(gargs(dl, d.E, bn, d.h, g->d_w_router, d.h, d.E, d.h, d.T),
                                      forge::splitk_splits((int)d.E, (int)d.h, (int)d.T),
-                                     at<float>(workspace, wk.wpart), s));
+                                     at<float>(workspace, wk.wpart), !g->overwrite, s));
   return FORGE_OK;
 }
 
@@ -589,16 +594,16 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
     uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
-    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), s));
     FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
-    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), s));
   }
   FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
-  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
   return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s);
 }
 
@@ -722,7 +727,7 @@ forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L
   FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
                         gargs(z, V, xn, h, d_w_lm, h, V, h, T), s));
   FORGE_HIP(forge::rmsnorm_bwd(x_L, final_norm, rstd, dxn, nullptr, d_x_L, dgp, (int)T, (int)h, s));
-  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, d_final_norm, (int)h, s));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, d_final_norm, (int)h, true, s));
   return ok();
 }
 

@@ -357,10 +357,11 @@ hipError_t launch_grouped_k(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <bool ACC>
 __global__ __launch_bounds__(256) void splitk_reduce_k(const float* __restrict__ part, int S,
                                                       long stride, int M, int N,
                                                       float* __restrict__ out, long ldo) {
-  // out[m][n..n+3] += sum over splits, in split order
+  // out[m][n..n+3] (+)= sum over splits, in split order
   const long q = (long)blockIdx.x * 256 + threadIdx.x;
   const int nq = N / 4;
   if (q >= (long)M * nq) return;
@@ -372,9 +373,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_k(const float* __restrict__
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
   float4* o = reinterpret_cast<float4*>(out + (long)m * ldo + n);
-  float4 c = *o;
-  c.x += acc.x; c.y += acc.y; c.z += acc.z; c.w += acc.w;
-  *o = c;
+  if (ACC) {
+    const float4 c = *o;
+    acc.x += c.x; acc.y += c.y; acc.z += c.z; acc.w += c.w;
+  }
+  *o = acc;
 }
 
 constexpr int kCUs = 256;
@@ -412,6 +415,7 @@ hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hi
 hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
   if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
+  if (epi == kStoreF32) return launch_grouped_k<256, 256, 4, 2, kStoreF32>(a, s);
   return hipErrorInvalidValue;
 }
 
@@ -423,9 +427,10 @@ int splitk_splits(int M, int N, int K) {
   return S < 1 ? 1 : (S > 32 ? 32 : S);
 }
 
-hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, hipStream_t s) {
+hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, bool accumulate,
+                             hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  if (splits <= 1 || a.K <= 0) return gemm(kMC, kMC, kAccF32, a, s);
+  if (splits <= 1 || a.K <= 0) return gemm(kMC, kMC, accumulate ? kAccF32 : kStoreF32, a, s);
   const long ks = ((a.K + splits - 1) / splits + BK - 1) / BK * BK;
   const int S = (int)((a.K + ks - 1) / ks);
   GemmArgs p = a;
@@ -438,8 +443,13 @@ hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, hipS
   hipLaunchKernelGGL((gemm_kernel<128, 128, 2, 2, kMC, kMC, kStoreF32, 3>), dim3((unsigned)tiles),
                      dim3(256), 0, s, p);
   const long n4 = (long)a.M * (a.N / 4);
-  hipLaunchKernelGGL(splitk_reduce_k, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, partial, S,
-                     (long)a.M * a.N, a.M, a.N, reinterpret_cast<float*>(a.C), a.ldc);
+  const dim3 grid((unsigned)((n4 + 255) / 256));
+  if (accumulate)
+    hipLaunchKernelGGL(splitk_reduce_k<true>, grid, dim3(256), 0, s, partial, S, (long)a.M * a.N,
+                       a.M, a.N, reinterpret_cast<float*>(a.C), a.ldc);
+  else
+    hipLaunchKernelGGL(splitk_reduce_k<false>, grid, dim3(256), 0, s, partial, S, (long)a.M * a.N,
+                       a.M, a.N, reinterpret_cast<float*>(a.C), a.ldc);
   return hipGetLastError();
 }
 

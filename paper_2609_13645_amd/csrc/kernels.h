@@ -44,24 +44,27 @@ hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& 
 //   K-grouped (MC, MC): C_e (+)= sum over rows g_off[e].. of A^T B, C_e = C + e * strideC.
 hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
 hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s);
-// Weight gradient C (+)= A^T B (both M/N-contiguous) with the reduction split
+// Weight gradient C += A^T B (or C = A^T B when !accumulate), both operands
+// M/N-contiguous, with the reduction split
 // into `splits` uniform slices: fp32 partials [splits][M][N] in `partial`,
 // then summed in slice order into C. For products with few output tiles and
 // a long reduction (N % 4 == 0). splitk_splits picks the split count (1 =
 // plain GEMM, no partials needed).
 int splitk_splits(int M, int N, int K);
-hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, hipStream_t s);
+hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, bool accumulate,
+                             hipStream_t s);
 
 // --------------------------------------------------------- elementwise ----
 hipError_t rmsnorm_fwd(const uint16_t* x, const uint16_t* g, uint16_t* y, float* rstd,
                        int T, int h, float eps, hipStream_t s);
 // dx = RMSNorm backward (+ resid if non-null); dg_partial [nblk, h] per-block
-// partial sums of dy*x*rstd, reduced into dg (+=) by rmsnorm_dg_reduce.
+// partial sums of dy*x*rstd, reduced into dg (+=, or = when !accumulate)
+// by rmsnorm_dg_reduce.
 int rmsnorm_bwd_blocks(int T);
 hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
                        const uint16_t* dy, const uint16_t* resid, uint16_t* dx,
                        float* dg_partial, int T, int h, hipStream_t s);
-hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h,
+hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h, bool accumulate,
                              hipStream_t s);
 hipError_t rope_table(int seq, int d, float base, float* cos_t, float* sin_t,
                       hipStream_t s);

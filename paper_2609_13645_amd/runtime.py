@@ -144,7 +144,10 @@ class Layer:
                              (self.aux if aux is None else aux) if self.cfg.get("n_experts", 0)
                              else None, self.stream)
 
-    def bwd(self, x_in, d_out, d_in, saved=None, workspace=None):
+    def bwd(self, x_in, d_out, d_in, saved=None, workspace=None, overwrite=False):
+        """Backward; weight gradients are accumulated (+=) into self.g, or
+        written (=) with overwrite (no zeroing needed beforehand)."""
+        self.grads.overwrite = int(overwrite)
         _lib.forge_layer_bwd(self.c, self.weights, self.saved if saved is None else saved,
                              x_in, d_out, d_in, self.grads,
                              self.workspace if workspace is None else workspace, self.stream)
@@ -174,6 +177,9 @@ class Model:
             for n, s in layer_shapes(cfg).items():
                 shapes[f"{i}.{n}"] = s
         self.flat = FlatParams(shapes, device)
+        # the embedding / head tensors come first in the flat buffers
+        self.head_grad_elems = max(self.flat.offsets[n][0] + int(np.prod(shapes[n]))
+                                   for n in shapes if "." not in n)
         self.flat.load_bits("embedding", inputs["embedding"])
         self.flat.load_bits("final_norm", inputs["final_norm"])
         if not self.tied:
@@ -206,10 +212,14 @@ class Model:
     def w_lm(self, buf):
         return self.flat.view(buf, "embedding" if self.tied else "w_lm")
 
-    def forward_backward(self):
+    def forward_backward(self, accumulate=True):
         """Cross-entropy loss (device scalar) and every gradient accumulated
-        into flat.grad; for MoE layers self.aux holds the summed aux losses."""
+        into flat.grad; for MoE layers self.aux holds the summed aux losses.
+        With accumulate=False the gradients are this step's alone: the layers
+        write theirs and only the head / embedding gradients are zeroed."""
         c, s = self.cfg, self.stream
+        if not accumulate:
+            self.flat.grad[:self.head_grad_elems].zero_()
         T, h, V = self.T, c["hidden"], c["vocab"]
         emb = self.flat.view(self.flat.param, "embedding")
         _lib.forge_embed_fwd(self.ids, emb, self.acts[0], T, h, V, s)
@@ -224,7 +234,7 @@ class Model:
                                 self.w_lm(self.flat.grad), self.head_ws, s)
         g_in, g_out = self.grad_a, self.grad_b
         for i in reversed(range(len(self.layers))):
-            self.layers[i].bwd(self.acts[i], g_in, g_out)
+            self.layers[i].bwd(self.acts[i], g_in, g_out, overwrite=not accumulate)
             g_in, g_out = g_out, g_in
         _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
                              T, h, V, s)
@@ -243,8 +253,7 @@ class Model:
                               self.scalars, self.stream)
 
     def train_step(self):
-        self.flat.grad.zero_()
-        loss = self.forward_backward()
+        loss = self.forward_backward(accumulate=False)
         self.optimizer_step()
         return loss
 

@@ -121,6 +121,7 @@ def test_optimizer_argument_rules():
     with pytest.raises(_lib.ForgeError):
         _lib.forge_loss_workspace_bytes(_lib.HeadCfg(16, 64, 1001, 1e-5))  # vocab % 8
     assert ctypes.sizeof(_lib.LayerCfg) == 14 * 4
+    assert ctypes.sizeof(_lib.LayerGrads) == 9 * 8 + 8    # 9 pointers + int32 + padding
 
 
 def test_moe_layer_sizes():

@@ -97,3 +97,32 @@ def test_layer_is_deterministic():
     b, _ = run_layer(cfg, seed=3)
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("which", ["dense", "moe"])
+def test_overwrite_grads_equal_accumulate_into_zeros(which):
+    """grads.overwrite writes every weight gradient: bitwise the values that
+    accumulating into zeroed buffers gives, whatever the buffers held."""
+    import torch
+    from paper_2609_13645_amd import runtime
+    if which == "dense":
+        cfg = fi.config("tiny", batch=2, seq=72, seed=17)
+    else:
+        cfg = fi.config("tiny", batch=1, seq=2048, ffn=0, n_experts=16, top_k=2,
+                        expert_ffn=64, aux_coef=0.05, seed=61)
+    banner(f"overwrite vs accumulate ({which})")
+    inp = fi.layer_inputs(cfg)
+    layer = runtime.Layer(cfg, inp["weights"])
+    x, dy = dev_bf16(inp["x"]), dev_bf16(inp["dy"])
+    out, dx = torch.empty_like(x), torch.empty_like(x)
+    layer.fwd(x, out)
+    layer.zero_grads()
+    layer.bwd(x, dy, dx)
+    torch.cuda.synchronize()
+    acc = {k: v.clone() for k, v in layer.g.items()}
+    for v in layer.g.values():
+        v.fill_(float("nan"))
+    layer.bwd(x, dy, dx, overwrite=True)
+    torch.cuda.synchronize()
+    for k, v in layer.g.items():
+        assert torch.equal(v, acc[k]), k

@@ -105,3 +105,28 @@ def test_model_step_is_deterministic_except_embedding_scatter():
             assert rel_fro(res[0][1][k], res[1][1][k]) <= 1e-6
         else:
             assert np.array_equal(res[0][1][k], res[1][1][k]), k
+
+
+def test_model_step_without_accumulation_matches_zeroed_accumulation():
+    """forward_backward(accumulate=False) gives this step's gradients whatever
+    the gradient buffer held: layers overwrite, head / embedding are zeroed."""
+    import torch
+    from paper_2609_13645_amd import runtime
+    cfg = fi.config("tiny", n_layers=2, tied=True, seq=64, vocab=512, seed=33)
+    banner("model step without accumulation")
+    inp = fi.model_inputs(cfg)
+    model = runtime.Model(cfg, inp)
+    model.flat.grad.zero_()
+    l1 = float(model.forward_backward().item())
+    torch.cuda.synchronize()
+    ref = model.flat.grad.clone()
+    model.flat.grad.fill_(float("nan"))
+    l2 = float(model.forward_backward(accumulate=False).item())
+    torch.cuda.synchronize()
+    assert l1 == l2
+    pad = torch.isnan(model.flat.grad) & (ref == 0)   # alignment gaps are never written
+    got = torch.where(pad, torch.zeros_like(ref), model.flat.grad)
+    assert torch.equal(got[:model.head_grad_elems] != 0, ref[:model.head_grad_elems] != 0)
+    assert rel_fro(got[:model.head_grad_elems].cpu().numpy(),
+                   ref[:model.head_grad_elems].cpu().numpy()) <= 1e-6
+    assert torch.equal(got[model.head_grad_elems:], ref[model.head_grad_elems:])
