@@ -198,22 +198,30 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     tm = first_m + (pid % in_group) % gsize;
     tn = (pid % in_group) / gsize;
   } else if (GROUP == 1) {
-    // M-grouped: global m-tile index -> (group, local m-tile); groups whose
-    // rows are exhausted leave the surplus blocks of the upper-bound grid idle
+    // M-grouped. The grid is an upper bound (host does not know the group
+    // sizes); the real tiles are counted from the device offsets and dealt
+    // to the 8 XCDs (workgroup b runs on XCD b % 8) as balanced contiguous
+    // ranges. Within a range, group by group, n-tile major with the group's
+    // m-tiles consecutive: a B_e column block is reused from L2 by all of the
+    // group's m-tiles, an A row block by neighbouring n-tiles.
     const int tiles_n = (p.N + BN - 1) / BN;
-    const int gt = blockIdx.x / tiles_n;
-    tn = blockIdx.x % tiles_n;
-    int e = 0, acc = 0, rows = 0;
+    int total = 0;
+    for (int e = 0; e < p.groups; ++e) total += (p.g_off[e + 1] - p.g_off[e] + BM - 1) / BM;
+    const int real = total * tiles_n;
+    const int per = (real + NUM_XCD - 1) / NUM_XCD;
+    const int li = blockIdx.x / NUM_XCD;
+    const int pid = (blockIdx.x % NUM_XCD) * per + li;
+    if (li >= per || pid >= real) return;
+    int e = 0, acc = 0, mte = 0;
     for (; e < p.groups; ++e) {
-      rows = p.g_off[e + 1] - p.g_off[e];
-      const int te = (rows + BM - 1) / BM;
-      if (gt < acc + te) break;
-      acc += te;
+      mte = (p.g_off[e + 1] - p.g_off[e] + BM - 1) / BM;
+      if (pid < acc + mte * tiles_n) break;
+      acc += mte * tiles_n;
     }
-    if (e >= p.groups) return;
-    tm = gt - acc;
+    tm = (pid - acc) % mte;
+    tn = (pid - acc) / mte;
     const long r0 = p.g_off[e];
-    p.M = rows;
+    p.M = p.g_off[e + 1] - p.g_off[e];
     p.A += r0 * p.lda;  // K-contiguous A: group rows are row blocks
     p.B += (long)e * p.strideB;
     p.C = (char*)p.C + r0 * p.ldc * (EPI == kStoreBF16 || EPI == kResidBF16 ? 2 : 4);
@@ -233,11 +241,15 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     p.B += k0 * p.ldb;
     p.C = (char*)p.C + (long)e * p.strideC * 4;
   } else {
-    // K-grouped: one (m, n) tile grid per group, reduction over the group's rows
+    // K-grouped: one (m, n) tile grid per group, reduction over the group's
+    // rows; XCD-contiguous ranges of tiles, group by group
     const int tiles_m = (p.M + BM - 1) / BM;
     const int tiles_n = (p.N + BN - 1) / BN;
-    const int e = blockIdx.x / (tiles_m * tiles_n);
-    const int t = blockIdx.x % (tiles_m * tiles_n);
+    const int nb = gridDim.x, bid = blockIdx.x;
+    const int nb8 = nb - nb % NUM_XCD;
+    const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
+    const int e = pid / (tiles_m * tiles_n);
+    const int t = pid % (tiles_m * tiles_n);
     tm = t / tiles_n;
     tn = t % tiles_n;
     const long r0 = p.g_off[e];
@@ -342,8 +354,10 @@ hipError_t launch(const GemmArgs& a, hipStream_t s) {
 // M-grouped: at most M / BM + groups m-tiles exist, whatever the group sizes.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LB, int EPI>
 hipError_t launch_grouped_m(const GemmArgs& a, hipStream_t s) {
+  // real tiles <= (M / BM + groups) * tiles_n; rounded up so that every XCD's
+  // share of the workgroups covers ceil(real / 8) tiles
   const long mt = a.M / BM + a.groups;
-  const long tiles = mt * ((a.N + BN - 1) / BN);
+  const long tiles = ((mt * ((a.N + BN - 1) / BN) + NUM_XCD - 1) / NUM_XCD + 1) * NUM_XCD;
   hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, kKC, LB, EPI, 1>), dim3((unsigned)tiles),
                      dim3(WAVES_M * WAVES_N * 64), 0, s, a);
   return hipGetLastError();
