@@ -33,6 +33,16 @@ constexpr int CHUNKS = BK / 8;  // 16-byte chunks per LDS tile row
 constexpr int GROUP_M = 8;
 constexpr int NUM_XCD = 8;
 
+__device__ __forceinline__ int wave_incl_scan_int(int v) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d, 64);
+    if ((int)(threadIdx.x & 63) >= d) v += u;
+  }
+  return v;
+}
+__device__ __forceinline__ int wave_sum_int(int v) { return __shfl(wave_incl_scan_int(v), 63, 64); }
+
 __device__ __forceinline__ int swz(int row, int c) {
   return row * CHUNKS + (c ^ ((row ^ (row >> 3)) & 7));
 }
@@ -205,19 +215,39 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     // m-tiles consecutive: a B_e column block is reused from L2 by all of the
     // group's m-tiles, an A row block by neighbouring n-tiles.
     const int tiles_n = (p.N + BN - 1) / BN;
+    // group sizes in m-tiles, 64 groups per wave-wide step (one coalesced
+    // load, a lane per group, prefix sums across the wave)
+    const int ln = threadIdx.x & 63;
     int total = 0;
-    for (int e = 0; e < p.groups; ++e) total += (p.g_off[e + 1] - p.g_off[e] + BM - 1) / BM;
+    for (int base = 0; base < p.groups; base += 64) {
+      const int g = base + ln;
+      const int mt = g < p.groups ? (p.g_off[g + 1] - p.g_off[g] + BM - 1) / BM : 0;
+      total += wave_sum_int(mt);
+    }
     const int real = total * tiles_n;
     const int per = (real + NUM_XCD - 1) / NUM_XCD;
     const int li = blockIdx.x / NUM_XCD;
     const int pid = (blockIdx.x % NUM_XCD) * per + li;
     if (li >= per || pid >= real) return;
-    int e = 0, acc = 0, mte = 0;
-    for (; e < p.groups; ++e) {
-      mte = (p.g_off[e + 1] - p.g_off[e] + BM - 1) / BM;
-      if (pid < acc + mte * tiles_n) break;
-      acc += mte * tiles_n;
+    int e = 0, acc = 0, mte = 1;
+    for (int base = 0; base < p.groups; base += 64) {
+      const int g = base + ln;
+      const int mt = g < p.groups ? (p.g_off[g + 1] - p.g_off[g] + BM - 1) / BM : 0;
+      const int incl = wave_incl_scan_int(mt * tiles_n);
+      const int excl = incl - mt * tiles_n;
+      const uint64_t hit = __ballot(mt > 0 && pid >= acc + excl && pid < acc + incl);
+      if (hit) {
+        const int l = __ffsll((unsigned long long)hit) - 1;
+        e = base + l;
+        mte = __shfl(mt, l, 64);
+        acc += __shfl(excl, l, 64);
+        break;
+      }
+      acc += __shfl(incl, 63, 64);
     }
+    e = __builtin_amdgcn_readfirstlane(e);
+    mte = __builtin_amdgcn_readfirstlane(mte);
+    acc = __builtin_amdgcn_readfirstlane(acc);
     tm = (pid - acc) % mte;
     tn = (pid - acc) / mte;
     const long r0 = p.g_off[e];
