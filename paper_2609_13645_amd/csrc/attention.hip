@@ -282,10 +282,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
 }
 
 // -------------------------------------------------- backward pre-pass ----
-// delta[b, n, s] = sum_d dO[t, n, d] O[t, n, d]; 8 lanes per (token, head).
+// delta[b, n, s] = sum_d dO[t, n, d] O[t, n, d] and, in the second half of
+// the buffer, -LSE[b, n, s] * log2(e) (the exponent offset of P = exp(S - LSE)
+// in base 2); 8 lanes per (token, head).
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* __restrict__ o,
                                                       const bf16_t* __restrict__ dout,
+                                                      const float* __restrict__ lse,
                                                       float* __restrict__ delta) {
   const long id = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
   const int sub = threadIdx.x & 7;
@@ -310,7 +313,9 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* 
   s += __shfl_xor(s, 4, 64);
   if (ok && sub == 0) {
     const long bb = t / a.seq, i = t % a.seq;
-    delta[(bb * a.n_heads + n) * a.seq + i] = s;
+    const long li = (bb * a.n_heads + n) * a.seq + i;
+    delta[li] = s;
+    delta[T * a.n_heads + li] = -lse[li] * kLog2e;
   }
 }
 
@@ -328,8 +333,8 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* 
 // registers) reads them in place.
 template <int D, int PASS>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
-    AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ lse,
-    const float* __restrict__ delta, float* __restrict__ pk, float* __restrict__ pv) {
+    AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ delta,
+    float* __restrict__ pk, float* __restrict__ pv) {
   constexpr int BKEY = 128, BQ = 64, NAT = BQ * D / 8;
   constexpr int STAGE = 2 * NAT + 32;  // Q tile, dO tile, lse[64], delta[64]
   __shared__ uint4 sm0[STAGE];
@@ -352,7 +357,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
   const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
   const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
   const bf16_t* dOg = dout + rb * ldo + (long)n * D;
-  const float* Lg = lse + ((long)b * a.n_heads + n) * S;
+  const long nrows = (long)a.batch * a.n_heads * S;
+  const float* Lg = delta + nrows + ((long)b * a.n_heads + n) * S;  // -LSE log2(e)
   const float* Dg = delta + ((long)b * a.n_heads + n) * S;
   // K (and, for PASS 1, V) rows of this lane's key: the B operands of S, dP
   bf16x8_t kf[D / 16], vf[PASS ? D / 16 : 1];
@@ -430,15 +436,27 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     }
     const bool diag = (q0 < kw0 + 31);
     const bool tail = (q0 + BQ > S);
+    // P = exp2(S c - LSE log2 e); the masks only on diagonal / tail tiles
+    if (diag || tail) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-        float p = fast_exp2(__builtin_fmaf(s[qb][i], c, -L[qi] * kLog2e));
-        if ((diag && key > q0 + qi) || (tail && q0 + qi >= S)) p = 0.0f;
-        s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
-      }
+        for (int i = 0; i < 16; ++i) {
+          const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+          float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
+          if (key > q0 + qi || q0 + qi >= S) p = 0.0f;
+          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
+        }
+    } else {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+          const float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
+          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
+        }
+    }
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -521,7 +539,6 @@ __global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict
 // fragment reads and explicit waits as in the forward.
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
-                                                const float* __restrict__ lse,
                                                 const float* __restrict__ delta,
                                                 bf16_t* __restrict__ dq, long ld_d) {
   constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
@@ -550,7 +567,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
     of[kk] = gload_frag(dOg + (long)q * ldo + kk * 16 + hh * 8, q < S);
   }
   const long li = ((long)b * a.n_heads + n) * S + q;
-  const float nl2 = q < S ? -lse[li] * kLog2e : -INFINITY;
+  const float nl2 = q < S ? delta[(long)a.batch * a.n_heads * S + li] : -INFINITY;
   const float dl = q < S ? delta[li] : 0.0f;
   f32x16_t dqa[DB];
 #pragma unroll
@@ -603,17 +620,23 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
 #pragma unroll
         for (int db = 0; db < DB; ++db) ft[kb][ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
     const bool diag = (k0 + BKV - 1 > q0w);
+    if (diag) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float p = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2));
-        if (diag) {
+        for (int i = 0; i < 16; ++i) {
+          float p = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2));
           const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
           if (key > q) p = 0.0f;
+          dp[kb][i] = p * (dp[kb][i] - dl);
         }
-        dp[kb][i] = p * (dp[kb][i] - dl);
-      }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          dp[kb][i] = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2)) * (dp[kb][i] - dl);
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -665,12 +688,12 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout, float* delta,
-                        hipStream_t s) {
+hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
+                        const float* lse, float* delta, hipStream_t s) {
   const long n = (long)a.batch * a.seq * a.n_heads * 8;
   const dim3 grid((unsigned)((n + 255) / 256)), block(256);
-  if (a.d == 128) hipLaunchKernelGGL(attn_bwd_pre_k<128>, grid, block, 0, s, a, o, dout, delta);
-  else if (a.d == 64) hipLaunchKernelGGL(attn_bwd_pre_k<64>, grid, block, 0, s, a, o, dout, delta);
+  if (a.d == 128) hipLaunchKernelGGL(attn_bwd_pre_k<128>, grid, block, 0, s, a, o, dout, lse, delta);
+  else if (a.d == 64) hipLaunchKernelGGL(attn_bwd_pre_k<64>, grid, block, 0, s, a, o, dout, lse, delta);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -679,16 +702,15 @@ size_t attn_bwd_partial_floats(const AttnArgs& a) {
   return (size_t)(a.n_heads / a.n_kv_heads) * a.batch * a.seq * a.n_kv_heads * a.d;
 }
 
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* lse,
-                         const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
+hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
                          long ld_d, hipStream_t s) {
   const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
   if (a.d == 128) {
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 0>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 1>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 0>), grid, block, 0, s, a, dout, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 1>), grid, block, 0, s, a, dout, delta, pk, pv);
   } else if (a.d == 64) {
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 0>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 1>), grid, block, 0, s, a, dout, lse, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 0>), grid, block, 0, s, a, dout, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 1>), grid, block, 0, s, a, dout, delta, pk, pv);
   } else {
     return hipErrorInvalidValue;
   }
@@ -702,13 +724,12 @@ hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* l
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* lse,
-                       const float* delta, uint16_t* dq, long ld_d, hipStream_t s) {
+hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* delta, uint16_t* dq, long ld_d, hipStream_t s) {
   const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
   if (a.d == 128)
-    hipLaunchKernelGGL(attn_bwd_dq_k<128>, grid, block, 0, s, a, dout, lse, delta, dq, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<128>, grid, block, 0, s, a, dout, delta, dq, ld_d);
   else if (a.d == 64)
-    hipLaunchKernelGGL(attn_bwd_dq_k<64>, grid, block, 0, s, a, dout, lse, delta, dq, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<64>, grid, block, 0, s, a, dout, delta, dq, ld_d);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -202,7 +202,7 @@ Work work_layout(const forge_layer_cfg& c) {
   w.db = take(d.T * d.h * 2);
   w.dh1 = take(d.T * d.h * 2);
   w.dO = take(d.T * d.hq * 2);
-  w.delta = take(d.B * d.nh * d.S * 4);
+  w.delta = take(2 * d.B * d.nh * d.S * 4);   // delta, then -lse log2(e)
   w.dqkv = take(d.T * d.qkv * 2);
   w.da = take(d.T * d.h * 2);
   w.dg = take((size_t)forge::rmsnorm_bwd_blocks((int)d.T) * d.h * 4);
@@ -343,11 +343,11 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                         gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
   FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                         gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
-  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, delta, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, lse, delta, at<float>(workspace, wk.pk),
+  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, lse, delta, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
                                  at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
                                  d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dq(aa, dO, lse, delta, dqkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, dO, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
                               (int)(d.nh + d.nkv), (int)d.d, true, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
@@ -939,7 +939,7 @@ forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size
   FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
   const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
                       cfg->n_kv_heads * cfg->head_dim * 4;
-  *bytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4) + 2 * up(part);
+  *bytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4) + 2 * up(part);
   return ok();
 }
 
@@ -957,15 +957,15 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
   const forge::AttnArgs aa = attn_args(d, qkv);
   hipStream_t s = (hipStream_t)stream;
   float* delta = static_cast<float*>(workspace);
-  const size_t dbytes = up((size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
+  const size_t dbytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
   const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
                       cfg->n_kv_heads * cfg->head_dim * 4;
   float* pk = at<float>(workspace, dbytes);
   float* pv = at<float>(workspace, dbytes + up(part));
-  FORGE_HIP(forge::attn_bwd_pre(aa, o, d_o, delta, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, lse, delta, pk, pv, d_qkv + d.hq,
+  FORGE_HIP(forge::attn_bwd_pre(aa, o, d_o, lse, delta, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, delta, pk, pv, d_qkv + d.hq,
                                  d_qkv + d.hq + d.hkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dq(aa, d_o, lse, delta, d_qkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, d_o, delta, d_qkv, d.qkv, s));
   return ok();
 }
 

@@ -102,19 +102,18 @@ struct AttnArgs {
 };
 // o [T, n_heads*d] bf16; lse [batch, n_heads, seq] fp32 (natural log).
 hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s);
-// delta[b,n,i] = sum_d dO*O (fp32).
+// delta: 2 * batch * n_heads * seq fp32: [b,n,i] = sum_d dO*O, then the
+// second half [b,n,i] = -lse * log2(e) (read by the two kernels below).
 hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
-                        float* delta, hipStream_t s);
+                        const float* lse, float* delta, hipStream_t s);
 // Floats of each of the two fp32 partial buffers attn_bwd_dkdv needs
 // ([n_heads / n_kv_heads][T][n_kv * d]).
 size_t attn_bwd_partial_floats(const AttnArgs& a);
 // dk, dv [T, n_kv*d] columns of the dqkv buffer (row stride ld_dqkv), via
 // per-query-head fp32 partials pk, pv summed in a fixed order.
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* lse,
-                         const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
+hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
                          long ld_dqkv, hipStream_t s);
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* lse,
-                       const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
+hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
 
 // ----------------------------------------------------------------- MoE ----
 // Routing of fp32 logits [T, E] (E <= 64): idx / gates [T, k], probs [T, E].
