@@ -402,7 +402,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       zero(s[qb]);
-      if (PASS) zero(dp[qb]);
+      if (PASS) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)   // dP - delta, formed by the MFMAs
+          dp[qb][i] = -Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
+      }
     }
     bf16x8_t fq[D / 16][2], fo[D / 16][2];
 #pragma unroll
@@ -445,7 +449,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
           const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
           float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
           if (key > q0 + qi || q0 + qi >= S) p = 0.0f;
-          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
+          s[qb][i] = PASS ? p * dp[qb][i] : p;
         }
     } else {
 #pragma unroll
@@ -454,7 +458,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
         for (int i = 0; i < 16; ++i) {
           const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
           const float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
-          s[qb][i] = PASS ? p * (dp[qb][i] - Dl[qi]) : p;
+          s[qb][i] = PASS ? p * dp[qb][i] : p;
         }
     }
 #pragma unroll
