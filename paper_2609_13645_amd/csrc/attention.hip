@@ -623,24 +623,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
       for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
         for (int db = 0; db < DB; ++db) ft[kb][ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
-    const bool diag = (k0 + BKV - 1 > q0w);
-    if (diag) {
+    // the causal mask (diagonal tiles only) as -inf scores: exp2 gives 0
+    if (k0 + BKV - 1 > q0w) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          float p = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2));
           const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          if (key > q) p = 0.0f;
-          dp[kb][i] = p * (dp[kb][i] - dl);
+          if (key > q) s[kb][i] = -INFINITY;
         }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          dp[kb][i] = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2)) * (dp[kb][i] - dl);
     }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        dp[kb][i] = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2)) * (dp[kb][i] - dl);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
