@@ -440,27 +440,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     }
     const bool diag = (q0 < kw0 + 31);
     const bool tail = (q0 + BQ > S);
-    // P = exp2(S c - LSE log2 e); the masks only on diagonal / tail tiles
+    // P = exp2(S c - LSE log2 e); on diagonal / tail tiles the masked
+    // scores are set to -inf first, so exp2 gives 0
     if (diag || tail) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
-          if (key > q0 + qi || q0 + qi >= S) p = 0.0f;
-          s[qb][i] = PASS ? p * dp[qb][i] : p;
-        }
-    } else {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          const float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
-          s[qb][i] = PASS ? p * dp[qb][i] : p;
+          if (key > q0 + qi || q0 + qi >= S) s[qb][i] = -INFINITY;
         }
     }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
+        const float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
+        s[qb][i] = PASS ? p * dp[qb][i] : p;
+      }
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
