@@ -8,7 +8,10 @@
 //
 //  * A block tile BM x BN x 64 is staged through LDS, double-buffered, with
 //    one barrier per k-step, placed before the step's last 16-deep slice so
-//    that MFMAs are ready to issue as the waves leave it. Tiles are filled by buffer_load ... lds (global
+//    that MFMAs are ready to issue as the waves leave it. The barrier also
+//    frees the buffer of the current step, which is refilled at once with
+//    the step after next: each tile's loads have a full k-step of MFMAs to
+//    land in. Tiles are filled by buffer_load ... lds (global
 //    to LDS without registers); out-of-range chunks read as zeros through the
 //    buffer descriptor's range check, so ragged edges need no branches.
 //  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
@@ -308,7 +311,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
 
   // ---- main loop: the barrier that publishes tile t+1 sits before the last
   // 16-deep k-slice of tile t, so every wave leaves it with that slice's
-  // MFMAs to issue while the first fragments of tile t+1 are read.
+  // MFMAs to issue while the first fragments of tile t+1 are read; right
+  // after it, tile t+2 is loaded into tile t's buffer.
   const int nk = (p.K + BK - 1) / BK;
   constexpr int KS = BK / 16;
   la.load(p.A, p.lda, m0, p.M, 0, p.K, lds[0], wave, lane);
@@ -319,15 +323,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   for (int i = 0; i < FN; ++i) fa[0][i] = frag<LB, BN>(lds[0] + A_ELEMS, wn * WN + i * 32, 0, lane);
 #pragma unroll
   for (int j = 0; j < FM; ++j) fb[0][j] = frag<LA, BM>(lds[0], wm * WM + j * 32, 0, lane);
+  // tile 1 into the second buffer (past the end: zeros into an unused buffer)
+  la.load(p.A, p.lda, m0, p.M, BK, p.K, lds[1], wave, lane);
+  lb.load(p.B, p.ldb, n0, p.N, BK, p.K, lds[1] + A_ELEMS, wave, lane);
 
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     const uint4* At = lds[cur];
     const uint4* Bt = lds[cur] + A_ELEMS;
-    // tile t+1 into the other buffer, whose last reads finished before the
-    // previous barrier; past the end it reads zeros into an unused buffer
-    la.load(p.A, p.lda, m0, p.M, (kt + 1) * BK, p.K, lds[cur ^ 1], wave, lane);
-    lb.load(p.B, p.ldb, n0, p.N, (kt + 1) * BK, p.K, lds[cur ^ 1] + A_ELEMS, wave, lane);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int cb = kk & 1, nx = cb ^ 1;
@@ -347,6 +350,10 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
         for (int i = 0; i < FN; ++i) fa[nx][i] = frag<LB, BN>(Bn, wn * WN + i * 32, 0, lane);
 #pragma unroll
         for (int j = 0; j < FM; ++j) fb[nx][j] = frag<LA, BM>(An, wm * WM + j * 32, 0, lane);
+        // every wave's reads of tile t are complete: its buffer takes tile
+        // t+2 (all zeros past the end)
+        la.load(p.A, p.lda, m0, p.M, (kt + 2) * BK, p.K, lds[cur], wave, lane);
+        lb.load(p.B, p.ldb, n0, p.N, (kt + 2) * BK, p.K, lds[cur] + A_ELEMS, wave, lane);
       }
 #pragma unroll
       for (int i = 0; i < FN; ++i)
@@ -356,6 +363,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+
+  __builtin_amdgcn_s_waitcnt(0);  // the last (all-zero) tile loads land before exit
 
   // ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block ------
 #pragma unroll
