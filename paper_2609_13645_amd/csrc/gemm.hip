@@ -4,21 +4,33 @@
 // backward of each GEMM is one data-gradient and one weight-gradient
 // product): y = x W^T (both operands K-contiguous), dX = dY W (W is
 // N-contiguous) and dW += dY^T X (both operands M/N-contiguous, reduction
-// over tokens). One kernel template covers all three:
+// over tokens). Two pipelines share tile order, operand layouts and epilogue:
 //
-//  * A block tile BM x BN x 64 is staged through LDS, double-buffered, with
-//    one barrier per k-step, placed before the step's last 16-deep slice so
-//    that MFMAs are ready to issue as the waves leave it. The barrier also
-//    frees the buffer of the current step, which is refilled at once with
-//    the step after next: each tile's loads have a full k-step of MFMAs to
-//    land in. Tiles are filled by buffer_load ... lds (global
-//    to LDS without registers); out-of-range chunks read as zeros through the
-//    buffer descriptor's range check, so ragged edges need no branches.
+//  * gemm_kernel (both operands K-contiguous): a block tile BM x BN x 64 is
+//    staged through LDS, double-buffered, with one barrier per k-step, placed
+//    before the step's last 16-deep slice so that MFMAs are ready to issue as
+//    the waves leave it. The barrier also frees the buffer of the current
+//    step, which is refilled at once with the step after next. Tiles are
+//    filled by buffer_load ... lds (global to LDS without registers) in
+//    128-byte row segments (whole cache lines); out-of-range chunks read as
+//    zeros through the buffer descriptor's range check, so ragged edges need
+//    no branches.
+//  * ring_kernel (an operand contiguous along M / N): a ring of four 32-deep
+//    stages. The barrier that publishes stage s + 1 sits after the first MFMAs
+//    of stage s's last slice; right after it the DMA for stage s + 4 starts
+//    into the slot stage s has just released, spread over the next two slices
+//    (one instruction per two MFMAs), so no burst fills the texture unit's
+//    queues and every stage has three stages of MFMAs to land in. Fragment
+//    reads are issued as inline asm with explicit lgkmcnt waits: the
+//    compiler cannot tell the transposing reads apart from the DMA writes and
+//    would otherwise wait for every outstanding DMA before each of them.
 //  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
-//    chunk c of row r at c ^ ((r ^ (r >> 3)) & 7)); each MFMA operand is one
-//    16-byte LDS read. An operand contiguous along M / N is stored as it lies
-//    in HBM and read with gfx950's ds_read_b64_tr_b16 transpose reads, so
-//    dgrad and wgrad need no transpose pass.
+//    chunk c of row r at c ^ ((r ^ (r >> 3)) & 7)) in gemm_kernel and 64-byte
+//    rows (chunk c of row r at c ^ ((r >> 2) & 3)) in a ring stage; both keep
+//    each group of 16 lanes of a fragment read on distinct banks. Each MFMA
+//    operand is one 16-byte LDS read. An operand contiguous along M / N is
+//    stored as it lies in HBM and read with gfx950's ds_read_b64_tr_b16
+//    transpose reads, so dgrad and wgrad need no transpose pass.
 //  * The MFMA computes D = Btile * Atile^T, i.e. C transposed, so each lane's
 //    four consecutive accumulator rows are four consecutive n of one row m of
 //    C: the epilogue writes 8-byte (bf16) or 16-byte (fp32) vectors.
@@ -188,15 +200,29 @@ __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const fl
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
-__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
-  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-  constexpr int FM = WM / 32, FN = WN / 32;
-  static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
-  constexpr int A_ELEMS = BM * CHUNKS, B_ELEMS = BN * CHUNKS;
-  __shared__ uint4 lds[2][A_ELEMS + B_ELEMS];
+// ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block -------
+template <int EPI, int FN, int FM>
+__device__ __forceinline__ void store_tile(const GemmArgs& p, const f32x16_t (&acc)[FN][FM],
+                                           int mw, int nw, int lane) {
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const int m = mw + j * 32 + (lane & 31);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = nw + i * 32 + g * 8 + (lane >> 5) * 4;
+        float v[4] = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
+                      acc[i][j][g * 4 + 3]};
+        store4<EPI>(p, m, n, v);
+      }
+    }
+}
 
-  int tm, tn;
+// Tile of this workgroup (tm, tn) and the group-adjusted arguments; false
+// when the workgroup has no tile (M-grouped launches over-provision).
+template <int BM, int BN, int EPI, int GROUP>
+__device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn) {
   if (GROUP == 0) {
     // ---- tile order: XCD-contiguous bands, GROUP_M rows of tiles per band ----
     const int tiles_m = (p.M + BM - 1) / BM;
@@ -231,7 +257,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     const int per = (real + NUM_XCD - 1) / NUM_XCD;
     const int li = blockIdx.x / NUM_XCD;
     const int pid = (blockIdx.x % NUM_XCD) * per + li;
-    if (li >= per || pid >= real) return;
+    if (li >= per || pid >= real) return false;
     int e = 0, acc = 0, mte = 1;
     for (int base = 0; base < p.groups; base += 64) {
       const int g = base + ln;
@@ -291,6 +317,19 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
     p.B += r0 * p.ldb;
     p.C = (char*)p.C + (long)e * p.strideC * 4;
   }
+  return true;
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
+  constexpr int A_ELEMS = BM * CHUNKS, B_ELEMS = BN * CHUNKS;
+  __shared__ uint4 lds[2][A_ELEMS + B_ELEMS];
+
+  int tm, tn;
+  if (!tile_setup<BM, BN, EPI, GROUP>(p, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int lane = threadIdx.x & 63;
@@ -365,28 +404,218 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   }
 
   __builtin_amdgcn_s_waitcnt(0);  // the last (all-zero) tile loads land before exit
+  store_tile<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
+}
 
-  // ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block ------
+// ---- ring pipeline: four 32-deep stages -----------------------------------
+// Stage slot = A part then B part. K-contiguous operand: ROWS rows of four
+// 16-byte chunks (k 0..31), chunk c of row r at c ^ ((r >> 2) & 3).
+// M/N-contiguous operand: 32 k-rows of ROWS elements (mc_elem layout).
+constexpr int SK = 32;
+
+template <int ROWS, int NW>
+struct RingPart {
+  static constexpr int ELEMS = ROWS * 4;         // 16-byte chunks per stage
+  static constexpr int PER = ROWS * 4 / 64 / NW;  // DMA instructions per wave per stage
+  static_assert(PER * 64 * NW == ROWS * 4, "stage tile must split over the waves");
+};
+
+__device__ __forceinline__ int kc4(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+
+__device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)ptr;
+}
+
+// DMA instruction i (of RingPart::PER) of this wave for one operand of a stage.
+template <int ROWS, int NW, int LAYOUT>
+__device__ __forceinline__ void ring_dma(int i, const bf16_t* __restrict__ src, long ld, int row0,
+                                         int rows_lim, int k0, int K, uint4* part, int wave,
+                                         int lane) {
+  const int blk = i * NW + wave;  // 1 KB block of the stage's part
+  if (LAYOUT == kKC) {
+    const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)row0 * ld + k0);
+    const int row = blk * 16 + (lane >> 2);
+    const int c = (lane & 3) ^ ((row >> 2) & 3);
+    const bool ok = (row0 + row < rows_lim) && (k0 + c * 8 < K);
+    const uint32_t off = ok ? (uint32_t)(((long)row * ld + c * 8) * 2) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(part + blk * 64), 16, off, 0, 0, 0);
+  } else {
+    constexpr int LPR = ROWS / 8;  // lanes per k-row
+    constexpr int RPI = 64 / LPR;  // k-rows per instruction
+    const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)k0 * ld + row0);
+    const int k = blk * RPI + lane / LPR;
+    const int c = (lane % LPR) ^ ((k & 3) << 2);
+    const bool ok = (k0 + k < K) && (row0 + c * 8 < rows_lim);
+    const uint32_t off = ok ? (uint32_t)(((long)k * ld + c * 8) * 2) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(part + blk * 64), 16, off, 0, 0, 0);
+  }
+}
+
+// Fragment of rows base..base+31 over 16-deep slice j of a stage; issued as
+// asm (not tracked by the compiler: ring_fence waits for it).
+template <int LAYOUT, int ROWS>
+__device__ __forceinline__ bf16x8_t ring_frag(const uint4* part, int base, int j, int lane) {
+  if (LAYOUT == kKC) {
+    const uint32_t a = lds_addr(part + kc4(base + (lane & 31), j * 2 + (lane >> 5)));
+    uint4 r;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a) : "memory");
+    return __builtin_bit_cast(bf16x8_t, r);
+  } else {
+    const uint16_t* t = reinterpret_cast<const uint16_t*>(part);
+    const int g = lane >> 4, i = lane & 15;
+    const int m = base + (g & 1) * 16 + 4 * (i & 3);
+    const int k = j * 16 + (g >> 1) * 8 + (i >> 2);
+    const uint32_t a0 = lds_addr(t + mc_elem<ROWS>(k, m));
+    const uint32_t a1 = lds_addr(t + mc_elem<ROWS>(k + 4, m));
+    uint2 lo, hi;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a0) : "memory");
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a1) : "memory");
+    return __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+  }
+}
+
+// Wait for every outstanding LDS read; the fragments count as rewritten here,
+// so nothing that uses (or reuses the registers of) them moves above the wait.
+template <int FN, int FM>
+__device__ __forceinline__ void ring_fence(bf16x8_t (&fa)[FN], bf16x8_t (&fb)[FM]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < FN; ++i) asm volatile("" : "+v"(fa[i]));
+#pragma unroll
+  for (int j = 0; j < FM; ++j) asm volatile("" : "+v"(fb[j]));
+}
+
+// At most N DMA instructions of this wave still outstanding.
+template <int N>
+__device__ __forceinline__ void wait_dma() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs p) {
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
+  constexpr int NW = WAVES_M * WAVES_N;
+  constexpr int AE = RingPart<BM, NW>::ELEMS, BE = RingPart<BN, NW>::ELEMS;
+  constexpr int DA = RingPart<BM, NW>::PER, DB = RingPart<BN, NW>::PER;
+  constexpr int D = DA + DB;  // DMA instructions per wave per stage
+  constexpr int NF = FN + FM, NM = FN * FM;
+  constexpr int SLOT = AE + BE;
+  constexpr int BAR_AT = 2;   // MFMAs of a stage's last slice issued before its barrier
+  static_assert(NM > BAR_AT, "wave tile too small for the barrier placement");
+  __shared__ uint4 lds[4 * SLOT];
+
+  int tm, tn;
+  if (!tile_setup<BM, BN, EPI, GROUP>(p, tm, tn)) return;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+
+  f32x16_t acc[FN][FM];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      const int m = m0 + wm * WM + j * 32 + (lane & 31);
+    for (int j = 0; j < FM; ++j)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * WN + i * 32 + g * 8 + (lane >> 5) * 4;
-        float v[4] = {acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2],
-                      acc[i][j][g * 4 + 3]};
-        store4<EPI>(p, m, n, v);
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+  const int nst = (p.K + SK - 1) / SK;
+
+  // DMA instruction d (0..D-1) of stage st into slot st % 4 (zeros past K)
+  auto dma = [&](int st, int d) {
+    uint4* slot = lds + (st & 3) * SLOT;
+    if (d < DA) ring_dma<BM, NW, LA>(d, p.A, p.lda, m0, p.M, st * SK, p.K, slot, wave, lane);
+    else ring_dma<BN, NW, LB>(d - DA, p.B, p.ldb, n0, p.N, st * SK, p.K, slot + AE, wave, lane);
+  };
+  // fragment f (B fragments first, then A) of slice j of stage st
+  auto read = [&](bf16x8_t* fa_, bf16x8_t* fb_, int st, int j, int f) {
+    const uint4* slot = lds + (st & 3) * SLOT;
+    if (f < FN) fa_[f] = ring_frag<LB, BN>(slot + AE, wn * WN + f * 32, j, lane);
+    else fb_[f - FN] = ring_frag<LA, BM>(slot, wm * WM + (f - FN) * 32, j, lane);
+  };
+
+  // prologue: stages 0..2 in flight; publish stage 0; its first fragments;
+  // first half of stage 3
+#pragma unroll
+  for (int st = 0; st < 3; ++st)
+#pragma unroll
+    for (int d = 0; d < D; ++d) dma(st, d);
+  wait_dma<2 * D>();
+  __builtin_amdgcn_s_barrier();
+  bf16x8_t fa[2][FN], fb[2][FM];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) read(fa[0], fb[0], 0, 0, f);
+#pragma unroll
+  for (int d = 0; d < D / 2; ++d) dma(3, d);
+
+  for (int st = 0; st < nst; ++st) {
+    // slice 0: fragments of slice 1 early, second half of stage st + 3 late
+    ring_fence<FN, FM>(fa[0], fb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    {
+      int fr = 0, dm = D / 2;
+#pragma unroll
+      for (int q = 0; q < NM; ++q) {
+        const int i = q / FM, j = q % FM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+        if (fr < NF) read(fa[1], fb[1], st, 1, fr++);
+        else if (dm < D && (q & 1)) dma(st + 3, dm++);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      for (; fr < NF; ++fr) read(fa[1], fb[1], st, 1, fr);  // small wave tiles
+      for (; dm < D; ++dm) dma(st + 3, dm);
     }
+    // slice 1: after BAR_AT MFMAs, wait for this wave's part of stage st + 1
+    // (stages st + 2, st + 3 may stay in flight) and publish it: every wave
+    // has then also finished reading slot st % 4, which takes stage st + 4
+    ring_fence<FN, FM>(fa[1], fb[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    {
+      int fr = 0, dm = 0;
+#pragma unroll
+      for (int q = 0; q < NM; ++q) {
+        const int i = q / FM, j = q % FM;
+        if (q == BAR_AT) {
+          wait_dma<2 * D>();
+          __builtin_amdgcn_s_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+        if (q >= BAR_AT) {
+          if (fr < NF) read(fa[0], fb[0], st + 1, 0, fr++);
+          else if (dm < D / 2 && (q & 1)) dma(st + 4, dm++);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      for (; fr < NF; ++fr) read(fa[0], fb[0], st + 1, 0, fr);  // small wave tiles
+      for (; dm < D / 2; ++dm) dma(st + 4, dm);
+    }
+  }
+  // every DMA has landed and every LDS read returned before the registers of
+  // the last (unused) fragments are reused and before the workgroup exits
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  ring_fence<FN, FM>(fa[0], fb[0]);
+  store_tile<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
+}
+
+// Operands contiguous along M / N run on the ring pipeline, K-contiguous
+// pairs on the double-buffered one.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP>
+void launch_kernel(const GemmArgs& a, long grid, hipStream_t s) {
+  if constexpr (LA == kMC || LB == kMC)
+    hipLaunchKernelGGL((ring_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, GROUP>),
+                       dim3((unsigned)grid), dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, GROUP>),
+                       dim3((unsigned)grid), dim3(WAVES_M * WAVES_N * 64), 0, s, a);
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI>
 hipError_t launch(const GemmArgs& a, hipStream_t s) {
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI>), dim3(tiles),
-                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  launch_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, 0>(a, tiles, s);
   return hipGetLastError();
 }
 
@@ -397,16 +626,14 @@ hipError_t launch_grouped_m(const GemmArgs& a, hipStream_t s) {
   // share of the workgroups covers ceil(real / 8) tiles
   const long mt = a.M / BM + a.groups;
   const long tiles = ((mt * ((a.N + BN - 1) / BN) + NUM_XCD - 1) / NUM_XCD + 1) * NUM_XCD;
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, kKC, LB, EPI, 1>), dim3((unsigned)tiles),
-                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  launch_kernel<BM, BN, WAVES_M, WAVES_N, kKC, LB, EPI, 1>(a, tiles, s);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 hipError_t launch_grouped_k(const GemmArgs& a, hipStream_t s) {
   const long tiles = (long)a.groups * ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, kMC, kMC, EPI, 2>), dim3((unsigned)tiles),
-                     dim3(WAVES_M * WAVES_N * 64), 0, s, a);
+  launch_kernel<BM, BN, WAVES_M, WAVES_N, kMC, kMC, EPI, 2>(a, tiles, s);
   return hipGetLastError();
 }
 
@@ -438,20 +665,26 @@ constexpr int kCUs = 256;
 template <int LA, int LB, int EPI>
 hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   // Large tiles once they fill the chip, smaller ones for small problems.
-  // 8 waves of 64x128 (two per SIMD) hide LDS latency better than 4 waves
-  // of 128x128 for every layout.
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
-  if (LB == kKC && big >= kCUs) {
-    // 256 x 192 tiles when 256 x 256 ones leave the last wave of workgroups
-    // partly empty: cost ~ waves x tile area, the narrower tile being ~11 %
-    // less efficient per FLOP
-    const long t192 = (long)((a.M + 255) / 256) * ((a.N + 191) / 192);
-    const double c256 = (double)((big + kCUs - 1) / kCUs) * 256.0;
-    const double c192 = (double)((t192 + kCUs - 1) / kCUs) * 192.0 / 0.89;
-    if (c192 < c256) return launch<256, 192, 4, 2, LA, LB, EPI>(a, s);
+  if constexpr (LA == kKC && LB == kKC) {
+    if (big >= kCUs) {
+      // 256 x 192 tiles when 256 x 256 ones leave the last wave of workgroups
+      // partly empty: cost ~ waves x tile area, the narrower tile being ~11 %
+      // less efficient per FLOP
+      const long t192 = (long)((a.M + 255) / 256) * ((a.N + 191) / 192);
+      const double c256 = (double)((big + kCUs - 1) / kCUs) * 256.0;
+      const double c192 = (double)((t192 + kCUs - 1) / kCUs) * 192.0 / 0.89;
+      if (c192 < c256) return launch<256, 192, 4, 2, LA, LB, EPI>(a, s);
+    }
   }
-  if (big >= 256) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
+  // both operands M/N-contiguous: 4 waves of 128 x 128 (two transposing
+  // reads per fragment make LDS reads the scarcer resource); otherwise 8
+  // waves of 64 x 128
+  if (big >= 256) {
+    if constexpr (LA == kMC && LB == kMC) return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
+    else return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
+  }
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
 }
@@ -467,8 +700,8 @@ hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hi
 
 hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
-  if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
-  if (epi == kStoreF32) return launch_grouped_k<256, 256, 4, 2, kStoreF32>(a, s);
+  if (epi == kAccF32) return launch_grouped_k<256, 256, 2, 2, kAccF32>(a, s);
+  if (epi == kStoreF32) return launch_grouped_k<256, 256, 2, 2, kStoreF32>(a, s);
   return hipErrorInvalidValue;
 }
 
@@ -493,8 +726,7 @@ hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, bool
   p.strideC = (long)a.M * a.N;
   p.groups = S;
   const long tiles = (long)S * ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  hipLaunchKernelGGL((gemm_kernel<128, 128, 2, 2, kMC, kMC, kStoreF32, 3>), dim3((unsigned)tiles),
-                     dim3(256), 0, s, p);
+  launch_kernel<128, 128, 2, 2, kMC, kMC, kStoreF32, 3>(p, tiles, s);
   const long n4 = (long)a.M * (a.N / 4);
   const dim3 grid((unsigned)((n4 + 255) / 256));
   if (accumulate)

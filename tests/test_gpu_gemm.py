@@ -78,12 +78,24 @@ def test_gemm_integer_exact(la, lb, epi, M, N, K):
 @pytest.mark.parametrize("la,lb,epi", [(KC, KC, STORE_BF16), (KC, MC, STORE_BF16),
                                        (MC, MC, ACC_F32)])
 @pytest.mark.parametrize("M,N,K", [(4096, 4096, 64), (4096, 2048, 72), (1024, 1536, 256),
-                                   (4096, 6144, 64)])
+                                   (4096, 6144, 64), (4096, 4096, 1000)])
 def test_gemm_tile_paths_random(la, lb, epi, M, N, K):
     banner(f"gemm rand la={la} lb={lb} epi={epi} M={M} N={N} K={K}")
     got, ref = run_gemm(la, lb, epi, M, N, K, seed=7, integer=False)
     tol = 1e-2 if epi == STORE_BF16 else 1e-5
     assert rel_fro(got, ref) <= tol
+
+
+@pytest.mark.parametrize("la,lb,epi", [(KC, MC, STORE_BF16), (MC, MC, ACC_F32), (MC, MC, STORE_F32)])
+def test_gemm_large_tiles_long_k_integer_exact(la, lb, epi):
+    """256 x 256 tiles over a long ragged reduction (K = 1000: 31 full
+    32-deep stages and a partial one), exact in fp32."""
+    M, N, K = 4096, 4096, 1000
+    banner(f"gemm int big tiles la={la} lb={lb} epi={epi} K={K}")
+    got, ref = run_gemm(la, lb, epi, M, N, K, seed=epi + 3)
+    want = (fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
+            if epi in (STORE_BF16, RESID_BF16) else ref)
+    assert np.array_equal(got, want)
 
 
 def test_gemm_zero_k_and_empty():
