@@ -25,6 +25,8 @@
 // in the log2 domain (scale * log2 e folded into one multiply); the causal
 // mask is evaluated only on tiles that straddle the diagonal, and waves whose
 // rows are fully masked skip their MFMAs.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -121,24 +123,75 @@ __device__ __forceinline__ void zero(f32x16_t& a) {
 
 // ------------------------------------------------------------- forward ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
-//  * K/V tiles alternate between two separately declared LDS arrays with the
-//    loop unrolled by two, so the compiler can see that the DMA filling one
-//    never aliases reads of the other (else it waits for the DMA before every
-//    read); each tile ends with an explicit wait + barrier.
-//  * All K fragments of a tile are read in one batch before its 16 score
-//    MFMAs; the V fragments are read into the same registers right after, so
-//    their latency hides under the softmax.
-//  * The softmax is VALU-bound on this chip (a wave64 VALU op takes 4 cycles,
-//    exp more), so it is trimmed: the scale is folded into the exponent's
-//    FMA, and the running max (log2 units) is raised only when a tile's max
-//    exceeds it by more than 8, so the output rescale runs on few tiles and
-//    probabilities stay below 2^8 (exact in the final normalisation).
+//  * K/V tiles are double-buffered in LDS; each tile ends with an explicit
+//    wait + barrier.
+//  * All K fragments of a tile are in flight before its 16 score MFMAs, and
+//    each MFMA pair waits only for its own fragments; the V^T fragments are
+//    read after the row max (whose lane exchange is an LDS operation that
+//    would otherwise wait for them) and land under the exp / row sums.
+//  * The softmax, not the MFMAs, bounds this kernel on this chip (a wave64
+//    VALU op takes 4 cycles, exp more), so the per-tile VALU work is cut to
+//    the softmax itself: the scale is folded into the exponent's FMA; the
+//    running max (log2 units) is raised only when a tile's max exceeds it by
+//    more than 8, so the output rescale runs on few tiles (behind a real
+//    branch) and probabilities stay below 2^8 (exact in the final
+//    normalisation); the causal mask runs only on the diagonal tile; the row
+//    max is a running chain the compiler turns into v_max3 without quieting
+//    each operand first; fragment reads are inline asm from per-lane LDS
+//    addresses computed once, with the stage, key block and row offsets as
+//    immediates (no address arithmetic per read, no compiler wait for the
+//    in-flight DMA of the other stage).
+//  * Inline asm here only reads LDS into registers and waits; it never reads
+//    an MFMA result (the compiler does not insert the wait states an MFMA
+//    result needs before an asm consumer).
+namespace fa {
+
+__device__ __forceinline__ uint32_t lds_off(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8_t rd_b128(uint32_t a) {
+  uint4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(a), "n"(OFF) : "memory");
+  return __builtin_bit_cast(bf16x8_t, r);
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8_t rd_tr(uint32_t lo, uint32_t hi) {
+  uint2 x, y;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(x) : "v"(lo), "n"(OFF) : "memory");
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(y) : "v"(hi), "n"(OFF) : "memory");
+  return __builtin_bit_cast(bf16x8_t, make_uint4(x.x, x.y, y.x, y.y));
+}
+// at most N LDS operations of this wave outstanding (the counter saturates
+// at 15: a larger N waits for all but 15)
+template <int N>
+__device__ __forceinline__ void wait_lds() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N < 15 ? N : 15) : "memory");
+}
+// the value counts as rewritten here, so its uses stay below the wait
+template <typename T>
+__device__ __forceinline__ void bind(T& x) {
+  asm volatile("" : "+v"(x));
+}
+__device__ __forceinline__ void sync_block() {
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+template <int I>
+using ic = std::integral_constant<int, I>;
+}  // namespace fa
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restrict__ o,
-                                                    float* __restrict__ lse) {
+                                                         float* __restrict__ lse) {
   constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
-  __shared__ uint4 sm0[2 * NAT];
-  __shared__ uint4 sm1[2 * NAT];
+  constexpr int TILE_B = NAT * 16;       // bytes of one K or V tile
+  constexpr int STAGE_B = 2 * TILE_B;    // K tile then V tile
+  constexpr int HALF_B = TILE_B / 2;     // rows 32..63 of a tile
+  constexpr int ROW16_B = 16 * D * 2;    // 16 rows of a tile
+  __shared__ uint4 smem[4 * NAT];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
   const int qt = nqt - 1 - (int)blockIdx.x;
@@ -165,39 +218,62 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
 
-  auto dma = [&](int kt, uint4* sm) __attribute__((always_inline)) {
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, ln);
-    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, ln);
+  // per-lane byte addresses in stage 0: K row fragment of slice kk (rows
+  // 0..31), V^T fragment of column block db (rows 0..15, both row quads)
+  const uint32_t base = fa::lds_off(smem);
+  uint32_t ka[KK], va[DB][2];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) ka[kk] = base + slot<D>(l32, kk * 2 + hh) * 16;
+  {
+    const int g4 = lane >> 4, i = lane & 15;
+    const int r = (g4 >> 1) * 4 + (i >> 2);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int d = db * 32 + (g4 & 1) * 16 + 4 * (i & 3);
+      va[db][0] = base + TILE_B + (slot<D>(r, d >> 3) * 8 + (d & 7)) * 2;
+      va[db][1] = base + TILE_B + (slot<D>(r + 8, d >> 3) * 8 + (d & 7)) * 2;
+    }
+  }
+
+  auto dma = [&](int kt) __attribute__((always_inline)) {
+    uint4* st = smem + (kt & 1) * 2 * NAT;
+    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, st, wave, lane);
+    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, st + NAT, wave, lane);
   };
-  auto tile = [&](const uint4* Ks, const uint4* Vs, int kt) __attribute__((always_inline)) {
+  auto tile = [&](auto STG, int kt) __attribute__((always_inline)) {
+    constexpr int SO = decltype(STG)::value * STAGE_B;
     const int k0 = kt * BKV;
     if (k0 > q0w + 31) return;   // every query of this wave is before the tile
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    bf16x8_t f[KK][2];           // K fragments, then V fragments
+    // scores: all K fragments in flight, each MFMA pair waits for its own
+    bf16x8_t f[KK][2];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) f[kk][kb] = row_frag<D>(Ks, kb * 32, kk, ln);
+    for (int kk = 0; kk < KK; ++kk) {
+      f[kk][0] = fa::rd_b128<SO>(ka[kk]);
+      f[kk][1] = fa::rd_b128<SO + HALF_B>(ka[kk]);
+    }
     f32x16_t s[2];
     zero(s[0]);
     zero(s[1]);
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
+    for (int kk = 0; kk < KK; ++kk) {
+      switch (KK - 1 - kk) {
+        case 7: fa::wait_lds<14>(); break;
+        case 6: fa::wait_lds<12>(); break;
+        case 5: fa::wait_lds<10>(); break;
+        case 4: fa::wait_lds<8>(); break;
+        case 3: fa::wait_lds<6>(); break;
+        case 2: fa::wait_lds<4>(); break;
+        case 1: fa::wait_lds<2>(); break;
+        default: fa::wait_lds<0>(); break;
+      }
+      fa::bind(f[kk][0]);
+      fa::bind(f[kk][1]);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) s[kb] = MFMA(f[kk][kb], qf[kk], s[kb]);
-    // V fragments for the P V products: read now, consumed after the softmax
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          f[(kb * 2 + ss) * DB / 2 + db / 2][db & 1] = tr_frag<D>(Vs, kb * 32 + ss * 16, db, ln);
-    const bool diag = (k0 + BKV - 1 > q0w);
-    if (diag) {
+    }
+    // causal mask on the tile that straddles this wave's diagonal
+    if (k0 + BKV - 1 > q0w) {
+      asm volatile("" ::: "memory");
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -206,17 +282,38 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
           if (key > q) s[kb][i] = -INFINITY;
         }
     }
-    float mx[4];
+    // row max: two running-max chains over the 32 scores of the lane (a
+    // running chain lets the compiler use v_max3 without first quieting
+    // every operand; a tree would quiet each leaf)
+    float mk[2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kb = r >> 1, o8 = (r & 1) * 8;
-      mx[r] = fmaxf(fmaxf(fmaxf(s[kb][o8 + 0], s[kb][o8 + 1]), fmaxf(s[kb][o8 + 2], s[kb][o8 + 3])),
-                    fmaxf(fmaxf(s[kb][o8 + 4], s[kb][o8 + 5]), fmaxf(s[kb][o8 + 6], s[kb][o8 + 7])));
+    for (int kb = 0; kb < 2; ++kb) {
+      float t = fmaxf(s[kb][0], s[kb][1]);
+#pragma unroll
+      for (int i = 2; i < 16; ++i) t = fmaxf(t, s[kb][i]);
+      mk[kb] = t;
     }
-    float mt = fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3]));
+    float mt = fmaxf(mk[0], mk[1]);
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * c;
+    // the lane exchange above waits for all LDS traffic of the wave: issue
+    // the V^T fragment reads only after it
+    __builtin_amdgcn_sched_barrier(0);
+    // V^T fragments for the P V products, in flight under the softmax
+    bf16x8_t v[2][2][DB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          if (kb == 0 && ss == 0) v[0][0][db] = fa::rd_tr<SO>(va[db][0], va[db][1]);
+          if (kb == 0 && ss == 1) v[0][1][db] = fa::rd_tr<SO + ROW16_B>(va[db][0], va[db][1]);
+          if (kb == 1 && ss == 0) v[1][0][db] = fa::rd_tr<SO + 2 * ROW16_B>(va[db][0], va[db][1]);
+          if (kb == 1 && ss == 1) v[1][1][db] = fa::rd_tr<SO + 3 * ROW16_B>(va[db][0], va[db][1]);
+        }
     const bool grow = mt > mrow + 8.0f;
     if (__ballot(grow)) {
+      asm volatile("" ::: "memory");
       const float mnew = grow ? mt : mrow;
       const float alpha = fast_exp2(mrow - mnew);
       lrow *= alpha;
@@ -235,33 +332,36 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
         s[kb][i] = pp;
         lrow += pp;
       }
+    // 4 DB fragments (2 reads each) per (kb, ss) step, in issue order
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss) {
         const bf16x8_t pf = pack_frag(s[kb], ss);
+        const int step = kb * 2 + ss;
+        switch (step) {
+          case 0: fa::wait_lds<6 * DB>(); break;
+          case 1: fa::wait_lds<4 * DB>(); break;
+          case 2: fa::wait_lds<2 * DB>(); break;
+          default: fa::wait_lds<0>(); break;
+        }
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-          oacc[db] = MFMA(f[(kb * 2 + ss) * DB / 2 + db / 2][db & 1], pf, oacc[db]);
+        for (int db = 0; db < DB; ++db) fa::bind(v[kb][ss][db]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] = MFMA(v[kb][ss][db], pf, oacc[db]);
       }
   };
-  auto sync = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-  };
 
-  dma(0, sm0);
-  sync();
+  dma(0);
+  fa::sync_block();
   for (int kt = 0; kt < nkt; kt += 2) {
-    if (kt + 1 < nkt) dma(kt + 1, sm1);
-    tile(sm0, sm0 + NAT, kt);
-    sync();
+    if (kt + 1 < nkt) dma(kt + 1);
+    tile(fa::ic<0>{}, kt);
+    fa::sync_block();
     if (kt + 1 < nkt) {
-      if (kt + 2 < nkt) dma(kt + 2, sm0);
-      tile(sm1, sm1 + NAT, kt + 1);
-      sync();
+      if (kt + 2 < nkt) dma(kt + 2);
+      tile(fa::ic<1>{}, kt + 1);
+      fa::sync_block();
     }
   }
   lrow += __shfl_xor(lrow, 32, 64);
