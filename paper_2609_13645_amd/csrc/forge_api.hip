@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "../../include/forge.h"
@@ -323,6 +324,51 @@ forge_status attn_block_fwd(const forge_layer_cfg& c, const Dims& d,
   return FORGE_OK;
 }
 
+// ---- side stream for the weight-gradient products ----------------------------
+// The dense layer backward runs its four weight-gradient GEMMs on a second
+// stream of the same device, forked from the caller's stream after each one's
+// inputs exist and joined back before the call's work ends, so they fill the
+// tail waves of the data-gradient GEMMs and the bandwidth-bound kernels in
+// between. One non-blocking stream of default priority and its events per
+// device, created on first use and kept for the life of the process; launch
+// sequences on one device are serialised by a mutex, so concurrent callers do
+// not interleave their event records.
+constexpr int kMaxDevices = 64;
+struct SideLane {
+  std::mutex mu;
+  bool ready = false;
+  hipStream_t stream = nullptr;
+  hipEvent_t ev[5] = {};
+};
+SideLane g_side[kMaxDevices];
+std::mutex g_side_init;
+
+hipError_t side_lane(SideLane** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  SideLane& L = g_side[dev];
+  std::lock_guard<std::mutex> lk(g_side_init);
+  if (!L.ready) {
+    e = hipStreamCreateWithFlags(&L.stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+    for (hipEvent_t& ev : L.ev) {
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) return e;
+    }
+    L.ready = true;
+  }
+  *out = &L;
+  return hipSuccess;
+}
+
+// everything enqueued on `from` so far happens before what is enqueued on `to` next
+hipError_t link(hipStream_t from, hipStream_t to, hipEvent_t ev) {
+  const hipError_t e = hipEventRecord(ev, from);
+  return e != hipSuccess ? e : hipStreamWaitEvent(to, ev, 0);
+}
+
 // Backward of attn_block_fwd from dh1 (the full gradient at h1, residual
 // path included) to d_in.
 forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
@@ -330,7 +376,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                             const uint16_t* x, const uint16_t* a, const float* rstd1,
                             const uint16_t* qkv, const uint16_t* o, const float* lse,
                             const uint16_t* dh1, uint16_t* d_in, void* workspace, const Work& wk,
-                            hipStream_t s) {
+                            hipStream_t s, SideLane* side = nullptr) {
   uint16_t* dO = at<uint16_t>(workspace, wk.dO);
   float* delta = at<float>(workspace, wk.delta);
   uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
@@ -339,10 +385,14 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   const int nblk = forge::rmsnorm_bwd_blocks((int)d.T);
   const forge::AttnArgs aa = attn_args(d, qkv);
   (void)c;
+  // weight gradients go to the side stream when there is one (dh1 and o
+  // exist: fork now; dqkv after the RoPE backward: fork again)
+  hipStream_t ws = side ? side->stream : s;
+  if (side) FORGE_HIP(link(s, ws, side->ev[2]));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), ws));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), s));
   FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, lse, delta, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
                                  at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
@@ -350,12 +400,14 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   FORGE_HIP(forge::attn_bwd_dq(aa, dO, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
                               (int)(d.nh + d.nkv), (int)d.d, true, s));
+  if (side) FORGE_HIP(link(s, ws, side->ev[3]));
+  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                        gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), ws));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                        gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), s));
   FORGE_HIP(forge::rmsnorm_bwd(x, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, !g->overwrite, s));
+  if (side) FORGE_HIP(link(ws, s, side->ev[4]));  // join: the call's work ends on s
   return FORGE_OK;
 }
 
@@ -592,15 +644,27 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
     const uint16_t* act = at<uint16_t>(saved, sv.act);
     uint16_t* dA = at<uint16_t>(workspace, wk.dA);
     uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
+    // weight gradients on the side stream (see SideLane): dW_down as soon
+    // as the call starts, dW_gate_up once dgu exists
+    SideLane* side = nullptr;
+    FORGE_HIP(side_lane(&side));
+    std::lock_guard<std::mutex> lk(side->mu);
+    hipStream_t ws = side->stream;
+    FORGE_HIP(link(s, ws, side->ev[0]));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                          gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
-    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                          gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), s));
     FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
+    FORGE_HIP(link(s, ws, side->ev[1]));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                          gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
-    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                          gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), s));
+    FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
+    FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
+    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
+                          side);
   }
   FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
