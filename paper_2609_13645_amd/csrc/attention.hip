@@ -429,8 +429,9 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* 
 //   PASS 1: S, dP = dO V^T, dS = P (dP - delta), dK^T += Q^T dS
 // (S is formed twice, 5 products instead of 4, for twice the occupancy.)
 // LDS double buffering in two separate arrays with explicit waits, as in the
-// forward; pass 0 batches its fragment reads, pass 1 (K and V both held in
-// registers) reads them in place.
+// forward. Each 64-query tile is processed as two 32-query halves, so a
+// half's scores, dP and fragments leave room for four 16-deep slices of Q /
+// dO fragment reads in flight.
 template <int D, int PASS>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ delta,
@@ -498,76 +499,61 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     const uint4* dOs = base + NAT;
     const float* L = reinterpret_cast<const float*>(base + 2 * NAT);
     const float* Dl = L + BQ;
-    f32x16_t s[2], dp[2];
+    const bool tail = (q0 + BQ > S);
+    // the two 32-query halves one after the other (a half's scores, dP and
+    // fragments fit with four slices of reads in flight)
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      zero(s[qb]);
+      f32x16_t sc, dp;
+      zero(sc);
       if (PASS) {
 #pragma unroll
         for (int i = 0; i < 16; ++i)   // dP - delta, formed by the MFMAs
-          dp[qb][i] = -Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
+          dp[i] = -Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
       }
-    }
-    bf16x8_t fq[D / 16][2], fo[D / 16][2];
+      bf16x8_t fq[D / 16], fo[D / 16];
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      constexpr int BAT = PASS ? 1 : 4;   // pass 1 holds V too: no room to batch
-      if (kk % BAT == 0) {
+      for (int kk = 0; kk < D / 16; ++kk) {
+        if (kk % 4 == 0) {
 #pragma unroll
-        for (int u = kk; u < kk + BAT; ++u)
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            fq[u][qb] = row_frag<D>(Qs, qb * 32, u, ln);
-            if (PASS) fo[u][qb] = row_frag<D>(dOs, qb * 32, u, ln);
+          for (int u = kk; u < kk + 4; ++u) {
+            fq[u] = row_frag<D>(Qs, qb * 32, u, ln);
+            if (PASS) fo[u] = row_frag<D>(dOs, qb * 32, u, ln);
           }
+        }
+        sc = MFMA(fq[kk], kf[kk], sc);
+        if (PASS) dp = MFMA(fo[kk], vf[kk], dp);
       }
+      // transposed fragments of the second product (dO^T for dV, Q^T for
+      // dK), in flight under the elementwise part
+      bf16x8_t ft[2][D / 32];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        s[qb] = MFMA(fq[kk][qb], kf[kk], s[qb]);
-        if (PASS) dp[qb] = MFMA(fo[kk][qb], vf[kk], dp[qb]);
-      }
-    }
-    // transposed fragments of the second product: pass 0 reads them before
-    // the elementwise part; pass 1 (more live registers) reads them in place
-    bf16x8_t ft[2][2][D / 32];
-    if (!PASS) {
+      for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db) ft[qb][ss][db] = tr_frag<D>(dOs, qb * 32 + ss * 16, db, ln);
-    }
-    const bool diag = (q0 < kw0 + 31);
-    const bool tail = (q0 + BQ > S);
-    // P = exp2(S c - LSE log2 e); on diagonal / tail tiles the masked
-    // scores are set to -inf first, so exp2 gives 0
-    if (diag || tail) {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+        for (int db = 0; db < D / 32; ++db)
+          ft[ss][db] = tr_frag<D>(PASS ? Qs : dOs, qb * 32 + ss * 16, db, ln);
+      // P = exp2(S c - LSE log2 e); on diagonal / tail tiles the masked
+      // scores are set to -inf first, so exp2 gives 0
+      if (q0 + qb * 32 < kw0 + 31 || tail) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          if (key > q0 + qi || q0 + qi >= S) s[qb][i] = -INFINITY;
+          if (key > q0 + qi || q0 + qi >= S) sc[i] = -INFINITY;
         }
-    }
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-        const float p = fast_exp2(__builtin_fmaf(s[qb][i], c, L[qi]));
-        s[qb][i] = PASS ? p * dp[qb][i] : p;
+        const float p = fast_exp2(__builtin_fmaf(sc[i], c, L[qi]));
+        sc[i] = PASS ? p * dp[i] : p;
       }
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss) {
-        const bf16x8_t f = pack_frag(s[qb], ss);
+        const bf16x8_t f = pack_frag(sc, ss);
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          acc[db] = MFMA(PASS ? tr_frag<D>(Qs, qb * 32 + ss * 16, db, ln) : ft[qb][ss][db], f, acc[db]);
+        for (int db = 0; db < D / 32; ++db) acc[db] = MFMA(ft[ss][db], f, acc[db]);
       }
+    }
   };
   auto sync = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -637,8 +623,10 @@ __global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict
 // ---------------------------------------------------------- backward dQ ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
 // P is recomputed from the saved LSE (exponent argument as one FMA), then
-// dS = P (dP - delta) and dQ^T += K^T dS^T. LDS double buffering, batched
-// fragment reads and explicit waits as in the forward.
+// dS = P (dP - delta) and dQ^T += K^T dS^T, one 32-key half of a tile at a
+// time (the whole tile's scores, dP and K^T fragments do not fit in the
+// registers of two waves per SIMD). LDS double buffering, batched fragment
+// reads and explicit waits.
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
                                                 const float* __restrict__ delta,
@@ -688,62 +676,50 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
     if (k0 > q0w + 31) return;
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    f32x16_t s[2], dp[2];
+    // the two 32-key halves one after the other: scores, dP, dS and the dQ
+    // products of a half need only that half's registers
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      zero(s[kb]);
-      zero(dp[kb]);
-    }
-    // scores and dP: K and V fragments read four 16-deep slices at a time
-    bf16x8_t fk[KK][2], fv[KK][2];
+      f32x16_t sc, dp;
+      zero(sc);
+      zero(dp);
+      // scores and dP: K and V fragments read four 16-deep slices at a time
+      bf16x8_t fk[KK], fv[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      if (kk % 4 == 0) {
+      for (int kk = 0; kk < KK; ++kk) {
+        if (kk % 4 == 0) {
 #pragma unroll
-        for (int u = kk; u < kk + 4; ++u)
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) {
-            fk[u][kb] = row_frag<D>(Ks, kb * 32, u, ln);
-            fv[u][kb] = row_frag<D>(Vs, kb * 32, u, ln);
+          for (int u = kk; u < kk + 4; ++u) {
+            fk[u] = row_frag<D>(Ks, kb * 32, u, ln);
+            fv[u] = row_frag<D>(Vs, kb * 32, u, ln);
           }
+        }
+        sc = MFMA(fk[kk], qf[kk], sc);
+        dp = MFMA(fv[kk], of[kk], dp);
       }
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = MFMA(fk[kk][kb], qf[kk], s[kb]);
-        dp[kb] = MFMA(fv[kk][kb], of[kk], dp[kb]);
-      }
-    }
-    // K^T fragments for dQ^T = K^T dS^T: read before the elementwise part
-    bf16x8_t ft[2][2][DB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      // K^T fragments for dQ^T = K^T dS^T: read before the elementwise part
+      bf16x8_t ft[2][DB];
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) ft[kb][ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
-    // the causal mask (diagonal tiles only) as -inf scores: exp2 gives 0
-    if (k0 + BKV - 1 > q0w) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int db = 0; db < DB; ++db) ft[ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
+      // the causal mask (diagonal tiles only) as -inf scores: exp2 gives 0
+      if (k0 + kb * 32 + 31 > q0w) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          if (key > q) s[kb][i] = -INFINITY;
+          if (key > q) sc[i] = -INFINITY;
         }
-    }
+      }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        dp[kb][i] = fast_exp2(__builtin_fmaf(s[kb][i], c, nl2)) * (dp[kb][i] - dl);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int i = 0; i < 16; ++i) dp[i] = fast_exp2(__builtin_fmaf(sc[i], c, nl2)) * (dp[i] - dl);
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss) {
-        const bf16x8_t df = pack_frag(dp[kb], ss);
+        const bf16x8_t df = pack_frag(dp, ss);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) dqa[db] = MFMA(ft[kb][ss][db], df, dqa[db]);
+        for (int db = 0; db < DB; ++db) dqa[db] = MFMA(ft[ss][db], df, dqa[db]);
       }
+    }
   };
   auto sync = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
