@@ -71,12 +71,19 @@ def is_model(cfg):
     return cfg["vocab"] > 0
 
 
-def tile_name(M, N):
-    """The tile the library's dispatch picks for a plain GEMM of this shape
-    (for labelling the roofline kernel only)."""
+def kc_kernel_name(M, N):
+    """Kernel and tile the library's dispatch picks for a plain GEMM with both
+    operands K-contiguous (for labelling the roofline kernel only): full
+    256 x 256 tiles on the ring pipeline, 256 x 192 when that fills the last
+    wave of workgroups better, smaller tiles for small problems."""
     big = -(-M // 256) * -(-N // 256)
     mid = -(-M // 256) * -(-N // 128)
-    return "256,256,4,2" if big >= 256 else ("256,128,2,2" if mid >= 256 else "128,128,2,2")
+    if big >= 256:
+        t192 = -(-M // 256) * -(-N // 192)
+        c256 = -(-big // 256) * 256.0
+        c192 = -(-t192 // 256) * 192.0 / 0.89
+        return "gemm_kernel<256,192,4,2" if c192 < c256 else "ring_kernel<256,256,4,2"
+    return "gemm_kernel<256,128,2,2" if mid >= 256 else "gemm_kernel<128,128,2,2"
 
 
 class Step:
@@ -172,7 +179,7 @@ def dominant_kernel(cfg, stream, step, reps):
             _lib.forge_gemm_grouped_rows(_lib.GEMM_KC, A, W, C, offsets, E, rows, 2 * fe, h,
                                          h, h, 2 * fe, 2 * fe * h, stream)
         flop = 2.0 * rows * 2 * fe * h
-        name = "gemm_kernel<256,256,4,2,KC,KC,StoreBF16,grouped rows> (expert gate/up fwd)"
+        name = "ring_kernel<256,256,4,2,KC,KC,StoreBF16,grouped rows> (expert gate/up fwd)"
         shape = f"rows={rows} E={E} N={2 * fe} K={h}"
     elif is_model(cfg):
         V = cfg["vocab"]
@@ -184,7 +191,7 @@ def dominant_kernel(cfg, stream, step, reps):
             _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
                             T, V, h, h, h, V, 0, stream)
         flop = 2.0 * T * V * h
-        name = f"gemm_kernel<{tile_name(T, V)},KC,KC,StoreBF16> (LM-head logits)"
+        name = f"{kc_kernel_name(T, V)},KC,KC,StoreBF16> (LM-head logits)"
         shape = f"M={T} N={V} K={h}"
     else:
         f = cfg["ffn"]
@@ -196,7 +203,7 @@ def dominant_kernel(cfg, stream, step, reps):
             _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
                             T, 2 * f, h, h, h, 2 * f, 0, stream)
         flop = 2.0 * T * 2 * f * h
-        name = f"gemm_kernel<{tile_name(T, 2 * f)},KC,KC,StoreBF16> (gate/up fwd)"
+        name = f"{kc_kernel_name(T, 2 * f)},KC,KC,StoreBF16> (gate/up fwd)"
         shape = f"M={T} N={2 * f} K={h}"
     for _ in range(3):
         launch()
@@ -253,7 +260,7 @@ def traffic_from_counters(fetch_csv, write_csv, kernel_grid, out=TRAFFIC_FILE):
             if r["Counter_Name"] != counter:
                 continue
             name, grid = r["Kernel_Name"], int(r["Grid_Size"])
-            if "gemm_kernel" in name and grid == kernel_grid:
+            if ("gemm_kernel" in name or "ring_kernel" in name) and grid == kernel_grid:
                 vals["kernel"].append(float(r["Counter_Value"]))
             elif "copyBuffer" in name or ("copy" in name.lower() and "gemm" not in name):
                 vals["copy"].append(float(r["Counter_Value"]))

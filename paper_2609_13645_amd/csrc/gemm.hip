@@ -1,36 +1,39 @@
-// bf16 GEMM on gfx950 MFMA (v_mfma_f32_32x32x16_bf16), fp32 accumulation.
+// bf16 GEMM on gfx950 MFMA, fp32 accumulation.
 //
 // Every projection of the layer is one of three products (App. C: the
 // backward of each GEMM is one data-gradient and one weight-gradient
 // product): y = x W^T (both operands K-contiguous), dX = dY W (W is
 // N-contiguous) and dW += dY^T X (both operands M/N-contiguous, reduction
-// over tokens). Two pipelines share tile order, operand layouts and epilogue:
+// over tokens). Two pipelines share tile order, operand layouts and epilogue
+// stores:
 //
-//  * gemm_kernel (both operands K-contiguous): a block tile BM x BN x 64 is
-//    staged through LDS, double-buffered, with one barrier per k-step, placed
-//    before the step's last 16-deep slice so that MFMAs are ready to issue as
-//    the waves leave it. The barrier also frees the buffer of the current
-//    step, which is refilled at once with the step after next. Tiles are
-//    filled by buffer_load ... lds (global to LDS without registers) in
-//    128-byte row segments (whole cache lines); out-of-range chunks read as
-//    zeros through the buffer descriptor's range check, so ragged edges need
-//    no branches.
-//  * ring_kernel (an operand contiguous along M / N): a ring of four 32-deep
-//    stages. The barrier that publishes stage s + 1 sits after the first MFMAs
-//    of stage s's last slice; right after it the DMA for stage s + 4 starts
-//    into the slot stage s has just released, spread over the next two slices
-//    (one instruction per two MFMAs), so no burst fills the texture unit's
-//    queues and every stage has three stages of MFMAs to land in. Fragment
-//    reads are issued as inline asm with explicit lgkmcnt waits: the
-//    compiler cannot tell the transposing reads apart from the DMA writes and
-//    would otherwise wait for every outstanding DMA before each of them.
+//  * ring_kernel (every layout; all 256 x 256 tiles): v_mfma_f32_16x16x32_bf16
+//    over a ring of four 32-deep LDS stages, one MFMA k-step per stage. The
+//    barrier that publishes stage s + 1 sits two MFMAs into stage s; after it
+//    the fragment reads of stage s + 1 and the DMA of stage s + 4 (into the
+//    slot stage s has just released) are spread evenly over the stage's
+//    MFMAs, so neither the LDS nor the texture unit sees a burst. Fragment
+//    reads are inline asm with explicit lgkmcnt waits: the compiler cannot
+//    tell the transposing reads apart from the DMA writes and would otherwise
+//    wait for every outstanding DMA before each of them. The 16x16x32 shape
+//    does the work of 32x32x16 at the same rate per cycle with less power,
+//    which keeps the clock higher under load.
+//  * gemm_kernel (K-contiguous 256 x 192 and small tiles): v_mfma_f32_32x32x16
+//    over a block tile BM x BN x 64 double-buffered in LDS, one barrier per
+//    k-step placed before the step's last 16-deep slice; the barrier also
+//    frees the current buffer, which is refilled at once with the step after
+//    next.
+//  * Tiles are filled by buffer_load ... lds (global to LDS without
+//    registers); out-of-range chunks read as zeros through the buffer
+//    descriptor's range check, so ragged edges need no branches.
 //  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
 //    chunk c of row r at c ^ ((r ^ (r >> 3)) & 7)) in gemm_kernel and 64-byte
 //    rows (chunk c of row r at c ^ ((r >> 2) & 3)) in a ring stage; both keep
 //    each group of 16 lanes of a fragment read on distinct banks. Each MFMA
 //    operand is one 16-byte LDS read. An operand contiguous along M / N is
-//    stored as it lies in HBM and read with gfx950's ds_read_b64_tr_b16
-//    transpose reads, so dgrad and wgrad need no transpose pass.
+//    stored as it lies in HBM (chunks XOR-swizzled per k-row) and read with
+//    gfx950's ds_read_b64_tr_b16 transpose reads, so dgrad and wgrad need no
+//    transpose pass.
 //  * The MFMA computes D = Btile * Atile^T, i.e. C transposed, so each lane's
 //    four consecutive accumulator rows are four consecutive n of one row m of
 //    C: the epilogue writes 8-byte (bf16) or 16-byte (fp32) vectors.
@@ -100,65 +103,11 @@ struct KcLoader {
   }
 };
 
-// ---- source contiguous along the row dim (M or N): LDS-DMA, read transposed --
-// The tile is stored as it lies in HBM: 64 k-rows of ROWS contiguous
-// elements, 16-byte chunk c of row k at slot c ^ (4 (k & 3)). MFMA fragments
-// are read with ds_read_b64_tr_b16: within each 16-lane group, lane 4r + j
-// points at row r, columns 4j..4j+3 of a 4 x 16 block and receives column
-// (lane % 16) of rows 0..3, i.e. four consecutive k of one m. Two such reads
-// give a lane its eight k values. The XOR keeps the 32 lanes of a half-wave
-// (4 rows x 4 chunks) on distinct banks.
-template <int ROWS, int NW>
-struct McLoader {
-  static constexpr int LPR = ROWS / 8;          // lanes (16-byte chunks) per tile row
-  static constexpr int RPI = 64 / LPR;          // tile rows per wave instruction
-  static constexpr int PER = 64 / RPI / NW;     // instructions per wave per tile
-  static_assert(PER * RPI * NW == 64, "tile k-rows must split over waves");
-  __device__ __forceinline__ void load(const bf16_t* __restrict__ src, long ld, int row0,
-                                       int rows_lim, int k0, int K, uint4* lds, int wave,
-                                       int lane) const {
-    const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)k0 * ld + row0);
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int q = i * NW + wave;
-      const int k = q * RPI + lane / LPR;
-      const int c = (lane % LPR) ^ ((k & 3) << 2);
-      const bool ok = (k0 + k < K) && (row0 + c * 8 < rows_lim);
-      const uint32_t off = ok ? (uint32_t)(((long)k * ld + c * 8) * 2) : kOOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + q * 64), 16, off, 0, 0, 0);
-    }
-  }
-};
-
-typedef short v4i16_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
-
-template <int ROWS>
-__device__ __forceinline__ int mc_elem(int k, int m) {
-  return k * ROWS + ((((m >> 3) ^ ((k & 3) << 2))) << 3) + (m & 7);
-}
-
 // Fragment of rows base..base+31 (the lane's row is base + lane % 32) over
 // k-slice kk: eight consecutive k starting at kk*16 + 8*(lane / 32).
-template <int LAYOUT, int ROWS>
 __device__ __forceinline__ bf16x8_t frag(const uint4* tile, int base, int kk, int lane) {
-  if (LAYOUT == kKC) {
-    return __builtin_bit_cast(bf16x8_t, tile[swz(base + (lane & 31), kk * 2 + (lane >> 5))]);
-  } else {
-    const uint16_t* t = reinterpret_cast<const uint16_t*>(tile);
-    const int g = lane >> 4, i = lane & 15;
-    const int m = base + (g & 1) * 16 + 4 * (i & 3);
-    const int k = kk * 16 + (g >> 1) * 8 + (i >> 2);
-    const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(t + mc_elem<ROWS>(k, m)));
-    const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(t + mc_elem<ROWS>(k + 4, m)));
-    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
-    return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
-  }
+  return __builtin_bit_cast(bf16x8_t, tile[swz(base + (lane & 31), kk * 2 + (lane >> 5))]);
 }
-
-template <int ROWS, int NW, int LAYOUT>
-using Loader = typename std::conditional<LAYOUT == kKC, KcLoader<ROWS, NW>,
-                                         McLoader<ROWS, NW>>::type;
 
 // ---- epilogue: four consecutive n of row m ---------------------------------
 template <int EPI>
@@ -200,7 +149,7 @@ __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const fl
   }
 }
 
-// ---- epilogue: lane holds C[m][n..n+3] for 4 groups per 32x32 block -------
+// ---- epilogue of a 32x32 block: lane holds C[m][n..n+3] for 4 groups ------
 template <int EPI, int FN, int FM>
 __device__ __forceinline__ void store_tile(const GemmArgs& p, const f32x16_t (&acc)[FN][FM],
                                            int mw, int nw, int lane) {
@@ -322,6 +271,7 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn) {
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs p) {
+  static_assert(LA == kKC && LB == kKC, "the double-buffered kernel takes K-contiguous operands");
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 32, FN = WN / 32;
   static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
@@ -337,8 +287,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   constexpr int NW = WAVES_M * WAVES_N;
 
-  Loader<BM, NW, LA> la;
-  Loader<BN, NW, LB> lb;
+  KcLoader<BM, NW> la;
+  KcLoader<BN, NW> lb;
 
   f32x16_t acc[FN][FM];
 #pragma unroll
@@ -359,9 +309,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   __syncthreads();
   bf16x8_t fa[2][FN], fb[2][FM];
 #pragma unroll
-  for (int i = 0; i < FN; ++i) fa[0][i] = frag<LB, BN>(lds[0] + A_ELEMS, wn * WN + i * 32, 0, lane);
+  for (int i = 0; i < FN; ++i) fa[0][i] = frag(lds[0] + A_ELEMS, wn * WN + i * 32, 0, lane);
 #pragma unroll
-  for (int j = 0; j < FM; ++j) fb[0][j] = frag<LA, BM>(lds[0], wm * WM + j * 32, 0, lane);
+  for (int j = 0; j < FM; ++j) fb[0][j] = frag(lds[0], wm * WM + j * 32, 0, lane);
   // tile 1 into the second buffer (past the end: zeros into an unused buffer)
   la.load(p.A, p.lda, m0, p.M, BK, p.K, lds[1], wave, lane);
   lb.load(p.B, p.ldb, n0, p.N, BK, p.K, lds[1] + A_ELEMS, wave, lane);
@@ -375,9 +325,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
       const int cb = kk & 1, nx = cb ^ 1;
       if (kk + 1 < KS) {
 #pragma unroll
-        for (int i = 0; i < FN; ++i) fa[nx][i] = frag<LB, BN>(Bt, wn * WN + i * 32, kk + 1, lane);
+        for (int i = 0; i < FN; ++i) fa[nx][i] = frag(Bt, wn * WN + i * 32, kk + 1, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) fb[nx][j] = frag<LA, BM>(At, wm * WM + j * 32, kk + 1, lane);
+        for (int j = 0; j < FM; ++j) fb[nx][j] = frag(At, wm * WM + j * 32, kk + 1, lane);
       } else {
         // publish tile t+1: this wave's DMA has landed and its reads of tile
         // t are complete; after the barrier every wave's are
@@ -386,9 +336,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
         const uint4* An = lds[cur ^ 1];
         const uint4* Bn = lds[cur ^ 1] + A_ELEMS;
 #pragma unroll
-        for (int i = 0; i < FN; ++i) fa[nx][i] = frag<LB, BN>(Bn, wn * WN + i * 32, 0, lane);
+        for (int i = 0; i < FN; ++i) fa[nx][i] = frag(Bn, wn * WN + i * 32, 0, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) fb[nx][j] = frag<LA, BM>(An, wm * WM + j * 32, 0, lane);
+        for (int j = 0; j < FM; ++j) fb[nx][j] = frag(An, wm * WM + j * 32, 0, lane);
         // every wave's reads of tile t are complete: its buffer takes tile
         // t+2 (all zeros past the end)
         la.load(p.A, p.lda, m0, p.M, (kt + 2) * BK, p.K, lds[cur], wave, lane);
@@ -407,10 +357,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_kernel(GemmArgs
   store_tile<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
 }
 
-// ---- ring pipeline: four 32-deep stages -----------------------------------
+// ---- ring pipeline: four 32-deep stages, 16x16x32 MFMAs ---------------------
 // Stage slot = A part then B part. K-contiguous operand: ROWS rows of four
 // 16-byte chunks (k 0..31), chunk c of row r at c ^ ((r >> 2) & 3).
-// M/N-contiguous operand: 32 k-rows of ROWS elements (mc_elem layout).
+// M/N-contiguous operand: 32 k-rows of ROWS elements, 16-byte chunk c of
+// k-row k at c ^ ((k & 3) << 2) ^ (((k >> 3) & 1) << 1). A fragment read
+// touches k-rows {0..3} and {8..11} (or their +4 / +16 shifts) in one
+// half-wave; the two XOR terms put those eight rows' 32-byte pieces on
+// distinct banks.
 constexpr int SK = 32;
 
 template <int ROWS, int NW>
@@ -421,6 +375,13 @@ struct RingPart {
 };
 
 __device__ __forceinline__ int kc4(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+
+__device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 2) ^ (((k >> 3) & 1) << 1); }
+
+template <int ROWS>
+__device__ __forceinline__ int mc_ring_elem(int k, int m) {
+  return k * ROWS + (((m >> 3) ^ mc_swz(k)) << 3) + (m & 7);
+}
 
 __device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)ptr;
@@ -442,31 +403,35 @@ __device__ __forceinline__ void ring_dma(int i, const bf16_t* __restrict__ src, 
   } else {
     constexpr int LPR = ROWS / 8;  // lanes per k-row
     constexpr int RPI = 64 / LPR;  // k-rows per instruction
+    static_assert(LPR >= 16, "the swizzle needs at least 16 chunks per k-row");
     const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)k0 * ld + row0);
     const int k = blk * RPI + lane / LPR;
-    const int c = (lane % LPR) ^ ((k & 3) << 2);
+    const int c = (lane % LPR) ^ mc_swz(k);
     const bool ok = (k0 + k < K) && (row0 + c * 8 < rows_lim);
     const uint32_t off = ok ? (uint32_t)(((long)k * ld + c * 8) * 2) : kOOB;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(part + blk * 64), 16, off, 0, 0, 0);
   }
 }
 
-// Fragment of rows base..base+31 over 16-deep slice j of a stage; issued as
-// asm (not tracked by the compiler: ring_fence waits for it).
+// 16x16x32 operand of rows base..base+15 over a whole stage: the lane holds
+// row base + lane % 16, k = 8 (lane / 16) .. + 7. Issued as asm (not tracked
+// by the compiler: ring_fence waits for it). M/N-contiguous: two transposing
+// reads, lane 4r + j of each 16-lane group pointing at k-row r, elements
+// 4j..4j+3 of a 4 x 16 block.
 template <int LAYOUT, int ROWS>
-__device__ __forceinline__ bf16x8_t ring_frag(const uint4* part, int base, int j, int lane) {
+__device__ __forceinline__ bf16x8_t ring_frag(const uint4* part, int base, int lane) {
   if (LAYOUT == kKC) {
-    const uint32_t a = lds_addr(part + kc4(base + (lane & 31), j * 2 + (lane >> 5)));
+    const uint32_t a = lds_addr(part + kc4(base + (lane & 15), lane >> 4));
     uint4 r;
     asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(a) : "memory");
     return __builtin_bit_cast(bf16x8_t, r);
   } else {
     const uint16_t* t = reinterpret_cast<const uint16_t*>(part);
     const int g = lane >> 4, i = lane & 15;
-    const int m = base + (g & 1) * 16 + 4 * (i & 3);
-    const int k = j * 16 + (g >> 1) * 8 + (i >> 2);
-    const uint32_t a0 = lds_addr(t + mc_elem<ROWS>(k, m));
-    const uint32_t a1 = lds_addr(t + mc_elem<ROWS>(k + 4, m));
+    const int m = base + 4 * (i & 3);
+    const int k = g * 8 + (i >> 2);
+    const uint32_t a0 = lds_addr(t + mc_ring_elem<ROWS>(k, m));
+    const uint32_t a1 = lds_addr(t + mc_ring_elem<ROWS>(k + 4, m));
     uint2 lo, hi;
     asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a0) : "memory");
     asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(hi) : "v"(a1) : "memory");
@@ -492,19 +457,46 @@ __device__ __forceinline__ void wait_dma() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0>
+// ---- epilogue of a 16x16 block: lane holds C[m][n..n+3] --------------------
+template <int EPI, int FN, int FM>
+__device__ __forceinline__ void store_tile16(const GemmArgs& p, const f32x4_t (&acc)[FN][FM],
+                                             int mw, int nw, int lane) {
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const int m = mw + j * 16 + (lane & 15);
+      const int n = nw + i * 16 + (lane >> 4) * 4;
+      const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      store4<EPI>(p, m, n, v);
+    }
+}
+
+// Each stage is one 16x16x32 k-step. Its fragments were read during the
+// previous stage (double-buffered registers); BAR_AT MFMAs into the stage the
+// wave waits for its own DMA of the next stage and meets the others at the
+// barrier, after which the next stage is readable and the slot of this stage
+// (every wave has fenced its reads) takes the stage four ahead. The NF
+// fragment reads of the next stage and the D DMA instructions of the stage
+// four ahead are then spread evenly over the MFMAs up to TAIL before the end,
+// reads and DMAs interleaved in proportion, so that neither the LDS nor the
+// texture unit sees a burst.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0,
+          int TAIL = 4>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs p) {
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-  constexpr int FM = WM / 32, FN = WN / 32;
-  static_assert(FM * 32 == WM && FN * 32 == WN, "wave tile must be a multiple of 32");
+  constexpr int FM = WM / 16, FN = WN / 16;
+  static_assert(FM * 16 == WM && FN * 16 == WN, "wave tile must be a multiple of 16");
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int AE = RingPart<BM, NW>::ELEMS, BE = RingPart<BN, NW>::ELEMS;
   constexpr int DA = RingPart<BM, NW>::PER, DB = RingPart<BN, NW>::PER;
   constexpr int D = DA + DB;  // DMA instructions per wave per stage
   constexpr int NF = FN + FM, NM = FN * FM;
   constexpr int SLOT = AE + BE;
-  constexpr int BAR_AT = 2;   // MFMAs of a stage's last slice issued before its barrier
-  static_assert(NM > BAR_AT, "wave tile too small for the barrier placement");
+  constexpr int BAR_AT = 2;   // MFMAs of a stage issued before its barrier
+  constexpr int E = NF + D;   // memory instructions spread over a stage
+  constexpr int W = NM - BAR_AT - TAIL;
+  static_assert(W > 0, "wave tile too small for the barrier placement and tail");
   __shared__ uint4 lds[4 * SLOT];
 
   int tm, tn;
@@ -514,13 +506,13 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
 
-  f32x16_t acc[FN][FM];
+  f32x4_t acc[FN][FM];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
     for (int j = 0; j < FM; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+      for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.0f;
   const int nst = (p.K + SK - 1) / SK;
 
   // DMA instruction d (0..D-1) of stage st into slot st % 4 (zeros past K)
@@ -529,82 +521,80 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs
     if (d < DA) ring_dma<BM, NW, LA>(d, p.A, p.lda, m0, p.M, st * SK, p.K, slot, wave, lane);
     else ring_dma<BN, NW, LB>(d - DA, p.B, p.ldb, n0, p.N, st * SK, p.K, slot + AE, wave, lane);
   };
-  // fragment f (B fragments first, then A) of slice j of stage st
-  auto read = [&](bf16x8_t* fa_, bf16x8_t* fb_, int st, int j, int f) {
+  // fragment f (B fragments first, then A) of stage st
+  auto read = [&](bf16x8_t* fa_, bf16x8_t* fb_, int st, int f) {
     const uint4* slot = lds + (st & 3) * SLOT;
-    if (f < FN) fa_[f] = ring_frag<LB, BN>(slot + AE, wn * WN + f * 32, j, lane);
-    else fb_[f - FN] = ring_frag<LA, BM>(slot, wm * WM + (f - FN) * 32, j, lane);
+    if (f < FN) fa_[f] = ring_frag<LB, BN>(slot + AE, wn * WN + f * 16, lane);
+    else fb_[f - FN] = ring_frag<LA, BM>(slot, wm * WM + (f - FN) * 16, lane);
   };
 
-  // prologue: stages 0..2 in flight; publish stage 0; its first fragments;
-  // first half of stage 3
+  // prologue: stages 0..3 in flight; publish stage 0; its fragments
 #pragma unroll
-  for (int st = 0; st < 3; ++st)
+  for (int st = 0; st < 4; ++st)
 #pragma unroll
     for (int d = 0; d < D; ++d) dma(st, d);
-  wait_dma<2 * D>();
+  wait_dma<3 * D>();
   __builtin_amdgcn_s_barrier();
   bf16x8_t fa[2][FN], fb[2][FM];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) read(fa[0], fb[0], 0, 0, f);
-#pragma unroll
-  for (int d = 0; d < D / 2; ++d) dma(3, d);
+  for (int f = 0; f < NF; ++f) read(fa[0], fb[0], 0, f);
 
-  for (int st = 0; st < nst; ++st) {
-    // slice 0: fragments of slice 1 early, second half of stage st + 3 late
-    ring_fence<FN, FM>(fa[0], fb[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    {
-      int fr = 0, dm = D / 2;
+  // two stages per iteration, so that the fragment buffers are fixed; past
+  // the last stage the ring holds zeros (an odd stage count runs one stage
+  // of zeros)
+  for (int st = 0; st < nst; st += 2) {
 #pragma unroll
-      for (int q = 0; q < NM; ++q) {
-        const int i = q / FM, j = q % FM;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
-        if (fr < NF) read(fa[1], fb[1], st, 1, fr++);
-        else if (dm < D && (q & 1)) dma(st + 3, dm++);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      for (; fr < NF; ++fr) read(fa[1], fb[1], st, 1, fr);  // small wave tiles
-      for (; dm < D; ++dm) dma(st + 3, dm);
-    }
-    // slice 1: after BAR_AT MFMAs, wait for this wave's part of stage st + 1
-    // (stages st + 2, st + 3 may stay in flight) and publish it: every wave
-    // has then also finished reading slot st % 4, which takes stage st + 4
-    ring_fence<FN, FM>(fa[1], fb[1]);
-    __builtin_amdgcn_sched_barrier(0);
-    {
+    for (int h = 0; h < 2; ++h) {
+      const int s = st + h;
+      bf16x8_t* ca = fa[h];
+      bf16x8_t* cb = fb[h];
+      bf16x8_t* na = fa[h ^ 1];
+      bf16x8_t* nb = fb[h ^ 1];
+      ring_fence<FN, FM>(fa[h], fb[h]);
+      __builtin_amdgcn_sched_barrier(0);
       int fr = 0, dm = 0;
 #pragma unroll
       for (int q = 0; q < NM; ++q) {
         const int i = q / FM, j = q % FM;
         if (q == BAR_AT) {
+          // this wave's part of stage s + 1 has landed (s + 2 and s + 3 may
+          // still be in flight)
           wait_dma<2 * D>();
           __builtin_amdgcn_s_barrier();
           __builtin_amdgcn_sched_barrier(0);
         }
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ca[i], cb[j], acc[i][j], 0, 0, 0);
         if (q >= BAR_AT) {
-          if (fr < NF) read(fa[0], fb[0], st + 1, 0, fr++);
-          else if (dm < D / 2 && (q & 1)) dma(st + 4, dm++);
+          // memory instructions due by the end of MFMA q: event e is a read
+          // when the read count steps between e and e + 1
+          const int due = q - BAR_AT + 1 >= W ? E : ((q - BAR_AT + 1) * E) / W;
+#pragma unroll
+          for (int t = 0; t < (E + W - 1) / W + 1; ++t) {
+            if (fr + dm < due) {
+              const int e = fr + dm;
+              const bool is_read = ((e + 1) * NF) / E > (e * NF) / E;
+              if ((is_read && fr < NF) || dm >= D) read(na, nb, s + 1, fr++);
+              else dma(s + 4, dm++);
+            }
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      for (; fr < NF; ++fr) read(fa[0], fb[0], st + 1, 0, fr);  // small wave tiles
-      for (; dm < D / 2; ++dm) dma(st + 4, dm);
     }
   }
   // every DMA has landed and every LDS read returned before the registers of
   // the last (unused) fragments are reused and before the workgroup exits
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   ring_fence<FN, FM>(fa[0], fb[0]);
-  store_tile<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
+  store_tile16<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
 }
 
-// Operands contiguous along M / N run on the ring pipeline, K-contiguous
-// pairs on the double-buffered one.
+// Operands contiguous along M / N and full 256 x 256 tiles run on the ring
+// pipeline; the remaining K-contiguous tiles (256 x 192 and the small ones)
+// on the double-buffered one.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP>
 void launch_kernel(const GemmArgs& a, long grid, hipStream_t s) {
-  if constexpr (LA == kMC || LB == kMC)
+  if constexpr (LA == kMC || LB == kMC || (BM == 256 && BN == 256))
     hipLaunchKernelGGL((ring_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, GROUP>),
                        dim3((unsigned)grid), dim3(WAVES_M * WAVES_N * 64), 0, s, a);
   else
@@ -678,13 +668,8 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
       if (c192 < c256) return launch<256, 192, 4, 2, LA, LB, EPI>(a, s);
     }
   }
-  // both operands M/N-contiguous: 4 waves of 128 x 128 (two transposing
-  // reads per fragment make LDS reads the scarcer resource); otherwise 8
-  // waves of 64 x 128
-  if (big >= 256) {
-    if constexpr (LA == kMC && LB == kMC) return launch<256, 256, 2, 2, LA, LB, EPI>(a, s);
-    else return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
-  }
+  // 8 waves of 64 x 128 (two per SIMD)
+  if (big >= 256) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
 }
@@ -700,8 +685,8 @@ hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hi
 
 hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
-  if (epi == kAccF32) return launch_grouped_k<256, 256, 2, 2, kAccF32>(a, s);
-  if (epi == kStoreF32) return launch_grouped_k<256, 256, 2, 2, kStoreF32>(a, s);
+  if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
+  if (epi == kStoreF32) return launch_grouped_k<256, 256, 4, 2, kStoreF32>(a, s);
   return hipErrorInvalidValue;
 }
 
