@@ -391,7 +391,6 @@ __device__ __forceinline__ void adam1(float& p, float& m, float& v, float g, flo
 // independent 16-byte requests in flight. Every stream is touched once, so
 // the accesses are nontemporal (no cache allocation): ~8 % faster than
 // plain loads and stores on this chip, at copy bandwidth.
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 __global__ __launch_bounds__(256) void adamw_k(float* __restrict__ master,
                                                bf16_t* __restrict__ param,
                                                const float* __restrict__ grad,

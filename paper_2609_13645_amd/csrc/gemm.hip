@@ -110,6 +110,11 @@ __device__ __forceinline__ bf16x8_t frag(const uint4* tile, int base, int kk, in
 }
 
 // ---- epilogue: four consecutive n of row m ---------------------------------
+// fp32 C (and the C it accumulates into) goes through nontemporal accesses: a
+// round of 256 x 256 tiles writes about as much C per XCD as the XCD's L2
+// holds, and ordinary stores would evict the operand rows that the next tiles
+// read there. bf16 pieces of 8 bytes stay ordinary stores (streaming stores
+// that small are slower than the eviction they avoid).
 template <int EPI>
 __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const float* v) {
   if (m >= p.M) return;
@@ -136,12 +141,9 @@ __device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const fl
   } else {
     float* C = reinterpret_cast<float*>(p.C) + (long)m * p.ldc + n;
     if (full) {
-      float4 o = make_float4(v[0], v[1], v[2], v[3]);
-      if (EPI == kAccF32) {
-        const float4 c = *reinterpret_cast<const float4*>(C);
-        o.x += c.x; o.y += c.y; o.z += c.z; o.w += c.w;
-      }
-      *reinterpret_cast<float4*>(C) = o;
+      f32x4_t o = {v[0], v[1], v[2], v[3]};
+      if (EPI == kAccF32) o += __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(C));
+      __builtin_nontemporal_store(o, reinterpret_cast<f32x4_t*>(C));
     } else {
       for (int e = 0; e < 4; ++e)
         if (n + e < p.N) C[e] = (EPI == kAccF32 ? C[e] : 0.0f) + v[e];
@@ -457,19 +459,73 @@ __device__ __forceinline__ void wait_dma() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// ---- epilogue of a 16x16 block: lane holds C[m][n..n+3] --------------------
+// ---- bf16 epilogue: eight consecutive n of row m ---------------------------
+// A full piece is one 16-byte nontemporal store (see store4): with whole
+// 16-byte pieces, 64 contiguous bytes per row and instruction, streaming
+// stores keep the XCD's L2 for the operand rows.
+template <int EPI>
+__device__ __forceinline__ void store8_bf16(const GemmArgs& p, int m, int n, float* x) {
+  if (m >= p.M) return;
+  bf16_t* C = reinterpret_cast<bf16_t*>(p.C) + (long)m * p.ldc + n;
+  const bool full = (n + 7 < p.N);
+  if (EPI == kResidBF16) {
+    const bf16_t* R = p.R + (long)m * p.ldr + n;
+    if (full) {
+      float r[8];
+      unpack8(*reinterpret_cast<const uint4*>(R), r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] += r[e];
+    } else {
+      for (int e = 0; e < 8; ++e)
+        if (n + e < p.N) x[e] += bf2f(R[e]);
+    }
+  }
+  if (full) {
+    __builtin_nontemporal_store(__builtin_bit_cast(f32x4_t, pack8(x)), reinterpret_cast<f32x4_t*>(C));
+  } else {
+    for (int e = 0; e < 8; ++e)
+      if (n + e < p.N) C[e] = f2bf(x[e]);
+  }
+}
+
+// ---- epilogue of 16x16 blocks: lane holds C[m][n..n+3] ---------------------
+// bf16 output: lanes l and l ^ 16 swap halves of two neighbouring blocks so
+// that each lane holds eight consecutive n, and a row takes 64 contiguous
+// bytes per store instruction.
 template <int EPI, int FN, int FM>
 __device__ __forceinline__ void store_tile16(const GemmArgs& p, const f32x4_t (&acc)[FN][FM],
                                              int mw, int nw, int lane) {
+  if constexpr (EPI == kStoreBF16 || EPI == kResidBF16) {
+    static_assert(FN % 2 == 0, "bf16 epilogue pairs neighbouring n-blocks");
+    const int g = lane >> 4;
+    const bool even = (g & 1) == 0;
 #pragma unroll
-  for (int i = 0; i < FN; ++i)
+    for (int i = 0; i < FN; i += 2)
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
-      const int m = mw + j * 16 + (lane & 15);
-      const int n = nw + i * 16 + (lane >> 4) * 4;
-      const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      store4<EPI>(p, m, n, v);
-    }
+      for (int j = 0; j < FM; ++j) {
+        const int m = mw + j * 16 + (lane & 15);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float send = even ? acc[i + 1][j][e] : acc[i][j][e];
+          const float recv = __shfl_xor(send, 16);
+          x[e] = even ? acc[i][j][e] : recv;
+          x[4 + e] = even ? recv : acc[i + 1][j][e];
+        }
+        const int n = nw + (even ? i * 16 + g * 4 : (i + 1) * 16 + (g - 1) * 4);
+        store8_bf16<EPI>(p, m, n, x);
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int j = 0; j < FM; ++j) {
+        const int m = mw + j * 16 + (lane & 15);
+        const int n = nw + i * 16 + (lane >> 4) * 4;
+        const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4<EPI>(p, m, n, v);
+      }
+  }
 }
 
 // Each stage is one 16x16x32 k-step. Its fragments were read during the

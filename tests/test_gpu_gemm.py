@@ -98,6 +98,21 @@ def test_gemm_large_tiles_long_k_integer_exact(la, lb, epi):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("la,lb,epi", [(KC, KC, STORE_BF16), (KC, KC, RESID_BF16),
+                                       (KC, MC, RESID_BF16), (MC, MC, STORE_F32)])
+def test_gemm_large_tiles_ragged_n_integer_exact(la, lb, epi):
+    """256 x 256 tiles (16 x 16 = 256 of them: one full round) whose last
+    column of tiles ends in a half 16-wide block (N % 16 == 8), over a ragged
+    reduction (K % 32 == 8): the paired 16-byte bf16 stores fall back to
+    element stores at the edge."""
+    M, N, K = 4096, 4008, 264
+    banner(f"gemm int big tiles ragged N la={la} lb={lb} epi={epi}")
+    got, ref = run_gemm(la, lb, epi, M, N, K, seed=epi + 11)
+    want = (fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
+            if epi in (STORE_BF16, RESID_BF16) else ref)
+    assert np.array_equal(got, want)
+
+
 def test_gemm_zero_k_and_empty():
     banner("gemm K=0 / empty")
     got, ref = run_gemm(KC, KC, ACC_F32, 64, 64, 0)
