@@ -287,6 +287,54 @@ forge_status forge_grad_norm_sq(const float* g, int64_t n, float* accum,
 forge_status forge_clip_coeff(const float* norm_sq, float max_norm, float eps,
                               float* dev_scalars, forge_stream stream);
 
+/* Optimizer state of one weight tensor: fp32 master copy, fp32 moments m
+ * and v, and the bf16 parameter, all with the weight's element count and
+ * 16-byte aligned (device). */
+typedef struct {
+  float* master;
+  forge_bf16* param;
+  float* m;
+  float* v;
+} forge_adamw_tensor;
+
+/* Optimizer state of one layer's weights, named as in forge_layer_weights.
+ * Entries of weights the layer does not have (the expert weights of a dense
+ * layer, w_gate_up / w_down of a MoE layer) are ignored and may be zero. */
+typedef struct {
+  forge_adamw_tensor attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
+  forge_adamw_tensor w_router, w_gate_up_e, w_down_e;
+} forge_layer_optim;
+
+/*
+ * forge_layer_bwd followed by forge_adamw_step on every weight of the layer
+ * (grad = the matching member of `grads`, n = the weight's element count),
+ * with the same results bit for bit (App. F: fused clip + AdamW + bf16
+ * write-back). In a dense layer each weight's update is issued as soon as
+ * its gradient is complete and the backward has read the weight for the
+ * last time, on a stream of the library's own, so the memory-bound updates
+ * of the FFN weights run while the compute-bound attention backward is in
+ * flight; a MoE layer runs the updates after its backward.
+ * opt: each used entry's param must be the same pointer as the matching
+ *   member of w (the update overwrites the weight in place, after the
+ *   backward's last read of it); master, m, v are updated in place.
+ * hp, dev_scalars: as forge_adamw_step. dev_scalars (the clip coefficient
+ *   included) are read by the update kernels while the call's work runs, so
+ *   they must hold their final values by the point of `stream` where the
+ *   call is enqueued: clipping by this step's own gradient norm needs
+ *   forge_layer_bwd, forge_grad_norm_sq, forge_clip_coeff, forge_adamw_step.
+ * grads: as forge_layer_bwd (with overwrite == 0 the update uses the
+ *   accumulated gradient, so call this on the last micro-batch only).
+ * All other arguments and the errors as forge_layer_bwd, plus
+ * INVALID_ARG / ALIGNMENT for opt, hp and dev_scalars. The call's work,
+ * updates included, is complete when `stream` reaches the point after it.
+ */
+forge_status forge_layer_bwd_adamw(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                                   const void* saved, const forge_bf16* x_in,
+                                   const forge_bf16* d_out, forge_bf16* d_in,
+                                   const forge_layer_grads* grads, const forge_layer_optim* opt,
+                                   const forge_adamw_hparams* hp, const float* dev_scalars,
+                                   void* workspace, forge_stream stream);
+
 /* ------------------------------------------------------------------------ */
 /* Building blocks, exposed for per-kernel measurement and tests            */
 /* ------------------------------------------------------------------------ */

@@ -67,6 +67,16 @@ class AdamwHparams(ctypes.Structure):
                 ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
 
 
+class AdamwTensor(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("master", "param", "m", "v")]
+
+
+class LayerOptim(ctypes.Structure):
+    _fields_ = [(n, AdamwTensor) for n in
+                ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down",
+                 "w_router", "w_gate_up_e", "w_down_e")]
+
+
 class AttnCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("batch", "seq", "n_heads", "n_kv_heads", "head_dim")]
@@ -106,6 +116,11 @@ def load():
         "forge_embed_bwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
         "forge_adamw_step": (ctypes.c_int, [P, P, P, P, P, I64,
                                             ctypes.POINTER(AdamwHparams), P, P]),
+        "forge_layer_bwd_adamw": (ctypes.c_int, [ctypes.POINTER(LayerCfg),
+                                                 ctypes.POINTER(LayerWeights), P, P, P, P,
+                                                 ctypes.POINTER(LayerGrads),
+                                                 ctypes.POINTER(LayerOptim),
+                                                 ctypes.POINTER(AdamwHparams), P, P, P]),
         "forge_grad_norm_sq": (ctypes.c_int, [P, I64, P, P, P]),
         "forge_clip_coeff": (ctypes.c_int, [P, F32, F32, P, P]),
         "forge_gemm": (ctypes.c_int, [I32, I32, I32, P, P, P, P, I32, I32, I32,
@@ -178,6 +193,15 @@ def layer_grads(g: dict, overwrite: bool = False) -> LayerGrads:
     return LayerGrads(*[_ptr(g.get(n)) for n, _ in LayerGrads._fields_[:-1]], int(overwrite))
 
 
+def layer_optim(t: dict) -> LayerOptim:
+    """t: weight name -> dict(master=, param=, m=, v=) of device tensors."""
+    o = LayerOptim()
+    for name, _ in LayerOptim._fields_:
+        if name in t:
+            setattr(o, name, AdamwTensor(*[_ptr(t[name][k]) for k in ("master", "param", "m", "v")]))
+    return o
+
+
 def attn_cfg(c: dict) -> AttnCfg:
     return AttnCfg(c["batch"], c["seq"], c["n_heads"], c["n_kv_heads"], c["head_dim"])
 
@@ -247,6 +271,15 @@ def forge_adamw_step(master, param, grad, m, v, n, hparams: AdamwHparams, dev_sc
     _check(load().forge_adamw_step(_ptr(master), _ptr(param), _ptr(grad), _ptr(m), _ptr(v),
                                    int(n), ctypes.byref(hparams), _ptr(dev_scalars),
                                    _stream(stream)))
+
+
+def forge_layer_bwd_adamw(cfg, weights, saved, x_in, d_out, d_in, grads, optim: LayerOptim,
+                          hparams: AdamwHparams, dev_scalars, workspace, stream=None):
+    _check(load().forge_layer_bwd_adamw(ctypes.byref(cfg), ctypes.byref(weights), _ptr(saved),
+                                        _ptr(x_in), _ptr(d_out), _ptr(d_in),
+                                        ctypes.byref(grads), ctypes.byref(optim),
+                                        ctypes.byref(hparams), _ptr(dev_scalars),
+                                        _ptr(workspace), _stream(stream)))
 
 
 def forge_grad_norm_sq(g, n, accum, workspace, stream=None):

@@ -324,21 +324,27 @@ forge_status attn_block_fwd(const forge_layer_cfg& c, const Dims& d,
   return FORGE_OK;
 }
 
-// ---- side stream for the weight-gradient products ----------------------------
+// ---- side streams of the layer backward ----------------------------------------
 // The dense layer backward runs its four weight-gradient GEMMs on a second
 // stream of the same device, forked from the caller's stream after each one's
 // inputs exist and joined back before the call's work ends, so they fill the
 // tail waves of the data-gradient GEMMs and the bandwidth-bound kernels in
-// between. One non-blocking stream of default priority and its events per
-// device, created on first use and kept for the life of the process; launch
-// sequences on one device are serialised by a mutex, so concurrent callers do
-// not interleave their event records.
+// between. forge_layer_bwd_adamw adds a third stream for the optimizer
+// updates, each forked once its weight's gradient is complete and its
+// data-gradient product (the last reader of the weight) has run. Non-blocking
+// streams of default priority and their events, one set per device, created
+// on first use and kept for the life of the process; launch sequences on one
+// device are serialised by a mutex, so concurrent callers do not interleave
+// their event records. Each event is recorded once per call and waited on
+// right after its record.
 constexpr int kMaxDevices = 64;
+constexpr int kLaneEvents = 24;
 struct SideLane {
   std::mutex mu;
   bool ready = false;
-  hipStream_t stream = nullptr;
-  hipEvent_t ev[5] = {};
+  hipStream_t stream = nullptr;  // weight gradients
+  hipStream_t opt = nullptr;     // optimizer updates
+  hipEvent_t ev[kLaneEvents] = {};
 };
 SideLane g_side[kMaxDevices];
 std::mutex g_side_init;
@@ -352,6 +358,8 @@ hipError_t side_lane(SideLane** out) {
   std::lock_guard<std::mutex> lk(g_side_init);
   if (!L.ready) {
     e = hipStreamCreateWithFlags(&L.stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+    e = hipStreamCreateWithFlags(&L.opt, hipStreamNonBlocking);
     if (e != hipSuccess) return e;
     for (hipEvent_t& ev : L.ev) {
       e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
@@ -369,6 +377,35 @@ hipError_t link(hipStream_t from, hipStream_t to, hipEvent_t ev) {
   return e != hipSuccess ? e : hipStreamWaitEvent(to, ev, 0);
 }
 
+// Optimizer updates of forge_layer_bwd_adamw, issued on the lane's optimizer
+// stream behind everything enqueued so far on the caller's stream s and the
+// weight-gradient stream ws (events 5 onwards; 0..4 are the backward's).
+struct OptPlan {
+  const forge_layer_optim* o;
+  const forge_adamw_hparams* hp;
+  const float* scalars;
+  SideLane* lane;
+  int next_ev;
+};
+
+hipError_t opt_update(OptPlan* P, hipStream_t s, hipStream_t ws, const forge_adamw_tensor& t,
+                      const float* grad, long n) {
+  if (P->next_ev + 2 > kLaneEvents) return hipErrorInvalidValue;
+  hipStream_t os = P->lane->opt;
+  hipError_t e = link(s, os, P->lane->ev[P->next_ev++]);
+  if (e == hipSuccess && ws != s) e = link(ws, os, P->lane->ev[P->next_ev++]);
+  if (e != hipSuccess) return e;
+  return forge::adamw(t.master, reinterpret_cast<uint16_t*>(t.param), grad, t.m, t.v, n,
+                      P->hp->beta1, P->hp->beta2, P->hp->eps, P->hp->weight_decay, P->scalars,
+                      os);
+}
+
+// the optimizer stream's work happens before what is enqueued on s next
+hipError_t opt_join(OptPlan* P, hipStream_t s) {
+  if (P->next_ev + 1 > kLaneEvents) return hipErrorInvalidValue;
+  return link(P->lane->opt, s, P->lane->ev[P->next_ev++]);
+}
+
 // Backward of attn_block_fwd from dh1 (the full gradient at h1, residual
 // path included) to d_in.
 forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
@@ -376,7 +413,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                             const uint16_t* x, const uint16_t* a, const float* rstd1,
                             const uint16_t* qkv, const uint16_t* o, const float* lse,
                             const uint16_t* dh1, uint16_t* d_in, void* workspace, const Work& wk,
-                            hipStream_t s, SideLane* side = nullptr) {
+                            hipStream_t s, SideLane* side = nullptr, OptPlan* opt = nullptr) {
   uint16_t* dO = at<uint16_t>(workspace, wk.dO);
   float* delta = at<float>(workspace, wk.delta);
   uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
@@ -393,6 +430,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                         gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), ws));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
+  if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_o, g->d_w_o, d.h * d.hq));
   FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, lse, delta, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
                                  at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
@@ -405,9 +443,12 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                         gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), ws));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
+  if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_qkv, g->d_w_qkv, d.qkv * d.h));
   FORGE_HIP(forge::rmsnorm_bwd(x, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, !g->overwrite, s));
+  if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->attn_norm, g->d_attn_norm, d.h));
   if (side) FORGE_HIP(link(ws, s, side->ev[4]));  // join: the call's work ends on s
+  if (opt) FORGE_HIP(opt_join(opt, s));
   return FORGE_OK;
 }
 
@@ -594,11 +635,11 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   return ok();
 }
 
-forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
-                             const void* saved, const forge_bf16* x_in,
-                             const forge_bf16* d_out, forge_bf16* d_in,
-                             const forge_layer_grads* g, void* workspace,
-                             forge_stream stream) {
+namespace {
+forge_status check_layer_bwd_args(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                                  const void* saved, const forge_bf16* x_in,
+                                  const forge_bf16* d_out, forge_bf16* d_in,
+                                  const forge_layer_grads* g, void* workspace) {
   if (forge_status s = check_cfg(cfg)) return s;
   if (forge_status s = check_weights(*cfg, w)) return s;
   FORGE_PTR(saved);
@@ -606,11 +647,18 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   FORGE_PTR(d_out);
   FORGE_PTR(d_in);
   FORGE_PTR(workspace);
-  if (forge_status s = check_grads(*cfg, g)) return s;
+  return check_grads(*cfg, g);
+}
+
+// The layer backward; with `opt` (dense layers) each weight's optimizer
+// update is issued on the lane's optimizer stream as soon as it is final.
+forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                       const void* saved, const forge_bf16* x_in, const forge_bf16* d_out,
+                       forge_bf16* d_in, const forge_layer_grads* g, void* workspace,
+                       hipStream_t s, OptPlan* opt) {
   const Dims d = dims(*cfg);
   const Saved sv = saved_layout(*cfg);
   const Work wk = work_layout(*cfg);
-  hipStream_t s = (hipStream_t)stream;
   const uint16_t* a = at<uint16_t>(saved, sv.a);
   const float* rstd1 = at<float>(saved, sv.rstd1);
   const uint16_t* qkv = at<uint16_t>(saved, sv.qkv);
@@ -650,6 +698,7 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
     FORGE_HIP(side_lane(&side));
     std::lock_guard<std::mutex> lk(side->mu);
     hipStream_t ws = side->stream;
+    if (opt) opt->lane = side;
     FORGE_HIP(link(s, ws, side->ev[0]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), ws));
@@ -661,14 +710,108 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
                           gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
+    // the updates start once the gate/up data gradient is done: its one
+    // round of long tiles is the kernel most hurt by losing CUs to them
+    if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_down, g->d_w_down, d.h * d.f));
+    if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_gate_up, g->d_w_gate_up, 2 * d.f * d.h));
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
     FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
+    if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
     return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
-                          side);
+                          side, opt);
   }
   FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
   return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s);
+}
+
+// Per-weight optimizer state of the layer's weights: each used entry's
+// buffers present and aligned, and param the very weight the layer reads.
+forge_status check_optim(const forge_layer_cfg& c, const forge_layer_weights* w,
+                         const forge_layer_optim* o) {
+  FORGE_CHECK(o != nullptr, FORGE_ERR_INVALID_ARG, "opt is NULL");
+  auto one = [&](const forge_adamw_tensor& t, const forge_bf16* weight,
+                 const char* name) -> forge_status {
+    FORGE_CHECK(t.master && t.param && t.m && t.v, FORGE_ERR_INVALID_ARG,
+                "opt->%s has a NULL buffer", name);
+    FORGE_CHECK(aligned16(t.master) && aligned16(t.param) && aligned16(t.m) && aligned16(t.v),
+                FORGE_ERR_ALIGNMENT, "opt->%s has a buffer that is not 16-byte aligned", name);
+    FORGE_CHECK(t.param == weight, FORGE_ERR_INVALID_ARG,
+                "opt->%s.param must be the layer's %s weight pointer", name, name);
+    return FORGE_OK;
+  };
+  if (forge_status e = one(o->attn_norm, w->attn_norm, "attn_norm")) return e;
+  if (forge_status e = one(o->w_qkv, w->w_qkv, "w_qkv")) return e;
+  if (forge_status e = one(o->w_o, w->w_o, "w_o")) return e;
+  if (forge_status e = one(o->ffn_norm, w->ffn_norm, "ffn_norm")) return e;
+  if (c.n_experts == 0) {
+    if (forge_status e = one(o->w_gate_up, w->w_gate_up, "w_gate_up")) return e;
+    if (forge_status e = one(o->w_down, w->w_down, "w_down")) return e;
+  } else {
+    if (forge_status e = one(o->w_router, w->w_router, "w_router")) return e;
+    if (forge_status e = one(o->w_gate_up_e, w->w_gate_up_e, "w_gate_up_e")) return e;
+    if (forge_status e = one(o->w_down_e, w->w_down_e, "w_down_e")) return e;
+  }
+  return FORGE_OK;
+}
+
+forge_status check_hparams(const forge_adamw_hparams* hp) {
+  FORGE_CHECK(hp != nullptr, FORGE_ERR_INVALID_ARG, "hparams is NULL");
+  FORGE_CHECK(hp->beta1 >= 0.0f && hp->beta1 < 1.0f && hp->beta2 >= 0.0f && hp->beta2 < 1.0f,
+              FORGE_ERR_INVALID_ARG, "betas must be in [0, 1)");
+  FORGE_CHECK(hp->eps >= 0.0f && std::isfinite(hp->eps), FORGE_ERR_INVALID_ARG, "bad eps");
+  FORGE_CHECK(std::isfinite(hp->weight_decay), FORGE_ERR_INVALID_ARG, "bad weight_decay");
+  return FORGE_OK;
+}
+}  // namespace
+
+forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                             const void* saved, const forge_bf16* x_in,
+                             const forge_bf16* d_out, forge_bf16* d_in,
+                             const forge_layer_grads* g, void* workspace,
+                             forge_stream stream) {
+  if (forge_status e = check_layer_bwd_args(cfg, w, saved, x_in, d_out, d_in, g, workspace))
+    return e;
+  if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace,
+                                 (hipStream_t)stream, nullptr))
+    return e;
+  return ok();
+}
+
+forge_status forge_layer_bwd_adamw(const forge_layer_cfg* cfg, const forge_layer_weights* w,
+                                   const void* saved, const forge_bf16* x_in,
+                                   const forge_bf16* d_out, forge_bf16* d_in,
+                                   const forge_layer_grads* g, const forge_layer_optim* opt,
+                                   const forge_adamw_hparams* hp, const float* dev_scalars,
+                                   void* workspace, forge_stream stream) {
+  if (forge_status e = check_layer_bwd_args(cfg, w, saved, x_in, d_out, d_in, g, workspace))
+    return e;
+  if (forge_status e = check_optim(*cfg, w, opt)) return e;
+  if (forge_status e = check_hparams(hp)) return e;
+  FORGE_PTR(dev_scalars);
+  hipStream_t s = (hipStream_t)stream;
+  const Dims d = dims(*cfg);
+  if (d.E == 0) {
+    OptPlan plan{opt, hp, dev_scalars, nullptr, 5};
+    if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace, s, &plan))
+      return e;
+    return ok();
+  }
+  // MoE layer: the backward, then every update in order on the caller's stream
+  if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace, s, nullptr))
+    return e;
+  auto upd = [&](const forge_adamw_tensor& t, const float* grad, long n) {
+    return forge::adamw(t.master, reinterpret_cast<uint16_t*>(t.param), grad, t.m, t.v, n,
+                        hp->beta1, hp->beta2, hp->eps, hp->weight_decay, dev_scalars, s);
+  };
+  FORGE_HIP(upd(opt->attn_norm, g->d_attn_norm, d.h));
+  FORGE_HIP(upd(opt->w_qkv, g->d_w_qkv, d.qkv * d.h));
+  FORGE_HIP(upd(opt->w_o, g->d_w_o, d.h * d.hq));
+  FORGE_HIP(upd(opt->ffn_norm, g->d_ffn_norm, d.h));
+  FORGE_HIP(upd(opt->w_router, g->d_w_router, d.E * d.h));
+  FORGE_HIP(upd(opt->w_gate_up_e, g->d_w_gate_up_e, d.E * 2 * d.fe * d.h));
+  FORGE_HIP(upd(opt->w_down_e, g->d_w_down_e, d.E * d.h * d.fe));
+  return ok();
 }
 
 // ---- MoE routing building block -----------------------------------------------
@@ -827,11 +970,7 @@ forge_status forge_adamw_step(float* master, forge_bf16* param, const float* gra
                               float* v, int64_t n, const forge_adamw_hparams* hp,
                               const float* dev_scalars, forge_stream stream) {
   FORGE_CHECK(n >= 0, FORGE_ERR_INVALID_ARG, "n must be >= 0");
-  FORGE_CHECK(hp != nullptr, FORGE_ERR_INVALID_ARG, "hparams is NULL");
-  FORGE_CHECK(hp->beta1 >= 0.0f && hp->beta1 < 1.0f && hp->beta2 >= 0.0f && hp->beta2 < 1.0f,
-              FORGE_ERR_INVALID_ARG, "betas must be in [0, 1)");
-  FORGE_CHECK(hp->eps >= 0.0f && std::isfinite(hp->eps), FORGE_ERR_INVALID_ARG, "bad eps");
-  FORGE_CHECK(std::isfinite(hp->weight_decay), FORGE_ERR_INVALID_ARG, "bad weight_decay");
+  if (forge_status e = check_hparams(hp)) return e;
   if (n == 0) return ok();
   FORGE_PTR(master);
   FORGE_PTR(param);

@@ -152,6 +152,19 @@ class Layer:
                              x_in, d_out, d_in, self.grads,
                              self.workspace if workspace is None else workspace, self.stream)
 
+    def bwd_adamw(self, x_in, d_out, d_in, flat: "FlatParams", hparams, dev_scalars,
+                  overwrite=True):
+        """Backward plus the AdamW update of every weight of this layer (its
+        weights must be views into `flat`), each update overlapping the rest
+        of the backward; dev_scalars = device fp32 {lr, bc1, bc2, clip}."""
+        self.grads.overwrite = int(overwrite)
+        opt = _lib.layer_optim({n: {k: flat.view(getattr(flat, k), n)
+                                    for k in ("master", "param", "m", "v")}
+                                for n in self.names})
+        _lib.forge_layer_bwd_adamw(self.c, self.weights, self.saved, x_in, d_out, d_in,
+                                   self.grads, opt, hparams, dev_scalars, self.workspace,
+                                   self.stream)
+
 
 class Model:
     """A whole decoder stack's training step through the C ABI.

@@ -124,6 +124,45 @@ def test_optimizer_argument_rules():
     assert ctypes.sizeof(_lib.LayerGrads) == 9 * 8 + 8    # 9 pointers + int32 + padding
 
 
+def test_layer_bwd_adamw_argument_rules():
+    """The fused backward + update checks its optimizer arguments before any
+    launch: every used weight's state present and aligned, param the very
+    weight pointer, valid hyper-parameters, non-NULL device scalars."""
+    c = _lib.layer_cfg(fi.config("tiny"))
+    ptrs = [0x10000 * (i + 1) for i in range(8)]
+    w = _lib.LayerWeights(*(ptrs + [0, 0, 0]))
+    g = _lib.LayerGrads(*([0x900000 + 0x1000 * i for i in range(6)] + [0, 0, 0]), 1)
+    names = ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")
+
+    def optim(**change):
+        t = {n: dict(master=0xA00000 + 0x1000 * i, param=ptrs[i], m=0xB00000 + 0x1000 * i,
+                     v=0xC00000 + 0x1000 * i) for i, n in enumerate(names)}
+        for k, v in change.items():
+            n, field = k.split("__")
+            t[n][field] = v
+        o = _lib.LayerOptim()
+        for n, d in t.items():
+            setattr(o, n, _lib.AdamwTensor(d["master"], d["param"], d["m"], d["v"]))
+        return o
+
+    hp = _lib.AdamwHparams(0.9, 0.95, 1e-8, 0.1)
+    args = (c, w, 0x2000, 0x3000, 0x4000, 0x5000, g)
+
+    def status(o, h=hp, sc=0x6000):
+        try:
+            _lib.forge_layer_bwd_adamw(*args, o, h, sc, 0x7000, 0)
+        except _lib.ForgeError as e:
+            return e.status
+        return _lib.FORGE_OK
+
+    assert status(optim(w_o__param=ptrs[1])) == _lib.FORGE_ERR_INVALID_ARG   # not the weight
+    assert status(optim(w_down__m=0)) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(optim(w_qkv__v=0xC01008)) == _lib.FORGE_ERR_ALIGNMENT
+    assert status(optim(), h=_lib.AdamwHparams(0.9, 1.0, 1e-8, 0.1)) == _lib.FORGE_ERR_INVALID_ARG
+    assert status(optim(), sc=None) == _lib.FORGE_ERR_INVALID_ARG
+    assert ctypes.sizeof(_lib.LayerOptim) == 9 * 4 * 8
+
+
 def test_moe_layer_sizes():
     c5 = fi.config("moe_layer")
     cfg = _lib.layer_cfg(c5)
