@@ -313,7 +313,9 @@ typedef struct {
  * its gradient is complete and the backward has read the weight for the
  * last time, on a stream of the library's own, so the memory-bound updates
  * of the FFN weights run while the compute-bound attention backward is in
- * flight; a MoE layer runs the updates after its backward.
+ * flight (dense layers of fewer than 2^20 token x hidden elements, where
+ * the stream hand-offs would cost more than they save, and MoE layers run
+ * the updates in order on `stream`).
  * opt: each used entry's param must be the same pointer as the matching
  *   member of w (the update overwrites the weight in place, after the
  *   backward's last read of it); master, m, v are updated in place.

@@ -325,8 +325,8 @@ forge_status attn_block_fwd(const forge_layer_cfg& c, const Dims& d,
 }
 
 // ---- side streams of the layer backward ----------------------------------------
-// The dense layer backward runs its four weight-gradient GEMMs on a second
-// stream of the same device, forked from the caller's stream after each one's
+// The dense layer backward (from 2^20 token x hidden elements up) runs its
+// four weight-gradient GEMMs on a second stream of the same device, forked from the caller's stream after each one's
 // inputs exist and joined back before the call's work ends, so they fill the
 // tail waves of the data-gradient GEMMs and the bandwidth-bound kernels in
 // between. forge_layer_bwd_adamw adds a third stream for the optimizer
@@ -348,6 +348,9 @@ struct SideLane {
 };
 SideLane g_side[kMaxDevices];
 std::mutex g_side_init;
+
+// side streams only for layers whose products outlast the event hand-offs
+bool use_side_streams(const Dims& d) { return d.T * d.h >= (1L << 20); }
 
 hipError_t side_lane(SideLane** out) {
   int dev = 0;
@@ -379,7 +382,8 @@ hipError_t link(hipStream_t from, hipStream_t to, hipEvent_t ev) {
 
 // Optimizer updates of forge_layer_bwd_adamw, issued on the lane's optimizer
 // stream behind everything enqueued so far on the caller's stream s and the
-// weight-gradient stream ws (events 5 onwards; 0..4 are the backward's).
+// weight-gradient stream ws (events 5 onwards; 0..4 are the backward's); a
+// layer without a lane issues them in order on s.
 struct OptPlan {
   const forge_layer_optim* o;
   const forge_adamw_hparams* hp;
@@ -390,11 +394,14 @@ struct OptPlan {
 
 hipError_t opt_update(OptPlan* P, hipStream_t s, hipStream_t ws, const forge_adamw_tensor& t,
                       const float* grad, long n) {
-  if (P->next_ev + 2 > kLaneEvents) return hipErrorInvalidValue;
-  hipStream_t os = P->lane->opt;
-  hipError_t e = link(s, os, P->lane->ev[P->next_ev++]);
-  if (e == hipSuccess && ws != s) e = link(ws, os, P->lane->ev[P->next_ev++]);
-  if (e != hipSuccess) return e;
+  hipStream_t os = s;  // without a lane (small layer): in order on the caller's stream
+  if (P->lane) {
+    if (P->next_ev + 2 > kLaneEvents) return hipErrorInvalidValue;
+    os = P->lane->opt;
+    hipError_t e = link(s, os, P->lane->ev[P->next_ev++]);
+    if (e == hipSuccess && ws != s) e = link(ws, os, P->lane->ev[P->next_ev++]);
+    if (e != hipSuccess) return e;
+  }
   return forge::adamw(t.master, reinterpret_cast<uint16_t*>(t.param), grad, t.m, t.v, n,
                       P->hp->beta1, P->hp->beta2, P->hp->eps, P->hp->weight_decay, P->scalars,
                       os);
@@ -402,6 +409,7 @@ hipError_t opt_update(OptPlan* P, hipStream_t s, hipStream_t ws, const forge_ada
 
 // the optimizer stream's work happens before what is enqueued on s next
 hipError_t opt_join(OptPlan* P, hipStream_t s) {
+  if (!P->lane) return hipSuccess;
   if (P->next_ev + 1 > kLaneEvents) return hipErrorInvalidValue;
   return link(P->lane->opt, s, P->lane->ev[P->next_ev++]);
 }
@@ -694,18 +702,21 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     uint16_t* dgu = at<uint16_t>(workspace, wk.dgu);
     // weight gradients on the side stream (see SideLane): dW_down as soon
     // as the call starts, dW_gate_up once dgu exists
+    // small layers stay on the caller's stream: there the event hand-offs
+    // cost more than the overlap gains
     SideLane* side = nullptr;
-    FORGE_HIP(side_lane(&side));
-    std::lock_guard<std::mutex> lk(side->mu);
-    hipStream_t ws = side->stream;
+    if (use_side_streams(d)) FORGE_HIP(side_lane(&side));
+    std::unique_lock<std::mutex> lk;
+    if (side) lk = std::unique_lock<std::mutex>(side->mu);
+    hipStream_t ws = side ? side->stream : s;
     if (opt) opt->lane = side;
-    FORGE_HIP(link(s, ws, side->ev[0]));
+    if (side) FORGE_HIP(link(s, ws, side->ev[0]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
     FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
-    FORGE_HIP(link(s, ws, side->ev[1]));
+    if (side) FORGE_HIP(link(s, ws, side->ev[1]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
