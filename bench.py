@@ -61,6 +61,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=WORKLOAD, choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step into a HIP graph and time replays of it "
+                         "(measured slower than issuing the calls on ROCm 7.2 for these "
+                         "workloads, so not the default)")
     ap.add_argument("--cpu-seq", type=int, default=4096,
                     help="tokens of the CPU-baseline sample (layer workloads)")
     ap.add_argument("--kernel-reps", type=int, default=20)
@@ -110,9 +114,10 @@ class Step:
             self.dx = torch.empty_like(self.x)
         self.hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"],
                                     cfg["weight_decay"])
-        self.scal = torch.zeros(4, dtype=torch.float32, device="cuda")
-        self.host_scal = torch.zeros(4, dtype=torch.float32).pin_memory()
-        self.t = 0
+        # step scalars {lr, 1 - b1^t, 1 - b2^t, clip = 1} advanced on the
+        # device each step, so the step needs no host writes (graph replay)
+        self.scal = torch.tensor([0.0, 0.0, 0.0, 1.0], dtype=torch.float32, device="cuda")
+        self.dstep = torch.zeros(1, dtype=torch.int32, device="cuda")
 
     def zero(self):
         # gradients are written, not accumulated, by the backward (one
@@ -133,12 +138,9 @@ class Step:
             self.layer.bwd(self.x, self.dy, self.dx, overwrite=True)
 
     def _scalars(self):
-        import torch
-        self.t += 1
         c = self.cfg
-        self.host_scal.copy_(torch.tensor([c["lr"], 1 - c["beta1"] ** self.t,
-                                           1 - c["beta2"] ** self.t, 1.0]))
-        self.scal.copy_(self.host_scal, non_blocking=True)
+        self.lib.forge_adamw_advance(self.scal, self.dstep, c["lr"], c["beta1"], c["beta2"],
+                                     self.stream)
 
     def adamw(self):
         self._scalars()
@@ -305,23 +307,45 @@ def recorded_traffic():
     return rec["traffic_bytes"] if rec.get("source_sha256") == source_digest() else None
 
 
-def gpu_step_bench(cfg, steps, warmup, kernel_reps):
+def gpu_step_bench(cfg, steps, warmup, kernel_reps, graph=False):
+    """Time `steps` training steps after `warmup` eager ones. With `graph`,
+    one step is captured into a HIP graph (every libforge call is
+    capturable: no allocation, memset or host synchronisation inside; the
+    side streams join the capture through events; the AdamW step scalars
+    advance on the device) and the timed steps are replays of it."""
     import torch
     torch.cuda.set_device(0)
-    stream = torch.cuda.current_stream()
-    step = Step(cfg, stream)
-    for _ in range(warmup):
-        step()
+    stream = torch.cuda.Stream() if graph else torch.cuda.current_stream()
     torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        step = Step(cfg, stream)
+        for _ in range(warmup):
+            step()
+    torch.cuda.synchronize()
+    run = step
+    if graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            step()
+        torch.cuda.synchronize()
+        run = g.replay
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(steps):
-        step()
-    e1.record(stream)
+    with torch.cuda.stream(stream):
+        e0.record(stream)
+        for _ in range(steps):
+            run()
+        e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     assert step.finite(), "non-finite output or master weights"
+    with torch.cuda.stream(stream):
+        phases, kernel = _phases_and_kernel(cfg, stream, step, steps, kernel_reps)
+    return ms, phases, kernel, step.flat.n
+
+
+def _phases_and_kernel(cfg, stream, step, steps, kernel_reps):
+    import torch
 
     # phase split (separate pass, not part of the headline number); a model's
     # forward and backward are one call (the loss head fuses them)
@@ -354,8 +378,7 @@ def gpu_step_bench(cfg, steps, warmup, kernel_reps):
             ev[2].record(stream)
             torch.cuda.synchronize()
             phases["bwd_adamw_overlapped"] += ev[1].elapsed_time(ev[2]) / reps
-    kernel = dominant_kernel(cfg, stream, step, kernel_reps)
-    return ms, phases, kernel, step.flat.n
+    return phases, dominant_kernel(cfg, stream, step, kernel_reps)
 
 
 def cpu_baseline(cfg, seq):
@@ -467,8 +490,8 @@ def main():
     step_flop = flops.step_flops(cfg)
     print(f"[bench] workload {args.workload}: {DESCRIPTION[args.workload]}; "
           f"warmup={args.warmup} steps={args.steps}", file=sys.stderr, flush=True)
-    ms, phases, kernel, nparams = gpu_step_bench(cfg, args.steps, args.warmup,
-                                                 args.kernel_reps)
+    ms, phases, kernel, nparams = gpu_step_bench(cfg, args.steps, args.warmup, args.kernel_reps,
+                                                 args.graph)
     tflops = step_flop / (ms * 1e-3) / 1e12
     print(f"[bench] {ms:.3f} ms/step, {tflops:.1f} TFLOP/s; phases {phases}",
           file=sys.stderr, flush=True)
@@ -491,6 +514,7 @@ def main():
         "mfu_fwd_bwd_pct": round(100.0 * step_flop / (fb_ms * 1e-3) / 1e12 / MFU_PEAK_TFLOPS, 2),
         "tokens_per_s": round(T / (ms * 1e-3), 1),
         "phases_ms": {k: round(v, 4) for k, v in phases.items()},
+        "launch": "graph replay of one captured step" if args.graph else "eager",
         "config": {"workload": args.workload, "description": DESCRIPTION[args.workload],
                    "batch": cfg["batch"], "seq": cfg["seq"], "hidden": cfg["hidden"],
                    "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"],

@@ -12,7 +12,8 @@
  * Conventions (every entry point):
  *   - Pointers are device memory owned by the caller unless a parameter says
  *     "host". The library allocates no device memory and keeps no state
- *     beyond a per-device property cache.
+ *     beyond a per-device property cache and, per device, the side streams
+ *     and events of the layer backward (created on first use).
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
  *     default stream). Nothing synchronises with the host.
  *   - Arguments are validated on the host before anything is launched; a
@@ -29,6 +30,14 @@
  *     except where a function says otherwise.
  *   - Calls on one stream are ordered; concurrent calls on different streams
  *     must not share workspace, saved or output buffers.
+ *   - Every call can be captured into a HIP graph on `stream` (App. E,
+ *     "Whole-forward graph capture", extended here to the whole step): no
+ *     allocation, memset, copy or host synchronisation happens inside; the
+ *     layer backward's side streams join the capture through events recorded
+ *     on `stream` and are joined back before the call returns. Run one
+ *     forge_layer_bwd / forge_layer_bwd_adamw on the device eagerly before
+ *     the first capture (it creates the side streams); keep step-dependent
+ *     scalars on the device (forge_adamw_advance, forge_clip_coeff).
  */
 #ifndef FORGE_H
 #define FORGE_H
@@ -271,6 +280,19 @@ forge_status forge_adamw_step(float* master, forge_bf16* param, const float* gra
                               float* m, float* v, int64_t n,
                               const forge_adamw_hparams* hp, const float* dev_scalars,
                               forge_stream stream);
+
+/* The step scalars of forge_adamw_step kept on the device, so a whole
+ * training step needs no host writes and can be captured into a graph and
+ * replayed (App. F, "Deep customization": step scalars on the device):
+ *   t = ++dev_step[0]; dev_scalars[0] = lr;
+ *   dev_scalars[1] = 1 - beta1^t; dev_scalars[2] = 1 - beta2^t
+ * (betas and powers in fp64, then rounded to fp32: the bias corrections of
+ * the exact betas, not of their fp32 roundings that the moment updates of
+ * forge_adamw_hparams use). dev_scalars[3] (the clip
+ * coefficient, from forge_clip_coeff or set once by the caller) is left as
+ * it is. dev_step: device int32, 0 before the first step. */
+forge_status forge_adamw_advance(float* dev_scalars, int32_t* dev_step, float lr, double beta1,
+                                 double beta2, forge_stream stream);
 
 /* Floats of scratch that forge_grad_norm_sq needs. */
 #define FORGE_GRAD_NORM_WORKSPACE_FLOATS 1024

@@ -121,6 +121,7 @@ def load():
                                                  ctypes.POINTER(LayerGrads),
                                                  ctypes.POINTER(LayerOptim),
                                                  ctypes.POINTER(AdamwHparams), P, P, P]),
+        "forge_adamw_advance": (ctypes.c_int, [P, P, F32, ctypes.c_double, ctypes.c_double, P]),
         "forge_grad_norm_sq": (ctypes.c_int, [P, I64, P, P, P]),
         "forge_clip_coeff": (ctypes.c_int, [P, F32, F32, P, P]),
         "forge_gemm": (ctypes.c_int, [I32, I32, I32, P, P, P, P, I32, I32, I32,
@@ -280,6 +281,11 @@ def forge_layer_bwd_adamw(cfg, weights, saved, x_in, d_out, d_in, grads, optim: 
                                         ctypes.byref(grads), ctypes.byref(optim),
                                         ctypes.byref(hparams), _ptr(dev_scalars),
                                         _ptr(workspace), _stream(stream)))
+
+
+def forge_adamw_advance(dev_scalars, dev_step, lr, beta1, beta2, stream=None):
+    _check(load().forge_adamw_advance(_ptr(dev_scalars), _ptr(dev_step), lr, beta1, beta2,
+                                      _stream(stream)))
 
 
 def forge_grad_norm_sq(g, n, accum, workspace, stream=None):

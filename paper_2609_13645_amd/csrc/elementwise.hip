@@ -431,6 +431,19 @@ __global__ __launch_bounds__(256) void adamw_k(float* __restrict__ master,
   }
 }
 
+// Step scalars of the next AdamW update, kept on the device: t = ++step;
+// {lr, 1 - b1^t, 1 - b2^t} into sc[0..2] (betas and powers in fp64, then
+// rounded to fp32); sc[3], the clip coefficient, is left as it is. One thread.
+__global__ void adamw_advance_k(float* __restrict__ sc, int32_t* __restrict__ step, float lr,
+                                double b1, double b2) {
+  if (threadIdx.x != 0) return;
+  const int32_t t = step[0] + 1;
+  step[0] = t;
+  sc[0] = lr;
+  sc[1] = (float)(1.0 - pow(b1, (double)t));
+  sc[2] = (float)(1.0 - pow(b2, (double)t));
+}
+
 // ------------------------------------------------ gradient norm, clip ----
 // Block b sums the squares of its fixed contiguous slice; then one block
 // adds the partials in a fixed tree order.
@@ -595,6 +608,11 @@ hipError_t adamw(float* master, uint16_t* param, const float* grad, float* m, fl
   const int64_t blocks = (work + 255) / 256;
   hipLaunchKernelGGL(adamw_k, dim3((unsigned)blocks), dim3(256), 0, s, master, param, grad, m, v,
                      n, b1, b2, eps, wd, sc);
+  return hipGetLastError();
+}
+
+hipError_t adamw_advance(float* sc, int32_t* step, float lr, double b1, double b2, hipStream_t s) {
+  hipLaunchKernelGGL(adamw_advance_k, dim3(1), dim3(64), 0, s, sc, step, lr, b1, b2);
   return hipGetLastError();
 }
 

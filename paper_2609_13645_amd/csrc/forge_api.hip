@@ -994,6 +994,18 @@ forge_status forge_adamw_step(float* master, forge_bf16* param, const float* gra
   return ok();
 }
 
+forge_status forge_adamw_advance(float* dev_scalars, int32_t* dev_step, float lr, double beta1,
+                                 double beta2, forge_stream stream) {
+  FORGE_CHECK(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0,
+              FORGE_ERR_INVALID_ARG, "betas must be in [0, 1)");
+  FORGE_CHECK(std::isfinite(lr), FORGE_ERR_INVALID_ARG, "bad lr");
+  FORGE_PTR(dev_scalars);
+  FORGE_CHECK(dev_step != nullptr && (reinterpret_cast<uintptr_t>(dev_step) & 3u) == 0,
+              FORGE_ERR_INVALID_ARG, "dev_step is NULL or not 4-byte aligned");
+  FORGE_HIP(forge::adamw_advance(dev_scalars, dev_step, lr, beta1, beta2, (hipStream_t)stream));
+  return ok();
+}
+
 forge_status forge_grad_norm_sq(const float* g, int64_t n, float* accum, float* workspace,
                                 forge_stream stream) {
   FORGE_CHECK(n >= 0, FORGE_ERR_INVALID_ARG, "n must be >= 0");

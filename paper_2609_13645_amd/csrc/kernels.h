@@ -85,6 +85,8 @@ hipError_t mean_reduce(const float* v, int n, float scale, float* out, hipStream
 hipError_t adamw(float* master, uint16_t* param, const float* grad, float* m, float* v,
                  int64_t n, float b1, float b2, float eps, float wd,
                  const float* scalars, hipStream_t s);
+hipError_t adamw_advance(float* scalars, int32_t* step, float lr, double b1, double b2,
+                         hipStream_t s);
 constexpr int kNormPartials = 1024;
 hipError_t sumsq_partials(const float* g, int64_t n, float* partials, hipStream_t s);
 hipError_t sumsq_finish(const float* partials, float* accum, hipStream_t s);

@@ -221,6 +221,7 @@ class Model:
         self.hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"],
                                     cfg["weight_decay"])
         self.step_count = 0
+        self.dev_step = torch.zeros(1, dtype=torch.int32, device=device)
 
     def w_lm(self, buf):
         return self.flat.view(buf, "embedding" if self.tied else "w_lm")
@@ -254,13 +255,14 @@ class Model:
         return self.loss
 
     def optimizer_step(self, lr=None, clip=1.0):
-        """One fused AdamW over all parameters; bias corrections for the next step."""
-        torch = _torch()
+        """One fused AdamW over all parameters. The step count and bias
+        corrections advance on the device (no host write: capturable)."""
         self.step_count += 1
-        c, t = self.cfg, self.step_count
+        c = self.cfg
         lr = c["lr"] if lr is None else lr
-        self.scalars.copy_(torch.tensor([lr, 1 - c["beta1"] ** t, 1 - c["beta2"] ** t, clip],
-                                        dtype=torch.float32))
+        self.scalars[3:4].fill_(clip)
+        _lib.forge_adamw_advance(self.scalars, self.dev_step, lr, c["beta1"], c["beta2"],
+                                 self.stream)
         f = self.flat
         _lib.forge_adamw_step(f.master, f.param, f.grad, f.m, f.v, f.n, self.hp,
                               self.scalars, self.stream)
