@@ -43,6 +43,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7FFFFFF0,
                                            0x00020000);
 }
+// A buffer of `bytes` bytes: loads at or past the end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_n(const void* base, long bytes) {
+  const int n = bytes <= 0 ? 0 : (bytes > 0x7FFFFFF0L ? 0x7FFFFFF0 : (int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
@@ -60,45 +65,71 @@ __device__ __forceinline__ int slot(int r, int c) {
   return r * (D / 8) + (c ^ fsw<D>(r));
 }
 
-// DMA 64 rows [row0, row0 + 64) of a [*, ld] bf16 matrix (column block at
-// base) into a natural tile; rows >= lim read as zeros.
+// DMA of 64 rows [row0, row0 + 64) of a [*, ld] bf16 matrix (column block at
+// base) into a natural tile, 1 KB per wave instruction. The lane's byte
+// offsets are computed once per block (dma_offsets; they do not depend on
+// the tile); rows at or past `lim` read as zeros, cut off by the buffer's
+// size rather than by a per-lane test.
 template <int D, int NW>
-__device__ __forceinline__ void dma_tile(const bf16_t* base, long ld, int row0, int lim,
-                                         uint4* lds, int wave, int lane) {
-  constexpr int LPR = D / 8;            // 16-byte chunks per row
-  constexpr int RPI = 64 / LPR;         // rows per 1 KB instruction
-  constexpr int PER = 64 / RPI / NW;    // instructions per wave
+struct DmaPlan {
+  static constexpr int LPR = D / 8, RPI = 64 / LPR, PER = 64 / RPI / NW;
   static_assert(PER * RPI * NW == 64, "tile rows must split over waves");
-  const __amdgpu_buffer_rsrc_t r = rsrc(base + (long)row0 * ld);
+};
+template <int D, int NW>
+__device__ __forceinline__ void dma_offsets(long ld, int wave, int lane, uint32_t* off) {
+  using P = DmaPlan<D, NW>;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int q = i * NW + wave;
-    const int row = q * RPI + lane / LPR;
-    const int c = (lane % LPR) ^ fsw<D>(row);
-    const uint32_t off = row0 + row < lim ? (uint32_t)(((long)row * ld + c * 8) * 2) : kOOB;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + q * 64), 16, off, 0, 0, 0);
+  for (int i = 0; i < P::PER; ++i) {
+    const int row = (i * NW + wave) * P::RPI + lane / P::LPR;
+    const int c = (lane % P::LPR) ^ fsw<D>(row);
+    off[i] = (uint32_t)(((long)row * ld + c * 8) * 2);
   }
 }
-
-// Row fragment: rows rb..rb+31 (lane row rb + lane % 32), d = kk*16 + 8*(lane/32) .. +7.
-template <int D>
-__device__ __forceinline__ bf16x8_t row_frag(const uint4* t, int rb, int kk, int lane) {
-  return __builtin_bit_cast(bf16x8_t, t[slot<D>(rb + (lane & 31), kk * 2 + (lane >> 5))]);
+template <int D, int NW>
+__device__ __forceinline__ void dma_tile_at(const bf16_t* base, long ld, int row0, int lim,
+                                            uint4* lds, int wave, const uint32_t* off) {
+  using P = DmaPlan<D, NW>;
+  const __amdgpu_buffer_rsrc_t r = rsrc_n(base + (long)row0 * ld, (long)(lim - row0) * ld * 2);
+#pragma unroll
+  for (int i = 0; i < P::PER; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + (i * NW + wave) * 64), 16, off[i],
+                                             0, 0, 0);
 }
 
-// Transposed fragment: column d = db*32 + lane % 32 of the tile, rows
-// (the reduction index) r16 + 4h + {0..3} and r16 + 8 + 4h + {0..3}, h = lane/32.
+// Row fragment: rows rb..rb+31 (lane row rb + lane % 32), d = kk*16 +
+// 8*(lane/32) .. +7. Transposed fragment: column d = db*32 + lane % 32 of the
+// tile, rows (the reduction index) r16 + 4h + {0..3} and r16 + 8 + 4h +
+// {0..3}, h = lane/32.
+// Both are read from per-lane byte offsets computed once per block
+// (frag_offsets) plus a compile-time offset OFF (tensor within the stage,
+// first row: a multiple of 16 rows, which leaves the swizzle unchanged), so
+// each read is one LDS instruction with an immediate offset and no address
+// arithmetic.
 template <int D>
-__device__ __forceinline__ bf16x8_t tr_frag(const uint4* t, int r16, int db, int lane) {
-  const uint16_t* e = reinterpret_cast<const uint16_t*>(t);
+__device__ __forceinline__ void frag_offsets(int lane, uint32_t (&ro)[D / 16],
+                                             uint32_t (&to)[D / 32][2]) {
+  const int hh = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) ro[kk] = slot<D>(l32, kk * 2 + hh) * 16;
   const int g = lane >> 4, i = lane & 15;
-  const int d = db * 32 + (g & 1) * 16 + 4 * (i & 3);
-  const int r = r16 + (g >> 1) * 4 + (i >> 2);
-  const int c = d >> 3, w = d & 7;
-  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_v4i16_ptr)(e + (long)slot<D>(r, c) * 8 + w));
-  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_v4i16_ptr)(e + (long)slot<D>(r + 8, c) * 8 + w));
+  const int r = (g >> 1) * 4 + (i >> 2);
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    const int d = db * 32 + (g & 1) * 16 + 4 * (i & 3);
+    to[db][0] = (slot<D>(r, d >> 3) * 8 + (d & 7)) * 2;
+    to[db][1] = (slot<D>(r + 8, d >> 3) * 8 + (d & 7)) * 2;
+  }
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8_t row_at(const uint4* t, uint32_t ro) {
+  return __builtin_bit_cast(bf16x8_t,
+                            *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(t) + ro + OFF));
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8_t tr_at(const uint4* t, const uint32_t (&to)[2]) {
+  const char* e = reinterpret_cast<const char*>(t) + OFF;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(e + to[0]));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)(e + to[1]));
   const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
   return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
 }
@@ -235,10 +266,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
     }
   }
 
+  uint32_t doff[DmaPlan<D, 4>::PER];
+  dma_offsets<D, 4>(a.ld_qkv, wave, lane, doff);
   auto dma = [&](int kt) __attribute__((always_inline)) {
     uint4* st = smem + (kt & 1) * 2 * NAT;
-    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, st, wave, lane);
-    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, st + NAT, wave, lane);
+    dma_tile_at<D, 4>(Kg, a.ld_qkv, kt * BKV, S, st, wave, doff);
+    dma_tile_at<D, 4>(Vg, a.ld_qkv, kt * BKV, S, st + NAT, wave, doff);
   };
   auto tile = [&](auto STG, int kt) __attribute__((always_inline)) {
     constexpr int SO = decltype(STG)::value * STAGE_B;
@@ -382,9 +415,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
 }
 
 // -------------------------------------------------- backward pre-pass ----
-// delta[b, n, s] = sum_d dO[t, n, d] O[t, n, d] and, in the second half of
-// the buffer, -LSE[b, n, s] * log2(e) (the exponent offset of P = exp(S - LSE)
-// in base 2); 8 lanes per (token, head).
+// delta[b, n, s] = -sum_d dO[t, n, d] O[t, n, d] (negated: it initialises the
+// dP accumulators, which then hold dP - rowsum(dO O)) and, in the second half
+// of the buffer, -LSE[b, n, s] * log2(e) (the exponent offset of
+// P = exp(S - LSE) in base 2); 8 lanes per (token, head).
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* __restrict__ o,
                                                       const bf16_t* __restrict__ dout,
@@ -414,7 +448,7 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* 
   if (ok && sub == 0) {
     const long bb = t / a.seq, i = t % a.seq;
     const long li = (bb * a.n_heads + n) * a.seq + i;
-    delta[li] = s;
+    delta[li] = -s;
     delta[T * a.n_heads + li] = -lse[li] * kLog2e;
   }
 }
@@ -476,12 +510,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
   const int qt0 = (kt * BKEY) / BQ;
   const int iters = nqt - qt0;
 
+  uint32_t qoff[DmaPlan<D, 4>::PER], ooff[DmaPlan<D, 4>::PER];
+  dma_offsets<D, 4>(a.ld_qkv, wave, lane, qoff);
+  dma_offsets<D, 4>(ldo, wave, lane, ooff);
   auto load_tile = [&](int it, uint4* base) __attribute__((always_inline)) {
     const int q0 = (qt0 + it) * BQ;
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    dma_tile<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, ln);
-    dma_tile<D, 4>(dOg, ldo, q0, S, base + NAT, wave, ln);
+    dma_tile_at<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, qoff);
+    dma_tile_at<D, 4>(dOg, ldo, q0, S, base + NAT, wave, ooff);
     if (wave == 0) {
       const uint32_t off = q0 + lane < S ? (uint32_t)((q0 + lane) * 4) : kOOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Lg), (lds_ptr_t)(base + 2 * NAT), 4, off, 0, 0, 0);
@@ -490,26 +525,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
     }
   };
 
+  // per-lane offsets of the Q / dO fragments within a tile
+  uint32_t ro[D / 16], to[D / 32][2];
+  frag_offsets<D>(lane, ro, to);
   auto tile = [&](const uint4* base, int it) __attribute__((always_inline)) {
     const int q0 = (qt0 + it) * BQ;
     if (q0 + BQ - 1 < kw0) return;
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    const uint4* Qs = base;
-    const uint4* dOs = base + NAT;
     const float* L = reinterpret_cast<const float*>(base + 2 * NAT);
     const float* Dl = L + BQ;
     const bool tail = (q0 + BQ > S);
     // the two 32-query halves one after the other (a half's scores, dP and
     // fragments fit with four slices of reads in flight)
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    auto half = [&](auto QB) __attribute__((always_inline)) {
+      constexpr int qb = decltype(QB)::value;
+      constexpr int RQ = qb * 32 * D * 2;            // byte offset of row 32 qb
       f32x16_t sc, dp;
-      zero(sc);
       if (PASS) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i)   // dP - delta, formed by the MFMAs
-          dp[i] = -Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
+        for (int i = 0; i < 16; ++i)   // dP - delta (stored negated), formed by the MFMAs
+          dp[i] = Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
       }
       bf16x8_t fq[D / 16], fo[D / 16];
 #pragma unroll
@@ -517,21 +551,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
         if (kk % 4 == 0) {
 #pragma unroll
           for (int u = kk; u < kk + 4; ++u) {
-            fq[u] = row_frag<D>(Qs, qb * 32, u, ln);
-            if (PASS) fo[u] = row_frag<D>(dOs, qb * 32, u, ln);
+            fq[u] = row_at<RQ>(base, ro[u]);
+            if (PASS) fo[u] = row_at<NAT * 16 + RQ>(base, ro[u]);
           }
         }
-        sc = MFMA(fq[kk], kf[kk], sc);
+        sc = MFMA(fq[kk], kf[kk], kk == 0 ? f32x16_t{} : sc);
         if (PASS) dp = MFMA(fo[kk], vf[kk], dp);
       }
       // transposed fragments of the second product (dO^T for dV, Q^T for
       // dK), in flight under the elementwise part
+      constexpr int TT = PASS ? 0 : NAT * 16;         // Q tile or dO tile
       bf16x8_t ft[2][D / 32];
 #pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-          ft[ss][db] = tr_frag<D>(PASS ? Qs : dOs, qb * 32 + ss * 16, db, ln);
+      for (int db = 0; db < D / 32; ++db) {
+        ft[0][db] = tr_at<TT + RQ>(base, to[db]);
+        ft[1][db] = tr_at<TT + RQ + 16 * D * 2>(base, to[db]);
+      }
       // P = exp2(S c - LSE log2 e); on diagonal / tail tiles the masked
       // scores are set to -inf first, so exp2 gives 0
       if (q0 + qb * 32 < kw0 + 31 || tail) {
@@ -553,7 +588,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) acc[db] = MFMA(ft[ss][db], f, acc[db]);
       }
-    }
+    };
+    half(std::integral_constant<int, 0>());
+    half(std::integral_constant<int, 1>());
   };
   auto sync = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -658,31 +695,33 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   }
   const long li = ((long)b * a.n_heads + n) * S + q;
   const float nl2 = q < S ? delta[(long)a.batch * a.n_heads * S + li] : -INFINITY;
-  const float dl = q < S ? delta[li] : 0.0f;
+  const float ndl = q < S ? delta[li] : 0.0f;   // -rowsum(dO O)
   f32x16_t dqa[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) zero(dqa[db]);
   const float c = a.scale * kLog2e;
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
+  uint32_t doff[DmaPlan<D, 4>::PER];
+  dma_offsets<D, 4>(a.ld_qkv, wave, lane, doff);
   auto dma = [&](int kt, uint4* sm) __attribute__((always_inline)) {
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    dma_tile<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, ln);
-    dma_tile<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, ln);
+    dma_tile_at<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, doff);
+    dma_tile_at<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, doff);
   };
-  auto tile = [&](const uint4* Ks, const uint4* Vs, int kt) __attribute__((always_inline)) {
+  // per-lane offsets of the K / V fragments within a tile
+  uint32_t ro[KK], to[DB][2];
+  frag_offsets<D>(lane, ro, to);
+  auto tile = [&](const uint4* Ks, int kt) __attribute__((always_inline)) {
     const int k0 = kt * BKV;
     if (k0 > q0w + 31) return;
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
     // the two 32-key halves one after the other: scores, dP, dS and the dQ
     // products of a half need only that half's registers
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    auto half = [&](auto KB) __attribute__((always_inline)) {
+      constexpr int kb = decltype(KB)::value;
+      constexpr int RK = kb * 32 * D * 2;            // byte offset of row 32 kb
       f32x16_t sc, dp;
-      zero(sc);
-      zero(dp);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dp[i] = ndl;       // dP - delta, formed by the MFMAs
       // scores and dP: K and V fragments read four 16-deep slices at a time
       bf16x8_t fk[KK], fv[KK];
 #pragma unroll
@@ -690,19 +729,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
         if (kk % 4 == 0) {
 #pragma unroll
           for (int u = kk; u < kk + 4; ++u) {
-            fk[u] = row_frag<D>(Ks, kb * 32, u, ln);
-            fv[u] = row_frag<D>(Vs, kb * 32, u, ln);
+            fk[u] = row_at<RK>(Ks, ro[u]);
+            fv[u] = row_at<NAT * 16 + RK>(Ks, ro[u]);
           }
         }
-        sc = MFMA(fk[kk], qf[kk], sc);
+        sc = MFMA(fk[kk], qf[kk], kk == 0 ? f32x16_t{} : sc);
         dp = MFMA(fv[kk], of[kk], dp);
       }
       // K^T fragments for dQ^T = K^T dS^T: read before the elementwise part
       bf16x8_t ft[2][DB];
 #pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) ft[ss][db] = tr_frag<D>(Ks, kb * 32 + ss * 16, db, ln);
+      for (int db = 0; db < DB; ++db) {
+        ft[0][db] = tr_at<RK>(Ks, to[db]);
+        ft[1][db] = tr_at<RK + 16 * D * 2>(Ks, to[db]);
+      }
       // the causal mask (diagonal tiles only) as -inf scores: exp2 gives 0
       if (k0 + kb * 32 + 31 > q0w) {
 #pragma unroll
@@ -712,14 +752,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
         }
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) dp[i] = fast_exp2(__builtin_fmaf(sc[i], c, nl2)) * (dp[i] - dl);
+      for (int i = 0; i < 16; ++i) dp[i] = fast_exp2(__builtin_fmaf(sc[i], c, nl2)) * dp[i];
 #pragma unroll
       for (int ss = 0; ss < 2; ++ss) {
         const bf16x8_t df = pack_frag(dp, ss);
 #pragma unroll
         for (int db = 0; db < DB; ++db) dqa[db] = MFMA(ft[ss][db], df, dqa[db]);
       }
-    }
+    };
+    half(std::integral_constant<int, 0>());
+    half(std::integral_constant<int, 1>());
   };
   auto sync = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
@@ -731,11 +773,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   sync();
   for (int kt = 0; kt < nkt; kt += 2) {
     if (kt + 1 < nkt) dma(kt + 1, sm1);
-    tile(sm0, sm0 + NAT, kt);
+    tile(sm0, kt);
     sync();
     if (kt + 1 < nkt) {
       if (kt + 2 < nkt) dma(kt + 2, sm0);
-      tile(sm1, sm1 + NAT, kt + 1);
+      tile(sm1, kt + 1);
       sync();
     }
   }
