@@ -331,13 +331,13 @@ typedef struct {
  * forge_layer_bwd followed by forge_adamw_step on every weight of the layer
  * (grad = the matching member of `grads`, n = the weight's element count),
  * with the same results bit for bit (App. F: fused clip + AdamW + bf16
- * write-back). In a dense layer each weight's update is issued as soon as
- * its gradient is complete and the backward has read the weight for the
- * last time, on a stream of the library's own, so the memory-bound updates
- * of the FFN weights run while the compute-bound attention backward is in
- * flight (dense layers of fewer than 2^20 token x hidden elements, where
- * the stream hand-offs would cost more than they save, and MoE layers run
- * the updates in order on `stream`).
+ * write-back). Each weight's update is issued as soon as its gradient is
+ * complete and the backward has read the weight for the last time, on a
+ * stream of the library's own, so the memory-bound updates of the FFN (or
+ * expert and router) weights run while the compute-bound attention backward
+ * is in flight (layers of fewer than 2^20 token x hidden elements, where
+ * the stream hand-offs would cost more than they save, run the updates in
+ * order on `stream`).
  * opt: each used entry's param must be the same pointer as the matching
  *   member of w (the update overwrites the weight in place, after the
  *   backward's last read of it); master, m, v are updated in place.

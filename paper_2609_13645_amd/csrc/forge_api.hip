@@ -695,6 +695,25 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
   if (d.E > 0) {
     if (forge_status e = moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s))
       return e;
+    // the expert and router weights are final (and read for the last time):
+    // their updates overlap the rest of the backward, whose attention
+    // weight gradients go to the side stream as in a dense layer
+    SideLane* side = nullptr;
+    if (use_side_streams(d)) FORGE_HIP(side_lane(&side));
+    std::unique_lock<std::mutex> lk;
+    if (side) lk = std::unique_lock<std::mutex>(side->mu);
+    if (opt) {
+      opt->lane = side;
+      FORGE_HIP(opt_update(opt, s, s, opt->o->w_down_e, g->d_w_down_e, d.E * d.h * d.fe));
+      FORGE_HIP(opt_update(opt, s, s, opt->o->w_gate_up_e, g->d_w_gate_up_e,
+                           d.E * 2 * d.fe * d.h));
+      FORGE_HIP(opt_update(opt, s, s, opt->o->w_router, g->d_w_router, d.E * d.h));
+    }
+    FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
+    FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
+    if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
+    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
+                          side, opt);
   } else {
     const uint16_t* gu = at<uint16_t>(saved, sv.gu);
     const uint16_t* act = at<uint16_t>(saved, sv.act);
@@ -731,9 +750,6 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
                           side, opt);
   }
-  FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
-  FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
-  return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s);
 }
 
 // Per-weight optimizer state of the layer's weights: each used entry's
@@ -800,28 +816,10 @@ forge_status forge_layer_bwd_adamw(const forge_layer_cfg* cfg, const forge_layer
   if (forge_status e = check_optim(*cfg, w, opt)) return e;
   if (forge_status e = check_hparams(hp)) return e;
   FORGE_PTR(dev_scalars);
-  hipStream_t s = (hipStream_t)stream;
-  const Dims d = dims(*cfg);
-  if (d.E == 0) {
-    OptPlan plan{opt, hp, dev_scalars, nullptr, 5};
-    if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace, s, &plan))
-      return e;
-    return ok();
-  }
-  // MoE layer: the backward, then every update in order on the caller's stream
-  if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace, s, nullptr))
+  OptPlan plan{opt, hp, dev_scalars, nullptr, 5};
+  if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace,
+                                 (hipStream_t)stream, &plan))
     return e;
-  auto upd = [&](const forge_adamw_tensor& t, const float* grad, long n) {
-    return forge::adamw(t.master, reinterpret_cast<uint16_t*>(t.param), grad, t.m, t.v, n,
-                        hp->beta1, hp->beta2, hp->eps, hp->weight_decay, dev_scalars, s);
-  };
-  FORGE_HIP(upd(opt->attn_norm, g->d_attn_norm, d.h));
-  FORGE_HIP(upd(opt->w_qkv, g->d_w_qkv, d.qkv * d.h));
-  FORGE_HIP(upd(opt->w_o, g->d_w_o, d.h * d.hq));
-  FORGE_HIP(upd(opt->ffn_norm, g->d_ffn_norm, d.h));
-  FORGE_HIP(upd(opt->w_router, g->d_w_router, d.E * d.h));
-  FORGE_HIP(upd(opt->w_gate_up_e, g->d_w_gate_up_e, d.E * 2 * d.fe * d.h));
-  FORGE_HIP(upd(opt->w_down_e, g->d_w_down_e, d.E * d.h * d.fe));
   return ok();
 }
 

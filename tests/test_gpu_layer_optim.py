@@ -2,8 +2,9 @@
 forge_adamw_step. Both run the same kernels per element, so every parameter,
 master weight, moment, gradient and the input gradient must agree bit for
 bit, over consecutive steps (the second step's forward reads the updated
-weights). Dense layers issue each update on the library's optimizer stream
-while the backward continues; MoE layers update after the backward.
+weights). Layers from 2^20 token x hidden elements issue each update on the
+library's optimizer stream while the backward continues; smaller ones
+update in order.
 """
 import numpy as np
 import pytest
@@ -18,6 +19,10 @@ CASES = {
     "dense_8b_geometry": lambda: fi.config("llama8b_layer", seq=512, seed=23),
     "moe": lambda: fi.config("tiny", batch=1, seq=1024, ffn=0, n_experts=16, top_k=2,
                              expert_ffn=64, aux_coef=0.05, seed=61),
+    # 512 x 2048 token x hidden elements: the expert updates overlap the
+    # attention backward on the library's streams
+    "moe_overlapped": lambda: fi.config("moe_layer", batch=1, seq=512, n_experts=16, top_k=2,
+                                        expert_ffn=256, seed=67),
 }
 
 
