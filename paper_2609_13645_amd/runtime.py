@@ -222,6 +222,10 @@ class Model:
                                     cfg["weight_decay"])
         self.step_count = 0
         self.dev_step = torch.zeros(1, dtype=torch.int32, device=device)
+        # global gradient norm for clipping, summed on the device
+        self.norm_sq = torch.zeros(1, dtype=torch.float32, device=device)
+        self.norm_ws = torch.empty(_lib.GRAD_NORM_WORKSPACE_FLOATS, dtype=torch.float32,
+                                   device=device)
 
     def w_lm(self, buf):
         return self.flat.view(buf, "embedding" if self.tied else "w_lm")
@@ -254,22 +258,31 @@ class Model:
                              T, h, V, s)
         return self.loss
 
-    def optimizer_step(self, lr=None, clip=1.0):
+    def optimizer_step(self, lr=None, clip=1.0, max_norm=None):
         """One fused AdamW over all parameters. The step count and bias
-        corrections advance on the device (no host write: capturable)."""
+        corrections advance on the device (no host write: capturable).
+        Gradients are scaled by `clip`, or, with `max_norm`, by
+        min(1, max_norm / (||g|| + 1e-6)) over the whole flat gradient,
+        computed on the device (App. F: norm, clip coefficient and step
+        scalars never visit the host)."""
         self.step_count += 1
         c = self.cfg
         lr = c["lr"] if lr is None else lr
-        self.scalars[3:4].fill_(clip)
+        f = self.flat
+        if max_norm is None:
+            self.scalars[3:4].fill_(clip)
+        else:
+            self.norm_sq.zero_()
+            _lib.forge_grad_norm_sq(f.grad, f.n, self.norm_sq, self.norm_ws, self.stream)
+            _lib.forge_clip_coeff(self.norm_sq, max_norm, 1e-6, self.scalars, self.stream)
         _lib.forge_adamw_advance(self.scalars, self.dev_step, lr, c["beta1"], c["beta2"],
                                  self.stream)
-        f = self.flat
         _lib.forge_adamw_step(f.master, f.param, f.grad, f.m, f.v, f.n, self.hp,
                               self.scalars, self.stream)
 
-    def train_step(self):
+    def train_step(self, max_norm=None):
         loss = self.forward_backward(accumulate=False)
-        self.optimizer_step()
+        self.optimizer_step(max_norm=max_norm)
         return loss
 
 

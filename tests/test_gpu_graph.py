@@ -104,34 +104,44 @@ def test_layer_step_graph_replays_match_eager():
             assert torch.equal(a[k], b[k]), (rep, k)
 
 
-def test_model_step_graph_replays_match_eager():
-    """Tiny model (embedding, layer, LM head + CE, flat AdamW); its embedding
-    backward uses fp32 atomics, so the comparison has a tolerance."""
+@pytest.mark.parametrize("max_norm", [None, 1e-3])
+def test_model_step_graph_replays_match_eager(max_norm):
+    """Tiny model (embedding, layer, LM head + CE, flat AdamW), with the clip
+    coefficient fixed at 1 or from the gradient norm on the device; its
+    embedding backward uses fp32 atomics, so the comparison has a
+    tolerance."""
     import torch
     from paper_2609_13645_amd import runtime
     cfg = fi.config("tiny")
-    banner("graph replay of a model step")
+    banner(f"graph replay of a model step (max_norm {max_norm})")
     inp = fi.model_inputs(cfg)
     s_eager, s_graph = torch.cuda.Stream(), torch.cuda.Stream()
     with torch.cuda.stream(s_eager):
         eager = runtime.Model(cfg, inp, stream=s_eager)
     with torch.cuda.stream(s_graph):
         graphed = runtime.Model(cfg, inp, stream=s_graph)
-        graphed.train_step()
+        graphed.train_step(max_norm)
     with torch.cuda.stream(s_eager):
-        eager.train_step()
+        eager.train_step(max_norm)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s_graph):
-        graphed.train_step()
+        graphed.train_step(max_norm)
     torch.cuda.synchronize()
     for rep in range(3):
         with torch.cuda.stream(s_graph):
             g.replay()
         with torch.cuda.stream(s_eager):
-            eager.train_step()
+            eager.train_step(max_norm)
         torch.cuda.synchronize()
         _eager_noise()
+        if max_norm is not None:
+            # the coefficient both paths used: min(1, max_norm / (||g|| + eps))
+            for m in (eager, graphed):
+                norm = float(torch.linalg.vector_norm(m.flat.grad.double()))
+                want = min(1.0, max_norm / (norm + 1e-6))
+                assert want < 1.0
+                assert abs(float(m.scalars[3]) - want) <= 1e-5 * want, rep
         assert int(eager.dev_step.item()) == int(graphed.dev_step.item()) == rep + 2
         assert torch.allclose(graphed.loss, eager.loss, rtol=1e-5, atol=0), rep
         for buf in ("master", "m", "v"):
