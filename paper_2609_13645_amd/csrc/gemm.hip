@@ -376,7 +376,14 @@ struct RingPart {
   static_assert(PER * 64 * NW == ROWS * 4, "stage tile must split over the waves");
 };
 
-__device__ __forceinline__ int kc4(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+// K-contiguous stage: 64-byte rows (four 16-byte chunks), two rows per 128-byte
+// bank window. A ds_read_b128 serves eight lanes per cycle, here eight
+// consecutive rows at one logical chunk: XOR-ing the chunk with (row / 2) % 4
+// puts the four rows of each parity on four different slots, so the eight
+// reads cover the window once (keying on row / 4 left two rows per slot, a
+// two-way conflict on every fragment read).
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 3; }
+__device__ __forceinline__ int kc4(int row, int c) { return row * 4 + (c ^ kc_swz(row)); }
 
 __device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 2) ^ (((k >> 3) & 1) << 1); }
 
@@ -398,7 +405,7 @@ __device__ __forceinline__ void ring_dma(int i, const bf16_t* __restrict__ src, 
   if (LAYOUT == kKC) {
     const __amdgpu_buffer_rsrc_t r = rsrc(src + (long)row0 * ld + k0);
     const int row = blk * 16 + (lane >> 2);
-    const int c = (lane & 3) ^ ((row >> 2) & 3);
+    const int c = (lane & 3) ^ kc_swz(row);
     const bool ok = (row0 + row < rows_lim) && (k0 + c * 8 < K);
     const uint32_t off = ok ? (uint32_t)(((long)row * ld + c * 8) * 2) : kOOB;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(part + blk * 64), 16, off, 0, 0, 0);
