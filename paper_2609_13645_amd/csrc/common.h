@@ -55,6 +55,24 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
 }
 
 // Wave-wide (64 lanes) butterfly reductions.
+// One AdamW element (App. F, fused clip + Adam + cast), shared by the
+// standalone update and the GEMM's fused weight-gradient epilogue so that
+// both give the same bits:
+//   g *= clip; m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2;
+//   p -= lr ((m/bc1) / (sqrt(v/bc2) + eps) + wd p); param = bf16(p).
+__device__ __forceinline__ void adam1(float& p, float& m, float& v, float g, float b1,
+                                      float b2, float eps, float wd, float lr, float ibc1,
+                                      float ibc2, float clip) {
+  // explicit fused multiply-adds and no other contraction: the kernels that
+  // inline this get the same roundings whatever their surroundings
+#pragma clang fp contract(off)
+  g *= clip;
+  m = __builtin_fmaf(b1, m, (1.0f - b1) * g);
+  v = __builtin_fmaf(b2, v, ((1.0f - b2) * g) * g);
+  const float upd = __builtin_fmaf(wd, p, (m * ibc1) / (sqrtf(v * ibc2) + eps));
+  p = __builtin_fmaf(-lr, upd, p);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -373,18 +373,8 @@ __global__ __launch_bounds__(1024) void mean_reduce_k(const float* __restrict__ 
 }
 
 // --------------------------------------------------------------- AdamW ----
-// Per element (App. F, fused clip + Adam + cast):
-//   g *= clip; m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2;
-//   p -= lr ((m/bc1) / (sqrt(v/bc2) + eps) + wd p); param = bf16(p).
-__device__ __forceinline__ void adam1(float& p, float& m, float& v, float g, float b1,
-                                      float b2, float eps, float wd, float lr, float ibc1,
-                                      float ibc2, float clip) {
-  g *= clip;
-  m = b1 * m + (1.0f - b1) * g;
-  v = b2 * v + (1.0f - b2) * g * g;
-  const float upd = (m * ibc1) / (sqrtf(v * ibc2) + eps) + wd * p;
-  p = p - lr * upd;
-}
+// adam1 (the per-element update, App. F) lives in common.h: the fused
+// weight-gradient epilogue of the GEMM applies the same arithmetic.
 
 // One float4 of parameters per thread and no grid-stride loop: with seven
 // streams (read g, p, m, v; write p, m, v and bf16 p) this keeps the most

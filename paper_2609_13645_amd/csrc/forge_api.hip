@@ -407,6 +407,31 @@ hipError_t opt_update(OptPlan* P, hipStream_t s, hipStream_t ws, const forge_ada
                       os);
 }
 
+// A weight gradient with the weight's AdamW update in the GEMM epilogue
+// (App. F, vertical integration): each tile's gradient is final when the
+// tile ends, so the tile updates the same elements of master, m, v and the
+// bf16 parameter, exactly as forge_adamw_step would, without another pass
+// over the gradient. The weight's data-gradient product must already have
+// read the parameter. Used for the MoE expert weights: as a separate pass
+// their update (most of an MoE layer's parameters) cannot overlap the rest
+// of the backward without holding its kernels off the CUs.
+GemmArgs with_adam(GemmArgs a, const OptPlan* P, const forge_adamw_tensor& t) {
+  a.o_master = t.master;
+  a.o_m = t.m;
+  a.o_v = t.v;
+  a.o_param = reinterpret_cast<uint16_t*>(t.param);
+  a.o_sc = P->scalars;
+  a.o_b1 = P->hp->beta1;
+  a.o_b2 = P->hp->beta2;
+  a.o_eps = P->hp->eps;
+  a.o_wd = P->hp->weight_decay;
+  return a;
+}
+
+forge::GemmEpilogue wgrad_adam_epi(const forge_layer_grads* g) {
+  return g->overwrite ? forge::kStoreF32Adam : forge::kAccF32Adam;
+}
+
 // the optimizer stream's work happens before what is enqueued on s next
 hipError_t opt_join(OptPlan* P, hipStream_t s) {
   if (!P->lane) return hipSuccess;
@@ -506,7 +531,7 @@ forge_status moe_ffn_fwd(const forge_layer_cfg& c, const Dims& d, const forge_la
 forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_layer_weights* w,
                          const forge_layer_grads* g, const void* saved, const Saved& sv,
                          void* workspace, const Work& wk, const uint16_t* d_out, uint16_t* db,
-                         hipStream_t s) {
+                         hipStream_t s, const OptPlan* opt = nullptr) {
   const uint16_t* bn = at<uint16_t>(saved, sv.b);
   const float* probs = at<float>(saved, sv.probs);
   const int32_t* idx = at<int32_t>(saved, sv.idx);
@@ -532,19 +557,21 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
       forge::kMC, forge::kStoreBF16,
       grouped(gargs(dys, d.h, w->w_down_e, d.fe, dact, d.fe, d.R, d.fe, d.h), offsets, E,
               d.h * d.fe, 0), s));
-  FORGE_HIP(forge::gemm_grouped_k(
-      wgrad_epi(g),
-      grouped(gargs(dys, d.h, act, d.fe, g->d_w_down_e, d.fe, d.h, d.fe, 0), offsets, E, 0,
-              d.h * d.fe), s));
+  // (with updates: in the epilogue, after the data gradient read the weights)
+  const GemmArgs wd = grouped(gargs(dys, d.h, act, d.fe, g->d_w_down_e, d.fe, d.h, d.fe, 0),
+                              offsets, E, 0, d.h * d.fe);
+  FORGE_HIP(opt ? forge::gemm_grouped_k(wgrad_adam_epi(g), with_adam(wd, opt, opt->o->w_down_e), s)
+                : forge::gemm_grouped_k(wgrad_epi(g), wd, s));
   FORGE_HIP(forge::swiglu_bwd(gu, dact, dgu, (int)d.R, (int)d.fe, s));
   FORGE_HIP(forge::gemm_grouped_m(
       forge::kMC, forge::kStoreBF16,
       grouped(gargs(dgu, 2 * d.fe, w->w_gate_up_e, d.h, dxs, d.h, d.R, d.h, 2 * d.fe), offsets,
               E, 2 * d.fe * d.h, 0), s));
-  FORGE_HIP(forge::gemm_grouped_k(
-      wgrad_epi(g),
-      grouped(gargs(dgu, 2 * d.fe, xs, d.h, g->d_w_gate_up_e, d.h, 2 * d.fe, d.h, 0), offsets,
-              E, 0, 2 * d.fe * d.h), s));
+  const GemmArgs wgu = grouped(gargs(dgu, 2 * d.fe, xs, d.h, g->d_w_gate_up_e, d.h, 2 * d.fe,
+                                     d.h, 0), offsets, E, 0, 2 * d.fe * d.h);
+  FORGE_HIP(opt ? forge::gemm_grouped_k(wgrad_adam_epi(g),
+                                        with_adam(wgu, opt, opt->o->w_gate_up_e), s)
+                : forge::gemm_grouped_k(wgrad_epi(g), wgu, s));
   FORGE_HIP(forge::moe_scatter_back(dxs, pos_of, d.T, (int)d.h, k, dbs, s));
   // router: dl through the softmax (gates and aux loss), then its two products
   FORGE_HIP(forge::moe_router_bwd(probs, idx, dgate, counts, T, E, k, c.aux_coef, dl, s));
@@ -693,20 +720,19 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
 
   // FFN branch: gradient at b, then RMSNorm backward plus the residual path
   if (d.E > 0) {
-    if (forge_status e = moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s))
+    // expert weights: updated in their gradient products' epilogues
+    if (forge_status e =
+            moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s, opt))
       return e;
-    // the expert and router weights are final (and read for the last time):
-    // their updates overlap the rest of the backward, whose attention
-    // weight gradients go to the side stream as in a dense layer
+    // the router weight is final: its update overlaps the rest of the
+    // backward, whose attention weight gradients go to the side stream as
+    // in a dense layer
     SideLane* side = nullptr;
     if (use_side_streams(d)) FORGE_HIP(side_lane(&side));
     std::unique_lock<std::mutex> lk;
     if (side) lk = std::unique_lock<std::mutex>(side->mu);
     if (opt) {
       opt->lane = side;
-      FORGE_HIP(opt_update(opt, s, s, opt->o->w_down_e, g->d_w_down_e, d.E * d.h * d.fe));
-      FORGE_HIP(opt_update(opt, s, s, opt->o->w_gate_up_e, g->d_w_gate_up_e,
-                           d.E * 2 * d.fe * d.h));
       FORGE_HIP(opt_update(opt, s, s, opt->o->w_router, g->d_w_router, d.E * d.h));
     }
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
@@ -740,8 +766,10 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
                           gargs(dgu, 2 * d.f, bn, d.h, g->d_w_gate_up, d.h, 2 * d.f, d.h, d.T), ws));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(dgu, 2 * d.f, w->w_gate_up, d.h, db, d.h, d.T, d.h, 2 * d.f), s));
-    // the updates start once the gate/up data gradient is done: its one
-    // round of long tiles is the kernel most hurt by losing CUs to them
+    // separate updates (dense weights): they start once the gate/up data
+    // gradient is done, beside the attention backward; updating in the
+    // weight-gradient epilogue instead would order each weight-gradient
+    // product after its data gradient and measured slower here
     if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_down, g->d_w_down, d.h * d.f));
     if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_gate_up, g->d_w_gate_up, 2 * d.f * d.h));
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));

@@ -267,6 +267,13 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn) {
     p.A += r0 * p.lda;  // both operands M/N-contiguous: group rows are k rows
     p.B += r0 * p.ldb;
     p.C = (char*)p.C + (long)e * p.strideC * 4;
+    if (EPI == kStoreF32Adam || EPI == kAccF32Adam) {
+      const long off = (long)e * p.strideC;
+      p.o_master += off;
+      p.o_m += off;
+      p.o_v += off;
+      p.o_param += off;
+    }
   }
   return true;
 }
@@ -499,6 +506,64 @@ __device__ __forceinline__ void store8_bf16(const GemmArgs& p, int m, int n, flo
 // bf16 output: lanes l and l ^ 16 swap halves of two neighbouring blocks so
 // that each lane holds eight consecutive n, and a row takes 64 contiguous
 // bytes per store instruction.
+// AdamW epilogue of C[m][n..n+3] (kStoreF32Adam / kAccF32Adam): the weight
+// gradient g (acc, or C + acc, rounded as the plain fp32 epilogues round it)
+// is stored to C, then the same elements of the optimizer state are updated
+// exactly as the standalone AdamW kernel does (adam1; sc = lr, 1 / bc1,
+// 1 / bc2, clip). Every stream is touched once: nontemporal accesses.
+struct AdamPiece {
+  f32x4_t g, w, m1, m2;
+};
+
+template <int EPI>
+__device__ __forceinline__ void adam_load(const GemmArgs& p, int m, int n, const float* v,
+                                          AdamPiece& a) {
+  a.g = f32x4_t{v[0], v[1], v[2], v[3]};
+  if (m >= p.M || n + 3 >= p.N) return;  // ragged pieces: adam_store, element by element
+  const long i = (long)m * p.ldc + n;
+  if (EPI == kAccF32Adam)
+    a.g += __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>((float*)p.C + i));
+  a.w = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p.o_master + i));
+  a.m1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p.o_m + i));
+  a.m2 = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p.o_v + i));
+}
+
+template <int EPI>
+__device__ __forceinline__ void adam_store(const GemmArgs& p, const float* sc, int m, int n,
+                                           AdamPiece& a) {
+  if (m >= p.M) return;
+  const long i = (long)m * p.ldc + n;
+  float* C = reinterpret_cast<float*>(p.C) + i;
+  if (n + 3 < p.N) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float we = a.w[e], me = a.m1[e], ve = a.m2[e];
+      adam1(we, me, ve, a.g[e], p.o_b1, p.o_b2, p.o_eps, p.o_wd, sc[0], sc[1], sc[2], sc[3]);
+      a.w[e] = we;
+      a.m1[e] = me;
+      a.m2[e] = ve;
+    }
+    __builtin_nontemporal_store(a.g, reinterpret_cast<f32x4_t*>(C));
+    __builtin_nontemporal_store(a.w, reinterpret_cast<f32x4_t*>(p.o_master + i));
+    __builtin_nontemporal_store(a.m1, reinterpret_cast<f32x4_t*>(p.o_m + i));
+    __builtin_nontemporal_store(a.m2, reinterpret_cast<f32x4_t*>(p.o_v + i));
+    const u32x2_t pb = {pack2(a.w[0], a.w[1]), pack2(a.w[2], a.w[3])};
+    __builtin_nontemporal_store(pb, reinterpret_cast<u32x2_t*>(p.o_param + i));
+  } else {
+    for (int e = 0; e < 4; ++e)
+      if (n + e < p.N) {
+        const float g = (EPI == kAccF32Adam ? C[e] : 0.0f) + a.g[e];
+        C[e] = g;
+        float we = p.o_master[i + e], me = p.o_m[i + e], ve = p.o_v[i + e];
+        adam1(we, me, ve, g, p.o_b1, p.o_b2, p.o_eps, p.o_wd, sc[0], sc[1], sc[2], sc[3]);
+        p.o_master[i + e] = we;
+        p.o_m[i + e] = me;
+        p.o_v[i + e] = ve;
+        p.o_param[i + e] = f2bf(we);
+      }
+  }
+}
+
 template <int EPI, int FN, int FM>
 __device__ __forceinline__ void store_tile16(const GemmArgs& p, const f32x4_t (&acc)[FN][FM],
                                              int mw, int nw, int lane) {
@@ -532,6 +597,62 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& p, const f32x4_t (&
         const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
         store4<EPI>(p, m, n, v);
       }
+  }
+}
+
+// AdamW epilogue of a whole tile (kStoreF32Adam / kAccF32Adam), through LDS:
+// the tile goes to the stage ring (free after the loop) as fp32, half of its
+// rows at a time, and comes back row by row, so that each wave streams whole
+// tile rows (1 KB per instruction for 256 columns) through the update's
+// streams (C, master, m and v in; those and the bf16 parameter out) instead
+// of 64-byte pieces of 16 rows, with the loads of U rows issued together.
+// Chunks are XOR-swizzled by row so that the column writes of 16 rows and
+// the row reads are both free of bank conflicts.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, int FN, int FM>
+__device__ __forceinline__ void adam_tile(const GemmArgs& p, const f32x4_t (&acc)[FN][FM],
+                                          float* lds, int m0, int n0, int wm, int wn, int wave,
+                                          int lane) {
+  constexpr int NW = WAVES_M * WAVES_N, WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int HR = BM / 2;            // rows per half
+  constexpr int CPR = BN / 4;           // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;         // rows per wave instruction
+  constexpr int IT = HR / (NW * RPI);   // row groups per wave and half
+  constexpr int U = IT >= 4 ? 4 : IT;   // row groups loaded together
+  static_assert(CPR <= 64 && 64 % CPR == 0 && CPR >= 16, "row must split over a wave");
+  static_assert(IT * NW * RPI == HR && IT % U == 0, "half tile must split over the waves");
+  static_assert(HR % WM == 0, "a wave's rows lie in one half");
+  const float sc[4] = {p.o_sc[0], 1.0f / p.o_sc[1], 1.0f / p.o_sc[2], p.o_sc[3]};
+  const int c = lane % CPR;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    __syncthreads();  // the ring (or the previous half) is no longer read
+    if ((wm * WM) / HR == h) {
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+          const int ml = wm * WM + j * 16 + (lane & 15) - h * HR;
+          const int cw = (wn * WN + i * 16 + (lane >> 4) * 4) / 4;
+          *reinterpret_cast<f32x4_t*>(lds + ml * BN + ((cw ^ (ml & 15)) * 4)) = acc[i][j];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it0 = 0; it0 < IT; it0 += U) {
+      AdamPiece a[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (wave + (it0 + u) * NW) * RPI + lane / CPR;
+        const f32x4_t g = *reinterpret_cast<const f32x4_t*>(lds + r * BN + ((c ^ (r & 15)) * 4));
+        const float v[4] = {g[0], g[1], g[2], g[3]};
+        adam_load<EPI>(p, m0 + h * HR + r, n0 + c * 4, v, a[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (wave + (it0 + u) * NW) * RPI + lane / CPR;
+        adam_store<EPI>(p, sc, m0 + h * HR + r, n0 + c * 4, a[u]);
+      }
+    }
   }
 }
 
@@ -649,7 +770,13 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs
   // the last (unused) fragments are reused and before the workgroup exits
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   ring_fence<FN, FM>(fa[0], fb[0]);
-  store_tile16<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
+  if constexpr (EPI == kStoreF32Adam || EPI == kAccF32Adam) {
+    static_assert(BM / 2 * BN <= 4 * SLOT * 4, "half a tile must fit the stage ring");
+    adam_tile<BM, BN, WAVES_M, WAVES_N, EPI, FN, FM>(p, acc, reinterpret_cast<float*>(lds), m0,
+                                                      n0, wm, wn, wave, lane);
+  } else {
+    store_tile16<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
+  }
 }
 
 // Operands contiguous along M / N and full 256 x 256 tiles run on the ring
@@ -750,6 +877,8 @@ hipError_t gemm_grouped_k(GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
   if (epi == kAccF32) return launch_grouped_k<256, 256, 4, 2, kAccF32>(a, s);
   if (epi == kStoreF32) return launch_grouped_k<256, 256, 4, 2, kStoreF32>(a, s);
+  if (epi == kAccF32Adam) return launch_grouped_k<256, 256, 4, 2, kAccF32Adam>(a, s);
+  if (epi == kStoreF32Adam) return launch_grouped_k<256, 256, 4, 2, kStoreF32Adam>(a, s);
   return hipErrorInvalidValue;
 }
 
@@ -795,6 +924,7 @@ hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& 
       case kResidBF16: return dispatch_tiles<kKC, kKC, kResidBF16>(a, s);
       case kAccF32: return dispatch_tiles<kKC, kKC, kAccF32>(a, s);
       case kStoreF32: return dispatch_tiles<kKC, kKC, kStoreF32>(a, s);
+      default: break;
     }
   } else if (la == kKC && lb == kMC) {
     switch (epi) {

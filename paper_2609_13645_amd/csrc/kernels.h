@@ -17,6 +17,12 @@ enum GemmEpilogue {
   kResidBF16 = 1,     // C bf16 = acc + R (bf16), one rounding
   kAccF32 = 2,        // C fp32 += acc
   kStoreF32 = 3,      // C fp32 = acc
+  // weight gradient and its AdamW update in one epilogue (per-group weight
+  // gradients, gemm_grouped_k): g = acc (kStoreF32Adam) or C + acc
+  // (kAccF32Adam) is stored to C and then applied to the optimizer state at
+  // the same position
+  kStoreF32Adam = 4,
+  kAccF32Adam = 5,
 };
 
 struct GemmArgs {
@@ -31,6 +37,15 @@ struct GemmArgs {
   const int* g_off = nullptr;
   int groups = 0;
   long strideB = 0, strideC = 0;
+  // AdamW epilogues: fp32 master, moments m and v and the bf16 parameter,
+  // laid out like C (leading dimension ldc; grouped: strideC apart), device
+  // step scalars {lr, 1 - b1^t, 1 - b2^t, clip} and the hyper-parameters
+  float* o_master = nullptr;
+  float* o_m = nullptr;
+  float* o_v = nullptr;
+  uint16_t* o_param = nullptr;
+  const float* o_sc = nullptr;
+  float o_b1 = 0.0f, o_b2 = 0.0f, o_eps = 0.0f, o_wd = 0.0f;
 };
 
 // Host-side shape rules (checked by the caller): K-contiguous operands need

@@ -2,9 +2,11 @@
 forge_adamw_step. Both run the same kernels per element, so every parameter,
 master weight, moment, gradient and the input gradient must agree bit for
 bit, over consecutive steps (the second step's forward reads the updated
-weights). Layers from 2^20 token x hidden elements issue each update on the
-library's optimizer stream while the backward continues; smaller ones
-update in order.
+weights). The weight matrices are updated in the epilogues of their gradient products
+(the standalone update's arithmetic per element); layers from 2^20 token x
+hidden elements run those products on the library's side stream and the
+small updates on its optimizer stream while the backward continues; smaller
+layers run everything in order.
 """
 import numpy as np
 import pytest
@@ -26,7 +28,7 @@ CASES = {
 }
 
 
-def run(cfg, inp, fused, steps=2):
+def run(cfg, inp, fused, steps=2, overwrite=True):
     import torch
     from paper_2609_13645_amd import _lib, runtime
     flat = runtime.FlatParams(runtime.layer_shapes(cfg))
@@ -47,9 +49,9 @@ def run(cfg, inp, fused, steps=2):
             layer.aux.zero_()
         layer.fwd(x, out)
         if fused:
-            layer.bwd_adamw(x, dy, dx, flat, hp, scal, overwrite=True)
+            layer.bwd_adamw(x, dy, dx, flat, hp, scal, overwrite=overwrite)
         else:
-            layer.bwd(x, dy, dx, overwrite=True)
+            layer.bwd(x, dy, dx, overwrite=overwrite)
             _lib.forge_adamw_step(flat.master, flat.param, flat.grad, flat.m, flat.v, flat.n,
                                   hp, scal)
     torch.cuda.synchronize()
@@ -60,14 +62,17 @@ def run(cfg, inp, fused, steps=2):
     return res
 
 
+@pytest.mark.parametrize("overwrite", [True, False])
 @pytest.mark.parametrize("case", list(CASES))
-def test_layer_bwd_adamw_equals_bwd_then_adamw(case):
+def test_layer_bwd_adamw_equals_bwd_then_adamw(case, overwrite):
+    """overwrite=False: the gradients accumulate over the two steps (and the
+    fused epilogues update from the accumulated gradient)."""
     import torch
     cfg = CASES[case]()
-    banner(f"layer bwd+adamw fused vs sequential ({case})")
+    banner(f"layer bwd+adamw fused vs sequential ({case}, overwrite={overwrite})")
     inp = fi.layer_inputs(cfg)
-    want = run(cfg, inp, fused=False)
-    got = run(cfg, inp, fused=True)
+    want = run(cfg, inp, fused=False, overwrite=overwrite)
+    got = run(cfg, inp, fused=True, overwrite=overwrite)
     for k, v in want.items():
         assert torch.equal(got[k], v), k
     # the updates moved the weights
