@@ -531,7 +531,7 @@ forge_status moe_ffn_fwd(const forge_layer_cfg& c, const Dims& d, const forge_la
 forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_layer_weights* w,
                          const forge_layer_grads* g, const void* saved, const Saved& sv,
                          void* workspace, const Work& wk, const uint16_t* d_out, uint16_t* db,
-                         hipStream_t s, const OptPlan* opt = nullptr) {
+                         hipStream_t s, SideLane* side = nullptr, const OptPlan* opt = nullptr) {
   const uint16_t* bn = at<uint16_t>(saved, sv.b);
   const float* probs = at<float>(saved, sv.probs);
   const int32_t* idx = at<int32_t>(saved, sv.idx);
@@ -557,11 +557,15 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
       forge::kMC, forge::kStoreBF16,
       grouped(gargs(dys, d.h, w->w_down_e, d.fe, dact, d.fe, d.R, d.fe, d.h), offsets, E,
               d.h * d.fe, 0), s));
-  // (with updates: in the epilogue, after the data gradient read the weights)
+  // the expert weight gradients (with updates: in their epilogues, after
+  // the data gradient read the weights) go to the side stream when there is
+  // one: their operands stay untouched for the rest of the call
+  hipStream_t ws = side ? side->stream : s;
+  if (side) FORGE_HIP(link(s, ws, side->ev[0]));
   const GemmArgs wd = grouped(gargs(dys, d.h, act, d.fe, g->d_w_down_e, d.fe, d.h, d.fe, 0),
                               offsets, E, 0, d.h * d.fe);
-  FORGE_HIP(opt ? forge::gemm_grouped_k(wgrad_adam_epi(g), with_adam(wd, opt, opt->o->w_down_e), s)
-                : forge::gemm_grouped_k(wgrad_epi(g), wd, s));
+  FORGE_HIP(opt ? forge::gemm_grouped_k(wgrad_adam_epi(g), with_adam(wd, opt, opt->o->w_down_e), ws)
+                : forge::gemm_grouped_k(wgrad_epi(g), wd, ws));
   FORGE_HIP(forge::swiglu_bwd(gu, dact, dgu, (int)d.R, (int)d.fe, s));
   FORGE_HIP(forge::gemm_grouped_m(
       forge::kMC, forge::kStoreBF16,
@@ -569,9 +573,10 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
               E, 2 * d.fe * d.h, 0), s));
   const GemmArgs wgu = grouped(gargs(dgu, 2 * d.fe, xs, d.h, g->d_w_gate_up_e, d.h, 2 * d.fe,
                                      d.h, 0), offsets, E, 0, 2 * d.fe * d.h);
+  if (side) FORGE_HIP(link(s, ws, side->ev[1]));
   FORGE_HIP(opt ? forge::gemm_grouped_k(wgrad_adam_epi(g),
-                                        with_adam(wgu, opt, opt->o->w_gate_up_e), s)
-                : forge::gemm_grouped_k(wgrad_epi(g), wgu, s));
+                                        with_adam(wgu, opt, opt->o->w_gate_up_e), ws)
+                : forge::gemm_grouped_k(wgrad_epi(g), wgu, ws));
   FORGE_HIP(forge::moe_scatter_back(dxs, pos_of, d.T, (int)d.h, k, dbs, s));
   // router: dl through the softmax (gates and aux loss), then its two products
   FORGE_HIP(forge::moe_router_bwd(probs, idx, dgate, counts, T, E, k, c.aux_coef, dl, s));
@@ -720,21 +725,19 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
 
   // FFN branch: gradient at b, then RMSNorm backward plus the residual path
   if (d.E > 0) {
-    // expert weights: updated in their gradient products' epilogues
-    if (forge_status e =
-            moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s, opt))
-      return e;
-    // the router weight is final: its update overlaps the rest of the
-    // backward, whose attention weight gradients go to the side stream as
-    // in a dense layer
+    // expert weight gradients on the side stream (updated in their
+    // epilogues), beside the rest of the backward, whose attention weight
+    // gradients go there too as in a dense layer
     SideLane* side = nullptr;
     if (use_side_streams(d)) FORGE_HIP(side_lane(&side));
     std::unique_lock<std::mutex> lk;
     if (side) lk = std::unique_lock<std::mutex>(side->mu);
-    if (opt) {
-      opt->lane = side;
-      FORGE_HIP(opt_update(opt, s, s, opt->o->w_router, g->d_w_router, d.E * d.h));
-    }
+    if (opt) opt->lane = side;
+    if (forge_status e =
+            moe_ffn_bwd(*cfg, d, w, g, saved, sv, workspace, wk, d_out, db, s, side, opt))
+      return e;
+    // the router weight is final: its update overlaps the rest
+    if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->w_router, g->d_w_router, d.E * d.h));
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
     FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
     if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
