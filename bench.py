@@ -11,8 +11,10 @@ one call (forge_layer_bwd_adamw): each weight's update starts once its
 gradient is final, overlapping the rest of the backward; the clip
 coefficient is 1 (no clipping), as in every step here. Other workloads (--workload): the same layer at seq 16384
 with attention recomputed in the backward, the 64-expert top-8 MoE layer,
-the 16-layer tied-head model (embedding, layers, LM head + cross-entropy)
-and the tiny one-layer model.
+the 16-layer tied-head model (embedding, layers, LM head + cross-entropy;
+each layer's weights updated inside its backward, the embedding and final
+norm after the embedding backward) and the tiny one-layer model (one AdamW
+over all parameters after the backward).
 
 Prints one JSON line: model TFLOP/s (App. C count of the fwd+bwd; the
 optimizer adds time but no model FLOPs), MFU against the MI355X dense bf16
@@ -104,6 +106,7 @@ class Step:
             inp = fi.model_inputs(cfg)
             self.model = runtime.Model(cfg, inp, stream=stream)
             self.flat = self.model.flat
+            self.overlapped = runtime.uses_side_streams(cfg)
         else:
             inp = fi.layer_inputs(cfg)
             self.flat = runtime.FlatParams(runtime.layer_shapes(cfg))
@@ -157,11 +160,15 @@ class Step:
 
     def __call__(self):
         self.zero()
-        self.fwd()
-        if is_model(self.cfg):
-            self.bwd()
+        if is_model(self.cfg) and self.overlapped:
+            # each layer's update inside its backward, overlapping the
+            # backward of the layers below; head and embedding updates last
+            self.model.train_step_overlapped()
+        elif is_model(self.cfg):
+            self.fwd()
             self.adamw()
         else:
+            self.fwd()
             self.bwd_adamw()
 
     def finite(self):

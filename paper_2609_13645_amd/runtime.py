@@ -197,9 +197,10 @@ class Model:
         self.flat.load_bits("final_norm", inputs["final_norm"])
         if not self.tied:
             self.flat.load_bits("w_lm", inputs["w_lm"])
-        self.layers = []
+        self.layers, self.layer_flats = [], []
         for i in range(L):
             view = _PrefixedFlat(self.flat, f"{i}.")
+            self.layer_flats.append(view)
             self.layers.append(Layer(cfg, inputs["layers"][i], device, stream, flat=view))
         ws = max(_lib.forge_layer_workspace_bytes(self.layers[0].c), 1)
         self.workspace = empty_bytes(ws, device)
@@ -230,11 +231,10 @@ class Model:
     def w_lm(self, buf):
         return self.flat.view(buf, "embedding" if self.tied else "w_lm")
 
-    def forward_backward(self, accumulate=True):
-        """Cross-entropy loss (device scalar) and every gradient accumulated
-        into flat.grad; for MoE layers self.aux holds the summed aux losses.
-        With accumulate=False the gradients are this step's alone: the layers
-        write theirs and only the head / embedding gradients are zeroed."""
+    def _forward_and_head(self, accumulate):
+        """Embedding, layers, then the loss head's forward and backward: the
+        loss, the head gradients and the gradient at the last layer's output
+        (self.grad_a)."""
         c, s = self.cfg, self.stream
         if not accumulate:
             self.flat.grad[:self.head_grad_elems].zero_()
@@ -250,12 +250,45 @@ class Model:
                                 self.w_lm(self.flat.param), self.targets, self.loss,
                                 self.grad_a, self.flat.view(self.flat.grad, "final_norm"),
                                 self.w_lm(self.flat.grad), self.head_ws, s)
+
+    def forward_backward(self, accumulate=True):
+        """Cross-entropy loss (device scalar) and every gradient accumulated
+        into flat.grad; for MoE layers self.aux holds the summed aux losses.
+        With accumulate=False the gradients are this step's alone: the layers
+        write theirs and only the head / embedding gradients are zeroed."""
+        c, s = self.cfg, self.stream
+        self._forward_and_head(accumulate)
         g_in, g_out = self.grad_a, self.grad_b
         for i in reversed(range(len(self.layers))):
             self.layers[i].bwd(self.acts[i], g_in, g_out, overwrite=not accumulate)
             g_in, g_out = g_out, g_in
         _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
-                             T, h, V, s)
+                             self.T, c["hidden"], c["vocab"], s)
+        return self.loss
+
+    def train_step_overlapped(self, lr=None, clip=1.0):
+        """The step of train_step() with each layer's AdamW update issued
+        inside its backward (forge_layer_bwd_adamw), where it overlaps the
+        backward of the layers below; the embedding / LM-head and final-norm
+        updates follow the embedding backward. The clip coefficient must be
+        known before the backward (no norm clipping here). Gives the same
+        bits as train_step() for every layer weight."""
+        c, s = self.cfg, self.stream
+        lr = c["lr"] if lr is None else lr
+        self.step_count += 1
+        self._forward_and_head(accumulate=False)
+        self.scalars[3:4].fill_(clip)
+        _lib.forge_adamw_advance(self.scalars, self.dev_step, lr, c["beta1"], c["beta2"], s)
+        g_in, g_out = self.grad_a, self.grad_b
+        for i in reversed(range(len(self.layers))):
+            self.layers[i].bwd_adamw(self.acts[i], g_in, g_out, self.layer_flats[i], self.hp,
+                                     self.scalars, overwrite=True)
+            g_in, g_out = g_out, g_in
+        _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
+                             self.T, c["hidden"], c["vocab"], s)
+        f, n = self.flat, self.head_grad_elems
+        _lib.forge_adamw_step(f.master[:n], f.param[:n], f.grad[:n], f.m[:n], f.v[:n], n,
+                              self.hp, self.scalars, s)
         return self.loss
 
     def optimizer_step(self, lr=None, clip=1.0, max_norm=None):
@@ -286,12 +319,21 @@ class Model:
         return loss
 
 
+def uses_side_streams(cfg: dict) -> bool:
+    """Whether libforge runs a layer's weight gradients and updates on its
+    own streams: from 2^20 token x hidden elements (below, the event
+    hand-offs cost more than the overlap gains, and one AdamW launch over
+    all parameters beats one per weight)."""
+    return cfg["batch"] * cfg["seq"] * cfg["hidden"] >= (1 << 20)
+
+
 class _PrefixedFlat:
     """View of a FlatParams under a name prefix (one layer's tensors)."""
 
     def __init__(self, flat: FlatParams, prefix: str):
         self._f, self._p = flat, prefix
         self.param, self.grad = flat.param, flat.grad
+        self.master, self.m, self.v = flat.master, flat.m, flat.v
 
     def view(self, buf, name):
         return self._f.view(buf, self._p + name)
