@@ -51,6 +51,8 @@ DESCRIPTION = {
     "tiny": "tiny decoder layer + untied LM head + CE + AdamW (B1 S128 h256)",
     "llama8b_layer": "Llama-8B-shape decoder layer fwd+bwd+AdamW (B1 S4096 h4096)",
     "dense1b": "16-layer dense model, tied LM head + CE + AdamW (B4 S2048 h2048 V32000)",
+    "dense1b_streaming_ce": "the 16-layer dense model with the streaming CE head (2048-token "
+                            "chunks: 2048 x 32000 logits at a time)",
     "llama8b_layer_16k": "Llama-8B-shape layer at S16384, attention recomputed in bwd",
     "moe_layer": "MoE decoder layer, 64 experts top-8, fe 1408 (B2 S4096 h2048)",
 }

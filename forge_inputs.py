@@ -56,6 +56,11 @@ CONFIGS = {
     "dense1b": _cfg(batch=4, seq=2048, hidden=2048, n_heads=32, n_kv_heads=8,
                     head_dim=64, ffn=8192, vocab=32000, n_layers=16, tied=True,
                     seed=3),
+    # the same model with the streaming cross-entropy head (2048 x 32000
+    # logits at a time instead of 8192 x 32000)
+    "dense1b_streaming_ce": _cfg(batch=4, seq=2048, hidden=2048, n_heads=32, n_kv_heads=8,
+                                 head_dim=64, ffn=8192, vocab=32000, n_layers=16, tied=True,
+                                 ce_chunk=2048, seed=3),
     # long-context 8B-shape layer with attention recompute in bwd
     "llama8b_layer_16k": _cfg(seq=16384, hidden=4096, n_heads=32, n_kv_heads=8,
                               head_dim=128, ffn=14336, rope_base=500000.0,

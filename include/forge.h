@@ -239,6 +239,29 @@ forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L
                                 forge_bf16* d_x_L, float* d_final_norm, float* d_w_lm,
                                 void* workspace, forge_stream stream);
 
+/* Scratch bytes for forge_loss_fwd_bwd_chunked: as forge_loss_workspace_bytes
+ * with min(chunk, T) rows of logits instead of T. chunk >= 1. */
+forge_status forge_loss_chunked_workspace_bytes(const forge_head_cfg* cfg, int32_t chunk,
+                                                size_t* bytes);
+
+/*
+ * forge_loss_fwd_bwd over token chunks of `chunk` rows (the chunked / streaming
+ * cross-entropy of App. G): per chunk, its logits, their cross-entropy
+ * forward and backward in place, the chunk's rows of the input gradient and
+ * its share of d_w_lm; only chunk x V logits exist at a time. Same arguments,
+ * ownership and accumulation rules as forge_loss_fwd_bwd (the loss is still
+ * the mean over all T tokens); d_w_lm gains the chunks' shares one after
+ * another, so its fp32 sums are ordered by chunk (equal to the unchunked
+ * result up to fp32 rounding). Costs one fp32 read-modify-write of d_w_lm
+ * per chunk. chunk >= 1; chunk >= T is the unchunked head.
+ */
+forge_status forge_loss_fwd_bwd_chunked(const forge_head_cfg* cfg, int32_t chunk,
+                                        const forge_bf16* x_L, const forge_bf16* final_norm,
+                                        const forge_bf16* w_lm, const int32_t* targets,
+                                        float* loss_out, forge_bf16* d_x_L,
+                                        float* d_final_norm, float* d_w_lm, void* workspace,
+                                        forge_stream stream);
+
 /* ------------------------------------------------------------------------ */
 /* Embedding                                                                */
 /* ------------------------------------------------------------------------ */

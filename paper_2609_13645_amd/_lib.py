@@ -110,6 +110,10 @@ def load():
                                            ctypes.POINTER(LayerWeights), P, P, P, P,
                                            ctypes.POINTER(LayerGrads), P, P]),
         "forge_loss_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(HeadCfg), SZ]),
+        "forge_loss_chunked_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(HeadCfg), I32,
+                                                               SZ]),
+        "forge_loss_fwd_bwd_chunked": (ctypes.c_int, [ctypes.POINTER(HeadCfg), I32, P, P, P, P,
+                                                      P, P, P, P, P, P]),
         "forge_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(HeadCfg), P, P, P, P, P, P,
                                               P, P, P, P]),
         "forge_embed_fwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
@@ -255,6 +259,21 @@ def forge_loss_fwd_bwd(cfg, x_L, final_norm, w_lm, targets, loss_out, d_x_L, d_f
                                      _ptr(w_lm), _ptr(targets), _ptr(loss_out), _ptr(d_x_L),
                                      _ptr(d_final_norm), _ptr(d_w_lm), _ptr(workspace),
                                      _stream(stream)))
+
+
+def forge_loss_chunked_workspace_bytes(cfg: HeadCfg, chunk: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_loss_chunked_workspace_bytes(ctypes.byref(cfg), int(chunk),
+                                                     ctypes.byref(n)))
+    return n.value
+
+
+def forge_loss_fwd_bwd_chunked(cfg, chunk, x_L, final_norm, w_lm, targets, loss_out, d_x_L,
+                               d_final_norm, d_w_lm, workspace, stream=None):
+    _check(load().forge_loss_fwd_bwd_chunked(ctypes.byref(cfg), int(chunk), _ptr(x_L),
+                                             _ptr(final_norm), _ptr(w_lm), _ptr(targets),
+                                             _ptr(loss_out), _ptr(d_x_L), _ptr(d_final_norm),
+                                             _ptr(d_w_lm), _ptr(workspace), _stream(stream)))
 
 
 def forge_embed_fwd(ids, emb, x0, tokens, hidden, vocab, stream=None):

@@ -915,14 +915,15 @@ forge_status check_head(const forge_head_cfg* c) {
               "tokens * vocab exceeds 2^31");
   return FORGE_OK;
 }
-HeadWork head_layout(const forge_head_cfg& c) {
+// zrows: rows of logits held at once (T, or the chunk of the streaming head)
+HeadWork head_layout(const forge_head_cfg& c, long zrows) {
   HeadWork w;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += up(bytes); return o; };
   const long T = c.tokens, h = c.hidden, V = c.vocab;
   w.xn = take(T * h * 2);
   w.rstd = take(T * 4);
-  w.z = take(T * V * 2);
+  w.z = take(zrows * V * 2);
   w.row_loss = take(T * 4);
   w.dxn = take(T * h * 2);
   w.dg = take((size_t)forge::rmsnorm_bwd_blocks((int)T) * h * 4);
@@ -934,15 +935,29 @@ HeadWork head_layout(const forge_head_cfg& c) {
 forge_status forge_loss_workspace_bytes(const forge_head_cfg* cfg, size_t* bytes) {
   if (forge_status s = check_head(cfg)) return s;
   FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
-  *bytes = head_layout(*cfg).total;
+  *bytes = head_layout(*cfg, cfg->tokens).total;
   return ok();
 }
 
-forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L,
-                                const forge_bf16* final_norm, const forge_bf16* w_lm,
-                                const int32_t* targets, float* loss_out, forge_bf16* d_x_L,
-                                float* d_final_norm, float* d_w_lm, void* workspace,
-                                forge_stream stream) {
+forge_status forge_loss_chunked_workspace_bytes(const forge_head_cfg* cfg, int32_t chunk,
+                                                size_t* bytes) {
+  if (forge_status s = check_head(cfg)) return s;
+  FORGE_CHECK(chunk >= 1, FORGE_ERR_INVALID_ARG, "chunk must be >= 1");
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = head_layout(*cfg, std::min<long>(chunk, std::max(cfg->tokens, 1))).total;
+  return ok();
+}
+
+namespace {
+// The head over token chunks of `chunk` rows: per chunk the logits, the
+// cross-entropy forward and backward in place, the input gradient rows and
+// the chunk's share of dW_lm (fp32, accumulated); a chunk of T is the plain
+// head.
+forge_status loss_impl(const forge_head_cfg* cfg, long chunk, const forge_bf16* x_L,
+                       const forge_bf16* final_norm, const forge_bf16* w_lm,
+                       const int32_t* targets, float* loss_out, forge_bf16* d_x_L,
+                       float* d_final_norm, float* d_w_lm, void* workspace,
+                       forge_stream stream) {
   if (forge_status s = check_head(cfg)) return s;
   FORGE_PTR(x_L);
   FORGE_PTR(final_norm);
@@ -954,7 +969,8 @@ forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L
   FORGE_PTR(d_w_lm);
   FORGE_PTR(workspace);
   const long T = cfg->tokens, h = cfg->hidden, V = cfg->vocab;
-  const HeadWork hw = head_layout(*cfg);
+  chunk = std::min(chunk, std::max(T, 1L));
+  const HeadWork hw = head_layout(*cfg, chunk);
   hipStream_t s = (hipStream_t)stream;
   uint16_t* xn = at<uint16_t>(workspace, hw.xn);
   float* rstd = at<float>(workspace, hw.rstd);
@@ -965,17 +981,44 @@ forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L
   const int nblk = forge::rmsnorm_bwd_blocks((int)T);
 
   FORGE_HIP(forge::rmsnorm_fwd(x_L, final_norm, xn, rstd, (int)T, (int)h, cfg->rms_eps, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
-                        gargs(xn, h, w_lm, h, z, V, T, V, h), s));
-  FORGE_HIP(forge::ce_fwd_bwd(z, targets, rl, (int)T, (int)V, (float)(1.0 / (double)T), s));
+  for (long t0 = 0; t0 < T; t0 += chunk) {
+    const long n = std::min(chunk, T - t0);
+    const uint16_t* xc = xn + t0 * h;
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                          gargs(xc, h, w_lm, h, z, V, n, V, h), s));
+    FORGE_HIP(forge::ce_fwd_bwd(z, targets + t0, rl + t0, (int)n, (int)V,
+                                (float)(1.0 / (double)T), s));
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                          gargs(z, V, w_lm, h, dxn + t0 * h, h, n, h, V), s));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
+                          gargs(z, V, xc, h, d_w_lm, h, V, h, n), s));
+  }
   FORGE_HIP(forge::mean_reduce(rl, (int)T, (float)(1.0 / (double)T), loss_out, s));
-  FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(z, V, w_lm, h, dxn, h, T, h, V), s));
-  FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
-                        gargs(z, V, xn, h, d_w_lm, h, V, h, T), s));
   FORGE_HIP(forge::rmsnorm_bwd(x_L, final_norm, rstd, dxn, nullptr, d_x_L, dgp, (int)T, (int)h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, d_final_norm, (int)h, true, s));
   return ok();
+}
+}  // namespace
+
+forge_status forge_loss_fwd_bwd(const forge_head_cfg* cfg, const forge_bf16* x_L,
+                                const forge_bf16* final_norm, const forge_bf16* w_lm,
+                                const int32_t* targets, float* loss_out, forge_bf16* d_x_L,
+                                float* d_final_norm, float* d_w_lm, void* workspace,
+                                forge_stream stream) {
+  FORGE_CHECK(cfg != nullptr, FORGE_ERR_INVALID_ARG, "cfg is NULL");
+  return loss_impl(cfg, cfg->tokens, x_L, final_norm, w_lm, targets, loss_out, d_x_L,
+                   d_final_norm, d_w_lm, workspace, stream);
+}
+
+forge_status forge_loss_fwd_bwd_chunked(const forge_head_cfg* cfg, int32_t chunk,
+                                        const forge_bf16* x_L, const forge_bf16* final_norm,
+                                        const forge_bf16* w_lm, const int32_t* targets,
+                                        float* loss_out, forge_bf16* d_x_L,
+                                        float* d_final_norm, float* d_w_lm, void* workspace,
+                                        forge_stream stream) {
+  FORGE_CHECK(chunk >= 1, FORGE_ERR_INVALID_ARG, "chunk must be >= 1");
+  return loss_impl(cfg, chunk, x_L, final_norm, w_lm, targets, loss_out, d_x_L, d_final_norm,
+                   d_w_lm, workspace, stream);
 }
 
 // ---- embedding --------------------------------------------------------------

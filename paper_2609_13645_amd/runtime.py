@@ -207,7 +207,11 @@ class Model:
         for ly in self.layers:               # one shared scratch buffer
             ly.workspace = self.workspace
         self.head = _lib.HeadCfg(self.T, h, V, cfg["rms_eps"])
-        self.head_ws = empty_bytes(_lib.forge_loss_workspace_bytes(self.head), device)
+        # ce_chunk: the streaming head (chunk x V logits at a time), else T x V
+        self.ce_chunk = int(cfg.get("ce_chunk", 0))
+        self.head_ws = empty_bytes(
+            _lib.forge_loss_chunked_workspace_bytes(self.head, self.ce_chunk) if self.ce_chunk
+            else _lib.forge_loss_workspace_bytes(self.head), device)
         self.ids = torch.from_numpy(inputs["ids"].astype(np.int32)).to(device)
         self.targets = torch.from_numpy(inputs["targets"].astype(np.int32)).to(device)
         self.acts = [torch.empty((self.T, h), dtype=torch.bfloat16, device=device)
@@ -245,11 +249,14 @@ class Model:
             self.aux.zero_()
         for i, ly in enumerate(self.layers):
             ly.fwd(self.acts[i], self.acts[i + 1], aux=self.aux)
-        _lib.forge_loss_fwd_bwd(self.head, self.acts[-1],
-                                self.flat.view(self.flat.param, "final_norm"),
-                                self.w_lm(self.flat.param), self.targets, self.loss,
-                                self.grad_a, self.flat.view(self.flat.grad, "final_norm"),
-                                self.w_lm(self.flat.grad), self.head_ws, s)
+        head_args = (self.acts[-1], self.flat.view(self.flat.param, "final_norm"),
+                     self.w_lm(self.flat.param), self.targets, self.loss, self.grad_a,
+                     self.flat.view(self.flat.grad, "final_norm"), self.w_lm(self.flat.grad),
+                     self.head_ws, s)
+        if self.ce_chunk:
+            _lib.forge_loss_fwd_bwd_chunked(self.head, self.ce_chunk, *head_args)
+        else:
+            _lib.forge_loss_fwd_bwd(self.head, *head_args)
 
     def forward_backward(self, accumulate=True):
         """Cross-entropy loss (device scalar) and every gradient accumulated

@@ -38,6 +38,13 @@ def test_size_queries_are_consistent():
     assert _lib.forge_layer_workspace_bytes(rec) > _lib.forge_layer_workspace_bytes(rec_nokeep)
     hc = _lib.HeadCfg(8192, 2048, 32000, 1e-5)
     assert _lib.forge_loss_workspace_bytes(hc) >= 8192 * 32000 * 2
+    # the streaming head holds chunk x V logits; chunk >= T is the plain head
+    plain = _lib.forge_loss_workspace_bytes(hc)
+    assert _lib.forge_loss_chunked_workspace_bytes(hc, 2048) <= plain - 6144 * 32000 * 2
+    assert _lib.forge_loss_chunked_workspace_bytes(hc, 8192) == plain
+    assert _lib.forge_loss_chunked_workspace_bytes(hc, 1 << 30) == plain
+    with pytest.raises(_lib.ForgeError):
+        _lib.forge_loss_chunked_workspace_bytes(hc, 0)
 
 
 @pytest.mark.parametrize("change,status", [

@@ -9,7 +9,7 @@ from gpu_util import rel_fro, dev_bf16, host_f64, banner
 pytestmark = pytest.mark.gpu
 
 
-def run_head(T, h, V, seed):
+def run_head(T, h, V, seed, chunk=0):
     import torch
     from paper_2609_13645_amd import _lib
     rng = np.random.default_rng(seed)
@@ -18,13 +18,19 @@ def run_head(T, h, V, seed):
     wb = fi.to_bf16_bits(0.02 * rng.standard_normal((V, h), dtype=np.float32))
     tg = rng.integers(0, V, size=T, dtype=np.int32)
     cfg = _lib.HeadCfg(T, h, V, 1e-5)
-    ws = torch.empty(_lib.forge_loss_workspace_bytes(cfg), dtype=torch.uint8, device="cuda")
+    nws = (_lib.forge_loss_chunked_workspace_bytes(cfg, chunk) if chunk
+           else _lib.forge_loss_workspace_bytes(cfg))
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
     loss = torch.full((1,), float("nan"), dtype=torch.float32, device="cuda")
     dx = torch.empty((T, h), dtype=torch.bfloat16, device="cuda")
     dg = torch.full((h,), 0.25, dtype=torch.float32, device="cuda")
     dw = torch.full((V, h), -0.125, dtype=torch.float32, device="cuda")
-    _lib.forge_loss_fwd_bwd(cfg, dev_bf16(xb), dev_bf16(gb), dev_bf16(wb),
-                            torch.from_numpy(tg).cuda(), loss, dx, dg, dw, ws)
+    args = (dev_bf16(xb), dev_bf16(gb), dev_bf16(wb), torch.from_numpy(tg).cuda(), loss, dx,
+            dg, dw, ws)
+    if chunk:
+        _lib.forge_loss_fwd_bwd_chunked(cfg, chunk, *args)
+    else:
+        _lib.forge_loss_fwd_bwd(cfg, *args)
     torch.cuda.synchronize()
     r_loss, r_dx, r_dg, r_dw = ohead.head_fwd_bwd(
         fi.bf16_bits_to_f64(xb), fi.bf16_bits_to_f64(gb), fi.bf16_bits_to_f64(wb), tg, 1e-5)
@@ -42,6 +48,27 @@ def test_head_parity(T, h, V):
     banner(f"  loss {gl:.6f} vs {rl:.6f}; errors {errs}")
     assert errs["dx"] <= 2e-2
     assert errs["dg"] <= 3e-2 and errs["dw"] <= 3e-2
+
+
+@pytest.mark.parametrize("T,h,V,chunk", [(200, 64, 1032, 48), (128, 256, 1024, 1),
+                                         (64, 2048, 32000, 24), (96, 128, 1024, 4096)])
+def test_streaming_head_parity(T, h, V, chunk):
+    """Chunked head (a ragged last chunk, one-row chunks, a chunk above T)
+    against the oracle, and against the unchunked head: the same loss and
+    input gradient up to the logits GEMM's tile choice, d_w_lm summed in
+    chunk order."""
+    banner(f"streaming head T={T} h={h} V={V} chunk={chunk}")
+    r = run_head(T, h, V, seed=T + V, chunk=chunk)
+    p = run_head(T, h, V, seed=T + V)
+    gl, rl = r["loss"]
+    assert abs(gl - rl) / abs(rl) <= 2e-3
+    errs = {k: rel_fro(*r[k]) for k in ("dx", "dg", "dw")}
+    banner(f"  loss {gl:.6f} vs {rl:.6f}; errors {errs}")
+    assert errs["dx"] <= 2e-2
+    assert errs["dg"] <= 3e-2 and errs["dw"] <= 3e-2
+    assert abs(gl - p["loss"][0]) <= 1e-5 * abs(gl)
+    for k in ("dx", "dg", "dw"):
+        assert rel_fro(r[k][0], p[k][0]) <= 1e-2, k
 
 
 def test_uniform_logits_loss_is_log_vocab_on_gpu():
