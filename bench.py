@@ -488,7 +488,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build runs the training step on one "
+        print("bench.py measures one GPU: the library runs the training step on one "
               "MI355X and has no multi-GPU path (--gpus must be 1).", file=sys.stderr)
         sys.exit(2)
     cfg = fi.config(args.workload)

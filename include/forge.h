@@ -55,7 +55,7 @@ typedef void* forge_stream;
 typedef enum {
   FORGE_OK = 0,
   FORGE_ERR_INVALID_ARG = 1,   /* null pointer, bad size, aliasing          */
-  FORGE_ERR_UNSUPPORTED = 2,   /* valid request this build does not handle  */
+  FORGE_ERR_UNSUPPORTED = 2,   /* valid request the library does not handle */
   FORGE_ERR_ALIGNMENT = 3,     /* base pointer not 16-byte aligned          */
   FORGE_ERR_HIP = 4            /* a HIP runtime call or launch failed       */
 } forge_status;
