@@ -113,6 +113,21 @@ def test_gemm_large_tiles_ragged_n_integer_exact(la, lb, epi):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("la,lb,epi", [(KC, KC, STORE_BF16), (KC, KC, RESID_BF16),
+                                       (KC, KC, STORE_F32), (KC, MC, STORE_BF16)])
+def test_gemm_single_round_long_k_integer_exact(la, lb, epi):
+    """One round of 256 x 256 tiles over a long reduction (the shape of the
+    down projection and the gate/up data gradient): ragged M and N edges
+    (M % 256 == 160, N % 16 == 8) and a ragged reduction (K % 32 == 8), exact
+    in fp32."""
+    M, N, K = 4000, 4008, 8200
+    banner(f"gemm int single round long K la={la} lb={lb} epi={epi}")
+    got, ref = run_gemm(la, lb, epi, M, N, K, seed=epi + 17)
+    want = (fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
+            if epi in (STORE_BF16, RESID_BF16) else ref)
+    assert np.array_equal(got, want)
+
+
 def test_gemm_zero_k_and_empty():
     banner("gemm K=0 / empty")
     got, ref = run_gemm(KC, KC, ACC_F32, 64, 64, 0)
