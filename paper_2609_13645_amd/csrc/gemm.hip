@@ -28,15 +28,20 @@
 //    descriptor's range check, so ragged edges need no branches.
 //  * A K-contiguous operand tile keeps 128-byte rows (eight 16-byte chunks,
 //    chunk c of row r at c ^ ((r ^ (r >> 3)) & 7)) in gemm_kernel and 64-byte
-//    rows (chunk c of row r at c ^ ((r >> 2) & 3)) in a ring stage; both keep
-//    each group of 16 lanes of a fragment read on distinct banks. Each MFMA
-//    operand is one 16-byte LDS read. An operand contiguous along M / N is
+//    rows (chunk c of row r at c ^ ((r >> 1) & 3)) in a ring stage; either
+//    way the eight lanes a 16-byte read serves per cycle cover a 128-byte
+//    bank window once (no bank conflicts). Each MFMA operand is one 16-byte
+//    LDS read. An operand contiguous along M / N is
 //    stored as it lies in HBM (chunks XOR-swizzled per k-row) and read with
 //    gfx950's ds_read_b64_tr_b16 transpose reads, so dgrad and wgrad need no
 //    transpose pass.
 //  * The MFMA computes D = Btile * Atile^T, i.e. C transposed, so each lane's
 //    four consecutive accumulator rows are four consecutive n of one row m of
-//    C: the epilogue writes 8-byte (bf16) or 16-byte (fp32) vectors.
+//    C: the epilogue writes 16-byte fp32 vectors, and in the ring kernel
+//    lanes l and l ^ 16 swap halves so that each writes eight consecutive
+//    bf16 (one 16-byte nontemporal store). The AdamW epilogues of the grouped
+//    weight gradients stage the fp32 tile through the free stage ring and
+//    stream it by rows through the optimizer state (adam_tile).
 //  * Workgroups are dispatched round-robin over the 8 XCDs; the tile order is
 //    remapped so each XCD works on a contiguous, M-grouped band of tiles and
 //    reuses operands in its own L2.
