@@ -478,7 +478,33 @@ def summarize_profile(db_path, out=sys.stdout):
               f"{max(d):.1f} | {sum(d) / 1e3:.3f} | {100 * sum(d) / total:.1f}% |", file=out)
 
 
+def summarize_counters(csv_paths, out=sys.stdout):
+    """Mean per dispatch of every counter, per kernel (libforge's GEMM and
+    attention kernels), from rocprofv3 --pmc counter_collection CSV files."""
+    import collections
+    import csv
+    import re
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    for path in csv_paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                m = re.search(r"((?:ring_kernel|gemm_kernel|attn_\w+)<[^()]*>|attn_\w+)",
+                              r["Kernel_Name"])
+                if m:
+                    agg[m.group(1)][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for cs in agg.values() for c in cs})
+    print("| kernel | " + " | ".join(names) + " |", file=out)
+    print("|---" * (len(names) + 1) + "|", file=out)
+    for k in sorted(agg):
+        vals = [agg[k].get(c) for c in names]
+        cells = [f"{sum(v) / len(v):.4g}" if v else "" for v in vals]
+        print(f"| `{k}` | " + " | ".join(cells) + " |", file=out)
+
+
 def main():
+    if len(sys.argv) >= 3 and sys.argv[1] == "--counters-summarize":
+        summarize_counters(sys.argv[2:])
+        return
     if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
         summarize_profile(sys.argv[2])
         return
