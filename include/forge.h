@@ -89,7 +89,7 @@ const char* forge_version(void);
  * expert id), each weighted by its softmax probability (no renormalisation);
  * the load-balance loss aux_coef * E * sum_e f_e P_e (f_e = share of routed
  * slots, a constant; P_e = mean router probability) is added to aux_loss.
- * MoE limits: n_experts a multiple of 8 and <= 64, 1 <= top_k <= min(E, 16),
+ * MoE limits: n_experts a multiple of 8 and <= 256, 1 <= top_k <= min(E, 16),
  * expert_ffn a multiple of 8.
  *
  * recompute_attn != 0: the forward does not keep the attention output and
@@ -161,6 +161,23 @@ forge_status forge_layer_saved_bytes(const forge_layer_cfg* cfg, size_t* bytes);
 /* Bytes of the scratch `workspace` of forge_layer_fwd / forge_layer_bwd.
  * Host only. The contents need not be preserved between calls. */
 forge_status forge_layer_workspace_bytes(const forge_layer_cfg* cfg, size_t* bytes);
+
+/* Items of a MoE layer's saved buffer that forge_layer_saved_item locates:
+ * the routing decision of the forward (App. B, routed experts with top-k
+ * selection), as the backward reads it. */
+#define FORGE_SAVED_ROUTE_IDX 0      /* int32 [T, top_k]: chosen experts, descending logit */
+#define FORGE_SAVED_ROUTE_GATES 1    /* fp32 [T, top_k]: their router probabilities */
+#define FORGE_SAVED_ROUTE_PROBS 2    /* fp32 [T, E]: router softmax over all experts */
+#define FORGE_SAVED_ROUTE_COUNTS 3   /* int32 [E]: routed (token, slot) entries per expert */
+#define FORGE_SAVED_ROUTE_OFFSETS 4  /* int32 [E + 1]: exclusive scan of the counts */
+#define FORGE_SAVED_ROUTE_PERM 5     /* int32 [T * top_k]: flat entries, expert-major order */
+
+/* Byte offset and size, within the `saved` buffer that forge_layer_fwd fills
+ * for this configuration, of one routing item above (valid after the
+ * forward has completed on its stream, unchanged by the backward). Host
+ * only. UNSUPPORTED for a dense layer; INVALID_ARG for an unknown item. */
+forge_status forge_layer_saved_item(const forge_layer_cfg* cfg, int32_t item, size_t* offset,
+                                    size_t* bytes);
 
 /*
  * RoPE tables: for position s < seq and pair index i < head_dim/2,
@@ -486,9 +503,11 @@ forge_status forge_moe_route_workspace_bytes(int32_t tokens, int32_t n_experts, 
 
 /*
  * Token routing of the MoE layer on given fp32 logits [tokens, n_experts]
- * (n_experts <= 64): probs [tokens, E] = softmax over all experts; idx
+ * (n_experts <= 256): probs [tokens, E] = softmax over all experts; idx
  * [tokens, top_k] = the top_k experts by descending logit, ties to the lower
- * expert id; gates [tokens, top_k] = their probabilities; counts [E] slots
+ * expert id, -0 equal to +0 and NaN ranked below -inf (so every index lies
+ * in [0, E) whatever the logits hold; a NaN logit makes that token's probs
+ * and gates NaN); gates [tokens, top_k] = their probabilities; counts [E] slots
  * per expert; offsets [E + 1] = exclusive scan of counts; perm [tokens *
  * top_k] = the flat (token * top_k + slot) entries in expert-major order,
  * tokens ascending within an expert, then slots ascending. Integer outputs

@@ -103,7 +103,36 @@ def attention_probs(q, k, scale):
     return e / l, (m + np.log(l))[:, 0]
 
 
-def attention_fwd(q, k, v, batch, seq):
+# Threads for the per-(batch row, kv head) loops of attention_fwd / _bwd. Each
+# task runs one kv head's query group in head order, exactly the serial
+# arithmetic, on slices no other task writes; more than one thread only
+# shortens the wall time on long sequences (NumPy releases the interpreter
+# lock inside its array operations).
+ATTENTION_WORKERS = 1
+# Optional callable(b, m), told when a kv head's group is done (for callers
+# that report progress on long sequences).
+ATTENTION_PROGRESS = None
+
+
+def _for_each_kv_head(batch, nkv, task, workers):
+    jobs = [(b, m) for b in range(batch) for m in range(nkv)]
+
+    def run(b, m):
+        task(b, m)
+        if ATTENTION_PROGRESS is not None:
+            ATTENTION_PROGRESS(b, m)
+
+    if workers <= 1:
+        for j in jobs:
+            run(*j)
+        return
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(workers) as ex:
+        for f in [ex.submit(run, *j) for j in jobs]:
+            f.result()
+
+
+def attention_fwd(q, k, v, batch, seq, workers=None):
     """o_i = sum_{j<=i} softmax_j(q_i.k_j / sqrt(d)) v_j per head.
 
     q [T, n_h, d], k/v [T, n_kv, d]. Returns o [T, n_h, d] and the row
@@ -115,16 +144,18 @@ def attention_fwd(q, k, v, batch, seq):
     scale = 1.0 / np.sqrt(d)
     o = np.zeros_like(q)
     lse = np.zeros((batch, nh, seq))
-    for b in range(batch):
+
+    def group(b, m):
         rows = slice(b * seq, (b + 1) * seq)
-        for n in range(nh):
-            m = n // grp
+        for n in range(m * grp, (m + 1) * grp):
             P, lse[b, n] = attention_probs(q[rows, n], k[rows, m], scale)
             o[rows, n] = P @ v[rows, m]
+
+    _for_each_kv_head(batch, nkv, group, ATTENTION_WORKERS if workers is None else workers)
     return o, lse
 
 
-def attention_bwd(q, k, v, do, batch, seq):
+def attention_bwd(q, k, v, do, batch, seq, workers=None):
     """Softmax-attention backward, per head, summed over each GQA group.
 
       dv_j = sum_i P_ij do_i
@@ -139,10 +170,10 @@ def attention_bwd(q, k, v, do, batch, seq):
     dq = np.zeros_like(q)
     dk = np.zeros_like(k)
     dv = np.zeros_like(v)
-    for b in range(batch):
+
+    def group(b, m):
         rows = slice(b * seq, (b + 1) * seq)
-        for n in range(nh):
-            m = n // grp
+        for n in range(m * grp, (m + 1) * grp):
             P, _ = attention_probs(q[rows, n], k[rows, m], scale)
             dO = do[rows, n]
             dv[rows, m] += P.T @ dO
@@ -150,6 +181,8 @@ def attention_bwd(q, k, v, do, batch, seq):
             ds = P * (dP - np.sum(P * dP, axis=1, keepdims=True))
             dq[rows, n] = scale * (ds @ k[rows, m])
             dk[rows, m] += scale * (ds.T @ q[rows, n])
+
+    _for_each_kv_head(batch, nkv, group, ATTENTION_WORKERS if workers is None else workers)
     return dq, dk, dv
 
 

@@ -50,15 +50,25 @@ def topk_margin(l32, k):
     return v[:, k - 1] - v[:, k]
 
 
-def route(l, k):
+def route(l, k, idx=None):
     """Routing decision for logits l [T, E].
 
     Returns idx [T, k] int32, gates [T, k], p [T, E], counts [E] int32,
     offsets [E + 1] int32 (exclusive scan of counts), perm [T k] int32.
+
+    With `idx` given, that choice of experts is taken instead of the top-k of
+    l (k distinct experts per token, in [0, E)): for a token whose k-th and
+    (k+1)-th logits lie within rounding of each other, either choice is a
+    correct top-k, and the caller may follow the one another implementation
+    made. Everything downstream (gates, counts, order) follows from it.
     """
     T, E = l.shape
-    l32 = np.asarray(l, dtype=np.float32)
-    idx = topk(l32, k)
+    if idx is None:
+        idx = topk(np.asarray(l, dtype=np.float32), k)
+    else:
+        idx = np.asarray(idx, dtype=np.int32)
+        assert idx.shape == (T, k) and idx.min() >= 0 and idx.max() < E
+        assert all(len(set(r)) == k for r in idx.tolist()), "experts repeat in a row"
     p = softmax(np.asarray(l, dtype=np.float64))
     gates = np.take_along_axis(p, idx, axis=1)
     counts = np.bincount(idx.reshape(-1), minlength=E).astype(np.int32)
@@ -86,16 +96,17 @@ def expert_ffn(xe, wgu, wd, fe):
     return A @ wd.T, (G, U, A)
 
 
-def moe_fwd(b, W, cfg):
+def moe_fwd(b, W, cfg, idx=None):
     """y_t = sum_{e in topk(t)} p_te * FFN_e(b_t); also returns the aux loss.
 
     Grouped form: rows gathered per expert in canonical order, one dense
-    product per expert, scattered back weighted by the gate.
+    product per expert, scattered back weighted by the gate. `idx` forces the
+    choice of experts (see route).
     """
     T, h = b.shape
     E, k, fe = cfg["n_experts"], cfg["top_k"], cfg["expert_ffn"]
     l = b @ W["w_router"].T
-    idx, gates, p, counts, offsets, perm = route(l, k)
+    idx, gates, p, counts, offsets, perm = route(l, k, idx)
     y = np.zeros_like(b)
     per_expert = []
     for e in range(E):
@@ -159,14 +170,14 @@ def moe_fwd_per_token(b, W, cfg):
     return y
 
 
-def layer_fwd(x, W, cfg):
+def layer_fwd(x, W, cfg, idx=None):
     """MoE decoder layer: attention block, then h1 + MoE(RMSNorm(h1)).
 
-    Returns (out, aux, cache).
+    Returns (out, aux, cache). `idx` forces the choice of experts (see route).
     """
     h1, ca = attention_block_fwd(x, W, cfg)
     bn, r2 = rmsnorm_fwd(h1, W["ffn_norm"], cfg["rms_eps"])
-    y, aux, cm = moe_fwd(bn, W, cfg)
+    y, aux, cm = moe_fwd(bn, W, cfg, idx)
     return h1 + y, aux, dict(attn=ca, moe=cm, h1=h1, r2=r2)
 
 

@@ -24,6 +24,10 @@ FORGE_ERR_ALIGNMENT = 3
 FORGE_ERR_HIP = 4
 GRAD_NORM_WORKSPACE_FLOATS = 1024
 
+# routing items of a MoE layer's saved buffer (forge_layer_saved_item)
+SAVED_ROUTE_IDX, SAVED_ROUTE_GATES, SAVED_ROUTE_PROBS = 0, 1, 2
+SAVED_ROUTE_COUNTS, SAVED_ROUTE_OFFSETS, SAVED_ROUTE_PERM = 3, 4, 5
+
 # GEMM operand layouts and epilogues (forge_gemm)
 GEMM_KC, GEMM_MC = 0, 1
 EPI_STORE_BF16, EPI_RESID_BF16, EPI_ACC_F32, EPI_STORE_F32 = 0, 1, 2, 3
@@ -103,6 +107,7 @@ def load():
         "forge_version": (ctypes.c_char_p, []),
         "forge_layer_saved_bytes": (ctypes.c_int, [ctypes.POINTER(LayerCfg), SZ]),
         "forge_layer_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(LayerCfg), SZ]),
+        "forge_layer_saved_item": (ctypes.c_int, [ctypes.POINTER(LayerCfg), I32, SZ, SZ]),
         "forge_rope_table": (ctypes.c_int, [I32, I32, F32, P, P, P]),
         "forge_layer_fwd": (ctypes.c_int, [ctypes.POINTER(LayerCfg),
                                            ctypes.POINTER(LayerWeights), P, P, P, P, P, P]),
@@ -227,6 +232,14 @@ def forge_layer_workspace_bytes(cfg: LayerCfg) -> int:
     n = ctypes.c_size_t()
     _check(load().forge_layer_workspace_bytes(ctypes.byref(cfg), ctypes.byref(n)))
     return n.value
+
+
+def forge_layer_saved_item(cfg: LayerCfg, item: int):
+    """(byte offset, bytes) of a routing item within a MoE layer's saved buffer."""
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().forge_layer_saved_item(ctypes.byref(cfg), int(item), ctypes.byref(off),
+                                         ctypes.byref(n)))
+    return off.value, n.value
 
 
 def forge_rope_table(seq, head_dim, base, cos_out, sin_out, stream=None):

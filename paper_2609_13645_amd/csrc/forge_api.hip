@@ -84,7 +84,7 @@ Dims dims(const forge_layer_cfg& c) {
   return d;
 }
 
-constexpr int kMaxExperts = 64;
+constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 16;
 
 forge_status check_cfg(const forge_layer_cfg* c) {
@@ -382,7 +382,7 @@ hipError_t link(hipStream_t from, hipStream_t to, hipEvent_t ev) {
 
 // Optimizer updates of forge_layer_bwd_adamw, issued on the lane's optimizer
 // stream behind everything enqueued so far on the caller's stream s and the
-// weight-gradient stream ws (events 5 onwards; 0..4 are the backward's); a
+// weight-gradient stream ws (events 6 onwards; 0..5 are the backward's); a
 // layer without a lane issues them in order on s.
 struct OptPlan {
   const forge_layer_optim* o;
@@ -446,7 +446,8 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                             const uint16_t* x, const uint16_t* a, const float* rstd1,
                             const uint16_t* qkv, const uint16_t* o, const float* lse,
                             const uint16_t* dh1, uint16_t* d_in, void* workspace, const Work& wk,
-                            hipStream_t s, SideLane* side = nullptr, OptPlan* opt = nullptr) {
+                            hipStream_t s, SideLane* side = nullptr, OptPlan* opt = nullptr,
+                            hipEvent_t before_d_in = nullptr) {
   uint16_t* dO = at<uint16_t>(workspace, wk.dO);
   float* delta = at<float>(workspace, wk.delta);
   uint16_t* dqkv = at<uint16_t>(workspace, wk.dqkv);
@@ -477,6 +478,9 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dqkv, d.qkv, w->w_qkv, d.h, da, d.h, d.T, d.h, d.qkv), s));
   if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_qkv, g->d_w_qkv, d.qkv * d.h));
+  // d_in may alias the layer's upstream gradient, which a side-stream
+  // product may still be reading: wait for that product first
+  if (before_d_in) FORGE_HIP(hipStreamWaitEvent(s, before_d_in, 0));
   FORGE_HIP(forge::rmsnorm_bwd(x, w->attn_norm, rstd1, da, dh1, d_in, dgp, (int)d.T, (int)d.h, s));
   FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_attn_norm, (int)d.h, !g->overwrite, s));
   if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->attn_norm, g->d_attn_norm, d.h));
@@ -622,6 +626,27 @@ forge_status forge_layer_workspace_bytes(const forge_layer_cfg* cfg, size_t* byt
   return ok();
 }
 
+forge_status forge_layer_saved_item(const forge_layer_cfg* cfg, int32_t item, size_t* offset,
+                                    size_t* bytes) {
+  if (forge_status s = check_cfg(cfg)) return s;
+  FORGE_CHECK(offset != nullptr && bytes != nullptr, FORGE_ERR_INVALID_ARG,
+              "offset or bytes is NULL");
+  FORGE_CHECK(cfg->n_experts > 0, FORGE_ERR_UNSUPPORTED,
+              "the saved routing exists for MoE layers only (n_experts == 0)");
+  const Saved sv = saved_layout(*cfg);
+  const Dims d = dims(*cfg);
+  switch (item) {
+    case FORGE_SAVED_ROUTE_IDX: *offset = sv.idx; *bytes = d.R * 4; break;
+    case FORGE_SAVED_ROUTE_GATES: *offset = sv.gates; *bytes = d.R * 4; break;
+    case FORGE_SAVED_ROUTE_PROBS: *offset = sv.probs; *bytes = d.T * d.E * 4; break;
+    case FORGE_SAVED_ROUTE_COUNTS: *offset = sv.counts; *bytes = d.E * 4; break;
+    case FORGE_SAVED_ROUTE_OFFSETS: *offset = sv.offsets; *bytes = (d.E + 1) * 4; break;
+    case FORGE_SAVED_ROUTE_PERM: *offset = sv.perm; *bytes = d.R * 4; break;
+    default: return fail(FORGE_ERR_INVALID_ARG, "unknown saved item %d", item);
+  }
+  return ok();
+}
+
 forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base, float* cos_out,
                               float* sin_out, forge_stream stream) {
   FORGE_CHECK(seq >= 1, FORGE_ERR_INVALID_ARG, "seq must be >= 1");
@@ -761,6 +786,14 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     if (side) FORGE_HIP(link(s, ws, side->ev[0]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                           gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), ws));
+    // the weight-gradient product above is the side stream's only reader of
+    // d_out; when d_in overlaps d_out, d_in is written only after it
+    hipEvent_t d_out_read = nullptr;
+    const bool alias = d_in < d_out + d.T * d.h && d_out < d_in + d.T * d.h;
+    if (side && alias) {
+      d_out_read = side->ev[5];
+      FORGE_HIP(hipEventRecord(d_out_read, ws));
+    }
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
     FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
@@ -779,7 +812,7 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
     if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
     return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
-                          side, opt);
+                          side, opt, d_out_read);
   }
 }
 
@@ -847,7 +880,7 @@ forge_status forge_layer_bwd_adamw(const forge_layer_cfg* cfg, const forge_layer
   if (forge_status e = check_optim(*cfg, w, opt)) return e;
   if (forge_status e = check_hparams(hp)) return e;
   FORGE_PTR(dev_scalars);
-  OptPlan plan{opt, hp, dev_scalars, nullptr, 5};
+  OptPlan plan{opt, hp, dev_scalars, nullptr, 6};
   if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace,
                                  (hipStream_t)stream, &plan))
     return e;

@@ -133,7 +133,8 @@ hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* d
 hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
 
 // ----------------------------------------------------------------- MoE ----
-// Routing of fp32 logits [T, E] (E <= 64): idx / gates [T, k], probs [T, E].
+// Routing of fp32 logits [T, E] (E <= 256): idx / gates [T, k], probs [T, E];
+// every idx entry lies in [0, E) (NaN logits rank below -inf).
 hipError_t moe_route(const float* logits, int T, int E, int k, int32_t* idx, float* gates,
                      float* probs, hipStream_t s);
 // Blocks of the counting sort; block_counts needs moe_sort_blocks(T) * E ints.

@@ -2,10 +2,12 @@
 // Table "H100 architecture configurations": routed experts with top-k
 // selection), dropless: every token goes to its top_k experts.
 //
-//  * route: one wave per token, lane e holds expert e's fp32 logit: softmax
-//    over all experts, then top_k rounds of wave argmax (largest logit, ties
-//    to the lower expert id). Gates are the softmax probabilities of the
-//    chosen experts (no renormalisation).
+//  * route: one wave per token, lane l holds the fp32 logits of experts
+//    l, l + 64, l + 128, l + 192 (E <= 256): softmax over all experts, then
+//    top_k rounds of wave argmax on a total order of the logits (numeric
+//    order, -0 equal to +0, NaN below -inf; ties to the lower expert id), so
+//    every index lies in [0, E) whatever the logits hold. Gates are the
+//    softmax probabilities of the chosen experts (no renormalisation).
 //  * permutation: a counting sort that is deterministic by construction —
 //    per-block expert histograms, a fixed-order scan over blocks, then each
 //    block assigns ranks in flat (token, slot) order with wave ballots, so
@@ -15,6 +17,8 @@
 //  * the load-balance auxiliary loss alpha * E * sum_e f_e P_e and its
 //    gradient through the softmax (f_e = count_e / (T k) is a constant);
 //    the column sums behind P_e are per-block partials summed in block order.
+#include <climits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -22,8 +26,36 @@ namespace forge {
 namespace {
 
 constexpr int kSortTokens = 128;  // tokens per counting-sort block
+constexpr int kMaxE = 256;        // experts (four per lane of a wave)
+constexpr int kSlots = kMaxE / 64;
 
 // ------------------------------------------------------------- routing ----
+// Order key of a logit for the top-k choice: larger key = preferred. The
+// integer image of the float is monotone in its value; -0 is first made +0
+// (they compare equal) and NaN gets the lowest key of all.
+__device__ __forceinline__ uint32_t order_key(float f) {
+  if (f == 0.0f) f = 0.0f;
+  const int b = __float_as_int(f);
+  const int key = b >= 0 ? b : (b ^ 0x7FFFFFFF);
+  return (uint32_t)(f != f ? INT_MIN : key) ^ 0x80000000u;
+}
+// Candidate word: order key, then the expert id reversed (a lower id wins a
+// tie of keys), then a 1 so that every real candidate is above 0, which
+// marks an expert that is taken or absent.
+__device__ __forceinline__ uint64_t cand_word(float l, int e) {
+  return ((uint64_t)order_key(l) << 32) | ((uint64_t)(kMaxE - 1 - e) << 1) | 1ull;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, o, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
+    const uint64_t w = ((uint64_t)hi << 32) | lo;
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
 __global__ __launch_bounds__(256) void route_k(const float* __restrict__ logits, int T, int E,
                                                int k, int32_t* __restrict__ idx,
                                                float* __restrict__ gates,
@@ -31,42 +63,76 @@ __global__ __launch_bounds__(256) void route_k(const float* __restrict__ logits,
   const int lane = threadIdx.x & 63;
   const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const float l = lane < E ? logits[t * E + lane] : -INFINITY;
-  const float mx = wave_max(l);
-  const float ex = lane < E ? __expf(l - mx) : 0.0f;
-  const float p = ex / wave_sum(ex);
-  if (lane < E) probs[t * E + lane] = p;
-  float cand = l;
+  float l[kSlots], p[kSlots];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int e = lane + 64 * i;
+    l[i] = e < E ? logits[t * E + e] : -INFINITY;
+    mx = fmaxf(mx, l[i]);
+  }
+  mx = wave_max(mx);
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int e = lane + 64 * i;
+    p[i] = e < E ? __expf(l[i] - mx) : 0.0f;
+    sum += p[i];
+  }
+  sum = wave_sum(sum);
+  uint64_t cand[kSlots];
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int e = lane + 64 * i;
+    p[i] /= sum;
+    if (e < E) probs[t * E + e] = p[i];
+    cand[i] = e < E ? cand_word(l[i], e) : 0ull;
+  }
   for (int j = 0; j < k; ++j) {
-    const float best = wave_max(cand);
-    const uint64_t hit = __ballot(cand == best && lane < E);
-    const int e = __ffsll((unsigned long long)hit) - 1;  // lowest lane among ties
-    const float g = __shfl(p, e, 64);
+    uint64_t best = cand[0];
+#pragma unroll
+    for (int i = 1; i < kSlots; ++i) best = cand[i] > best ? cand[i] : best;
+    best = wave_max_u64(best);
+    // k <= E, so a real candidate is left in every round
+    const int e = kMaxE - 1 - (int)((best >> 1) & (kMaxE - 1));
+    const int owner = e & 63, slot = e >> 6;
+    float ps = p[0];
+#pragma unroll
+    for (int i = 1; i < kSlots; ++i) ps = slot == i ? p[i] : ps;
+    const float g = __shfl(ps, owner, 64);
     if (lane == 0) {
       idx[t * k + j] = e;
       gates[t * k + j] = g;
     }
-    if (lane == e) cand = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kSlots; ++i)
+      if (lane == owner && slot == i) cand[i] = 0ull;
   }
 }
 
-// Per-block expert histogram of the flat (token, slot) entries.
+// Per-block expert histogram of the flat (token, slot) entries (entries
+// outside [0, E) are not counted).
 __global__ __launch_bounds__(256) void sort_count_k(const int32_t* __restrict__ idx, int T, int E,
                                                     int k, int32_t* __restrict__ block_counts) {
-  __shared__ int hist[64];
-  if (threadIdx.x < 64) hist[threadIdx.x] = 0;
+  __shared__ int hist[kMaxE];
+  hist[threadIdx.x] = 0;
   __syncthreads();
   const long f0 = (long)blockIdx.x * kSortTokens * k;
   const long f1 = min((long)T * k, f0 + (long)kSortTokens * k);
-  for (long f = f0 + threadIdx.x; f < f1; f += blockDim.x) atomicAdd(&hist[idx[f]], 1);
+  for (long f = f0 + threadIdx.x; f < f1; f += blockDim.x) {
+    const int e = idx[f];
+    if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
+  }
   __syncthreads();
   if (threadIdx.x < E) block_counts[(long)blockIdx.x * E + threadIdx.x] = hist[threadIdx.x];
 }
 
 // Fixed-order scan: offsets[e] (exclusive over experts), per-block bases.
-__global__ void sort_scan_k(int32_t* __restrict__ block_counts, int nblk, int E,
-                            int32_t* __restrict__ counts, int32_t* __restrict__ offsets) {
-  __shared__ int tot[64];
+// One block of kMaxE threads.
+__global__ __launch_bounds__(256) void sort_scan_k(int32_t* __restrict__ block_counts, int nblk,
+                                                   int E, int32_t* __restrict__ counts,
+                                                   int32_t* __restrict__ offsets) {
+  __shared__ int tot[kMaxE];
   const int e = threadIdx.x;
   if (e < E) {
     int run = 0;
@@ -99,23 +165,25 @@ __global__ __launch_bounds__(64) void sort_scatter_k(const int32_t* __restrict__
                                                      int32_t* __restrict__ pos_of) {
   // One wave walks the block's entries 64 at a time in flat order. The lanes
   // holding the same expert are found with one ballot per bit of the expert
-  // id (E <= 64: six bits), so each lane's rank among the earlier lanes of
+  // id (E <= 256: eight bits), so each lane's rank among the earlier lanes of
   // its expert is a popcount, and the group's lowest lane advances the
-  // expert's running position.
-  __shared__ int run[64];
+  // expert's running position. Entries outside [0, E) are skipped.
+  __shared__ int run[kMaxE];
   const int lane = threadIdx.x;
-  if (lane < E) run[lane] = offsets[lane] + block_base[(long)blockIdx.x * E + lane];
+  for (int e = lane; e < E; e += 64)
+    run[e] = offsets[e] + block_base[(long)blockIdx.x * E + e];
   __syncthreads();
   const long f0 = (long)blockIdx.x * kSortTokens * k;
   const long f1 = min((long)T * k, f0 + (long)kSortTokens * k);
   const uint64_t below = (1ull << lane) - 1ull;
   for (long base = f0; base < f1; base += 64) {
     const long f = base + lane;
-    const bool ok = f < f1;
-    const int e = ok ? idx[f] : 0;
+    const int raw = f < f1 ? idx[f] : -1;
+    const bool ok = (unsigned)raw < (unsigned)E;
+    const int e = ok ? raw : 0;
     uint64_t same = __ballot(ok);
 #pragma unroll
-    for (int b = 0; b < 6; ++b) {
+    for (int b = 0; b < 8; ++b) {
       const uint64_t ones = __ballot(ok && ((e >> b) & 1));
       same &= ((e >> b) & 1) ? ones : ~ones;
     }
@@ -238,43 +306,44 @@ __global__ __launch_bounds__(256) void scatter_back_k(const bf16_t* __restrict__
   reinterpret_cast<uint4*>(db + t * h)[c] = pack8(acc);
 }
 
-// P_e = sum_t p[t, e] (fixed order) and aux += alpha E sum_e f_e P_e / T.
-// One block; wave w sums the token stripe t = w mod 16 for each expert lane.
 // Column sums of the router probabilities over kAuxTokens-token blocks,
-// partial[block][e]; summed in block order by aux_loss_k.
+// partial[block][e] (thread e sums its expert's column in token order);
+// aux_loss_k adds the blocks in block order: P_e = sum_t p[t, e], and
+// aux += alpha E sum_e f_e P_e / T.
 constexpr int kAuxTokens = 64;
 __global__ __launch_bounds__(256) void prob_colsum_k(const float* __restrict__ probs, int T, int E,
                                                      float* __restrict__ partial) {
-  __shared__ float part[4][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int e = threadIdx.x;
   const long t0 = (long)blockIdx.x * kAuxTokens;
+  const long t1 = min((long)T, t0 + kAuxTokens);
+  if (e >= E) return;
   float sum = 0.0f;
-  if (lane < E)
-    for (int i = wave; i < kAuxTokens && t0 + i < T; i += 4) sum += probs[(t0 + i) * E + lane];
-  part[wave][lane] = sum;
-  __syncthreads();
-  if (threadIdx.x < E)
-    partial[(long)blockIdx.x * E + threadIdx.x] =
-        ((part[0][threadIdx.x] + part[1][threadIdx.x]) + part[2][threadIdx.x]) + part[3][threadIdx.x];
+  for (long t = t0; t < t1; ++t) sum += probs[t * E + e];
+  partial[(long)blockIdx.x * E + e] = sum;
 }
 
-__global__ __launch_bounds__(64) void aux_loss_k(const float* __restrict__ partial, int nblk,
-                                                 const int32_t* __restrict__ counts, int T, int E,
-                                                 int k, float alpha, float* __restrict__ colsum,
-                                                 float* __restrict__ aux) {
+__global__ __launch_bounds__(256) void aux_loss_k(const float* __restrict__ partial, int nblk,
+                                                  const int32_t* __restrict__ counts, int T, int E,
+                                                  int k, float alpha, float* __restrict__ colsum,
+                                                  float* __restrict__ aux) {
+  __shared__ float part[4];
   const int e = threadIdx.x;
   float c = 0.0f;
   if (e < E)
     for (int b = 0; b < nblk; ++b) c += partial[(long)b * E + e];
   if (e < E) colsum[e] = c;
   const float fe = e < E ? (float)counts[e] / ((float)T * k) : 0.0f;
-  const float term = wave_sum(fe * (e < E ? c : 0.0f));
-  if (e == 0 && aux) aux[0] += alpha * (float)E * term / (float)T;
+  const float term = wave_sum(fe * c);
+  if ((e & 63) == 0) part[e >> 6] = term;
+  __syncthreads();
+  if (e == 0 && aux) aux[0] += alpha * (float)E * ((part[0] + part[1]) + (part[2] + part[3])) /
+                               (float)T;
 }
 
 // dl[t, e] = p (dp - sum_e p dp) with dp = dgate on chosen experts plus the
 // aux term alpha E f_e / T on every expert; written as bf16 for the router
-// data / weight gradient products. One wave per token.
+// data / weight gradient products. One wave per token, lane l holding
+// experts l + 64 i.
 __global__ __launch_bounds__(256) void router_bwd_k(const float* __restrict__ probs,
                                                     const int32_t* __restrict__ idx,
                                                     const float* __restrict__ dgate,
@@ -284,12 +353,23 @@ __global__ __launch_bounds__(256) void router_bwd_k(const float* __restrict__ pr
   const int lane = threadIdx.x & 63;
   const long t = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const float p = lane < E ? probs[t * E + lane] : 0.0f;
-  float dp = lane < E ? alpha * (float)E * ((float)counts[lane] / ((float)T * k)) / (float)T : 0.0f;
-  for (int j = 0; j < k; ++j)
-    if (idx[t * k + j] == lane) dp += dgate[t * k + j];
-  const float dot = wave_sum(p * dp);
-  if (lane < E) dl[t * E + lane] = f2bf(p * (dp - dot));
+  float p[kSlots], dp[kSlots];
+  float part = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int e = lane + 64 * i;
+    p[i] = e < E ? probs[t * E + e] : 0.0f;
+    dp[i] = e < E ? alpha * (float)E * ((float)counts[e] / ((float)T * k)) / (float)T : 0.0f;
+    for (int j = 0; j < k; ++j)
+      if (idx[t * k + j] == e) dp[i] += dgate[t * k + j];
+    part += p[i] * dp[i];
+  }
+  const float dot = wave_sum(part);
+#pragma unroll
+  for (int i = 0; i < kSlots; ++i) {
+    const int e = lane + 64 * i;
+    if (e < E) dl[t * E + e] = f2bf(p[i] * (dp[i] - dot));
+  }
 }
 
 inline unsigned nblocks(long work, int threads) { return (unsigned)((work + threads - 1) / threads); }
@@ -310,7 +390,7 @@ hipError_t moe_sort(const int32_t* idx, int T, int E, int k, int32_t* block_coun
                     hipStream_t s) {
   const int nb = moe_sort_blocks(T);
   hipLaunchKernelGGL(sort_count_k, dim3(nb), dim3(256), 0, s, idx, T, E, k, block_counts);
-  hipLaunchKernelGGL(sort_scan_k, dim3(1), dim3(64), 0, s, block_counts, nb, E, counts, offsets);
+  hipLaunchKernelGGL(sort_scan_k, dim3(1), dim3(kMaxE), 0, s, block_counts, nb, E, counts, offsets);
   hipLaunchKernelGGL(sort_scatter_k, dim3(nb), dim3(64), 0, s, idx, T, E, k, block_counts, offsets,
                      perm, pos_of);
   return hipGetLastError();
@@ -353,7 +433,7 @@ hipError_t moe_aux_loss(const float* probs, const int32_t* counts, int T, int E,
   const int nb = moe_aux_blocks(T);
   float* partial = colsum + E;
   hipLaunchKernelGGL(prob_colsum_k, dim3(nb), dim3(256), 0, s, probs, T, E, partial);
-  hipLaunchKernelGGL(aux_loss_k, dim3(1), dim3(64), 0, s, partial, nb, counts, T, E, k, alpha, colsum, aux);
+  hipLaunchKernelGGL(aux_loss_k, dim3(1), dim3(256), 0, s, partial, nb, counts, T, E, k, alpha, colsum, aux);
   return hipGetLastError();
 }
 

@@ -53,7 +53,8 @@ def test_size_queries_are_consistent():
     (dict(hidden=260), _lib.FORGE_ERR_INVALID_ARG),
     (dict(ffn=690), _lib.FORGE_ERR_INVALID_ARG),
     (dict(seq=0), _lib.FORGE_ERR_INVALID_ARG),
-    (dict(n_experts=96, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
+    (dict(n_experts=264, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
+    (dict(n_experts=100, top_k=8, expert_ffn=1408), _lib.FORGE_ERR_UNSUPPORTED),
     (dict(n_experts=64, top_k=0, expert_ffn=1408), _lib.FORGE_ERR_INVALID_ARG),
     (dict(n_experts=64, top_k=8, expert_ffn=1404), _lib.FORGE_ERR_INVALID_ARG),
 ])
@@ -179,5 +180,19 @@ def test_moe_layer_sizes():
     assert saved >= 2 * T * k * (h + 2 * fe + fe + h)
     assert _lib.forge_layer_workspace_bytes(cfg) >= 2 * T * k * (2 * h + 3 * fe)
     assert _lib.forge_moe_route_workspace_bytes(T, 64, 8) >= T * 8 * 4
+    assert _lib.forge_moe_route_workspace_bytes(T, 160, 16) >= T * 16 * 4
     with pytest.raises(_lib.ForgeError):
-        _lib.forge_moe_route_workspace_bytes(T, 65, 8)
+        _lib.forge_moe_route_workspace_bytes(T, 257, 8)
+    # the routing items lie inside the saved buffer and do not overlap
+    items = sorted(_lib.forge_layer_saved_item(cfg, i) for i in range(6))
+    sizes = dict(zip(range(6), [T * k * 4, T * k * 4, T * 64 * 4, 64 * 4, 65 * 4, T * k * 4]))
+    assert sorted(n for _, n in items) == sorted(sizes.values())
+    for (o1, n1), (o2, _) in zip(items, items[1:]):
+        assert o1 + n1 <= o2
+    assert items[-1][0] + items[-1][1] <= saved
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_layer_saved_item(cfg, 6)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_layer_saved_item(_lib.layer_cfg(fi.config("tiny")), 0)
+    assert e.value.status == _lib.FORGE_ERR_UNSUPPORTED

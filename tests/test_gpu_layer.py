@@ -70,6 +70,43 @@ def test_layer_8b_geometry_short_seq():
     check(*run_layer(cfg, seed=21))
 
 
+@pytest.mark.parametrize("name,over,seed", [
+    ("tiny", dict(batch=2, seq=77), 13),
+    ("tiny", dict(seq=160, head_dim=128, n_heads=2, n_kv_heads=1), 5),
+    ("llama8b_layer", dict(seq=320), 22),
+])
+def test_layer_recompute_attention_vs_oracle(name, over, seed):
+    # attention recomputed in the backward (O and LSE not kept, Sec. 3.3
+    # recompute policies): the whole layer backward against the oracle
+    cfg = fi.config(name, recompute_attn=1, **over)
+    banner(f"layer recompute_attn {name} {over}")
+    check(*run_layer(cfg, seed=seed))
+
+
+def test_layer_bwd_d_in_aliasing_d_out():
+    """d_in may be the very buffer of d_out: with the side streams on (T x h
+    >= 2^20) the result must equal the one with separate buffers, bit for
+    bit, whatever the weight-gradient stream still reads."""
+    import torch
+    from paper_2609_13645_amd import runtime
+    cfg = fi.config("llama8b_layer", seq=320)
+    assert runtime.uses_side_streams(cfg)
+    banner("layer backward with d_in == d_out (side streams)")
+    inp = fi.layer_inputs(cfg, seed=23)
+    res = []
+    for alias in (False, True):
+        layer = runtime.Layer(cfg, inp["weights"])
+        x, dy = dev_bf16(inp["x"]), dev_bf16(inp["dy"])
+        out = torch.empty_like(x)
+        layer.fwd(x, out)
+        dx = dy if alias else torch.empty_like(x)
+        layer.bwd(x, dy, dx, overwrite=True)
+        torch.cuda.synchronize()
+        res.append([host_f64(dx)] + [host_f64(layer.g["d_" + n]) for n in NAMES])
+    for n, a, b in zip(("dx",) + NAMES, *res):
+        assert np.array_equal(a, b), n
+
+
 def test_layer_recompute_matches_stored():
     import torch
     from paper_2609_13645_amd import runtime

@@ -52,19 +52,57 @@ def test_adamw_matches_oracle(n, step, clip):
 
 
 def test_adamw_is_deterministic_and_resumable():
-    banner("adamw determinism / resume")
-    st = fi.optimizer_inputs(100_000, seed=9, step=3)
-    a = _adamw_gpu(st, 3)
-    b = _adamw_gpu(st, 3)
-    for k in a:
-        assert np.array_equal(a[k], b[k]), k
-    # two steps in one go == one step, "checkpoint" to host, one more step
-    s2 = dict(st, master=a["master"], m=a["m"], v=a["v"])
-    c = _adamw_gpu(s2, 4)
-    s2b = {k: v.copy() for k, v in s2.items()}
-    d = _adamw_gpu(s2b, 4)
-    for k in c:
-        assert np.array_equal(c[k], d[k]), k
+    """N + M steps in one go on the device equal N steps, a save of master,
+    m and v to the host, a restore into fresh device buffers and M more
+    steps, bit for bit; the step scalars advance on the device
+    (forge_adamw_advance) and each step has its own gradient."""
+    import torch
+    from paper_2609_13645_amd import _lib
+    banner("adamw determinism / save-restore resume over 3 + 2 steps")
+    n, N, M = 100_003, 3, 2
+    st = fi.optimizer_inputs(n, seed=9, step=1)
+    rng = np.random.default_rng(10)
+    grads = [(rng.standard_normal(n, dtype=np.float32) * np.float32(1e-2)) for _ in range(N + M)]
+    hp = _lib.AdamwHparams(HP["beta1"], HP["beta2"], HP["eps"], HP["wd"])
+
+    def fresh(state, step0):
+        dev = {k: torch.from_numpy(np.ascontiguousarray(state[k]).copy()).cuda()
+               for k in ("master", "m", "v")}
+        dev["param"] = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+        dev["sc"] = torch.tensor([0.0, 0.0, 0.0, 1.0], dtype=torch.float32, device="cuda")
+        dev["step"] = torch.tensor([step0], dtype=torch.int32, device="cuda")
+        return dev
+
+    def steps(dev, gs):
+        for g in gs:
+            gd = torch.from_numpy(g).cuda()
+            _lib.forge_adamw_advance(dev["sc"], dev["step"], HP["lr"], HP["beta1"], HP["beta2"])
+            _lib.forge_adamw_step(dev["master"], dev["param"], gd, dev["m"], dev["v"], n, hp,
+                                  dev["sc"])
+        torch.cuda.synchronize()
+        out = {k: dev[k].cpu().numpy() for k in ("master", "m", "v")}
+        out["param"] = dev["param"].view(torch.int16).cpu().numpy().view(np.uint16)
+        out["step"] = int(dev["step"].item())
+        return out
+
+    whole = steps(fresh(st, 0), grads)
+    again = steps(fresh(st, 0), grads)
+    for k in whole:
+        assert np.array_equal(whole[k], again[k]), k
+    first = steps(fresh(st, 0), grads[:N])
+    saved = {k: first[k].copy() for k in ("master", "m", "v")}     # host checkpoint
+    resumed = steps(fresh(saved, first["step"]), grads[N:])
+    assert resumed["step"] == whole["step"] == N + M
+    for k in ("master", "m", "v", "param"):
+        assert np.array_equal(resumed[k], whole[k]), k
+    # and the whole run matches the oracle's N + M steps from the same state
+    p, m, v = (st[k].astype(np.float64) for k in ("master", "m", "v"))
+    f32 = lambda x: float(np.float32(x))
+    for t, g in enumerate(grads, start=1):
+        p, m, v = oadam.adamw_step(p, g, m, v, f32(HP["lr"]), f32(HP["beta1"]),
+                                   f32(HP["beta2"]), f32(HP["eps"]), f32(HP["wd"]), t)
+    p0 = st["master"].astype(np.float64)
+    assert rel_fro(whole["master"].astype(np.float64) - p0, p - p0) <= 1e-5
 
 
 def test_grad_norm_and_clip_coeff():

@@ -229,3 +229,19 @@ def test_layer_rows_equals_full_layer():
     out, _ = dense.layer_fwd(x, W, cfg)
     rows = [0, 3, 4, 5, 9]
     assert np.allclose(dense.layer_fwd_rows(x, W, cfg, rows), out[rows], rtol=1e-12, atol=1e-13)
+
+
+def test_attention_threaded_equals_serial():
+    # the per-kv-head tasks run the serial arithmetic: identical bits
+    rng = np.random.default_rng(12)
+    B, S, nh, nkv, d = 2, 9, 6, 3, 4
+    q = rng.standard_normal((B * S, nh, d))
+    k = rng.standard_normal((B * S, nkv, d))
+    v = rng.standard_normal((B * S, nkv, d))
+    do = rng.standard_normal((B * S, nh, d))
+    o1, l1 = dense.attention_fwd(q, k, v, B, S, workers=1)
+    o4, l4 = dense.attention_fwd(q, k, v, B, S, workers=4)
+    assert np.array_equal(o1, o4) and np.array_equal(l1, l4)
+    for a, b in zip(dense.attention_bwd(q, k, v, do, B, S, workers=1),
+                    dense.attention_bwd(q, k, v, do, B, S, workers=4)):
+        assert np.array_equal(a, b)

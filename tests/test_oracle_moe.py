@@ -133,3 +133,32 @@ def test_topk_margin_brute_force():
     d = (0.49 * m[:, None] * rng.uniform(-1, 1, l.shape)).astype(np.float32)
     keep = m > 1e-3
     assert np.array_equal(np.sort(moe.topk(l + d, k)[keep], 1), np.sort(moe.topk(l, k)[keep], 1))
+
+
+def test_forced_routing_reproduces_free_routing_and_stays_valid():
+    rng = np.random.default_rng(9)
+    T, E, k = 41, 16, 4
+    l = rng.standard_normal((T, E))
+    free = moe.route(l, k)
+    forced = moe.route(l, k, moe.topk(np.asarray(l, np.float32), k))
+    for a, b in zip(free, forced):
+        assert np.array_equal(a, b)
+    # another valid choice: swap the k-th expert of token 3 for its (k+1)-th
+    order = np.argsort(-l[3], kind="stable")
+    alt = free[0].copy()
+    alt[3, k - 1] = order[k]
+    idx, gates, p, counts, offsets, perm = moe.route(l, k, alt)
+    assert counts[order[k]] == free[3][order[k]] + 1
+    assert counts[order[k - 1]] == free[3][order[k - 1]] - 1
+    assert np.array_equal(gates, np.take_along_axis(p, alt, 1))
+    flat = alt.reshape(-1)
+    for e in range(E):
+        seg = perm[offsets[e]:offsets[e + 1]]
+        assert np.all(flat[seg] == e) and np.all(np.diff(seg) > 0)
+
+
+def test_topk_order_of_signed_zero_and_nan():
+    # -0 and +0 tie (lower id first); NaN ranks below every number, -inf too
+    l = np.array([[np.nan, -np.inf, -0.0, 0.0, -1.0],
+                  [0.0, -0.0, np.nan, np.nan, -np.inf]], np.float32)
+    assert np.array_equal(moe.topk(l, 5), [[2, 3, 4, 1, 0], [0, 1, 4, 2, 3]])
