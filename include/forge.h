@@ -518,6 +518,31 @@ forge_status forge_moe_route(const float* logits, int32_t tokens, int32_t n_expe
                              int32_t* counts, int32_t* offsets, int32_t* perm,
                              void* workspace, forge_stream stream);
 
+/* Limits of forge_moe_route_noalloc's fixed scratch. */
+#define FORGE_MOE_ROUTE_NOALLOC_MAX_ENTRIES (1 << 19)  /* tokens * top_k */
+#define FORGE_MOE_ROUTE_NOALLOC_MAX_HIST (1 << 17)     /* ceil(tokens / 128) * n_experts */
+
+/*
+ * forge_moe_route without the workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation. Same arguments, results (bit for bit)
+ * and errors as forge_moe_route otherwise. The counting sort's scratch (per
+ * block expert histograms, then the inverse permutation) is a fixed device
+ * array inside the library, 2.5 MiB on each GPU the library runs on, held
+ * until the process ends; every call writes the parts it reads, so nothing
+ * in it needs to start at zero. All calls on one GPU share that array: calls
+ * that overlap on one GPU (other streams, other threads) race and must be
+ * serialised by the caller. Limits: tokens * top_k <=
+ * FORGE_MOE_ROUTE_NOALLOC_MAX_ENTRIES and ceil(tokens / 128) * n_experts <=
+ * FORGE_MOE_ROUTE_NOALLOC_MAX_HIST, else FORGE_ERR_UNSUPPORTED before any
+ * launch. Allocates nothing (the array's device address is looked up once
+ * per GPU on its first call).
+ */
+forge_status forge_moe_route_noalloc(const float* logits, int32_t tokens, int32_t n_experts,
+                                     int32_t top_k, int32_t* idx, float* gates, float* probs,
+                                     int32_t* counts, int32_t* offsets, int32_t* perm,
+                                     forge_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

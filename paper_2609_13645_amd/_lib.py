@@ -146,6 +146,7 @@ def load():
                                                P, P]),
         "forge_moe_route_workspace_bytes": (ctypes.c_int, [I32, I32, I32, SZ]),
         "forge_moe_route": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P, P, P, P, P]),
+        "forge_moe_route_noalloc": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P, P, P, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)
@@ -377,3 +378,14 @@ def forge_moe_route(logits, tokens, n_experts, top_k, idx, gates, probs, counts,
     _check(load().forge_moe_route(_ptr(logits), tokens, n_experts, top_k, _ptr(idx), _ptr(gates),
                                   _ptr(probs), _ptr(counts), _ptr(offsets), _ptr(perm),
                                   _ptr(workspace), _stream(stream)))
+
+
+MOE_ROUTE_NOALLOC_MAX_ENTRIES = 1 << 19
+MOE_ROUTE_NOALLOC_MAX_HIST = 1 << 17
+
+
+def forge_moe_route_noalloc(logits, tokens, n_experts, top_k, idx, gates, probs, counts, offsets,
+                            perm, stream=None):
+    _check(load().forge_moe_route_noalloc(_ptr(logits), tokens, n_experts, top_k, _ptr(idx),
+                                          _ptr(gates), _ptr(probs), _ptr(counts), _ptr(offsets),
+                                          _ptr(perm), _stream(stream)))

@@ -932,6 +932,70 @@ forge_status forge_moe_route(const float* logits, int32_t tokens, int32_t n_expe
   return ok();
 }
 
+// ---- MoE routing without a workspace argument -------------------------------
+// The counting sort's scratch of forge_moe_route_noalloc (block histograms,
+// then the inverse permutation) lives in this fixed device array, one copy
+// per GPU for the life of the process. In host code its name is not a device
+// address: each device's address comes from hipGetSymbolAddress, taken once
+// per device with that device current, and only that address reaches the
+// kernels.
+namespace {
+constexpr size_t kRouteScratchEntries = size_t(1) << 19;  // tokens * top_k
+constexpr size_t kRouteScratchHist = size_t(1) << 17;     // sort blocks * n_experts
+}  // namespace
+static __device__ __align__(256) int32_t scratch[kRouteScratchHist + kRouteScratchEntries];
+
+namespace {
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+hipError_t route_scratch(int32_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+forge_status forge_moe_route_noalloc(const float* logits, int32_t tokens, int32_t n_experts,
+                                     int32_t top_k, int32_t* idx, float* gates, float* probs,
+                                     int32_t* counts, int32_t* offsets, int32_t* perm,
+                                     forge_stream stream) {
+  FORGE_CHECK(tokens >= 1, FORGE_ERR_INVALID_ARG, "tokens must be >= 1");
+  FORGE_CHECK(n_experts >= 1 && n_experts <= kMaxExperts, FORGE_ERR_UNSUPPORTED,
+              "n_experts must be in [1, %d]", kMaxExperts);
+  FORGE_CHECK(top_k >= 1 && top_k <= n_experts, FORGE_ERR_INVALID_ARG,
+              "top_k must be in [1, n_experts]");
+  FORGE_CHECK((size_t)tokens * top_k <= kRouteScratchEntries, FORGE_ERR_UNSUPPORTED,
+              "tokens * top_k = %lld exceeds the fixed scratch limit %zu",
+              (long long)tokens * top_k, kRouteScratchEntries);
+  FORGE_CHECK((size_t)forge::moe_sort_blocks(tokens) * n_experts <= kRouteScratchHist,
+              FORGE_ERR_UNSUPPORTED,
+              "ceil(tokens / 128) * n_experts = %lld exceeds the fixed scratch limit %zu",
+              (long long)forge::moe_sort_blocks(tokens) * n_experts, kRouteScratchHist);
+  for (const void* p : {(const void*)logits, (const void*)idx, (const void*)gates,
+                        (const void*)probs, (const void*)counts, (const void*)offsets,
+                        (const void*)perm})
+    FORGE_CHECK(p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3u) == 0,
+                FORGE_ERR_INVALID_ARG, "a pointer argument is NULL or not 4-byte aligned");
+  int32_t* ws = nullptr;
+  FORGE_HIP(route_scratch(&ws));
+  hipStream_t s = (hipStream_t)stream;
+  FORGE_HIP(forge::moe_route(logits, tokens, n_experts, top_k, idx, gates, probs, s));
+  FORGE_HIP(forge::moe_sort(idx, tokens, n_experts, top_k, ws, counts, offsets, perm,
+                            ws + kRouteScratchHist, s));
+  return ok();
+}
+
 // ---- output head ----------------------------------------------------------
 namespace {
 struct HeadWork {

@@ -196,3 +196,17 @@ def test_moe_layer_sizes():
     with pytest.raises(_lib.ForgeError) as e:
         _lib.forge_layer_saved_item(_lib.layer_cfg(fi.config("tiny")), 0)
     assert e.value.status == _lib.FORGE_ERR_UNSUPPORTED
+
+
+def test_moe_route_noalloc_refuses_requests_beyond_its_scratch():
+    # host-side limits of the fixed scratch: refused before any launch
+    big = _lib.MOE_ROUTE_NOALLOC_MAX_ENTRIES // 16 + 1
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_moe_route_noalloc(16, big, 64, 16, 16, 16, 16, 16, 16, 16, stream=0)
+    assert e.value.status == _lib.FORGE_ERR_UNSUPPORTED
+    with pytest.raises(_lib.ForgeError) as e:   # histogram limit: blocks * experts
+        _lib.forge_moe_route_noalloc(16, 128 * 1024, 256, 1, 16, 16, 16, 16, 16, 16, stream=0)
+    assert e.value.status == _lib.FORGE_ERR_UNSUPPORTED
+    with pytest.raises(_lib.ForgeError) as e:
+        _lib.forge_moe_route_noalloc(16, 100, 64, 8, 0, 16, 16, 16, 16, 16, stream=0)
+    assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
