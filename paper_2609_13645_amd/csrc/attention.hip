@@ -1,7 +1,7 @@
 // Causal grouped-query flash attention on gfx950 MFMA: forward, and the
-// backward as a pre-pass (delta = rowsum(dO * O)), key-owned kernels that
-// accumulate dV and dK, a query-owned kernel that accumulates dQ, and a
-// small reduction of the dK, dV partials over each GQA group. The paper's H100
+// backward as a query-owned kernel that accumulates dQ (and on the way forms
+// delta = rowsum(dO * O) for the rest), key-owned kernels that accumulate dV
+// and dK, and a small reduction of the dK, dV partials over each GQA group. The paper's H100
 // kernel accumulates dQ through a flat global buffer (App. D, "Anatomy of a
 // Forged Kernel"); here the dQ kernel recomputes two products instead, with no
 // fp32 atomics, so every output is deterministic.
@@ -414,45 +414,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   }
 }
 
-// -------------------------------------------------- backward pre-pass ----
-// delta[b, n, s] = -sum_d dO[t, n, d] O[t, n, d] (negated: it initialises the
-// dP accumulators, which then hold dP - rowsum(dO O)) and, in the second half
-// of the buffer, -LSE[b, n, s] * log2(e) (the exponent offset of
-// P = exp(S - LSE) in base 2); 8 lanes per (token, head).
-template <int D>
-__global__ __launch_bounds__(256) void attn_bwd_pre_k(AttnArgs a, const bf16_t* __restrict__ o,
-                                                      const bf16_t* __restrict__ dout,
-                                                      const float* __restrict__ lse,
-                                                      float* __restrict__ delta) {
-  const long id = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 3;
-  const int sub = threadIdx.x & 7;
-  const long T = (long)a.batch * a.seq;
-  const bool ok = id < T * a.n_heads;
-  const long t = ok ? id / a.n_heads : 0;
-  const int n = ok ? (int)(id % a.n_heads) : 0;
-  const long off = t * (long)(a.n_heads * D) + (long)n * D;
-  float s = 0.0f;
-  if (ok) {
-#pragma unroll
-    for (int c = sub; c < D / 8; c += 8) {
-      float x[8], y[8];
-      unpack8(reinterpret_cast<const uint4*>(o + off)[c], x);
-      unpack8(reinterpret_cast<const uint4*>(dout + off)[c], y);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += x[e] * y[e];
-    }
-  }
-  s += __shfl_xor(s, 1, 64);
-  s += __shfl_xor(s, 2, 64);
-  s += __shfl_xor(s, 4, 64);
-  if (ok && sub == 0) {
-    const long bb = t / a.seq, i = t % a.seq;
-    const long li = (bb * a.n_heads + n) * a.seq + i;
-    delta[li] = -s;
-    delta[T * a.n_heads + li] = -lse[li] * kLog2e;
-  }
-}
-
 // ------------------------------------------------------ backward dK, dV ----
 // Block: 128 keys (32 per wave) of one (batch, query head); loops over the
 // 64-query tiles at or after its first key and writes fp32 partials of its
@@ -659,14 +620,22 @@ __global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict
 
 // ---------------------------------------------------------- backward dQ ----
 // Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
+// Runs first in the backward: each lane forms its query's
+// delta = rowsum(dO * O) from the dO row it holds anyway and the O row (the
+// two halves of d meet through one lane exchange), and stores, for the
+// key-owned kernels, -delta (it initialises their dP accumulators, which
+// then hold dP - delta) and, in the second half of the buffer,
+// -LSE * log2(e) (the exponent offset of P = exp(S - LSE) in base 2).
 // P is recomputed from the saved LSE (exponent argument as one FMA), then
 // dS = P (dP - delta) and dQ^T += K^T dS^T, one 32-key half of a tile at a
 // time (the whole tile's scores, dP and K^T fragments do not fit in the
 // registers of two waves per SIMD). LDS double buffering, batched fragment
 // reads and explicit waits.
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ dout,
-                                                const float* __restrict__ delta,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ o,
+                                                const bf16_t* __restrict__ dout,
+                                                const float* __restrict__ lse,
+                                                float* __restrict__ delta,
                                                 bf16_t* __restrict__ dq, long ld_d) {
   constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
   __shared__ uint4 sm0[2 * NAT];
@@ -688,14 +657,23 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   const int q0w = qt * BQ + wave * 32;
   const int q = q0w + l32;
   bf16x8_t qf[KK], of[KK];
+  float dsum = 0.0f;
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     qf[kk] = gload_frag(Qg + (long)q * a.ld_qkv + kk * 16 + hh * 8, q < S);
     of[kk] = gload_frag(dOg + (long)q * ldo + kk * 16 + hh * 8, q < S);
+    const bf16x8_t ov = gload_frag(o + (rb + q) * ldo + (long)n * D + kk * 16 + hh * 8, q < S);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dsum += (float)of[kk][e] * (float)ov[e];
   }
+  dsum += __shfl_xor(dsum, 32, 64);
   const long li = ((long)b * a.n_heads + n) * S + q;
-  const float nl2 = q < S ? delta[(long)a.batch * a.n_heads * S + li] : -INFINITY;
-  const float ndl = q < S ? delta[li] : 0.0f;   // -rowsum(dO O)
+  const float nl2 = q < S ? -lse[li] * kLog2e : -INFINITY;
+  const float ndl = -dsum;   // -rowsum(dO O)
+  if (q < S && hh == 0) {
+    delta[li] = ndl;
+    delta[(long)a.batch * a.n_heads * S + li] = nl2;
+  }
   f32x16_t dqa[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) zero(dqa[db]);
@@ -805,16 +783,6 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
-                        const float* lse, float* delta, hipStream_t s) {
-  const long n = (long)a.batch * a.seq * a.n_heads * 8;
-  const dim3 grid((unsigned)((n + 255) / 256)), block(256);
-  if (a.d == 128) hipLaunchKernelGGL(attn_bwd_pre_k<128>, grid, block, 0, s, a, o, dout, lse, delta);
-  else if (a.d == 64) hipLaunchKernelGGL(attn_bwd_pre_k<64>, grid, block, 0, s, a, o, dout, lse, delta);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
 size_t attn_bwd_partial_floats(const AttnArgs& a) {
   return (size_t)(a.n_heads / a.n_kv_heads) * a.batch * a.seq * a.n_kv_heads * a.d;
 }
@@ -841,12 +809,13 @@ hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* d
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* delta, uint16_t* dq, long ld_d, hipStream_t s) {
+hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
+                       const float* lse, float* delta, uint16_t* dq, long ld_d, hipStream_t s) {
   const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
   if (a.d == 128)
-    hipLaunchKernelGGL(attn_bwd_dq_k<128>, grid, block, 0, s, a, dout, delta, dq, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<128>, grid, block, 0, s, a, o, dout, lse, delta, dq, ld_d);
   else if (a.d == 64)
-    hipLaunchKernelGGL(attn_bwd_dq_k<64>, grid, block, 0, s, a, dout, delta, dq, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<64>, grid, block, 0, s, a, o, dout, lse, delta, dq, ld_d);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

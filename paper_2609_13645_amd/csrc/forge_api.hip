@@ -465,11 +465,10 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
   if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_o, g->d_w_o, d.h * d.hq));
-  FORGE_HIP(forge::attn_bwd_pre(aa, o, dO, lse, delta, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, o, dO, lse, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
                                  at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
                                  d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dq(aa, dO, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
                               (int)(d.nh + d.nkv), (int)d.d, true, s));
   if (side) FORGE_HIP(link(s, ws, side->ev[3]));
@@ -1357,10 +1356,9 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
                       cfg->n_kv_heads * cfg->head_dim * 4;
   float* pk = at<float>(workspace, dbytes);
   float* pv = at<float>(workspace, dbytes + up(part));
-  FORGE_HIP(forge::attn_bwd_pre(aa, o, d_o, lse, delta, s));
+  FORGE_HIP(forge::attn_bwd_dq(aa, o, d_o, lse, delta, d_qkv, d.qkv, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, delta, pk, pv, d_qkv + d.hq,
                                  d_qkv + d.hq + d.hkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dq(aa, d_o, delta, d_qkv, d.qkv, s));
   return ok();
 }
 

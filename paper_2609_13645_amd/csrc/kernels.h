@@ -119,10 +119,14 @@ struct AttnArgs {
 };
 // o [T, n_heads*d] bf16; lse [batch, n_heads, seq] fp32 (natural log).
 hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s);
-// delta: 2 * batch * n_heads * seq fp32: [b,n,i] = sum_d dO*O, then the
-// second half [b,n,i] = -lse * log2(e) (read by the two kernels below).
-hipError_t attn_bwd_pre(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
-                        const float* lse, float* delta, hipStream_t s);
+// Backward, in this order: attn_bwd_dq, then attn_bwd_dkdv.
+// attn_bwd_dq: dq [T, n_heads*d] columns of the dqkv buffer (row stride
+// ld_dqkv); also fills delta (2 * batch * n_heads * seq fp32): [b,n,i] =
+// -sum_d dO*O, then the second half [b,n,i] = -lse * log2(e), which
+// attn_bwd_dkdv reads.
+hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
+                       const float* lse, float* delta, uint16_t* dq, long ld_dqkv,
+                       hipStream_t s);
 // Floats of each of the two fp32 partial buffers attn_bwd_dkdv needs
 // ([n_heads / n_kv_heads][T][n_kv * d]).
 size_t attn_bwd_partial_floats(const AttnArgs& a);
@@ -130,7 +134,6 @@ size_t attn_bwd_partial_floats(const AttnArgs& a);
 // per-query-head fp32 partials pk, pv summed in a fixed order.
 hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
                          long ld_dqkv, hipStream_t s);
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* dout, const float* delta, uint16_t* dq, long ld_dqkv, hipStream_t s);
 
 // ----------------------------------------------------------------- MoE ----
 // Routing of fp32 logits [T, E] (E <= 256): idx / gates [T, k], probs [T, E];
