@@ -20,6 +20,17 @@ Readings where the paper is silent:
   * Layer order (Llama): a = RMSNorm(x); h1 = x + Attn(a) W_o^T;
     b = RMSNorm(h1); out = h1 + (silu(b W_g^T) * (b W_u^T)) W_d^T.
 
+Model variants of App. B, each off unless the config asks for it:
+  * qk_norm (Qwen3's per-head QK-Norm): every q and k head vector is
+    RMS-normalised over head_dim with gains q_norm / k_norm [head_dim] (shared
+    by the heads), before RoPE: q <- RoPE(RMSNorm_d(q; q_norm)), same for k.
+  * positions (document-aware RoPE, App. A step 23): cfg["positions"] [T]
+    gives each token's RoPE position (e.g. its offset inside its document in
+    a packed row); absent, a token's position is its index in its batch row.
+    Attention stays causal over the whole batch row.
+  * branch_scale (MiniCPM's muP scale_depth / sqrt(n_layers)): both residual
+    branches are multiplied by it, h1 = x + s Attn, out = h1 + s FFN.
+
 Shapes: x is [T, h] with T = batch * seq, batch-row major.
 """
 from __future__ import annotations
@@ -56,33 +67,36 @@ def rmsnorm_bwd(x, g, r, dy):
 # RoPE
 # --------------------------------------------------------------------------
 
-def rope_angles(seq, head_dim, base):
-    """phi[s, i] = s * base^(-2i/d) for s < seq, i < d/2 (fp64)."""
+def rope_angles(seq, head_dim, base, pos=None):
+    """phi[s, i] = pos_s * base^(-2i/d) for i < d/2 (fp64); pos defaults to
+    0 .. seq-1."""
     i = np.arange(head_dim // 2, dtype=np.float64)
     inv_freq = base ** (-2.0 * i / head_dim)
-    return np.arange(seq, dtype=np.float64)[:, None] * inv_freq[None, :]
+    p = np.arange(seq, dtype=np.float64) if pos is None else np.asarray(pos, np.float64)
+    return p[:, None] * inv_freq[None, :]
 
 
-def _positions(batch, seq):
-    return np.tile(np.arange(seq), batch)
+def _positions(batch, seq, pos=None):
+    return np.tile(np.arange(seq), batch) if pos is None else np.asarray(pos)
 
 
-def rope_fwd(x, batch, seq, base):
+def rope_fwd(x, batch, seq, base, pos=None):
     """Rotate each head of x [T, n, d] by its token's angles (rotate-half).
 
     y_i = x_i cos - x_{i+d/2} sin,  y_{i+d/2} = x_{i+d/2} cos + x_i sin.
+    pos [T]: the tokens' positions (default: index within the batch row).
     """
     d = x.shape[-1]
-    phi = rope_angles(seq, d, base)[_positions(batch, seq)]      # [T, d/2]
+    phi = rope_angles(0, d, base, _positions(batch, seq, pos))      # [T, d/2]
     c, s = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
     x1, x2 = x[..., : d // 2], x[..., d // 2:]
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
-def rope_bwd(dy, batch, seq, base):
+def rope_bwd(dy, batch, seq, base, pos=None):
     """Transpose of the rotation (rotation by -phi)."""
     d = dy.shape[-1]
-    phi = rope_angles(seq, d, base)[_positions(batch, seq)]
+    phi = rope_angles(0, d, base, _positions(batch, seq, pos))
     c, s = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
     d1, d2 = dy[..., : d // 2], dy[..., d // 2:]
     return np.concatenate([d1 * c + d2 * s, d2 * c - d1 * s], axis=-1)
@@ -220,22 +234,42 @@ def _dims(cfg):
         cfg["n_heads"] * d, cfg["n_kv_heads"] * d
 
 
+def head_rmsnorm_fwd(x, g, eps):
+    """RMSNorm of every head vector x [T, n, d] over d with gain g [d]."""
+    T, n, d = x.shape
+    y, r = rmsnorm_fwd(x.reshape(T * n, d), g, eps)
+    return y.reshape(T, n, d), r.reshape(T, n)
+
+
+def head_rmsnorm_bwd(x, g, r, dy):
+    T, n, d = x.shape
+    dx, dg = rmsnorm_bwd(x.reshape(T * n, d), g, r.reshape(T * n), dy.reshape(T * n, d))
+    return dx.reshape(T, n, d), dg
+
+
 def attention_block_fwd(x, W, cfg):
-    """a = RMSNorm(x; g1); qkv = a W_qkv^T; RoPE; attention; h1 = x + o W_o^T."""
+    """a = RMSNorm(x; g1); qkv = a W_qkv^T; [QK-Norm]; RoPE; attention;
+    h1 = x + s o W_o^T (s = branch_scale, 1 unless set)."""
     h, nh, nkv, d, hq, hkv = _dims(cfg)
     B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    pos = cfg.get("positions")
+    bs = cfg.get("branch_scale", 1.0) or 1.0
     T = x.shape[0]
     a, r1 = rmsnorm_fwd(x, W["attn_norm"], cfg["rms_eps"])
     qkv = a @ W["w_qkv"].T
     q = qkv[:, :hq].reshape(T, nh, d)
     k = qkv[:, hq:hq + hkv].reshape(T, nkv, d)
     v = qkv[:, hq + hkv:].reshape(T, nkv, d)
-    qr = rope_fwd(q, B, S, base)
-    kr = rope_fwd(k, B, S, base)
+    cache = dict(x=x, a=a, r1=r1, v=v, q_raw=q, k_raw=k)
+    if cfg.get("qk_norm"):
+        q, cache["rq"] = head_rmsnorm_fwd(q, W["q_norm"], cfg["rms_eps"])
+        k, cache["rk"] = head_rmsnorm_fwd(k, W["k_norm"], cfg["rms_eps"])
+    qr = rope_fwd(q, B, S, base, pos)
+    kr = rope_fwd(k, B, S, base, pos)
     o, lse = attention_fwd(qr, kr, v, B, S)
     o = o.reshape(T, hq)
-    h1 = x + o @ W["w_o"].T
-    cache = dict(x=x, a=a, r1=r1, qr=qr, kr=kr, v=v, o=o, lse=lse)
+    h1 = x + bs * (o @ W["w_o"].T)
+    cache.update(qr=qr, kr=kr, o=o, lse=lse)
     return h1, cache
 
 
@@ -243,14 +277,20 @@ def attention_block_bwd(c, W, cfg, dh1):
     """Backward of attention_block_fwd; dh1 flows through the residual."""
     h, nh, nkv, d, hq, hkv = _dims(cfg)
     B, S, base = cfg["batch"], cfg["seq"], cfg["rope_base"]
+    pos = cfg.get("positions")
+    bs = cfg.get("branch_scale", 1.0) or 1.0
     T = dh1.shape[0]
     g = {}
-    g["w_o"] = dh1.T @ c["o"]
-    do = (dh1 @ W["w_o"]).reshape(T, nh, d)
+    db = bs * dh1
+    g["w_o"] = db.T @ c["o"]
+    do = (db @ W["w_o"]).reshape(T, nh, d)
     dqr, dkr, dv = attention_bwd(c["qr"], c["kr"], c["v"], do, B, S)
-    dq = rope_bwd(dqr, B, S, base).reshape(T, hq)
-    dk = rope_bwd(dkr, B, S, base).reshape(T, hkv)
-    dqkv = np.concatenate([dq, dk, dv.reshape(T, hkv)], axis=1)
+    dq = rope_bwd(dqr, B, S, base, pos)
+    dk = rope_bwd(dkr, B, S, base, pos)
+    if cfg.get("qk_norm"):
+        dq, g["q_norm"] = head_rmsnorm_bwd(c["q_raw"], W["q_norm"], c["rq"], dq)
+        dk, g["k_norm"] = head_rmsnorm_bwd(c["k_raw"], W["k_norm"], c["rk"], dk)
+    dqkv = np.concatenate([dq.reshape(T, hq), dk.reshape(T, hkv), dv.reshape(T, hkv)], axis=1)
     g["w_qkv"] = dqkv.T @ c["a"]
     da = dqkv @ W["w_qkv"]
     dxn, g["attn_norm"] = rmsnorm_bwd(c["x"], W["attn_norm"], c["r1"], da)
@@ -258,20 +298,23 @@ def attention_block_bwd(c, W, cfg, dh1):
 
 
 def ffn_fwd(h1, W, cfg):
-    """b = RMSNorm(h1; g2); [G|U] = b W_gu^T; out = h1 + (silu(G) U) W_d^T."""
+    """b = RMSNorm(h1; g2); [G|U] = b W_gu^T; out = h1 + s (silu(G) U) W_d^T."""
     f = cfg["ffn"]
+    bs = cfg.get("branch_scale", 1.0) or 1.0
     b, r2 = rmsnorm_fwd(h1, W["ffn_norm"], cfg["rms_eps"])
     gu = b @ W["w_gate_up"].T
     G, U = gu[:, :f], gu[:, f:]
     A = swiglu_fwd(G, U)
-    out = h1 + A @ W["w_down"].T
+    out = h1 + bs * (A @ W["w_down"].T)
     return out, dict(h1=h1, b=b, r2=r2, G=G, U=U, A=A)
 
 
 def ffn_bwd(c, W, cfg, dout):
+    bs = cfg.get("branch_scale", 1.0) or 1.0
     g = {}
-    g["w_down"] = dout.T @ c["A"]
-    dA = dout @ W["w_down"]
+    dy = bs * dout
+    g["w_down"] = dy.T @ c["A"]
+    dA = dy @ W["w_down"]
     dG, dU = swiglu_bwd(c["G"], c["U"], dA)
     dgu = np.concatenate([dG, dU], axis=1)
     g["w_gate_up"] = dgu.T @ c["b"]

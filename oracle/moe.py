@@ -17,6 +17,12 @@ Readings where the paper is silent:
     then slot ascending; entries are flat (token * k + slot) indices.
   * Aux loss (Switch style): alpha * E * sum_e f_e P_e with f_e = count_e / (T k)
     (no gradient) and P_e = mean_t p_te.
+  * Shared expert (MiniCPM5 16B-A3B's 512-wide shared expert, App. B): with
+    cfg["shared_ffn"] = fs > 0, every token also goes through one SwiGLU FFN
+    of width fs (w_gate_up_s [2fs, h], w_down_s [h, fs]) with weight 1, added
+    to the routed experts' sum; the router does not see it.
+  * branch_scale (muP): the whole FFN branch (routed + shared) is multiplied
+    by it; the aux loss is not.
 """
 from __future__ import annotations
 
@@ -170,20 +176,40 @@ def moe_fwd_per_token(b, W, cfg):
     return y
 
 
+def shared_fwd(b, W, cfg):
+    """The shared expert on every token: (silu(b Wg^T) * (b Wu^T)) Wd^T."""
+    return expert_ffn(b, W["w_gate_up_s"], W["w_down_s"], cfg["shared_ffn"])
+
+
 def layer_fwd(x, W, cfg, idx=None):
-    """MoE decoder layer: attention block, then h1 + MoE(RMSNorm(h1)).
+    """MoE decoder layer: attention block, then h1 + s (MoE + shared)(RMSNorm(h1)).
 
     Returns (out, aux, cache). `idx` forces the choice of experts (see route).
     """
+    bs = cfg.get("branch_scale", 1.0) or 1.0
     h1, ca = attention_block_fwd(x, W, cfg)
     bn, r2 = rmsnorm_fwd(h1, W["ffn_norm"], cfg["rms_eps"])
     y, aux, cm = moe_fwd(bn, W, cfg, idx)
-    return h1 + y, aux, dict(attn=ca, moe=cm, h1=h1, r2=r2)
+    if cfg.get("shared_ffn", 0):
+        ys, cm["shared"] = shared_fwd(bn, W, cfg)
+        y = y + ys
+    return h1 + bs * y, aux, dict(attn=ca, moe=cm, h1=h1, r2=r2)
 
 
 def layer_bwd(cache, W, cfg, dout):
     """Backward of layer_fwd for the objective <out, dout> + aux."""
-    db, g = moe_bwd(cache["moe"], W, cfg, dout)
+    bs = cfg.get("branch_scale", 1.0) or 1.0
+    # <h1 + s y, dout> + aux: the branch sees s dout, the aux term is unscaled
+    db, g = moe_bwd(cache["moe"], W, cfg, bs * dout)
+    if cfg.get("shared_ffn", 0):
+        fs = cfg["shared_ffn"]
+        G, U, A = cache["moe"]["shared"]
+        dy = bs * dout
+        g["w_down_s"] = dy.T @ A
+        dG, dU = swiglu_bwd(G, U, dy @ W["w_down_s"])
+        dgu = np.concatenate([dG, dU], axis=1)
+        g["w_gate_up_s"] = dgu.T @ cache["moe"]["b"]
+        db = db + dgu @ W["w_gate_up_s"]
     dh1n, g["ffn_norm"] = rmsnorm_bwd(cache["h1"], W["ffn_norm"], cache["r2"], db)
     dx, ga = attention_block_bwd(cache["attn"], W, cfg, dout + dh1n)
     g.update(ga)
