@@ -96,6 +96,17 @@ const char* forge_version(void);
  * its row statistics; the backward re-runs the attention forward (a
  * recomputation policy, Sec. 3.3, "Surpass" stage).
  *
+ * Model variants of App. B (all off when zero):
+ *   qk_norm != 0: per-head QK-Norm (Qwen3): every q and k head vector is
+ *     RMS-normalised over head_dim (eps = rms_eps) with the gains q_norm /
+ *     k_norm [head_dim] before RoPE.
+ *   branch_scale: both residual branches are multiplied by it (MiniCPM's
+ *     muP scale_depth / sqrt(n_layers)): h1 = x + s Attn, out = h1 + s FFN;
+ *     0 means 1.
+ *   shared_ffn (MoE layers): width of an always-on shared SwiGLU expert
+ *     added to the routed experts' sum (MiniCPM5 16B-A3B's 512-wide shared
+ *     expert); a multiple of 8, 0 for none.
+ *
  * Supported: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
  * hidden, ffn, hq multiples of 8; seq >= 1; batch >= 1.
  */
@@ -105,6 +116,9 @@ typedef struct {
   int32_t n_experts, top_k, expert_ffn;
   float aux_coef;
   int32_t recompute_attn;
+  int32_t qk_norm;
+  float branch_scale;
+  int32_t shared_ffn;
 } forge_layer_cfg;
 
 /*
@@ -119,6 +133,13 @@ typedef struct {
  *   rope_cos, rope_sin [seq, head_dim/2] fp32 tables from forge_rope_table
  *   MoE only (unused when n_experts == 0):
  *   w_router [E, h], w_gate_up_e [E, 2fe, h], w_down_e [E, h, fe]
+ *   qk_norm only: q_norm [head_dim], k_norm [head_dim]
+ *   shared_ffn only: w_gate_up_s [2fs, h] (gate rows, then up rows), w_down_s [h, fs]
+ *   positions: device int32 [T], the RoPE position of every token (document-
+ *     aware RoPE, App. A step 23: e.g. each token's offset inside its
+ *     document of a packed row), in [0, seq) (values outside are clamped);
+ *     NULL: a token's position is its index in its batch row. Attention
+ *     stays causal over the whole batch row either way.
  */
 typedef struct {
   const forge_bf16* attn_norm;
@@ -132,6 +153,11 @@ typedef struct {
   const forge_bf16* w_router;
   const forge_bf16* w_gate_up_e;
   const forge_bf16* w_down_e;
+  const forge_bf16* q_norm;
+  const forge_bf16* k_norm;
+  const int32_t* positions;
+  const forge_bf16* w_gate_up_s;
+  const forge_bf16* w_down_s;
 } forge_layer_weights;
 
 /*
@@ -151,6 +177,10 @@ typedef struct {
   float* d_w_router;
   float* d_w_gate_up_e;
   float* d_w_down_e;
+  float* d_q_norm;
+  float* d_k_norm;
+  float* d_w_gate_up_s;
+  float* d_w_down_s;
   int32_t overwrite;
 } forge_layer_grads;
 
@@ -229,9 +259,12 @@ forge_status forge_layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weigh
 /* Output head: final RMSNorm + LM head + softmax cross-entropy            */
 /* ------------------------------------------------------------------------ */
 
+/* logit_scale: the logits are multiplied by it before the softmax (MiniCPM's
+ * muP: the final hidden state divided by hidden / dim_model_base); 0 means 1. */
 typedef struct {
   int32_t tokens, hidden, vocab;
   float rms_eps;
+  float logit_scale;
 } forge_head_cfg;
 
 /* Scratch bytes for forge_loss_fwd_bwd (holds the [T, V] bf16 logits). */
@@ -242,8 +275,9 @@ forge_status forge_loss_workspace_bytes(const forge_head_cfg* cfg, size_t* bytes
  * cross-entropy of App. A (framework-level trajectory) and App. G (fused
  * FP32 cross-entropy)):
  *   xn = RMSNorm(x_L; final_norm), z = xn w_lm^T (bf16 logits, [T, V]),
- *   loss = (1/T) sum_t (logsumexp(z_t) - z_t[targets_t]), softmax in fp32,
- *   then dz = (softmax(z) - onehot) / T and the gradients.
+ *   u = logit_scale z, loss = (1/T) sum_t (logsumexp(u_t) - u_t[targets_t]),
+ *   softmax in fp32, then dz = logit_scale (softmax(u) - onehot) / T and the
+ *   gradients.
  * x_L [T, h] bf16; final_norm [h] bf16; w_lm [V, h] bf16 (the embedding
  * matrix when the head is tied); targets [T] int32 in [0, V) (checked on the
  * device: an out-of-range target contributes nothing and sets loss to NaN).
@@ -283,17 +317,18 @@ forge_status forge_loss_fwd_bwd_chunked(const forge_head_cfg* cfg, int32_t chunk
 /* Embedding                                                                */
 /* ------------------------------------------------------------------------ */
 
-/* x0[t, :] = emb[ids[t], :]. ids [T] int32, emb [V, h] bf16, x0 [T, h] bf16.
- * An id outside [0, V) yields a zero row. */
+/* x0[t, :] = scale * emb[ids[t], :]. ids [T] int32, emb [V, h] bf16, x0
+ * [T, h] bf16; scale is MiniCPM's muP scale_emb (App. B), 1 for a plain
+ * copy (bit for bit). An id outside [0, V) yields a zero row. */
 forge_status forge_embed_fwd(const int32_t* ids, const forge_bf16* emb, forge_bf16* x0,
-                             int32_t tokens, int32_t hidden, int32_t vocab,
+                             int32_t tokens, int32_t hidden, int32_t vocab, float scale,
                              forge_stream stream);
 
-/* d_emb[ids[t], :] += dx0[t, :] (fp32 +=). Ids outside [0, V) are skipped.
- * Uses fp32 atomics: the summation order over repeated ids varies between
- * runs (not bit-deterministic). */
+/* d_emb[ids[t], :] += scale * dx0[t, :] (fp32 +=). Ids outside [0, V) are
+ * skipped. Uses fp32 atomics: the summation order over repeated ids varies
+ * between runs (not bit-deterministic). */
 forge_status forge_embed_bwd(const int32_t* ids, const forge_bf16* dx0, float* d_emb,
-                             int32_t tokens, int32_t hidden, int32_t vocab,
+                             int32_t tokens, int32_t hidden, int32_t vocab, float scale,
                              forge_stream stream);
 
 /* ------------------------------------------------------------------------ */
@@ -365,6 +400,7 @@ typedef struct {
 typedef struct {
   forge_adamw_tensor attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
   forge_adamw_tensor w_router, w_gate_up_e, w_down_e;
+  forge_adamw_tensor q_norm, k_norm, w_gate_up_s, w_down_s;
 } forge_layer_optim;
 
 /*

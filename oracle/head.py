@@ -81,13 +81,14 @@ def layer_cfg(cfg, i):
     return cfg
 
 
-def model_fwd_bwd(P, ids, targets, cfg):
+def model_fwd_bwd(P, ids, targets, cfg, route_idx=None):
     """Whole model: embedding, layers, final norm, head, CE; then backward.
 
     P holds 'embedding' [V, h], 'layers' (list of weight dicts),
     'final_norm' [h] and 'w_lm' [V, h] (None when tied). Returns
     (loss, grads) with grads mirroring P. For MoE layers the loss includes
-    the per-layer aux losses.
+    the per-layer aux losses. route_idx: optional {layer index: [T, k]
+    experts} forcing those layers' choice of experts (see moe.route).
     """
     V = cfg["vocab"]
     tied = P["w_lm"] is None
@@ -99,7 +100,7 @@ def model_fwd_bwd(P, ids, targets, cfg):
     for i, W in enumerate(P["layers"]):
         lc = layer_cfg(cfg, i)
         if lc["n_experts"]:
-            x, aux, c = moe.layer_fwd(x, W, lc)
+            x, aux, c = moe.layer_fwd(x, W, lc, (route_idx or {}).get(i))
             aux_total += aux
         else:
             x, c = dense.layer_fwd(x, W, lc)

@@ -45,25 +45,29 @@ class LayerCfg(ctypes.Structure):
         ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
         ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
         ("expert_ffn", ctypes.c_int32), ("aux_coef", ctypes.c_float),
-        ("recompute_attn", ctypes.c_int32)]
+        ("recompute_attn", ctypes.c_int32), ("qk_norm", ctypes.c_int32),
+        ("branch_scale", ctypes.c_float), ("shared_ffn", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down",
-                 "rope_cos", "rope_sin", "w_router", "w_gate_up_e", "w_down_e")]
+                 "rope_cos", "rope_sin", "w_router", "w_gate_up_e", "w_down_e",
+                 "q_norm", "k_norm", "positions", "w_gate_up_s", "w_down_s")]
 
 
 class LayerGrads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("d_attn_norm", "d_w_qkv", "d_w_o", "d_ffn_norm", "d_w_gate_up",
-                 "d_w_down", "d_w_router", "d_w_gate_up_e", "d_w_down_e")] + \
+                 "d_w_down", "d_w_router", "d_w_gate_up_e", "d_w_down_e", "d_q_norm",
+                 "d_k_norm", "d_w_gate_up_s", "d_w_down_s")] + \
         [("overwrite", ctypes.c_int32)]
 
 
 class HeadCfg(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_int32), ("hidden", ctypes.c_int32),
-                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("logit_scale", ctypes.c_float)]
 
 
 class AdamwHparams(ctypes.Structure):
@@ -78,7 +82,8 @@ class AdamwTensor(ctypes.Structure):
 class LayerOptim(ctypes.Structure):
     _fields_ = [(n, AdamwTensor) for n in
                 ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down",
-                 "w_router", "w_gate_up_e", "w_down_e")]
+                 "w_router", "w_gate_up_e", "w_down_e", "q_norm", "k_norm", "w_gate_up_s",
+                 "w_down_s")]
 
 
 class AttnCfg(ctypes.Structure):
@@ -121,8 +126,8 @@ def load():
                                                       P, P, P, P, P, P]),
         "forge_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(HeadCfg), P, P, P, P, P, P,
                                               P, P, P, P]),
-        "forge_embed_fwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
-        "forge_embed_bwd": (ctypes.c_int, [P, P, P, I32, I32, I32, P]),
+        "forge_embed_fwd": (ctypes.c_int, [P, P, P, I32, I32, I32, F32, P]),
+        "forge_embed_bwd": (ctypes.c_int, [P, P, P, I32, I32, I32, F32, P]),
         "forge_adamw_step": (ctypes.c_int, [P, P, P, P, P, I64,
                                             ctypes.POINTER(AdamwHparams), P, P]),
         "forge_layer_bwd_adamw": (ctypes.c_int, [ctypes.POINTER(LayerCfg),
@@ -193,7 +198,8 @@ def layer_cfg(c: dict) -> LayerCfg:
     return LayerCfg(c["batch"], c["seq"], c["hidden"], c["n_heads"], c["n_kv_heads"],
                     c["head_dim"], c.get("ffn", 0), c["rope_base"], c["rms_eps"],
                     c.get("n_experts", 0), c.get("top_k", 0), c.get("expert_ffn", 0),
-                    c.get("aux_coef", 0.0), c.get("recompute_attn", 0))
+                    c.get("aux_coef", 0.0), c.get("recompute_attn", 0), c.get("qk_norm", 0),
+                    c.get("branch_scale", 0.0), c.get("shared_ffn", 0))
 
 
 def layer_weights(w: dict) -> LayerWeights:
@@ -290,14 +296,14 @@ def forge_loss_fwd_bwd_chunked(cfg, chunk, x_L, final_norm, w_lm, targets, loss_
                                              _ptr(d_w_lm), _ptr(workspace), _stream(stream)))
 
 
-def forge_embed_fwd(ids, emb, x0, tokens, hidden, vocab, stream=None):
+def forge_embed_fwd(ids, emb, x0, tokens, hidden, vocab, scale=1.0, stream=None):
     _check(load().forge_embed_fwd(_ptr(ids), _ptr(emb), _ptr(x0), tokens, hidden, vocab,
-                                  _stream(stream)))
+                                  float(scale), _stream(stream)))
 
 
-def forge_embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, stream=None):
+def forge_embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, scale=1.0, stream=None):
     _check(load().forge_embed_bwd(_ptr(ids), _ptr(dx0), _ptr(d_emb), tokens, hidden, vocab,
-                                  _stream(stream)))
+                                  float(scale), _stream(stream)))
 
 
 def forge_adamw_step(master, param, grad, m, v, n, hparams: AdamwHparams, dev_scalars,

@@ -183,10 +183,16 @@ __global__ void rope_table_k(int seq, int d, double base, float* cos_t, float* s
   sin_t[id] = (float)sin(ang);
 }
 
+// RoPE position of token t: pos[t] (document-aware RoPE, App. A step 23;
+// clamped to the table's seq rows) or, without pos, its index in its row.
+__device__ __forceinline__ int rope_pos(const int32_t* pos, long t, int seq) {
+  return pos ? min(max(pos[t], 0), seq - 1) : (int)(t % seq);
+}
+
 // One thread per (token, head, 8-pair chunk), in place.
 __global__ void rope_apply_k(bf16_t* __restrict__ qkv, long ld, const float* __restrict__ cos_t,
-                             const float* __restrict__ sin_t, int T, int seq, int nrot, int d,
-                             int inverse) {
+                             const float* __restrict__ sin_t, const int32_t* __restrict__ pos,
+                             int T, int seq, int nrot, int d, int inverse) {
   const int half = d / 2, cpr = half / 8;  // chunks per head
   const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= (long)T * nrot * cpr) return;
@@ -194,7 +200,7 @@ __global__ void rope_apply_k(bf16_t* __restrict__ qkv, long ld, const float* __r
   const long th = id / cpr;
   const int hd = (int)(th % nrot);
   const long t = th / nrot;
-  const int s = (int)(t % seq);
+  const int s = rope_pos(pos, t, seq);
   bf16_t* base = qkv + t * ld + (long)hd * d + c * 8;
   uint4* p1 = reinterpret_cast<uint4*>(base);
   uint4* p2 = reinterpret_cast<uint4*>(base + half);
@@ -218,6 +224,134 @@ __global__ void rope_apply_k(bf16_t* __restrict__ qkv, long ld, const float* __r
   }
   *p1 = pack8(y1);
   *p2 = pack8(y2);
+}
+
+// ------------------------------------------------------ QK-Norm + RoPE ----
+// Per-head RMSNorm of q and k over head_dim (gains gq / gk [d], shared by the
+// heads; Qwen3's QK-Norm, App. B), then RoPE, in place on the qkv buffer.
+// d / 8 lanes hold one (token, head) row, eight elements each; the row's sum
+// of squares and the rotate-half partner (d / 16 lanes away) stay inside the
+// wave. The forward keeps the un-normalised rows (raw [T, nrot * d]) and
+// their rstd [T, nrot] for the backward.
+template <int D>
+__global__ __launch_bounds__(256) void qknorm_rope_fwd_k(
+    bf16_t* __restrict__ qkv, long ld, bf16_t* __restrict__ raw, float* __restrict__ rstd,
+    const bf16_t* __restrict__ gq, const bf16_t* __restrict__ gk,
+    const float* __restrict__ cos_t, const float* __restrict__ sin_t,
+    const int32_t* __restrict__ pos, int T, int seq, int nh, int nkv, float eps) {
+  constexpr int LPR = D / 8, HALF = LPR / 2;
+  const int nrot = nh + nkv;
+  const long row = ((long)blockIdx.x * blockDim.x + threadIdx.x) / LPR;
+  const int c = threadIdx.x % LPR;
+  const bool ok = row < (long)T * nrot;
+  const long t = ok ? row / nrot : 0;
+  const int hd = ok ? (int)(row % nrot) : 0;
+  bf16_t* xr = qkv + t * ld + (long)hd * D + c * 8;
+  float x[8];
+  uint4 xv = ok ? *reinterpret_cast<const uint4*>(xr) : make_uint4(0, 0, 0, 0);
+  unpack8(xv, x);
+  float ss = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += x[e] * x[e];
+#pragma unroll
+  for (int o = LPR / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  const float r = 1.0f / sqrtf(ss / (float)D + eps);
+  float g[8], y[8], yp[8];
+  unpack8(*reinterpret_cast<const uint4*>((hd < nh ? gq : gk) + c * 8), g);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) y[e] = x[e] * r * g[e];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) yp[e] = __shfl_xor(y[e], HALF, 64);
+  const int s = rope_pos(pos, t, seq);
+  const float* cp = cos_t + (long)s * (D / 2) + (c % HALF) * 8;
+  const float* sp = sin_t + (long)s * (D / 2) + (c % HALF) * 8;
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    o[e] = c < HALF ? y[e] * cp[e] - yp[e] * sp[e] : y[e] * cp[e] + yp[e] * sp[e];
+  if (ok) {
+    *reinterpret_cast<uint4*>(xr) = pack8(o);
+    *reinterpret_cast<uint4*>(raw + (t * nrot + hd) * D + c * 8) = xv;
+    if (c == 0) rstd[t * nrot + hd] = r;
+  }
+}
+
+// Backward in place on the gradient rows: inverse rotation, then the RMSNorm
+// backward dx = r (g dn) - x r^3 sum(g dn x) / d; the gain gradients
+// sum_rows dn x r go to per-block partials [2][nblk][d] (q heads, then k
+// heads), each block summing a fixed set of rows in a fixed order.
+constexpr int kQkBlocks = 256;
+template <int D>
+__global__ __launch_bounds__(256) void qknorm_rope_bwd_k(
+    bf16_t* __restrict__ dqkv, long ld, const bf16_t* __restrict__ raw,
+    const float* __restrict__ rstd, const bf16_t* __restrict__ gq,
+    const bf16_t* __restrict__ gk, const float* __restrict__ cos_t,
+    const float* __restrict__ sin_t, const int32_t* __restrict__ pos, int T, int seq, int nh,
+    int nkv, float* __restrict__ dg_partial) {
+  constexpr int LPR = D / 8, HALF = LPR / 2, RPB = 256 / LPR;
+  __shared__ float red[4][2][D];
+  const int nrot = nh + nkv;
+  const long nrows = (long)T * nrot;
+  const int c = threadIdx.x % LPR;
+  float accq[8], acck[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) accq[e] = acck[e] = 0.0f;
+  for (long row0 = (long)blockIdx.x * RPB; row0 < nrows; row0 += (long)gridDim.x * RPB) {
+    const long row = row0 + threadIdx.x / LPR;
+    const bool ok = row < nrows;
+    const long t = ok ? row / nrot : 0;
+    const int hd = ok ? (int)(row % nrot) : 0;
+    bf16_t* dr = dqkv + t * ld + (long)hd * D + c * 8;
+    float dy[8], dp[8], x[8], g[8], dn[8];
+    unpack8(ok ? *reinterpret_cast<const uint4*>(dr) : make_uint4(0, 0, 0, 0), dy);
+    unpack8(ok ? *reinterpret_cast<const uint4*>(raw + row * D + c * 8) : make_uint4(0, 0, 0, 0), x);
+    unpack8(*reinterpret_cast<const uint4*>((hd < nh ? gq : gk) + c * 8), g);
+    const float r = ok ? rstd[row] : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dp[e] = __shfl_xor(dy[e], HALF, 64);
+    const int s = rope_pos(pos, t, seq);
+    const float* cp = cos_t + (long)s * (D / 2) + (c % HALF) * 8;
+    const float* sp = sin_t + (long)s * (D / 2) + (c % HALF) * 8;
+    float proj = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      dn[e] = c < HALF ? dy[e] * cp[e] + dp[e] * sp[e] : dy[e] * cp[e] - dp[e] * sp[e];
+      proj += dn[e] * g[e] * x[e];
+    }
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) proj += __shfl_xor(proj, o, 64);
+    const float k3 = r * r * r * proj / (float)D;
+    float dx[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      dx[e] = r * (dn[e] * g[e]) - x[e] * k3;
+      const float dg = dn[e] * x[e] * r;
+      if (hd < nh) accq[e] += dg;
+      else acck[e] += dg;
+    }
+    if (ok) *reinterpret_cast<uint4*>(dr) = pack8(dx);
+  }
+  // lanes of one chunk c: fold within the wave, then the four waves in order
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      accq[e] += __shfl_xor(accq[e], o, 64);
+      acck[e] += __shfl_xor(acck[e], o, 64);
+    }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane < LPR)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      red[wave][0][c * 8 + e] = accq[e];
+      red[wave][1][c * 8 + e] = acck[e];
+    }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 2 * D; i += blockDim.x) {
+    const int which = i / D, col = i % D;
+    dg_partial[((long)which * gridDim.x + blockIdx.x) * D + col] =
+        (red[0][which][col] + red[1][which][col]) + (red[2][which][col] + red[3][which][col]);
+  }
 }
 
 // -------------------------------------------------------------- SwiGLU ----
@@ -267,8 +401,9 @@ __global__ void swiglu_bwd_k(const bf16_t* __restrict__ gu, const bf16_t* __rest
 }
 
 // ----------------------------------------------------------- embedding ----
+// x0 = scale * E[id] (scale: muP's scale_emb; 1 copies the row bit for bit)
 __global__ void embed_fwd_k(const int32_t* __restrict__ ids, const bf16_t* __restrict__ emb,
-                            bf16_t* __restrict__ x, int T, int h, int V) {
+                            bf16_t* __restrict__ x, int T, int h, int V, float scale) {
   const int cpr = h / 8;
   const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= (long)T * cpr) return;
@@ -277,11 +412,18 @@ __global__ void embed_fwd_k(const int32_t* __restrict__ ids, const bf16_t* __res
   const int v = ids[t];
   uint4 val = make_uint4(0, 0, 0, 0);
   if (v >= 0 && v < V) val = *reinterpret_cast<const uint4*>(emb + (long)v * h + c * 8);
+  if (scale != 1.0f) {
+    float f[8];
+    unpack8(val, f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] *= scale;
+    val = pack8(f);
+  }
   *reinterpret_cast<uint4*>(x + t * h + c * 8) = val;
 }
 
 __global__ void embed_bwd_k(const int32_t* __restrict__ ids, const bf16_t* __restrict__ dx,
-                            float* __restrict__ demb, int T, int h, int V) {
+                            float* __restrict__ demb, int T, int h, int V, float scale) {
   const int cpr = h / 8;
   const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= (long)T * cpr) return;
@@ -293,12 +435,13 @@ __global__ void embed_bwd_k(const int32_t* __restrict__ ids, const bf16_t* __res
   unpack8(*reinterpret_cast<const uint4*>(dx + t * h + c * 8), f);
   float* dst = demb + (long)v * h + c * 8;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) unsafeAtomicAdd(dst + e, f[e]);
+  for (int e = 0; e < 8; ++e) unsafeAtomicAdd(dst + e, f[e] * scale);
 }
 
 // ------------------------------------------------------- cross-entropy ----
-// One block per row: online max / sum-exp in fp32 over bf16 logits, then
-// dz = (exp(z - lse) - [j == y]) * inv_T written over the logits.
+// One block per row: online max / sum-exp in fp32 over the scaled logits
+// u = scale * z (scale: muP's dim_model_base / hidden, 1 otherwise), then
+// dz = scale * (exp(u - lse) - [j == y]) * inv_T written over the logits.
 __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
   const float mn = fmaxf(m, m2);
   if (mn == -INFINITY) return;
@@ -308,7 +451,8 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
 
 __global__ __launch_bounds__(256) void ce_k(bf16_t* __restrict__ z,
                                             const int32_t* __restrict__ targets,
-                                            float* __restrict__ row_loss, int V, float inv_T) {
+                                            float* __restrict__ row_loss, int V, float inv_T,
+                                            float scale) {
   __shared__ float sm[4], ss[4];
   const long row = blockIdx.x;
   bf16_t* zr = z + row * V;
@@ -318,6 +462,8 @@ __global__ __launch_bounds__(256) void ce_k(bf16_t* __restrict__ z,
   for (int c = threadIdx.x; c < nch; c += blockDim.x) {
     float f[8];
     unpack8(*reinterpret_cast<const uint4*>(zr + c * 8), f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] *= scale;
     float cm = f[0];
 #pragma unroll
     for (int e = 1; e < 8; ++e) cm = fmaxf(cm, f[e]);
@@ -326,7 +472,8 @@ __global__ __launch_bounds__(256) void ce_k(bf16_t* __restrict__ z,
     for (int e = 0; e < 8; ++e) cs += __expf(f[e] - cm);
     lse_merge(m, s, cm, cs);
   }
-  for (int j = nch * 8 + threadIdx.x; j < V; j += blockDim.x) lse_merge(m, s, bf2f(zr[j]), 1.0f);
+  for (int j = nch * 8 + threadIdx.x; j < V; j += blockDim.x)
+    lse_merge(m, s, bf2f(zr[j]) * scale, 1.0f);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(s, o, 64);
@@ -340,20 +487,21 @@ __global__ __launch_bounds__(256) void ce_k(bf16_t* __restrict__ z,
   const float lse = m + __logf(s);
   const int y = targets[row];
   const bool ok = (y >= 0 && y < V);
-  if (threadIdx.x == 0) row_loss[row] = ok ? lse - bf2f(zr[y]) : __builtin_nanf("");
+  if (threadIdx.x == 0) row_loss[row] = ok ? lse - bf2f(zr[y]) * scale : __builtin_nanf("");
   __syncthreads();  // z[y] read before it is overwritten
+  const float gs = inv_T * scale;
   for (int c = threadIdx.x; c < nch; c += blockDim.x) {
     float f[8];
     unpack8(*reinterpret_cast<const uint4*>(zr + c * 8), f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int j = c * 8 + e;
-      f[e] = (__expf(f[e] - lse) - (j == y ? 1.0f : 0.0f)) * inv_T;
+      f[e] = (__expf(f[e] * scale - lse) - (j == y ? 1.0f : 0.0f)) * gs;
     }
     *reinterpret_cast<uint4*>(zr + c * 8) = pack8(f);
   }
   for (int j = nch * 8 + threadIdx.x; j < V; j += blockDim.x)
-    zr[j] = f2bf((__expf(bf2f(zr[j]) - lse) - (j == y ? 1.0f : 0.0f)) * inv_T);
+    zr[j] = f2bf((__expf(bf2f(zr[j]) * scale - lse) - (j == y ? 1.0f : 0.0f)) * gs);
 }
 
 // out = scale * sum(v), one block, fixed order.
@@ -538,12 +686,50 @@ hipError_t rope_table(int seq, int d, float base, float* cos_t, float* sin_t, hi
   return hipGetLastError();
 }
 
-hipError_t rope_apply(uint16_t* qkv, long ld, const float* cos_t, const float* sin_t, int T,
-                      int seq, int nrot, int d, bool inverse, hipStream_t s) {
+hipError_t rope_apply(uint16_t* qkv, long ld, const float* cos_t, const float* sin_t,
+                      const int32_t* pos, int T, int seq, int nrot, int d, bool inverse,
+                      hipStream_t s) {
   const long n = (long)T * nrot * (d / 16);
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(rope_apply_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, qkv, ld, cos_t,
-                     sin_t, T, seq, nrot, d, inverse ? 1 : 0);
+                     sin_t, pos, T, seq, nrot, d, inverse ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t qknorm_rope_fwd(uint16_t* qkv, long ld, uint16_t* raw, float* rstd, const uint16_t* gq,
+                           const uint16_t* gk, const float* cos_t, const float* sin_t,
+                           const int32_t* pos, int T, int seq, int nh, int nkv, int d, float eps,
+                           hipStream_t s) {
+  const long n = (long)T * (nh + nkv) * (d / 8);
+  if (n == 0) return hipSuccess;
+  if (d == 128)
+    hipLaunchKernelGGL(qknorm_rope_fwd_k<128>, dim3(blocks_for(n, 256)), dim3(256), 0, s, qkv, ld,
+                       raw, rstd, gq, gk, cos_t, sin_t, pos, T, seq, nh, nkv, eps);
+  else if (d == 64)
+    hipLaunchKernelGGL(qknorm_rope_fwd_k<64>, dim3(blocks_for(n, 256)), dim3(256), 0, s, qkv, ld,
+                       raw, rstd, gq, gk, cos_t, sin_t, pos, T, seq, nh, nkv, eps);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+int qknorm_bwd_blocks(int T, int nrot, int d) {
+  const long rows = (long)T * nrot, rpb = 256 / (d / 8);
+  const long b = (rows + rpb - 1) / rpb;
+  return (int)(b < kQkBlocks ? b : kQkBlocks);
+}
+
+hipError_t qknorm_rope_bwd(uint16_t* dqkv, long ld, const uint16_t* raw, const float* rstd,
+                           const uint16_t* gq, const uint16_t* gk, const float* cos_t,
+                           const float* sin_t, const int32_t* pos, int T, int seq, int nh, int nkv,
+                           int d, float* dg_partial, hipStream_t s) {
+  const int nb = qknorm_bwd_blocks(T, nh + nkv, d);
+  if (d == 128)
+    hipLaunchKernelGGL(qknorm_rope_bwd_k<128>, dim3(nb), dim3(256), 0, s, dqkv, ld, raw, rstd, gq,
+                       gk, cos_t, sin_t, pos, T, seq, nh, nkv, dg_partial);
+  else if (d == 64)
+    hipLaunchKernelGGL(qknorm_rope_bwd_k<64>, dim3(nb), dim3(256), 0, s, dqkv, ld, raw, rstd, gq,
+                       gk, cos_t, sin_t, pos, T, seq, nh, nkv, dg_partial);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -563,25 +749,27 @@ hipError_t swiglu_bwd(const uint16_t* gu, const uint16_t* da, uint16_t* dgu, int
 }
 
 hipError_t embed_fwd(const int32_t* ids, const uint16_t* emb, uint16_t* x, int T, int h, int V,
-                     hipStream_t s) {
+                     float scale, hipStream_t s) {
   const long n = (long)T * (h / 8);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_fwd_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, emb, x, T, h, V);
+  hipLaunchKernelGGL(embed_fwd_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, emb, x, T, h, V,
+                     scale);
   return hipGetLastError();
 }
 
 hipError_t embed_bwd(const int32_t* ids, const uint16_t* dx, float* demb, int T, int h, int V,
-                     hipStream_t s) {
+                     float scale, hipStream_t s) {
   const long n = (long)T * (h / 8);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_bwd_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, dx, demb, T, h, V);
+  hipLaunchKernelGGL(embed_bwd_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, dx, demb, T, h, V,
+                     scale);
   return hipGetLastError();
 }
 
 hipError_t ce_fwd_bwd(uint16_t* z, const int32_t* targets, float* row_loss, int T, int V,
-                      float inv_T, hipStream_t s) {
+                      float inv_T, float scale, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ce_k, dim3(T), dim3(256), 0, s, z, targets, row_loss, V, inv_T);
+  hipLaunchKernelGGL(ce_k, dim3(T), dim3(256), 0, s, z, targets, row_loss, V, inv_T, scale);
   return hipGetLastError();
 }
 

@@ -62,6 +62,9 @@ size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Dims {
   long T, h, hq, hkv, qkv, f, nh, nkv, d, B, S;
   long E, k, fe, R;  // MoE: experts, top-k, expert FFN width, routed rows T*k
+  long fs;           // MoE: shared expert width (0: none)
+  bool qkn;          // QK-Norm
+  float bs;          // residual-branch scale (1 unless set)
 };
 
 Dims dims(const forge_layer_cfg& c) {
@@ -81,6 +84,9 @@ Dims dims(const forge_layer_cfg& c) {
   d.k = c.top_k;
   d.fe = c.expert_ffn;
   d.R = d.T * d.k;
+  d.fs = c.n_experts > 0 ? c.shared_ffn : 0;
+  d.qkn = c.qk_norm != 0;
+  d.bs = c.branch_scale == 0.0f ? 1.0f : c.branch_scale;
   return d;
 }
 
@@ -116,10 +122,16 @@ forge_status check_cfg(const forge_layer_cfg* c) {
   }
   FORGE_CHECK(c->rms_eps >= 0.0f && std::isfinite(c->rms_eps), FORGE_ERR_INVALID_ARG,
               "rms_eps must be finite and >= 0");
+  FORGE_CHECK(c->branch_scale >= 0.0f && std::isfinite(c->branch_scale), FORGE_ERR_INVALID_ARG,
+              "branch_scale must be finite and >= 0 (0 means 1)");
+  FORGE_CHECK(c->shared_ffn >= 0 && c->shared_ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "shared_ffn must be a non-negative multiple of 8 (got %d)", c->shared_ffn);
+  FORGE_CHECK(c->shared_ffn == 0 || c->n_experts > 0, FORGE_ERR_INVALID_ARG,
+              "shared_ffn needs a MoE layer (n_experts > 0)");
   FORGE_CHECK(c->rope_base > 0.0f && std::isfinite(c->rope_base), FORGE_ERR_INVALID_ARG,
               "rope_base must be finite and > 0");
   const Dims d = dims(*c);
-  const long widest = std::max(std::max(d.qkv, 2 * d.f), d.h);
+  const long widest = std::max(std::max(d.qkv, 2 * d.f), std::max(d.h, 2 * d.fs));
   FORGE_CHECK(d.T * widest < (1L << 31), FORGE_ERR_UNSUPPORTED,
               "a [T, width] activation exceeds 2^31 elements");
   FORGE_CHECK(d.E == 0 || d.R * std::max(2 * d.fe, d.h) < (1L << 31), FORGE_ERR_UNSUPPORTED,
@@ -134,6 +146,7 @@ forge_status check_cfg(const forge_layer_cfg* c) {
 struct Saved {
   size_t a, rstd1, qkv, o, lse, h1, rstd2, b, gu, act;
   size_t probs, idx, gates, counts, offsets, perm, pos_of, xs, ys;
+  size_t qk_raw, rstd_qk, gu_s, act_s;  // QK-Norm; shared expert
   size_t total;
 };
 
@@ -145,6 +158,10 @@ Saved saved_layout(const forge_layer_cfg& c) {
   s.a = take(d.T * d.h * 2);
   s.rstd1 = take(d.T * 4);
   s.qkv = take(d.T * d.qkv * 2);
+  if (d.qkn) {
+    s.qk_raw = take(d.T * (d.hq + d.hkv) * 2);
+    s.rstd_qk = take(d.T * (d.nh + d.nkv) * 4);
+  }
   const bool keep = c.recompute_attn == 0;
   s.o = keep ? take(d.T * d.hq * 2) : 0;
   s.lse = keep ? take(d.B * d.nh * d.S * 4) : 0;
@@ -166,6 +183,10 @@ Saved saved_layout(const forge_layer_cfg& c) {
     s.gu = take(d.R * 2 * d.fe * 2);
     s.act = take(d.R * d.fe * 2);
     s.ys = take(d.R * d.h * 2);
+    if (d.fs) {
+      s.gu_s = take(d.T * 2 * d.fs * 2);
+      s.act_s = take(d.T * d.fs * 2);
+    }
   }
   s.total = off;
   return s;
@@ -175,6 +196,7 @@ Saved saved_layout(const forge_layer_cfg& c) {
 struct Work {
   size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv;
   size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs, wpart;  // MoE
+  size_t qk_dg, h1s, dA_s, dgu_s, db1;  // QK-Norm; shared expert
   size_t total;
 };
 
@@ -199,7 +221,16 @@ Work work_layout(const forge_layer_cfg& c) {
     w.dbs = take(d.T * d.h * 2);
     const int rs = forge::splitk_splits((int)d.E, (int)d.h, (int)d.T);
     w.wpart = rs > 1 ? take((size_t)rs * d.E * d.h * 4) : 0;
+    if (d.fs) {
+      w.h1s = take(d.T * d.h * 2);
+      w.dA_s = take(d.T * d.fs * 2);
+      w.dgu_s = take(d.T * 2 * d.fs * 2);
+      w.db1 = take(d.T * d.h * 2);
+    }
   }
+  if (d.qkn)
+    w.qk_dg = take((size_t)2 * forge::qknorm_bwd_blocks((int)d.T, (int)(d.nh + d.nkv), (int)d.d) *
+                   d.d * 4);
   w.db = take(d.T * d.h * 2);
   w.dh1 = take(d.T * d.h * 2);
   w.dO = take(d.T * d.hq * 2);
@@ -240,6 +271,13 @@ GemmArgs gargs(const void* A, long lda, const void* B, long ldb, void* C, long l
   g.ldb = ldb;
   g.ldc = ldc;
   g.ldr = ldr;
+  return g;
+}
+
+// the same product with every epilogue value multiplied by alpha (a residual
+// branch's scale)
+GemmArgs scaled(GemmArgs g, float alpha) {
+  g.alpha = alpha;
   return g;
 }
 
@@ -287,6 +325,16 @@ forge_status check_weights(const forge_layer_cfg& c, const forge_layer_weights* 
     FORGE_PTR(w->w_gate_up_e);
     FORGE_PTR(w->w_down_e);
   }
+  if (c.qk_norm) {
+    FORGE_PTR(w->q_norm);
+    FORGE_PTR(w->k_norm);
+  }
+  if (c.n_experts > 0 && c.shared_ffn > 0) {
+    FORGE_PTR(w->w_gate_up_s);
+    FORGE_PTR(w->w_down_s);
+  }
+  FORGE_CHECK((reinterpret_cast<uintptr_t>(w->positions) & 3u) == 0, FORGE_ERR_ALIGNMENT,
+              "positions is not 4-byte aligned");
   return FORGE_OK;
 }
 
@@ -304,23 +352,38 @@ forge_status check_grads(const forge_layer_cfg& c, const forge_layer_grads* g) {
     FORGE_PTR(g->d_w_gate_up_e);
     FORGE_PTR(g->d_w_down_e);
   }
+  if (c.qk_norm) {
+    FORGE_PTR(g->d_q_norm);
+    FORGE_PTR(g->d_k_norm);
+  }
+  if (c.n_experts > 0 && c.shared_ffn > 0) {
+    FORGE_PTR(g->d_w_gate_up_s);
+    FORGE_PTR(g->d_w_down_s);
+  }
   return FORGE_OK;
 }
 
 // ---- attention block (shared by the dense and MoE layers) -----------------
-// a = RMSNorm(x), qkv = a W_qkv^T, RoPE, attention, h1 = x + O W_o^T.
+// a = RMSNorm(x), qkv = a W_qkv^T, [QK-Norm], RoPE, attention,
+// h1 = x + s O W_o^T (s: the branch scale).
 forge_status attn_block_fwd(const forge_layer_cfg& c, const Dims& d,
                             const forge_layer_weights* w, const uint16_t* x, uint16_t* a,
                             float* rstd1, uint16_t* qkv, uint16_t* o, float* lse, uint16_t* h1,
-                            hipStream_t s) {
+                            uint16_t* qk_raw, float* rstd_qk, hipStream_t s) {
   FORGE_HIP(forge::rmsnorm_fwd(x, w->attn_norm, a, rstd1, (int)d.T, (int)d.h, c.rms_eps, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
                         gargs(a, d.h, w->w_qkv, d.h, qkv, d.qkv, d.T, d.qkv, d.h), s));
-  FORGE_HIP(forge::rope_apply(qkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
-                              (int)(d.nh + d.nkv), (int)d.d, false, s));
+  if (d.qkn)
+    FORGE_HIP(forge::qknorm_rope_fwd(qkv, d.qkv, qk_raw, rstd_qk, w->q_norm, w->k_norm,
+                                     w->rope_cos, w->rope_sin, w->positions, (int)d.T, (int)d.S,
+                                     (int)d.nh, (int)d.nkv, (int)d.d, c.rms_eps, s));
+  else
+    FORGE_HIP(forge::rope_apply(qkv, d.qkv, w->rope_cos, w->rope_sin, w->positions, (int)d.T,
+                                (int)d.S, (int)(d.nh + d.nkv), (int)d.d, false, s));
   FORGE_HIP(forge::attn_fwd(attn_args(d, qkv), o, lse, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
-                        gargs(o, d.hq, w->w_o, d.hq, h1, d.h, d.T, d.h, d.hq, x, d.h), s));
+                        scaled(gargs(o, d.hq, w->w_o, d.hq, h1, d.h, d.T, d.h, d.hq, x, d.h), d.bs),
+                        s));
   return FORGE_OK;
 }
 
@@ -382,7 +445,7 @@ hipError_t link(hipStream_t from, hipStream_t to, hipEvent_t ev) {
 
 // Optimizer updates of forge_layer_bwd_adamw, issued on the lane's optimizer
 // stream behind everything enqueued so far on the caller's stream s and the
-// weight-gradient stream ws (events 6 onwards; 0..5 are the backward's); a
+// weight-gradient stream ws (events 7 onwards; 0..6 are the backward's); a
 // layer without a lane issues them in order on s.
 struct OptPlan {
   const forge_layer_optim* o;
@@ -445,6 +508,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                             const forge_layer_weights* w, const forge_layer_grads* g,
                             const uint16_t* x, const uint16_t* a, const float* rstd1,
                             const uint16_t* qkv, const uint16_t* o, const float* lse,
+                            const uint16_t* qk_raw, const float* rstd_qk,
                             const uint16_t* dh1, uint16_t* d_in, void* workspace, const Work& wk,
                             hipStream_t s, SideLane* side = nullptr, OptPlan* opt = nullptr,
                             hipEvent_t before_d_in = nullptr) {
@@ -461,16 +525,31 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   hipStream_t ws = side ? side->stream : s;
   if (side) FORGE_HIP(link(s, ws, side->ev[2]));
   FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                        gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), ws));
+                        scaled(gargs(dh1, d.h, o, d.hq, g->d_w_o, d.hq, d.h, d.hq, d.T), d.bs),
+                        ws));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                        gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), s));
+                        scaled(gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), d.bs), s));
   if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_o, g->d_w_o, d.h * d.hq));
   FORGE_HIP(forge::attn_bwd_dq(aa, o, dO, lse, delta, dqkv, d.qkv, s));
   FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
                                  at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
                                  d.qkv, s));
-  FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, (int)d.T, (int)d.S,
-                              (int)(d.nh + d.nkv), (int)d.d, true, s));
+  if (d.qkn) {
+    // inverse RoPE and the QK-Norm backward in place; gain gradients
+    float* qdg = at<float>(workspace, wk.qk_dg);
+    const int nq = forge::qknorm_bwd_blocks((int)d.T, (int)(d.nh + d.nkv), (int)d.d);
+    FORGE_HIP(forge::qknorm_rope_bwd(dqkv, d.qkv, qk_raw, rstd_qk, w->q_norm, w->k_norm,
+                                     w->rope_cos, w->rope_sin, w->positions, (int)d.T, (int)d.S,
+                                     (int)d.nh, (int)d.nkv, (int)d.d, qdg, s));
+    FORGE_HIP(forge::rmsnorm_dg_reduce(qdg, nq, g->d_q_norm, (int)d.d, !g->overwrite, s));
+    FORGE_HIP(forge::rmsnorm_dg_reduce(qdg + (size_t)nq * d.d, nq, g->d_k_norm, (int)d.d,
+                                       !g->overwrite, s));
+    if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->q_norm, g->d_q_norm, d.d));
+    if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->k_norm, g->d_k_norm, d.d));
+  } else {
+    FORGE_HIP(forge::rope_apply(dqkv, d.qkv, w->rope_cos, w->rope_sin, w->positions, (int)d.T,
+                                (int)d.S, (int)(d.nh + d.nkv), (int)d.d, true, s));
+  }
   if (side) FORGE_HIP(link(s, ws, side->ev[3]));
   FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
                         gargs(dqkv, d.qkv, a, d.h, g->d_w_qkv, d.h, d.qkv, d.h, d.T), ws));
@@ -523,7 +602,23 @@ forge_status moe_ffn_fwd(const forge_layer_cfg& c, const Dims& d, const forge_la
       forge::kKC, forge::kStoreBF16,
       grouped(gargs(act, d.fe, w->w_down_e, d.fe, ys, d.h, d.R, d.h, d.fe), offsets, E,
               d.h * d.fe, 0), s));
-  FORGE_HIP(forge::moe_combine(ys, gates, pos_of, h1, d.T, (int)d.h, k, out, s));
+  // the shared expert on every token: h1s = h1 + s (silu(b Wg^T) (b Wu^T)) Wd^T,
+  // then the routed sum is added on top of it
+  const uint16_t* resid = h1;
+  if (d.fs) {
+    uint16_t* gu_s = at<uint16_t>(saved, sv.gu_s);
+    uint16_t* act_s = at<uint16_t>(saved, sv.act_s);
+    uint16_t* h1s = at<uint16_t>(workspace, wk.h1s);
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
+                          gargs(bn, d.h, w->w_gate_up_s, d.h, gu_s, 2 * d.fs, d.T, 2 * d.fs, d.h),
+                          s));
+    FORGE_HIP(forge::swiglu_fwd(gu_s, act_s, (int)d.T, (int)d.fs, s));
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
+                          scaled(gargs(act_s, d.fs, w->w_down_s, d.fs, h1s, d.h, d.T, d.h, d.fs,
+                                       h1, d.h), d.bs), s));
+    resid = h1s;
+  }
+  FORGE_HIP(forge::moe_combine(ys, gates, pos_of, resid, d.T, (int)d.h, k, d.bs, out, s));
   FORGE_HIP(forge::moe_aux_loss(probs, counts, T, E, k, c.aux_coef,
                                 at<float>(workspace, wk.colsum), aux, s));
   return FORGE_OK;
@@ -554,7 +649,8 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
   uint16_t* dl = at<uint16_t>(workspace, wk.dl);
   uint16_t* dbs = at<uint16_t>(workspace, wk.dbs);
   const int T = (int)d.T, E = (int)d.E, k = (int)d.k;
-  FORGE_HIP(forge::moe_combine_bwd(ys, gates, pos_of, d_out, d.T, (int)d.h, k, dgate, dys, s));
+  FORGE_HIP(forge::moe_combine_bwd(ys, gates, pos_of, d_out, d.T, (int)d.h, k, d.bs, dgate, dys,
+                                   s));
   // down projection: dgrad into the routed rows, wgrad per expert
   FORGE_HIP(forge::gemm_grouped_m(
       forge::kMC, forge::kStoreBF16,
@@ -583,8 +679,32 @@ forge_status moe_ffn_bwd(const forge_layer_cfg& c, const Dims& d, const forge_la
   FORGE_HIP(forge::moe_scatter_back(dxs, pos_of, d.T, (int)d.h, k, dbs, s));
   // router: dl through the softmax (gates and aux loss), then its two products
   FORGE_HIP(forge::moe_router_bwd(probs, idx, dgate, counts, T, E, k, c.aux_coef, dl, s));
+  uint16_t* db_r = d.fs ? at<uint16_t>(workspace, wk.db1) : db;
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kResidBF16,
-                        gargs(dl, d.E, w->w_router, d.h, db, d.h, d.T, d.h, d.E, dbs, d.h), s));
+                        gargs(dl, d.E, w->w_router, d.h, db_r, d.h, d.T, d.h, d.E, dbs, d.h), s));
+  if (d.fs) {
+    // shared expert: weight gradients beside the rest (side stream when there
+    // is one), data gradient added to db
+    const uint16_t* gu_s = at<uint16_t>(saved, sv.gu_s);
+    const uint16_t* act_s = at<uint16_t>(saved, sv.act_s);
+    uint16_t* dA_s = at<uint16_t>(workspace, wk.dA_s);
+    uint16_t* dgu_s = at<uint16_t>(workspace, wk.dgu_s);
+    if (side) FORGE_HIP(link(s, ws, side->ev[5]));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                          scaled(gargs(d_out, d.h, act_s, d.fs, g->d_w_down_s, d.fs, d.h, d.fs,
+                                       d.T), d.bs), ws));
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
+                          scaled(gargs(d_out, d.h, w->w_down_s, d.fs, dA_s, d.fs, d.T, d.fs, d.h),
+                                 d.bs), s));
+    FORGE_HIP(forge::swiglu_bwd(gu_s, dA_s, dgu_s, (int)d.T, (int)d.fs, s));
+    if (side) FORGE_HIP(link(s, ws, side->ev[6]));
+    FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
+                          gargs(dgu_s, 2 * d.fs, bn, d.h, g->d_w_gate_up_s, d.h, 2 * d.fs, d.h,
+                                d.T), ws));
+    FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kResidBF16,
+                          gargs(dgu_s, 2 * d.fs, w->w_gate_up_s, d.h, db, d.h, d.T, d.h, 2 * d.fs,
+                                db_r, d.h), s));
+  }
   // router weight gradient: 64 x h output tiles over T tokens, split over T
   FORGE_HIP(forge::gemm_wgrad_splitk(gargs(dl, d.E, bn, d.h, g->d_w_router, d.h, d.E, d.h, d.T),
                                      forge::splitk_splits((int)d.E, (int)d.h, (int)d.T),
@@ -686,7 +806,11 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
   uint16_t* o = cfg->recompute_attn ? at<uint16_t>(workspace, wk.o) : at<uint16_t>(saved, sv.o);
   float* lse = cfg->recompute_attn ? at<float>(workspace, wk.lse) : at<float>(saved, sv.lse);
 
-  if (forge_status e = attn_block_fwd(*cfg, d, w, x_in, a, rstd1, qkv, o, lse, h1, s)) return e;
+  uint16_t* qk_raw = d.qkn ? at<uint16_t>(saved, sv.qk_raw) : nullptr;
+  float* rstd_qk = d.qkn ? at<float>(saved, sv.rstd_qk) : nullptr;
+  if (forge_status e =
+          attn_block_fwd(*cfg, d, w, x_in, a, rstd1, qkv, o, lse, h1, qk_raw, rstd_qk, s))
+    return e;
   FORGE_HIP(forge::rmsnorm_fwd(h1, w->ffn_norm, bn, rstd2, (int)d.T, (int)d.h, cfg->rms_eps, s));
   if (moe) return moe_ffn_fwd(*cfg, d, w, saved, sv, workspace, wk, h1, x_out, aux_loss, s);
   uint16_t* gu = at<uint16_t>(saved, sv.gu);
@@ -695,7 +819,8 @@ forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weigh
                         gargs(bn, d.h, w->w_gate_up, d.h, gu, 2 * d.f, d.T, 2 * d.f, d.h), s));
   FORGE_HIP(forge::swiglu_fwd(gu, act, (int)d.T, (int)d.f, s));
   FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kResidBF16,
-                        gargs(act, d.f, w->w_down, d.f, x_out, d.h, d.T, d.h, d.f, h1, d.h), s));
+                        scaled(gargs(act, d.f, w->w_down, d.f, x_out, d.h, d.T, d.h, d.f, h1, d.h),
+                               d.bs), s));
   return ok();
 }
 
@@ -729,6 +854,8 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
   const uint16_t* h1 = at<uint16_t>(saved, sv.h1);
   const float* rstd2 = at<float>(saved, sv.rstd2);
   const uint16_t* bn = at<uint16_t>(saved, sv.b);
+  const uint16_t* qk_raw = d.qkn ? at<uint16_t>(saved, sv.qk_raw) : nullptr;
+  const float* rstd_qk = d.qkn ? at<float>(saved, sv.rstd_qk) : nullptr;
   uint16_t* db = at<uint16_t>(workspace, wk.db);
   uint16_t* dh1 = at<uint16_t>(workspace, wk.dh1);
   float* dgp = at<float>(workspace, wk.dg);
@@ -762,11 +889,16 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
       return e;
     // the router weight is final: its update overlaps the rest
     if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->w_router, g->d_w_router, d.E * d.h));
+    if (opt && d.fs) {
+      hipStream_t ws = side ? side->stream : s;
+      FORGE_HIP(opt_update(opt, s, ws, opt->o->w_down_s, g->d_w_down_s, d.h * d.fs));
+      FORGE_HIP(opt_update(opt, s, ws, opt->o->w_gate_up_s, g->d_w_gate_up_s, 2 * d.fs * d.h));
+    }
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
     FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
     if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
-    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
-                          side, opt);
+    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, qk_raw, rstd_qk, dh1, d_in,
+                          workspace, wk, s, side, opt);
   } else {
     const uint16_t* gu = at<uint16_t>(saved, sv.gu);
     const uint16_t* act = at<uint16_t>(saved, sv.act);
@@ -784,7 +916,8 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     if (opt) opt->lane = side;
     if (side) FORGE_HIP(link(s, ws, side->ev[0]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
-                          gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T), ws));
+                          scaled(gargs(d_out, d.h, act, d.f, g->d_w_down, d.f, d.h, d.f, d.T),
+                                 d.bs), ws));
     // the weight-gradient product above is the side stream's only reader of
     // d_out; when d_in overlaps d_out, d_in is written only after it
     hipEvent_t d_out_read = nullptr;
@@ -794,7 +927,8 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
       FORGE_HIP(hipEventRecord(d_out_read, ws));
     }
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
-                          gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), s));
+                          scaled(gargs(d_out, d.h, w->w_down, d.f, dA, d.f, d.T, d.f, d.h), d.bs),
+                          s));
     FORGE_HIP(forge::swiglu_bwd(gu, dA, dgu, (int)d.T, (int)d.f, s));
     if (side) FORGE_HIP(link(s, ws, side->ev[1]));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, wgrad_epi(g),
@@ -810,8 +944,8 @@ forge_status layer_bwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
     FORGE_HIP(forge::rmsnorm_bwd(h1, w->ffn_norm, rstd2, db, d_out, dh1, dgp, (int)d.T, (int)d.h, s));
     FORGE_HIP(forge::rmsnorm_dg_reduce(dgp, nblk, g->d_ffn_norm, (int)d.h, !g->overwrite, s));
     if (opt) FORGE_HIP(opt_update(opt, s, s, opt->o->ffn_norm, g->d_ffn_norm, d.h));
-    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, dh1, d_in, workspace, wk, s,
-                          side, opt, d_out_read);
+    return attn_block_bwd(*cfg, d, w, g, x_in, a, rstd1, qkv, o, lse, qk_raw, rstd_qk, dh1, d_in,
+                          workspace, wk, s, side, opt, d_out_read);
   }
 }
 
@@ -841,6 +975,14 @@ forge_status check_optim(const forge_layer_cfg& c, const forge_layer_weights* w,
     if (forge_status e = one(o->w_router, w->w_router, "w_router")) return e;
     if (forge_status e = one(o->w_gate_up_e, w->w_gate_up_e, "w_gate_up_e")) return e;
     if (forge_status e = one(o->w_down_e, w->w_down_e, "w_down_e")) return e;
+    if (c.shared_ffn > 0) {
+      if (forge_status e = one(o->w_gate_up_s, w->w_gate_up_s, "w_gate_up_s")) return e;
+      if (forge_status e = one(o->w_down_s, w->w_down_s, "w_down_s")) return e;
+    }
+  }
+  if (c.qk_norm) {
+    if (forge_status e = one(o->q_norm, w->q_norm, "q_norm")) return e;
+    if (forge_status e = one(o->k_norm, w->k_norm, "k_norm")) return e;
   }
   return FORGE_OK;
 }
@@ -879,7 +1021,7 @@ forge_status forge_layer_bwd_adamw(const forge_layer_cfg* cfg, const forge_layer
   if (forge_status e = check_optim(*cfg, w, opt)) return e;
   if (forge_status e = check_hparams(hp)) return e;
   FORGE_PTR(dev_scalars);
-  OptPlan plan{opt, hp, dev_scalars, nullptr, 6};
+  OptPlan plan{opt, hp, dev_scalars, nullptr, 7};
   if (forge_status e = layer_bwd(cfg, w, saved, x_in, d_out, d_in, g, workspace,
                                  (hipStream_t)stream, &plan))
     return e;
@@ -1009,6 +1151,8 @@ forge_status check_head(const forge_head_cfg* c) {
               "vocab must be a positive multiple of 8 (got %d)", c->vocab);
   FORGE_CHECK((long)c->tokens * c->vocab < (1L << 31), FORGE_ERR_UNSUPPORTED,
               "tokens * vocab exceeds 2^31");
+  FORGE_CHECK(std::isfinite(c->logit_scale) && c->logit_scale >= 0.0f, FORGE_ERR_INVALID_ARG,
+              "logit_scale must be finite and >= 0 (0 means 1)");
   return FORGE_OK;
 }
 // zrows: rows of logits held at once (T, or the chunk of the streaming head)
@@ -1083,7 +1227,8 @@ forge_status loss_impl(const forge_head_cfg* cfg, long chunk, const forge_bf16* 
     FORGE_HIP(forge::gemm(forge::kKC, forge::kKC, forge::kStoreBF16,
                           gargs(xc, h, w_lm, h, z, V, n, V, h), s));
     FORGE_HIP(forge::ce_fwd_bwd(z, targets + t0, rl + t0, (int)n, (int)V,
-                                (float)(1.0 / (double)T), s));
+                                (float)(1.0 / (double)T),
+                                cfg->logit_scale == 0.0f ? 1.0f : cfg->logit_scale, s));
     FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                           gargs(z, V, w_lm, h, dxn + t0 * h, h, n, h, V), s));
     FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kAccF32,
@@ -1119,7 +1264,8 @@ forge_status forge_loss_fwd_bwd_chunked(const forge_head_cfg* cfg, int32_t chunk
 
 // ---- embedding --------------------------------------------------------------
 forge_status forge_embed_fwd(const int32_t* ids, const forge_bf16* emb, forge_bf16* x0,
-                             int32_t tokens, int32_t hidden, int32_t vocab, forge_stream stream) {
+                             int32_t tokens, int32_t hidden, int32_t vocab, float scale,
+                             forge_stream stream) {
   FORGE_CHECK(tokens >= 0 && vocab >= 1, FORGE_ERR_INVALID_ARG, "bad tokens/vocab");
   FORGE_CHECK(hidden >= 8 && hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
               "hidden must be a positive multiple of 8");
@@ -1127,12 +1273,14 @@ forge_status forge_embed_fwd(const int32_t* ids, const forge_bf16* emb, forge_bf
   FORGE_PTR(ids);
   FORGE_PTR(emb);
   FORGE_PTR(x0);
-  FORGE_HIP(forge::embed_fwd(ids, emb, x0, tokens, hidden, vocab, (hipStream_t)stream));
+  FORGE_CHECK(std::isfinite(scale), FORGE_ERR_INVALID_ARG, "scale must be finite");
+  FORGE_HIP(forge::embed_fwd(ids, emb, x0, tokens, hidden, vocab, scale, (hipStream_t)stream));
   return ok();
 }
 
 forge_status forge_embed_bwd(const int32_t* ids, const forge_bf16* dx0, float* d_emb,
-                             int32_t tokens, int32_t hidden, int32_t vocab, forge_stream stream) {
+                             int32_t tokens, int32_t hidden, int32_t vocab, float scale,
+                             forge_stream stream) {
   FORGE_CHECK(tokens >= 0 && vocab >= 1, FORGE_ERR_INVALID_ARG, "bad tokens/vocab");
   FORGE_CHECK(hidden >= 8 && hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
               "hidden must be a positive multiple of 8");
@@ -1140,7 +1288,8 @@ forge_status forge_embed_bwd(const int32_t* ids, const forge_bf16* dx0, float* d
   FORGE_PTR(ids);
   FORGE_PTR(dx0);
   FORGE_PTR(d_emb);
-  FORGE_HIP(forge::embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, (hipStream_t)stream));
+  FORGE_CHECK(std::isfinite(scale), FORGE_ERR_INVALID_ARG, "scale must be finite");
+  FORGE_HIP(forge::embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, scale, (hipStream_t)stream));
   return ok();
 }
 

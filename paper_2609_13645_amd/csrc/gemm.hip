@@ -121,9 +121,10 @@ __device__ __forceinline__ bf16x8_t frag(const uint4* tile, int base, int kk, in
 // read there. bf16 pieces of 8 bytes stay ordinary stores (streaming stores
 // that small are slower than the eviction they avoid).
 template <int EPI>
-__device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const float* v) {
+__device__ __forceinline__ void store4(const GemmArgs& p, int m, int n, const float* vin) {
   if (m >= p.M) return;
   const bool full = (n + 3 < p.N);
+  const float v[4] = {vin[0] * p.alpha, vin[1] * p.alpha, vin[2] * p.alpha, vin[3] * p.alpha};
   if (EPI == kStoreBF16 || EPI == kResidBF16) {
     bf16_t* C = reinterpret_cast<bf16_t*>(p.C) + (long)m * p.ldc + n;
     float x[4] = {v[0], v[1], v[2], v[3]};
@@ -485,6 +486,8 @@ __device__ __forceinline__ void wait_dma() {
 template <int EPI>
 __device__ __forceinline__ void store8_bf16(const GemmArgs& p, int m, int n, float* x) {
   if (m >= p.M) return;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] *= p.alpha;
   bf16_t* C = reinterpret_cast<bf16_t*>(p.C) + (long)m * p.ldc + n;
   const bool full = (n + 7 < p.N);
   if (EPI == kResidBF16) {
@@ -523,7 +526,7 @@ struct AdamPiece {
 template <int EPI>
 __device__ __forceinline__ void adam_load(const GemmArgs& p, int m, int n, const float* v,
                                           AdamPiece& a) {
-  a.g = f32x4_t{v[0], v[1], v[2], v[3]};
+  a.g = f32x4_t{v[0] * p.alpha, v[1] * p.alpha, v[2] * p.alpha, v[3] * p.alpha};
   if (m >= p.M || n + 3 >= p.N) return;  // ragged pieces: adam_store, element by element
   const long i = (long)m * p.ldc + n;
   if (EPI == kAccF32Adam)

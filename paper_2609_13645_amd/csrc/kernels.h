@@ -32,6 +32,9 @@ struct GemmArgs {
   const uint16_t* R;
   int M, N, K;
   long lda, ldb, ldc, ldr;
+  // every epilogue takes alpha * acc in place of acc (a residual branch's
+  // scale, App. B muP); 1 leaves every result bit-identical
+  float alpha = 1.0f;
   // grouped products (MoE experts): g_off[E + 1] device row offsets of the
   // groups; strideB / strideC elements between consecutive groups' B / C.
   const int* g_off = nullptr;
@@ -83,19 +86,35 @@ hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h
                              hipStream_t s);
 hipError_t rope_table(int seq, int d, float base, float* cos_t, float* sin_t,
                       hipStream_t s);
+// pos: RoPE position of every token (NULL: index within its batch row).
 hipError_t rope_apply(uint16_t* qkv, long row_stride, const float* cos_t,
-                      const float* sin_t, int T, int seq, int n_heads_rot, int d,
-                      bool inverse, hipStream_t s);
+                      const float* sin_t, const int32_t* pos, int T, int seq, int n_heads_rot,
+                      int d, bool inverse, hipStream_t s);
+// QK-Norm then RoPE on the nh q heads and nkv k heads of the qkv buffer, in
+// place; raw [T, (nh + nkv) * d] keeps the un-normalised rows, rstd
+// [T, nh + nkv] their rstd. The backward turns the post-RoPE gradient rows
+// into the pre-norm gradient in place and writes gain-gradient partials
+// [2][qknorm_bwd_blocks][d] (q, then k) for rmsnorm_dg_reduce.
+hipError_t qknorm_rope_fwd(uint16_t* qkv, long ld, uint16_t* raw, float* rstd, const uint16_t* gq,
+                           const uint16_t* gk, const float* cos_t, const float* sin_t,
+                           const int32_t* pos, int T, int seq, int nh, int nkv, int d, float eps,
+                           hipStream_t s);
+int qknorm_bwd_blocks(int T, int nrot, int d);
+hipError_t qknorm_rope_bwd(uint16_t* dqkv, long ld, const uint16_t* raw, const float* rstd,
+                           const uint16_t* gq, const uint16_t* gk, const float* cos_t,
+                           const float* sin_t, const int32_t* pos, int T, int seq, int nh, int nkv,
+                           int d, float* dg_partial, hipStream_t s);
 hipError_t swiglu_fwd(const uint16_t* gu, uint16_t* a, int T, int f, hipStream_t s);
 hipError_t swiglu_bwd(const uint16_t* gu, const uint16_t* da, uint16_t* dgu, int T,
                       int f, hipStream_t s);
 hipError_t embed_fwd(const int32_t* ids, const uint16_t* emb, uint16_t* x, int T,
-                     int h, int V, hipStream_t s);
+                     int h, int V, float scale, hipStream_t s);
 hipError_t embed_bwd(const int32_t* ids, const uint16_t* dx, float* demb, int T,
-                     int h, int V, hipStream_t s);
-// In place: z [T, V] bf16 logits -> dz = (softmax - onehot) * inv_T; row_loss[t].
+                     int h, int V, float scale, hipStream_t s);
+// In place: z [T, V] bf16 logits -> dz = scale (softmax(scale z) - onehot)
+// * inv_T; row_loss[t] of the scaled logits.
 hipError_t ce_fwd_bwd(uint16_t* z, const int32_t* targets, float* row_loss, int T,
-                      int V, float inv_T, hipStream_t s);
+                      int V, float inv_T, float scale, hipStream_t s);
 hipError_t mean_reduce(const float* v, int n, float scale, float* out, hipStream_t s);
 hipError_t adamw(float* master, uint16_t* param, const float* grad, float* m, float* v,
                  int64_t n, float b1, float b2, float eps, float wd,
@@ -148,10 +167,12 @@ hipError_t moe_sort(const int32_t* idx, int T, int E, int k, int32_t* block_coun
                     hipStream_t s);
 hipError_t moe_gather(const uint16_t* b, const int32_t* perm, long rows, int h, int k,
                       uint16_t* xs, hipStream_t s);
+// out = h1 + scale * sum_j gate_j ys_j; backward with the same scale.
 hipError_t moe_combine(const uint16_t* ys, const float* gates, const int32_t* pos_of,
-                       const uint16_t* h1, long T, int h, int k, uint16_t* out, hipStream_t s);
+                       const uint16_t* h1, long T, int h, int k, float scale, uint16_t* out,
+                       hipStream_t s);
 hipError_t moe_combine_bwd(const uint16_t* ys, const float* gates, const int32_t* pos_of,
-                           const uint16_t* dy, long T, int h, int k, float* dgate,
+                           const uint16_t* dy, long T, int h, int k, float scale, float* dgate,
                            uint16_t* dys, hipStream_t s);
 hipError_t moe_scatter_back(const uint16_t* dxs, const int32_t* pos_of, long T, int h, int k,
                             uint16_t* db, hipStream_t s);

@@ -211,12 +211,13 @@ __global__ __launch_bounds__(256) void gather_k(const bf16_t* __restrict__ b,
   reinterpret_cast<uint4*>(xs + r * h)[c] = reinterpret_cast<const uint4*>(b + t * h)[c];
 }
 
-// out[t] = h1[t] + sum_j gate[t, j] * ys[pos_of[t k + j]] (fp32, slot order).
+// out[t] = h1[t] + scale * sum_j gate[t, j] * ys[pos_of[t k + j]] (fp32,
+// slot order; scale: the branch scale of muP, 1 otherwise).
 __global__ __launch_bounds__(256) void combine_k(const bf16_t* __restrict__ ys,
                                                  const float* __restrict__ gates,
                                                  const int32_t* __restrict__ pos_of,
                                                  const bf16_t* __restrict__ h1, long T, int h,
-                                                 int k, bf16_t* __restrict__ out) {
+                                                 int k, float scale, bf16_t* __restrict__ out) {
   const int cpr = h / 8;
   const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= T * cpr) return;
@@ -233,17 +234,17 @@ __global__ __launch_bounds__(256) void combine_k(const bf16_t* __restrict__ ys,
   float r[8];
   unpack8(reinterpret_cast<const uint4*>(h1 + t * h)[c], r);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] += acc[e];
+  for (int e = 0; e < 8; ++e) r[e] += scale * acc[e];
   reinterpret_cast<uint4*>(out + t * h)[c] = pack8(r);
 }
 
-// Backward of combine for one token per block: dgate[t, j] = dy_t . ys_row and
-// dys_row = gate[t, j] * dy_t. k <= 16.
+// Backward of combine for one token per block: dgate[t, j] = scale dy_t .
+// ys_row and dys_row = scale gate[t, j] dy_t. k <= 16.
 __global__ __launch_bounds__(256) void combine_bwd_k(const bf16_t* __restrict__ ys,
                                                      const float* __restrict__ gates,
                                                      const int32_t* __restrict__ pos_of,
                                                      const bf16_t* __restrict__ dy, int h, int k,
-                                                     float* __restrict__ dgate,
+                                                     float scale, float* __restrict__ dgate,
                                                      bf16_t* __restrict__ dys) {
   __shared__ float red[4][16];
   const long t = blockIdx.x;
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(256) void combine_bwd_k(const bf16_t* __restrict__ 
         const long row = pos_of[t * k + j];
         float y[8], o[8];
         unpack8(reinterpret_cast<const uint4*>(ys + row * h)[c], y);
-        const float g = gates[t * k + j];
+        const float g = scale * gates[t * k + j];
         float s = 0.0f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(256) void combine_bwd_k(const bf16_t* __restrict__ 
   __syncthreads();
   if (threadIdx.x < k) {
     const int j = threadIdx.x;
-    dgate[t * k + j] = (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]);
+    dgate[t * k + j] = scale * ((red[0][j] + red[1][j]) + (red[2][j] + red[3][j]));
   }
 }
 
@@ -404,17 +405,18 @@ hipError_t moe_gather(const uint16_t* b, const int32_t* perm, long rows, int h, 
 }
 
 hipError_t moe_combine(const uint16_t* ys, const float* gates, const int32_t* pos_of,
-                       const uint16_t* h1, long T, int h, int k, uint16_t* out, hipStream_t s) {
+                       const uint16_t* h1, long T, int h, int k, float scale, uint16_t* out,
+                       hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_k, dim3(nblocks(T * (h / 8), 256)), dim3(256), 0, s, ys, gates, pos_of, h1, T, h, k, out);
+  hipLaunchKernelGGL(combine_k, dim3(nblocks(T * (h / 8), 256)), dim3(256), 0, s, ys, gates, pos_of, h1, T, h, k, scale, out);
   return hipGetLastError();
 }
 
 hipError_t moe_combine_bwd(const uint16_t* ys, const float* gates, const int32_t* pos_of,
-                           const uint16_t* dy, long T, int h, int k, float* dgate, uint16_t* dys,
-                           hipStream_t s) {
+                           const uint16_t* dy, long T, int h, int k, float scale, float* dgate,
+                           uint16_t* dys, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_bwd_k, dim3((unsigned)T), dim3(256), 0, s, ys, gates, pos_of, dy, h, k, dgate, dys);
+  hipLaunchKernelGGL(combine_bwd_k, dim3((unsigned)T), dim3(256), 0, s, ys, gates, pos_of, dy, h, k, scale, dgate, dys);
   return hipGetLastError();
 }
 

@@ -39,23 +39,36 @@ def to_device(arr: np.ndarray, device="cuda"):
 
 
 def layer_weight_names(cfg: dict):
-    if cfg.get("n_experts", 0):
-        return ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_router", "w_gate_up_e", "w_down_e")
-    return LAYER_WEIGHTS
+    return tuple(layer_shapes(cfg))
 
 
 def layer_shapes(cfg: dict) -> dict:
-    """Shapes of one layer's weights (dense or MoE)."""
+    """Shapes of one layer's weights (dense or MoE, with the variants the
+    configuration turns on: QK-Norm gains, shared expert)."""
     h, d = cfg["hidden"], cfg["head_dim"]
     hq, hkv = cfg["n_heads"] * d, cfg["n_kv_heads"] * d
     out = {"attn_norm": (h,), "w_qkv": (hq + 2 * hkv, h), "w_o": (h, hq), "ffn_norm": (h,)}
     if cfg.get("n_experts", 0):
         E, fe = cfg["n_experts"], cfg["expert_ffn"]
         out.update({"w_router": (E, h), "w_gate_up_e": (E, 2 * fe, h), "w_down_e": (E, h, fe)})
+        fs = cfg.get("shared_ffn", 0)
+        if fs:
+            out.update({"w_gate_up_s": (2 * fs, h), "w_down_s": (h, fs)})
     else:
         f = cfg["ffn"]
         out.update({"w_gate_up": (2 * f, h), "w_down": (h, f)})
+    if cfg.get("qk_norm", 0):
+        out.update({"q_norm": (d,), "k_norm": (d,)})
     return out
+
+
+def model_layer_cfg(cfg: dict, i: int) -> dict:
+    """Configuration of layer i of a model: the first dense_first_layers
+    layers of a MoE model use the dense FFN of width ffn (App. B, the sparse
+    model's dense layer 0)."""
+    if cfg.get("n_experts", 0) and i < cfg.get("dense_first_layers", 0):
+        return dict(cfg, n_experts=0, top_k=0, expert_ffn=0, shared_ffn=0)
+    return cfg
 
 
 def empty_bytes(n: int, device="cuda"):
@@ -118,6 +131,9 @@ class Layer:
         half = cfg["head_dim"] // 2
         self.w["rope_cos"] = torch.empty((cfg["seq"], half), dtype=torch.float32, device=device)
         self.w["rope_sin"] = torch.empty((cfg["seq"], half), dtype=torch.float32, device=device)
+        if cfg.get("positions") is not None:    # document-aware RoPE positions [T]
+            self.w["positions"] = torch.from_numpy(
+                np.ascontiguousarray(cfg["positions"], dtype=np.int32)).to(device)
         _lib.forge_rope_table(cfg["seq"], cfg["head_dim"], cfg["rope_base"],
                               self.w["rope_cos"], self.w["rope_sin"], stream)
         self.weights = _lib.layer_weights(self.w)
@@ -187,7 +203,7 @@ class Model:
         if not self.tied:
             shapes["w_lm"] = (V, h)
         for i in range(L):
-            for n, s in layer_shapes(cfg).items():
+            for n, s in layer_shapes(model_layer_cfg(cfg, i)).items():
                 shapes[f"{i}.{n}"] = s
         self.flat = FlatParams(shapes, device)
         # the embedding / head tensors come first in the flat buffers
@@ -201,12 +217,14 @@ class Model:
         for i in range(L):
             view = _PrefixedFlat(self.flat, f"{i}.")
             self.layer_flats.append(view)
-            self.layers.append(Layer(cfg, inputs["layers"][i], device, stream, flat=view))
-        ws = max(_lib.forge_layer_workspace_bytes(self.layers[0].c), 1)
+            self.layers.append(Layer(model_layer_cfg(cfg, i), inputs["layers"][i], device, stream,
+                                     flat=view))
+        ws = max(max(_lib.forge_layer_workspace_bytes(ly.c) for ly in self.layers), 1)
         self.workspace = empty_bytes(ws, device)
         for ly in self.layers:               # one shared scratch buffer
             ly.workspace = self.workspace
-        self.head = _lib.HeadCfg(self.T, h, V, cfg["rms_eps"])
+        self.head = _lib.HeadCfg(self.T, h, V, cfg["rms_eps"], cfg.get("logit_scale", 0.0))
+        self.embed_scale = cfg.get("embed_scale", 0.0) or 1.0
         # ce_chunk: the streaming head (chunk x V logits at a time), else T x V
         self.ce_chunk = int(cfg.get("ce_chunk", 0))
         self.head_ws = empty_bytes(
@@ -244,8 +262,8 @@ class Model:
             self.flat.grad[:self.head_grad_elems].zero_()
         T, h, V = self.T, c["hidden"], c["vocab"]
         emb = self.flat.view(self.flat.param, "embedding")
-        _lib.forge_embed_fwd(self.ids, emb, self.acts[0], T, h, V, s)
-        if c.get("n_experts", 0):
+        _lib.forge_embed_fwd(self.ids, emb, self.acts[0], T, h, V, self.embed_scale, s)
+        if any(ly.cfg.get("n_experts", 0) for ly in self.layers):
             self.aux.zero_()
         for i, ly in enumerate(self.layers):
             ly.fwd(self.acts[i], self.acts[i + 1], aux=self.aux)
@@ -270,7 +288,7 @@ class Model:
             self.layers[i].bwd(self.acts[i], g_in, g_out, overwrite=not accumulate)
             g_in, g_out = g_out, g_in
         _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
-                             self.T, c["hidden"], c["vocab"], s)
+                             self.T, c["hidden"], c["vocab"], self.embed_scale, s)
         return self.loss
 
     def train_step_overlapped(self, lr=None, clip=1.0):
@@ -292,7 +310,7 @@ class Model:
                                      self.scalars, overwrite=True)
             g_in, g_out = g_out, g_in
         _lib.forge_embed_bwd(self.ids, g_in, self.flat.view(self.flat.grad, "embedding"),
-                             self.T, c["hidden"], c["vocab"], s)
+                             self.T, c["hidden"], c["vocab"], self.embed_scale, s)
         f, n = self.flat, self.head_grad_elems
         _lib.forge_adamw_step(f.master[:n], f.param[:n], f.grad[:n], f.m[:n], f.v[:n], n,
                               self.hp, self.scalars, s)

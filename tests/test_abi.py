@@ -128,8 +128,6 @@ def test_optimizer_argument_rules():
     _lib.forge_adamw_step(None, None, None, None, None, 0, ok, None, 0)   # n = 0: no-op
     with pytest.raises(_lib.ForgeError):
         _lib.forge_loss_workspace_bytes(_lib.HeadCfg(16, 64, 1001, 1e-5))  # vocab % 8
-    assert ctypes.sizeof(_lib.LayerCfg) == 14 * 4
-    assert ctypes.sizeof(_lib.LayerGrads) == 9 * 8 + 8    # 9 pointers + int32 + padding
 
 
 def test_layer_bwd_adamw_argument_rules():
@@ -168,7 +166,6 @@ def test_layer_bwd_adamw_argument_rules():
     assert status(optim(w_qkv__v=0xC01008)) == _lib.FORGE_ERR_ALIGNMENT
     assert status(optim(), h=_lib.AdamwHparams(0.9, 1.0, 1e-8, 0.1)) == _lib.FORGE_ERR_INVALID_ARG
     assert status(optim(), sc=None) == _lib.FORGE_ERR_INVALID_ARG
-    assert ctypes.sizeof(_lib.LayerOptim) == 9 * 4 * 8
 
 
 def test_moe_layer_sizes():
@@ -210,3 +207,37 @@ def test_moe_route_noalloc_refuses_requests_beyond_its_scratch():
     with pytest.raises(_lib.ForgeError) as e:
         _lib.forge_moe_route_noalloc(16, 100, 64, 8, 0, 16, 16, 16, 16, 16, stream=0)
     assert e.value.status == _lib.FORGE_ERR_INVALID_ARG
+
+
+def test_binding_structs_match_the_c_header(tmp_path):
+    """Every struct of include/forge.h as the C compiler lays it out (size and
+    each member's offset) equals the ctypes mirror in the binding."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"forge_layer_cfg": _lib.LayerCfg, "forge_layer_weights": _lib.LayerWeights,
+               "forge_layer_grads": _lib.LayerGrads, "forge_head_cfg": _lib.HeadCfg,
+               "forge_adamw_hparams": _lib.AdamwHparams, "forge_adamw_tensor": _lib.AdamwTensor,
+               "forge_layer_optim": _lib.LayerOptim, "forge_attn_cfg": _lib.AttnCfg}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{_lib.HEADER_PATH}"',
+             "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'  printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-o", str(exe), str(src)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    got = {}
+    for line in out.splitlines():
+        cname, field, val = line.split()
+        got[(cname, field)] = int(val)
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)

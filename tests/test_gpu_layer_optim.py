@@ -24,6 +24,11 @@ CASES = {
     # attention backward on the library's streams
     "moe_overlapped": lambda: fi.config("moe_layer", batch=1, seq=512, n_experts=16, top_k=2,
                                         expert_ffn=256, seed=67),
+    # model variants: QK-Norm with document positions and a branch scale (side
+    # streams on), and the shared expert of the 160-expert top-16 layer
+    "qk_norm_packed": lambda: fi.config("qwen3_layer", batch=1, seq=1024, packed_docs=100,
+                                        branch_scale=0.5, seed=71),
+    "moe_shared_expert": lambda: fi.config("minicpm5_moe_layer", batch=1, seq=512, seed=73),
     # the benchmarked workloads at full size, in the bench's launch configuration
     "llama8b_layer_full": lambda: fi.config("llama8b_layer"),
     "moe_layer_full": lambda: fi.config("moe_layer"),
