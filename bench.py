@@ -55,6 +55,12 @@ DESCRIPTION = {
                             "chunks: 2048 x 32000 logits at a time)",
     "llama8b_layer_16k": "Llama-8B-shape layer at S16384, attention recomputed in bwd",
     "moe_layer": "MoE decoder layer, 64 experts top-8, fe 1408 (B2 S4096 h2048)",
+    "qwen3_layer": "Qwen3-0.6B-shape layer with per-head QK-Norm (B4 S4096 h1024, 16/8 x 128, "
+                   "f3072)",
+    "minicpm5_moe_layer": "MiniCPM5-16B-A3B-shape MoE layer: 160 experts top-16 fe 512 + shared "
+                          "expert 512, muP branch scale (B4 S4096 h2048, 32/2 x 128)",
+    "packed_docs_layer": "the 8B-shape layer over rows packed with documents (mean length "
+                         "512), RoPE positions restarting per document",
 }
 
 
@@ -417,6 +423,8 @@ def cpu_baseline(cfg, seq):
     else:
         seq = min(seq, cfg["seq"])
         c = dict(cfg, seq=seq, batch=1)
+        if cfg.get("positions") is not None:
+            c["positions"] = cfg["positions"][:seq]
         inp = fi.layer_inputs(c)
         W = {k: f64(v) for k, v in inp["weights"].items()}
         x, dy = f64(inp["x"]), f64(inp["dy"])
@@ -564,6 +572,10 @@ def main():
     if cfg["n_experts"]:
         res["config"].update(n_experts=cfg["n_experts"], top_k=cfg["top_k"],
                              expert_ffn=cfg["expert_ffn"], aux_coef=cfg["aux_coef"])
+    for key in ("qk_norm", "shared_ffn", "branch_scale", "packed_docs", "dense_first_layers",
+                "embed_scale", "logit_scale"):
+        if cfg.get(key):
+            res["config"][key] = cfg[key]
     if is_model(cfg):
         res["config"].update(n_layers=cfg["n_layers"], vocab=cfg["vocab"], tied=cfg["tied"])
     if cfg["recompute_attn"]:

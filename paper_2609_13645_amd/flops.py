@@ -12,14 +12,16 @@ the layers; the head is counted once at the same 1:2 ratio. Recomputation is
 not model FLOPs (it counts toward hardware FLOPs only).
 
 MoE extension (the paper's formula is dense only): the FFN term becomes
-top_k * 6 h fe (each token runs k SwiGLU experts) plus the router 2 h E;
-routing, permutation and combine are not counted.
+top_k * 6 h fe (each token runs k SwiGLU experts) plus the router 2 h E,
+plus 6 h fs for a shared expert of width fs; routing, permutation and
+combine are not counted. The first dense_first_layers layers of a MoE model
+count as dense layers. QK-Norm and the muP scalars add no model FLOPs.
 """
 from __future__ import annotations
 
 
 def per_token_fwd(hidden, n_heads, n_kv_heads, head_dim, seq, ffn=0, vocab=0,
-                  n_experts=0, top_k=0, expert_ffn=0):
+                  n_experts=0, top_k=0, expert_ffn=0, shared_ffn=0):
     """Forward FLOPs per token by operator class, for one layer (+ head)."""
     h, d = hidden, head_dim
     hq, hkv = n_heads * d, n_kv_heads * d
@@ -29,7 +31,7 @@ def per_token_fwd(hidden, n_heads, n_kv_heads, head_dim, seq, ffn=0, vocab=0,
         "head": 2 * h * vocab,
     }
     if n_experts:
-        out["ffn"] = top_k * 6 * h * expert_ffn + 2 * h * n_experts
+        out["ffn"] = top_k * 6 * h * expert_ffn + 2 * h * n_experts + 6 * h * shared_ffn
     else:
         out["ffn"] = 2 * (2 * h * ffn) + 2 * ffn * h
     return out
@@ -40,19 +42,22 @@ def per_token(cfg: dict, with_head: bool | None = None) -> dict:
 
     with_head defaults to vocab > 0.
     """
-    f = per_token_fwd(cfg["hidden"], cfg["n_heads"], cfg["n_kv_heads"],
-                      cfg["head_dim"], cfg["seq"], cfg.get("ffn", 0),
-                      cfg.get("vocab", 0), cfg.get("n_experts", 0),
-                      cfg.get("top_k", 0), cfg.get("expert_ffn", 0))
     L = cfg.get("n_layers", 1)
     if with_head is None:
         with_head = cfg.get("vocab", 0) > 0
-    res = {
-        "attn_proj": 3 * L * f["attn_proj"],
-        "attn_core": 3 * L * f["attn_core"],
-        "ffn": 3 * L * f["ffn"],
-        "head": 3 * f["head"] if with_head else 0,
-    }
+    res = {"attn_proj": 0, "attn_core": 0, "ffn": 0, "head": 0}
+    for i in range(L):
+        dense = not cfg.get("n_experts", 0) or i < cfg.get("dense_first_layers", 0)
+        f = per_token_fwd(cfg["hidden"], cfg["n_heads"], cfg["n_kv_heads"],
+                          cfg["head_dim"], cfg["seq"], cfg.get("ffn", 0),
+                          cfg.get("vocab", 0), 0 if dense else cfg["n_experts"],
+                          0 if dense else cfg.get("top_k", 0),
+                          0 if dense else cfg.get("expert_ffn", 0),
+                          0 if dense else cfg.get("shared_ffn", 0))
+        for k in ("attn_proj", "attn_core", "ffn"):
+            res[k] += 3 * f[k]
+    if with_head:
+        res["head"] = 3 * 2 * cfg["hidden"] * cfg.get("vocab", 0)
     res["total"] = sum(res.values())
     return res
 
