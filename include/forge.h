@@ -469,26 +469,6 @@ forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
                         forge_stream stream);
 
 /*
- * The two backward products of a projection y = x W^T in one launch (App. E,
- * "backward-pass fusion"): with dY [T, N] (leading dim ldy), W [N, K] (ldw)
- * and X [T, K] (ldx), all bf16,
- *   dX [T, K] bf16 (lddx) = dY W
- *   dW [N, K] fp32 (lddw) += dY^T X   (= when overwrite != 0)
- * Bit for bit the results of forge_gemm (KC, MC, STORE_BF16) and forge_gemm
- * (MC, MC, ACC_F32 / STORE_F32) with the same operands. When both products
- * fill the chip with 256 x 256 tiles they run as one launch (the first
- * workgroups take the data gradient's tiles, the rest the weight
- * gradient's), else as the two launches. Rules (else INVALID_ARG): N, K and
- * every leading dimension multiples of 8, each at least its contiguous
- * extent; dX must not overlap the inputs.
- */
-forge_status forge_gemm_dgrad_wgrad(const forge_bf16* dY, const forge_bf16* W,
-                                    const forge_bf16* X, forge_bf16* dX, float* dW, int32_t T,
-                                    int32_t N, int32_t K, int64_t ldy, int64_t ldw, int64_t ldx,
-                                    int64_t lddx, int64_t lddw, int32_t overwrite,
-                                    forge_stream stream);
-
-/*
  * Grouped products over row groups: the per-expert projections of a routed
  * mixture-of-experts FFN (App. B, MoE configurations), whose routed rows are
  * stored expert-major so that group e owns rows [offsets[e], offsets[e+1]).

@@ -140,8 +140,6 @@ def load():
         "forge_clip_coeff": (ctypes.c_int, [P, F32, F32, P, P]),
         "forge_gemm": (ctypes.c_int, [I32, I32, I32, P, P, P, P, I32, I32, I32,
                                       I64, I64, I64, I64, P]),
-        "forge_gemm_dgrad_wgrad": (ctypes.c_int, [P, P, P, P, P, I32, I32, I32, I64, I64, I64,
-                                                  I64, I64, I32, P]),
         "forge_gemm_grouped_rows": (ctypes.c_int, [I32, P, P, P, P, I32, I32, I32, I32,
                                                    I64, I64, I64, I64, P]),
         "forge_gemm_grouped_wgrad": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I64, I64,
@@ -343,13 +341,6 @@ def forge_gemm(layout_a, layout_b, epilogue, A, B, C, R, M, N, K, lda, ldb, ldc,
                stream=None):
     _check(load().forge_gemm(layout_a, layout_b, epilogue, _ptr(A), _ptr(B), _ptr(C),
                              _ptr(R), M, N, K, lda, ldb, ldc, ldr, _stream(stream)))
-
-
-def forge_gemm_dgrad_wgrad(dY, W, X, dX, dW, T, N, K, ldy, ldw, ldx, lddx, lddw, overwrite=False,
-                           stream=None):
-    _check(load().forge_gemm_dgrad_wgrad(_ptr(dY), _ptr(W), _ptr(X), _ptr(dX), _ptr(dW), T, N, K,
-                                         ldy, ldw, ldx, lddx, lddw, int(overwrite),
-                                         _stream(stream)))
 
 
 def forge_gemm_grouped_rows(layout_b, A, B, C, offsets, groups, rows, N, K, lda, ldb, ldc,

@@ -1391,36 +1391,6 @@ forge_status forge_gemm(int32_t layout_a, int32_t layout_b, int32_t epilogue,
   return ok();
 }
 
-forge_status forge_gemm_dgrad_wgrad(const forge_bf16* dY, const forge_bf16* W,
-                                    const forge_bf16* X, forge_bf16* dX, float* dW, int32_t T,
-                                    int32_t N, int32_t K, int64_t ldy, int64_t ldw, int64_t ldx,
-                                    int64_t lddx, int64_t lddw, int32_t overwrite,
-                                    forge_stream stream) {
-  FORGE_CHECK(T >= 0 && N >= 0 && K >= 0, FORGE_ERR_INVALID_ARG, "negative size");
-  if (N == 0 || K == 0) return ok();
-  FORGE_PTR(dX);
-  FORGE_PTR(dW);
-  FORGE_PTR(dY);
-  FORGE_PTR(W);
-  FORGE_PTR(X);
-  FORGE_CHECK(N % 8 == 0 && K % 8 == 0, FORGE_ERR_INVALID_ARG, "N and K must be multiples of 8");
-  FORGE_CHECK(ldy % 8 == 0 && ldw % 8 == 0 && ldx % 8 == 0 && lddx % 8 == 0 && lddw % 8 == 0,
-              FORGE_ERR_INVALID_ARG, "leading dimensions must be multiples of 8");
-  FORGE_CHECK(ldy >= N && ldw >= K && ldx >= K && lddx >= K && lddw >= K, FORGE_ERR_INVALID_ARG,
-              "leading dimension smaller than the contiguous extent");
-  FORGE_CHECK((int64_t)T * lddx < (1LL << 40) && (int64_t)N * lddw < (1LL << 40),
-              FORGE_ERR_INVALID_ARG, "output too large");
-  if (T == 0) {
-    if (overwrite) FORGE_HIP(forge::gemm(forge::kMC, forge::kMC, forge::kStoreF32,
-                                         gargs(dY, ldy, X, ldx, dW, lddw, N, K, 0), (hipStream_t)stream));
-    return ok();
-  }
-  const GemmArgs d = gargs(dY, ldy, W, ldw, dX, lddx, T, K, N);
-  const GemmArgs w = gargs(dY, ldy, X, ldx, dW, lddw, N, K, T);
-  FORGE_HIP(forge::gemm_dgrad_wgrad(d, w, overwrite == 0, (hipStream_t)stream));
-  return ok();
-}
-
 forge_status forge_gemm_grouped_rows(int32_t layout_b, const forge_bf16* A, const forge_bf16* B,
                                      forge_bf16* C, const int32_t* offsets, int32_t groups,
                                      int32_t rows, int32_t N, int32_t K, int64_t lda,

@@ -179,18 +179,13 @@ __device__ __forceinline__ void store_tile(const GemmArgs& p, const f32x16_t (&a
 // Tile of this workgroup (tm, tn) and the group-adjusted arguments; false
 // when the workgroup has no tile (M-grouped launches over-provision).
 template <int BM, int BN, int EPI, int GROUP>
-__device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn, int bid_ = -1,
-                                           int nb_ = -1) {
-  // the workgroup's index and count within its product (a launch can carry
-  // two products: ring_pair_kernel)
-  const int blk = bid_ < 0 ? (int)blockIdx.x : bid_;
-  const int nblk = nb_ < 0 ? (int)gridDim.x : nb_;
+__device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn) {
   if (GROUP == 0) {
     // ---- tile order: XCD-contiguous bands, GROUP_M rows of tiles per band ----
     const int tiles_m = (p.M + BM - 1) / BM;
     const int tiles_n = (p.N + BN - 1) / BN;
-    const int nb = nblk;
-    const int bid = blk;
+    const int nb = gridDim.x;
+    const int bid = blockIdx.x;
     const int nb8 = nb - nb % NUM_XCD;
     const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
     const int in_group = GROUP_M * tiles_n;
@@ -217,8 +212,8 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn, int bi
     }
     const int real = total * tiles_n;
     const int per = (real + NUM_XCD - 1) / NUM_XCD;
-    const int li = blk / NUM_XCD;
-    const int pid = (blk % NUM_XCD) * per + li;
+    const int li = blockIdx.x / NUM_XCD;
+    const int pid = (blockIdx.x % NUM_XCD) * per + li;
     if (li >= per || pid >= real) return false;
     int e = 0, acc = 0, mte = 1;
     for (int base = 0; base < p.groups; base += 64) {
@@ -252,8 +247,8 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn, int bi
     // (ks = p.strideB) and stores its partial product to C + e * strideC
     const int tiles_m = (p.M + BM - 1) / BM;
     const int tiles_n = (p.N + BN - 1) / BN;
-    const int e = blk / (tiles_m * tiles_n);
-    const int t = blk % (tiles_m * tiles_n);
+    const int e = blockIdx.x / (tiles_m * tiles_n);
+    const int t = blockIdx.x % (tiles_m * tiles_n);
     tm = t / tiles_n;
     tn = t % tiles_n;
     const long k0 = (long)e * p.strideB;
@@ -266,7 +261,7 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn, int bi
     // rows; XCD-contiguous ranges of tiles, group by group
     const int tiles_m = (p.M + BM - 1) / BM;
     const int tiles_n = (p.N + BN - 1) / BN;
-    const int nb = nblk, bid = blk;
+    const int nb = gridDim.x, bid = blockIdx.x;
     const int nb8 = nb - nb % NUM_XCD;
     const int pid = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
     const int e = pid / (tiles_m * tiles_n);
@@ -678,18 +673,9 @@ __device__ __forceinline__ void adam_tile(const GemmArgs& p, const f32x4_t (&acc
 // four ahead are then spread evenly over the MFMAs up to TAIL before the end,
 // reads and DMAs interleaved in proportion, so that neither the LDS nor the
 // texture unit sees a burst.
-template <int BM, int BN, int WAVES_M, int WAVES_N>
-struct RingLds {
-  static constexpr int NW = WAVES_M * WAVES_N;
-  static constexpr int SLOT = RingPart<BM, NW>::ELEMS + RingPart<BN, NW>::ELEMS;
-  static constexpr int CHUNKS = 4 * SLOT;  // 16-byte chunks of the four-stage ring
-};
-
-// One workgroup's tile of a product (bid of nb workgroups of that product),
-// on the four-stage ring in `lds`.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0,
           int TAIL = 4>
-__device__ __forceinline__ void ring_body(GemmArgs p, int bid, int nb, uint4* lds) {
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs p) {
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 16, FN = WN / 16;
   static_assert(FM * 16 == WM && FN * 16 == WN, "wave tile must be a multiple of 16");
@@ -703,9 +689,10 @@ __device__ __forceinline__ void ring_body(GemmArgs p, int bid, int nb, uint4* ld
   constexpr int E = NF + D;   // memory instructions spread over a stage
   constexpr int W = NM - BAR_AT - TAIL;
   static_assert(W > 0, "wave tile too small for the barrier placement and tail");
+  __shared__ uint4 lds[4 * SLOT];
 
   int tm, tn;
-  if (!tile_setup<BM, BN, EPI, GROUP>(p, tm, tn, bid, nb)) return;
+  if (!tile_setup<BM, BN, EPI, GROUP>(p, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -798,26 +785,6 @@ __device__ __forceinline__ void ring_body(GemmArgs p, int bid, int nb, uint4* ld
   } else {
     store_tile16<EPI, FN, FM>(p, acc, m0 + wm * WM, n0 + wn * WN, lane);
   }
-}
-
-template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP = 0,
-          int TAIL = 4>
-__global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs p) {
-  __shared__ uint4 lds[RingLds<BM, BN, WAVES_M, WAVES_N>::CHUNKS];
-  ring_body<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, GROUP, TAIL>(p, blockIdx.x, gridDim.x, lds);
-}
-
-// The backward of one projection in one launch (App. E, backward-pass
-// fusion): the first nd workgroups compute the data gradient dX = dY W
-// (KC, MC, bf16), the others the weight gradient dW (+)= dY^T X (MC, MC,
-// fp32), each on the 256 x 256 ring with the tile order of its own launch.
-template <int EPI_W>
-__global__ __launch_bounds__(512, 1) void ring_pair_kernel(GemmArgs pd, GemmArgs pw, int nd) {
-  __shared__ uint4 lds[RingLds<256, 256, 4, 2>::CHUNKS];
-  if ((int)blockIdx.x < nd)
-    ring_body<256, 256, 4, 2, kKC, kMC, kStoreBF16>(pd, blockIdx.x, nd, lds);
-  else
-    ring_body<256, 256, 4, 2, kMC, kMC, EPI_W>(pw, blockIdx.x - nd, gridDim.x - nd, lds);
 }
 
 // Operands contiguous along M / N and full 256 x 256 tiles run on the ring
@@ -953,30 +920,6 @@ hipError_t gemm_wgrad_splitk(const GemmArgs& a, int splits, float* partial, bool
   else
     hipLaunchKernelGGL(splitk_reduce_k<false>, grid, dim3(256), 0, s, partial, S, (long)a.M * a.N,
                        a.M, a.N, reinterpret_cast<float*>(a.C), a.ldc);
-  return hipGetLastError();
-}
-
-bool gemm_pair_fits(const GemmArgs& d, const GemmArgs& w) {
-  const long td = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
-  const long tw = (long)((w.M + 255) / 256) * ((w.N + 255) / 256);
-  // both products on 256 x 256 tiles (as their own launches would run them)
-  return td >= kCUs && tw >= kCUs && d.M > 0 && d.N > 0 && w.M > 0 && w.N > 0;
-}
-
-hipError_t gemm_dgrad_wgrad(const GemmArgs& d, const GemmArgs& w, bool accumulate,
-                            hipStream_t s) {
-  if (!gemm_pair_fits(d, w)) {
-    hipError_t e = gemm(kKC, kMC, kStoreBF16, d, s);
-    if (e != hipSuccess) return e;
-    return gemm(kMC, kMC, accumulate ? kAccF32 : kStoreF32, w, s);
-  }
-  const long td = (long)((d.M + 255) / 256) * ((d.N + 255) / 256);
-  const long tw = (long)((w.M + 255) / 256) * ((w.N + 255) / 256);
-  const dim3 grid((unsigned)(td + tw)), block(512);
-  if (accumulate)
-    hipLaunchKernelGGL(ring_pair_kernel<kAccF32>, grid, block, 0, s, d, w, (int)td);
-  else
-    hipLaunchKernelGGL(ring_pair_kernel<kStoreF32>, grid, block, 0, s, d, w, (int)td);
   return hipGetLastError();
 }
 

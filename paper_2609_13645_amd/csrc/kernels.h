@@ -56,13 +56,6 @@ struct GemmArgs {
 // dimensions % 8 == 0; base pointers 16-byte aligned.
 hipError_t gemm(GemmLayout la, GemmLayout lb, GemmEpilogue epi, const GemmArgs& a,
                 hipStream_t stream);
-// The two backward products of one projection in one launch: d = the data
-// gradient (KC, MC, bf16 store), w = the weight gradient (MC, MC, fp32 +=
-// when accumulate, else =). Falls back to two launches unless both products
-// fill the chip with 256 x 256 tiles (gemm_pair_fits).
-bool gemm_pair_fits(const GemmArgs& d, const GemmArgs& w);
-hipError_t gemm_dgrad_wgrad(const GemmArgs& d, const GemmArgs& w, bool accumulate,
-                            hipStream_t s);
 // Grouped forms, one product per group e with rows [g_off[e], g_off[e+1]):
 //   M-grouped (KC or MC B): C rows g_off[e].. = A rows g_off[e].. x B_e, where
 //     B_e = B + e * strideB; M is an upper bound of the total rows (T * k).

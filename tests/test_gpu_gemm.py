@@ -200,29 +200,3 @@ def test_grouped_wgrad_integer_exact(M, N):
         r0, r1 = off[e], off[e + 1]
         want = init[e] + A[r0:r1].T.astype(np.float64) @ B[r0:r1]
         assert np.array_equal(got[e], want), e
-
-
-@pytest.mark.parametrize("T,N,K,overwrite", [(4096, 4096, 4096, True), (4096, 4096, 14336, False),
-                                             (4096, 1024, 4096, True), (300, 200, 520, False)])
-def test_dgrad_wgrad_in_one_launch_equals_the_two_products(T, N, K, overwrite):
-    """forge_gemm_dgrad_wgrad (one launch when both products fill the chip)
-    gives the bits of the two separate products."""
-    import torch
-    from paper_2609_13645_amd import _lib
-    banner(f"gemm dgrad+wgrad in one launch T={T} N={N} K={K} overwrite={overwrite}")
-    rng = np.random.default_rng(T + N + K)
-    bf = lambda shape, s: dev_bf16(fi.to_bf16_bits(rng.standard_normal(shape, dtype=np.float32)
-                                                   * np.float32(s)))
-    dY, W, X = bf((T, N), 0.1), bf((N, K), 0.05), bf((T, K), 1.0)
-    init = torch.from_numpy(rng.standard_normal((N, K), dtype=np.float32)).cuda()
-    dX1 = torch.empty((T, K), dtype=torch.bfloat16, device="cuda")
-    dW1 = init.clone()
-    _lib.forge_gemm(KC, MC, STORE_BF16, dY, W, dX1, None, T, K, N, N, K, K)
-    _lib.forge_gemm(MC, MC, STORE_F32 if overwrite else ACC_F32, dY, X, dW1, None, N, K, T, N, K,
-                    K)
-    dX2 = torch.full((T, K), float("nan"), dtype=torch.bfloat16, device="cuda")
-    dW2 = init.clone()
-    _lib.forge_gemm_dgrad_wgrad(dY, W, X, dX2, dW2, T, N, K, N, K, K, K, K, overwrite)
-    torch.cuda.synchronize()
-    assert torch.equal(dX1.view(torch.int16), dX2.view(torch.int16))
-    assert torch.equal(dW1, dW2)
