@@ -1,10 +1,10 @@
 // Causal grouped-query flash attention on gfx950 MFMA: forward, and the
 // backward as a query-owned kernel that accumulates dQ (and on the way forms
-// delta = rowsum(dO * O) for the rest), key-owned kernels that accumulate dV
-// and dK, and a small reduction of the dK, dV partials over each GQA group. The paper's H100
-// kernel accumulates dQ through a flat global buffer (App. D, "Anatomy of a
-// Forged Kernel"); here the dQ kernel recomputes two products instead, with no
-// fp32 atomics, so every output is deterministic.
+// delta = rowsum(dO * O) for the rest), and a key-owned kernel that
+// accumulates dV and dK of a kv head over every query head of its GQA group.
+// The paper's H100 kernel accumulates dQ through a flat global buffer
+// (App. D, "Anatomy of a Forged Kernel"); here the dQ kernel recomputes two
+// products instead, with no fp32 atomics, so every output is deterministic.
 //
 // Operand layout. The 32x32x16 MFMA gives each lane one column of its 32x32
 // result and sixteen rows. Scores are formed with the lane-owned index on the
@@ -415,207 +415,261 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
 }
 
 // ------------------------------------------------------ backward dK, dV ----
-// Block: 128 keys (32 per wave) of one (batch, query head); loops over the
-// 64-query tiles at or after its first key and writes fp32 partials of its
-// query head; attn_bwd_reduce_k sums the GQA group's partials. The work is
-// split into two passes so each keeps one d x 32 accumulator per wave and
-// the kernel runs two blocks per CU:
-//   PASS 0: S = Q K^T, P = exp(S - LSE), dV^T += dO^T P
-//   PASS 1: S, dP = dO V^T, dS = P (dP - delta), dK^T += Q^T dS
-// (S is formed twice, 5 products instead of 4, for twice the occupancy.)
-// LDS double buffering in two separate arrays with explicit waits, as in the
-// forward. Each 64-query tile is processed as two 32-query halves, so a
-// half's scores, dP and fragments leave room for four 16-deep slices of Q /
-// dO fragment reads in flight.
+// Block: 64 keys [k0, k0 + 64) of one (batch, kv head), four waves, one wave
+// per SIMD. The block's work is every (query head of the GQA group, 32-query
+// slab at or after k0) pair; wave w takes pairs w, w + 4, w + 8, ... and
+// accumulates over them, for all 64 keys,
+//   PASS 0: S = Q K^T, P = exp2(S c - LSE log2 e), dV^T += dO^T P
+//   PASS 1: S, P, dP = dO V^T - delta (accumulators start at -delta),
+//           dS = P dP, dK^T += Q^T dS.
+// The wave keeps K (and V) of its 64 keys in registers as two 32-key column
+// blocks, so every Q / dO fragment read from LDS feeds two MFMAs (a 32-key
+// wave reads twice the LDS bytes per FLOP, which at the MFMA rate is the
+// LDS bandwidth of the whole CU). S is formed in both passes (5 products
+// instead of 4): one pass holding both d x 64 accumulators, K and V does
+// not fit the register file.
+// Each wave streams its own pairs' Q / dO slabs (with their LSE and delta)
+// through a private double buffer in LDS, so the waves never wait for each
+// other inside the loop. At the end the four waves' accumulators are summed
+// through LDS in wave order, so the result does not depend on timing, and
+// written as bf16: no partials leave the block, and K / V are read once per
+// GQA group.
+template <int D>
+struct KvPlan {
+  static constexpr int BK = 64, BQ = 32;
+  static constexpr int SLAB = BQ * D / 8;         // 16-byte chunks of a 32-row tile
+  static constexpr int WBUF = 2 * SLAB + 16;      // Q, dO slabs, LSE[32] | delta[32]
+  static constexpr int RED = BK * (D + 4) / 4;    // one wave's [64][D + 4] fp32 sums
+  static constexpr int ARR = 4 * WBUF > 2 * RED ? 4 * WBUF : 2 * RED;
+  static constexpr int LPR = D / 8, RPI = 64 / LPR, PER = BQ / RPI;  // DMA of a slab
+  static constexpr int DMA = 2 * PER + 1;         // DMA instructions per pair
+};
+// s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding: vmcnt
+// bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 at their maxima)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+template <int D>
+__device__ __forceinline__ void slab_offsets(long ld, int lane, uint32_t (&off)[KvPlan<D>::PER]) {
+  using P = KvPlan<D>;
+#pragma unroll
+  for (int i = 0; i < P::PER; ++i) {
+    const int row = i * P::RPI + lane / P::LPR;
+    const int c = (lane % P::LPR) ^ fsw<D>(row);
+    off[i] = (uint32_t)(((long)row * ld + c * 8) * 2);
+  }
+}
+// 32 rows [row0, row0 + 32) of a [*, ld] bf16 matrix into a natural tile;
+// rows at or past lim read as zeros.
+template <int D>
+__device__ __forceinline__ void dma_slab(const bf16_t* base, long ld, int row0, int lim,
+                                         uint4* lds, const uint32_t* off) {
+  using P = KvPlan<D>;
+  const __amdgpu_buffer_rsrc_t r = rsrc_n(base + (long)row0 * ld, (long)(lim - row0) * ld * 2);
+#pragma unroll
+  for (int i = 0; i < P::PER; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + i * 64), 16, off[i], 0, 0, 0);
+}
+
 template <int D, int PASS>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_k(
-    AttnArgs a, const bf16_t* __restrict__ dout, const float* __restrict__ delta,
-    float* __restrict__ pk, float* __restrict__ pv) {
-  constexpr int BKEY = 128, BQ = 64, NAT = BQ * D / 8;
-  constexpr int STAGE = 2 * NAT + 32;  // Q tile, dO tile, lse[64], delta[64]
-  __shared__ uint4 sm0[STAGE];
-  __shared__ uint4 sm1[STAGE];
+__global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
+                                                        const bf16_t* __restrict__ dout,
+                                                        const float* __restrict__ delta,
+                                                        bf16_t* __restrict__ out, long ld_d) {
+  using P = KvPlan<D>;
+  constexpr int BK = P::BK, BQ = P::BQ, SLAB = P::SLAB, KK = D / 16, DB = D / 32;
+  __shared__ uint4 sm0[P::ARR];
+  __shared__ uint4 sm1[P::ARR];
 
   const int S = a.seq;
-  const int kt = blockIdx.x;  // low key tiles have the most work: dispatched first
-  const int n = blockIdx.y, b = blockIdx.z;
   const int grp = a.n_heads / a.n_kv_heads;
-  const int m = n / grp;
-  const long rb = (long)b * S;
-  const long ldo = (long)a.n_heads * D;
+  // block order: key tile slowest, so the low key tiles (the most work)
+  // are dispatched first
+  const int per_kt = a.n_kv_heads * a.batch;
+  const int kt = (int)blockIdx.x / per_kt;
+  const int m = (int)blockIdx.x % per_kt % a.n_kv_heads;
+  const int b = (int)blockIdx.x % per_kt / a.n_kv_heads;
+  const int k0 = kt * BK;
+  const int j0 = k0 / BQ;                      // first slab holding a query >= k0
+  const int ns = (S + BQ - 1) / BQ - j0;       // slabs per query head
+  const int total = grp * ns;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
-  const int kw0 = kt * BKEY + wave * 32;
-  const int key = kw0 + l32;
-
-  const bf16_t* Kg = a.k + rb * a.ld_qkv + (long)m * D;
-  const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
-  const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
-  const bf16_t* dOg = dout + rb * ldo + (long)n * D;
+  const long rb = (long)b * S;
+  const long ldo = (long)a.n_heads * D;
   const long nrows = (long)a.batch * a.n_heads * S;
-  const float* Lg = delta + nrows + ((long)b * a.n_heads + n) * S;  // -LSE log2(e)
-  const float* Dg = delta + ((long)b * a.n_heads + n) * S;
-  // K (and, for PASS 1, V) rows of this lane's key: the B operands of S, dP
-  bf16x8_t kf[D / 16], vf[PASS ? D / 16 : 1];
+
+  // K (and V) rows of the lane's two keys k0 + l32 and k0 + 32 + l32: the
+  // B operands of S and dP
+  bf16x8_t kf[2][KK], vf[2][PASS ? KK : 1];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    kf[kk] = gload_frag(Kg + (long)key * a.ld_qkv + kk * 16 + hh * 8, key < S);
-    if (PASS) vf[kk] = gload_frag(Vg + (long)key * a.ld_qkv + kk * 16 + hh * 8, key < S);
+  for (int kb = 0; kb < 2; ++kb) {
+    const int key = k0 + kb * 32 + l32;
+    const long r = (rb + key) * a.ld_qkv + (long)m * D + hh * 8;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      kf[kb][kk] = gload_frag(a.k + r + kk * 16, key < S);
+      if constexpr (PASS) vf[kb][kk] = gload_frag(a.v + r + kk * 16, key < S);
+    }
   }
-  f32x16_t acc[D / 32];
+  f32x16_t acc[DB][2];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db) zero(acc[db]);
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) zero(acc[db][kb]);
   const float c = a.scale * kLog2e;
-  const int nqt = (S + BQ - 1) / BQ;
-  const int qt0 = (kt * BKEY) / BQ;
-  const int iters = nqt - qt0;
 
-  uint32_t qoff[DmaPlan<D, 4>::PER], ooff[DmaPlan<D, 4>::PER];
-  dma_offsets<D, 4>(a.ld_qkv, wave, lane, qoff);
-  dma_offsets<D, 4>(ldo, wave, lane, ooff);
-  auto load_tile = [&](int it, uint4* base) __attribute__((always_inline)) {
-    const int q0 = (qt0 + it) * BQ;
-    dma_tile_at<D, 4>(Qg, a.ld_qkv, q0, S, base, wave, qoff);
-    dma_tile_at<D, 4>(dOg, ldo, q0, S, base + NAT, wave, ooff);
-    if (wave == 0) {
-      const uint32_t off = q0 + lane < S ? (uint32_t)((q0 + lane) * 4) : kOOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Lg), (lds_ptr_t)(base + 2 * NAT), 4, off, 0, 0, 0);
-      if (PASS)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc(Dg), (lds_ptr_t)(base + 2 * NAT + 16), 4, off, 0, 0, 0);
-    }
-  };
-
-  // per-lane offsets of the Q / dO fragments within a tile
-  uint32_t ro[D / 16], to[D / 32][2];
+  uint32_t qoff[P::PER], ooff[P::PER];
+  slab_offsets<D>(a.ld_qkv, lane, qoff);
+  slab_offsets<D>(ldo, lane, ooff);
+  uint32_t ro[KK], to[DB][2];
   frag_offsets<D>(lane, ro, to);
-  auto tile = [&](const uint4* base, int it) __attribute__((always_inline)) {
-    const int q0 = (qt0 + it) * BQ;
-    if (q0 + BQ - 1 < kw0) return;
-    const float* L = reinterpret_cast<const float*>(base + 2 * NAT);
-    const float* Dl = L + BQ;
-    const bool tail = (q0 + BQ > S);
-    // the two 32-query halves one after the other (a half's scores, dP and
-    // fragments fit with four slices of reads in flight)
-    auto half = [&](auto QB) __attribute__((always_inline)) {
-      constexpr int qb = decltype(QB)::value;
-      constexpr int RQ = qb * 32 * D * 2;            // byte offset of row 32 qb
-      f32x16_t sc, dp;
-      if (PASS) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i)   // dP - delta (stored negated), formed by the MFMAs
-          dp[i] = Dl[qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3)];
-      }
-      bf16x8_t fq[D / 16], fo[D / 16];
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        if (kk % 4 == 0) {
-#pragma unroll
-          for (int u = kk; u < kk + 4; ++u) {
-            fq[u] = row_at<RQ>(base, ro[u]);
-            if (PASS) fo[u] = row_at<NAT * 16 + RQ>(base, ro[u]);
-          }
-        }
-        sc = MFMA(fq[kk], kf[kk], kk == 0 ? f32x16_t{} : sc);
-        if (PASS) dp = MFMA(fo[kk], vf[kk], dp);
-      }
-      // transposed fragments of the second product (dO^T for dV, Q^T for
-      // dK), in flight under the elementwise part
-      constexpr int TT = PASS ? 0 : NAT * 16;         // Q tile or dO tile
-      bf16x8_t ft[2][D / 32];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        ft[0][db] = tr_at<TT + RQ>(base, to[db]);
-        ft[1][db] = tr_at<TT + RQ + 16 * D * 2>(base, to[db]);
-      }
-      // P = exp2(S c - LSE log2 e); on diagonal / tail tiles the masked
-      // scores are set to -inf first, so exp2 gives 0
-      if (q0 + qb * 32 < kw0 + 31 || tail) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          if (key > q0 + qi || q0 + qi >= S) sc[i] = -INFINITY;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int qi = qb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-        const float p = fast_exp2(__builtin_fmaf(sc[i], c, L[qi]));
-        sc[i] = PASS ? p * dp[i] : p;
-      }
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
-        const bf16x8_t f = pack_frag(sc, ss);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] = MFMA(ft[ss][db], f, acc[db]);
-      }
-    };
-    half(std::integral_constant<int, 0>());
-    half(std::integral_constant<int, 1>());
-  };
-  auto sync = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  load_tile(0, sm0);
-  sync();
-  for (int it = 0; it < iters; it += 2) {
-    if (it + 1 < iters) load_tile(it + 1, sm1);
-    tile(sm0, it);
-    sync();
-    if (it + 1 < iters) {
-      if (it + 2 < iters) load_tile(it + 2, sm0);
-      tile(sm1, it + 1);
-      sync();
-    }
-  }
+  const __amdgpu_buffer_rsrc_t drs = rsrc(delta);
 
-  // partials: [grp][T][hkv] fp32, this block's query head is slot n % grp
-  if (key < S) {
-    const long hkv = (long)a.n_kv_heads * D;
-    const long base = ((long)(n % grp) * a.batch * S + rb + key) * hkv + (long)m * D;
-    float* dst = PASS ? pk : pv;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+  // pair p: query head m * grp + p / ns, slab j0 + p % ns
+  auto load = [&](int p, uint4* base) __attribute__((always_inline)) {
+    const int n = m * grp + p / ns;
+    const int q0 = (j0 + p % ns) * BQ;
+    dma_slab<D>(a.q + rb * a.ld_qkv + (long)n * D, a.ld_qkv, q0, S, base, qoff);
+    dma_slab<D>(dout + rb * ldo + (long)n * D, ldo, q0, S, base + SLAB, ooff);
+    // lanes 0-31: -LSE log2(e) of the slab's queries; lanes 32-63: -delta
+    const long li = ((long)b * a.n_heads + n) * S + q0 + l32;
+    const uint32_t off = q0 + l32 < S ? (uint32_t)(((hh ? 0 : nrows) + li) * 4) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(drs, (lds_ptr_t)(base + 2 * SLAB), 4, off, 0, 0, 0);
+  };
+
+  auto pair = [&](const uint4* base, int p) __attribute__((always_inline)) {
+    // this buffer's DMA has landed once only the other buffer's (issued
+    // after it) can still be in flight
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(P::DMA));
+    __builtin_amdgcn_sched_barrier(0);
+    const int q0 = (j0 + p % ns) * BQ;
+    const float* L = reinterpret_cast<const float*>(base + 2 * SLAB);
+    const float* Dl = L + BQ;
+    f32x16_t sc[2], dp[PASS ? 2 : 1];
+    if constexpr (PASS) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = db * 32 + g * 8 + hh * 4;
-        *reinterpret_cast<float4*>(dst + base + d) =
-            make_float4(acc[db][g * 4], acc[db][g * 4 + 1], acc[db][g * 4 + 2], acc[db][g * 4 + 3]);
-      }
-  }
-}
-
-// dk = scale * sum_g pk[g], dv = sum_g pv[g] (fixed order) -> bf16 into the
-// dk / dv columns of the dqkv buffer. One thread per 8 elements.
-__global__ __launch_bounds__(256) void attn_bwd_reduce_k(const float* __restrict__ pk,
-                                                         const float* __restrict__ pv, int grp,
-                                                         long T, int hkv, float scale,
-                                                         bf16_t* __restrict__ dk,
-                                                         bf16_t* __restrict__ dv, long ld_d) {
-  const long id = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  const int cpr = hkv / 8;
-  if (id >= T * cpr) return;
-  const long t = id / cpr;
-  const int c = (int)(id % cpr);
-  float k8[8] = {}, v8[8] = {};
-  for (int g = 0; g < grp; ++g) {
-    const long off = ((long)g * T + t) * hkv + c * 8;
-    const float4 k0 = *reinterpret_cast<const float4*>(pk + off);
-    const float4 k1 = *reinterpret_cast<const float4*>(pk + off + 4);
-    const float4 v0 = *reinterpret_cast<const float4*>(pv + off);
-    const float4 v1 = *reinterpret_cast<const float4*>(pv + off + 4);
-    k8[0] += k0.x; k8[1] += k0.y; k8[2] += k0.z; k8[3] += k0.w;
-    k8[4] += k1.x; k8[5] += k1.y; k8[6] += k1.z; k8[7] += k1.w;
-    v8[0] += v0.x; v8[1] += v0.y; v8[2] += v0.z; v8[3] += v0.w;
-    v8[4] += v1.x; v8[5] += v1.y; v8[6] += v1.z; v8[7] += v1.w;
-  }
+        const float4 dd = *reinterpret_cast<const float4*>(Dl + g * 8 + hh * 4);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) k8[e] *= scale;
-  *reinterpret_cast<uint4*>(dk + t * ld_d + c * 8) = pack8(k8);
-  *reinterpret_cast<uint4*>(dv + t * ld_d + c * 8) = pack8(v8);
+        for (int kb = 0; kb < 2; ++kb) {
+          dp[kb][g * 4 + 0] = dd.x;
+          dp[kb][g * 4 + 1] = dd.y;
+          dp[kb][g * 4 + 2] = dd.z;
+          dp[kb][g * 4 + 3] = dd.w;
+        }
+      }
+    }
+    // S and dP: each row fragment feeds both key blocks
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const bf16x8_t fq = row_at<0>(base, ro[kk]);
+      sc[0] = MFMA(fq, kf[0][kk], kk == 0 ? f32x16_t{} : sc[0]);
+      sc[1] = MFMA(fq, kf[1][kk], kk == 0 ? f32x16_t{} : sc[1]);
+    }
+    if constexpr (PASS) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8_t fo = row_at<SLAB * 16>(base, ro[kk]);
+        dp[0] = MFMA(fo, vf[0][kk], dp[0]);
+        dp[1] = MFMA(fo, vf[1][kk], dp[1]);
+      }
+    }
+    // causal mask and sequence tail (diagonal and last slabs only): -inf
+    // scores, so exp2 gives 0
+    if (q0 < k0 + BK - 1 || q0 + BQ > S) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int q = q0 + (i >> 2) * 8 + hh * 4 + (i & 3);
+          if (k0 + kb * 32 + l32 > q || q >= S) sc[kb][i] = -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 ll = *reinterpret_cast<const float4*>(L + g * 8 + hh * 4);
+      const float lv[4] = {ll.x, ll.y, ll.z, ll.w};
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = g * 4 + e;
+          const float pr = fast_exp2(__builtin_fmaf(sc[kb][i], c, lv[e]));
+          if constexpr (PASS) sc[kb][i] = pr * dp[kb][i];
+          else sc[kb][i] = pr;
+        }
+    }
+    // dV^T += dO^T P (PASS 0) or dK^T += Q^T dS (PASS 1), 16 queries at a
+    // time; each transposed fragment feeds both key blocks
+    auto quarter = [&](auto SS) __attribute__((always_inline)) {
+      constexpr int ss = decltype(SS)::value;
+      constexpr int T0 = PASS ? 0 : SLAB * 16;       // Q slab or dO slab
+      const bf16x8_t p0 = pack_frag(sc[0], ss), p1 = pack_frag(sc[1], ss);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const bf16x8_t ft = tr_at<T0 + ss * 16 * D * 2>(base, to[db]);
+        acc[db][0] = MFMA(ft, p0, acc[db][0]);
+        acc[db][1] = MFMA(ft, p1, acc[db][1]);
+      }
+    };
+    quarter(std::integral_constant<int, 0>());
+    quarter(std::integral_constant<int, 1>());
+  };
+
+  // the wave's pairs through its two buffers (two arrays, so the compiler
+  // waits only for the DMA of the buffer being read)
+  // Every step issues the same DMA count (past the last pair it reloads the
+  // last pair, which is not used), so the compiler's wait before reading a
+  // buffer can leave the other buffer's DMA in flight.
+  uint4* my0 = sm0 + wave * P::WBUF;
+  uint4* my1 = sm1 + wave * P::WBUF;
+  load(min(wave, total - 1), my0);
+  for (int p = wave; p < total; p += 8) {
+    load(min(p + 4, total - 1), my1);
+    pair(my0, p);
+    if (p + 4 >= total) break;
+    load(min(p + 8, total - 1), my0);
+    pair(my1, p + 4);
+  }
+
+  // sum the four waves' accumulators in wave order: each wave stores its
+  // [64 keys][D] fp32 sums (rows padded to D + 4), then thread t adds key
+  // t / 4, columns (t % 4) * D / 4 .. + D / 4, and stores bf16
+  float* red = reinterpret_cast<float*>((wave < 2 ? sm0 : sm1) + (wave & 1) * P::RED);
+  {
+    const float scale = PASS ? a.scale : 1.0f;
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the unused last reload
+    __syncthreads();
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<float4*>(red + (kb * 32 + l32) * (D + 4) + db * 32 + g * 8 + hh * 4) =
+              make_float4(acc[db][kb][g * 4], acc[db][kb][g * 4 + 1], acc[db][kb][g * 4 + 2],
+                          acc[db][kb][g * 4 + 3]);
+    __syncthreads();
+    const int key = threadIdx.x >> 2;
+    const int d0 = (threadIdx.x & 3) * (D / 4);
+    if (k0 + key < S) {
+      const float* w0 = reinterpret_cast<const float*>(sm0);
+      const float* w1 = reinterpret_cast<const float*>(sm0 + P::RED);
+      const float* w2 = reinterpret_cast<const float*>(sm1);
+      const float* w3 = reinterpret_cast<const float*>(sm1 + P::RED);
+      bf16_t* orow = out + (rb + k0 + key) * ld_d + (long)m * D + d0;
+#pragma unroll
+      for (int e = 0; e < D / 4; e += 8) {
+        const int o = key * (D + 4) + d0 + e;
+        float f[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) f[u] = (((w0[o + u] + w1[o + u]) + w2[o + u]) + w3[o + u]) * scale;
+        *reinterpret_cast<uint4*>(orow + e) = pack8(f);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------- backward dQ ----
@@ -783,29 +837,18 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t attn_bwd_partial_floats(const AttnArgs& a) {
-  return (size_t)(a.n_heads / a.n_kv_heads) * a.batch * a.seq * a.n_kv_heads * a.d;
-}
-
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
-                         long ld_d, hipStream_t s) {
-  const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
+hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta,
+                         uint16_t* dk, uint16_t* dv, long ld_d, hipStream_t s) {
+  const dim3 grid((unsigned)((a.seq + 63) / 64 * a.n_kv_heads * a.batch)), block(256);
   if (a.d == 128) {
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 0>), grid, block, 0, s, a, dout, delta, pk, pv);
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<128, 1>), grid, block, 0, s, a, dout, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_kv_k<128, 0>), grid, block, 0, s, a, dout, delta, dv, ld_d);
+    hipLaunchKernelGGL((attn_bwd_kv_k<128, 1>), grid, block, 0, s, a, dout, delta, dk, ld_d);
   } else if (a.d == 64) {
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 0>), grid, block, 0, s, a, dout, delta, pk, pv);
-    hipLaunchKernelGGL((attn_bwd_dkdv_k<64, 1>), grid, block, 0, s, a, dout, delta, pk, pv);
+    hipLaunchKernelGGL((attn_bwd_kv_k<64, 0>), grid, block, 0, s, a, dout, delta, dv, ld_d);
+    hipLaunchKernelGGL((attn_bwd_kv_k<64, 1>), grid, block, 0, s, a, dout, delta, dk, ld_d);
   } else {
     return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const long T = (long)a.batch * a.seq;
-  const int hkv = a.n_kv_heads * a.d;
-  const long work = T * (hkv / 8);
-  hipLaunchKernelGGL(attn_bwd_reduce_k, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s,
-                     pk, pv, a.n_heads / a.n_kv_heads, T, hkv, a.scale, dk, dv, ld_d);
   return hipGetLastError();
 }
 

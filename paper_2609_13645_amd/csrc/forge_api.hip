@@ -194,7 +194,7 @@ Saved saved_layout(const forge_layer_cfg& c) {
 
 // ---- workspace -------------------------------------------------------------
 struct Work {
-  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse, pk, pv;
+  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse;
   size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs, wpart;  // MoE
   size_t qk_dg, h1s, dA_s, dgu_s, db1;  // QK-Norm; shared expert
   size_t total;
@@ -241,9 +241,6 @@ Work work_layout(const forge_layer_cfg& c) {
   const bool rec = c.recompute_attn != 0;
   w.o = rec ? take(d.T * d.hq * 2) : 0;
   w.lse = rec ? take(d.B * d.nh * d.S * 4) : 0;
-  const size_t part = (size_t)(d.nh / d.nkv) * d.T * d.hkv * 4;
-  w.pk = take(part);
-  w.pv = take(part);
   w.total = off;
   return w;
 }
@@ -531,8 +528,7 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
                         scaled(gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), d.bs), s));
   if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_o, g->d_w_o, d.h * d.hq));
   FORGE_HIP(forge::attn_bwd_dq(aa, o, dO, lse, delta, dqkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, at<float>(workspace, wk.pk),
-                                 at<float>(workspace, wk.pv), dqkv + d.hq, dqkv + d.hq + d.hkv,
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, dqkv + d.hq, dqkv + d.hq + d.hkv,
                                  d.qkv, s));
   if (d.qkn) {
     // inverse RoPE and the QK-Norm backward in place; gain gradients
@@ -1480,9 +1476,7 @@ forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qk
 forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes) {
   if (forge_status s = check_attn(cfg)) return s;
   FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
-  const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
-                      cfg->n_kv_heads * cfg->head_dim * 4;
-  *bytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4) + 2 * up(part);
+  *bytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
   return ok();
 }
 
@@ -1500,14 +1494,9 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
   const forge::AttnArgs aa = attn_args(d, qkv);
   hipStream_t s = (hipStream_t)stream;
   float* delta = static_cast<float*>(workspace);
-  const size_t dbytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
-  const size_t part = (size_t)(cfg->n_heads / cfg->n_kv_heads) * cfg->batch * cfg->seq *
-                      cfg->n_kv_heads * cfg->head_dim * 4;
-  float* pk = at<float>(workspace, dbytes);
-  float* pv = at<float>(workspace, dbytes + up(part));
   FORGE_HIP(forge::attn_bwd_dq(aa, o, d_o, lse, delta, d_qkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, delta, pk, pv, d_qkv + d.hq,
-                                 d_qkv + d.hq + d.hkv, d.qkv, s));
+  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, delta, d_qkv + d.hq, d_qkv + d.hq + d.hkv, d.qkv,
+                                 s));
   return ok();
 }
 

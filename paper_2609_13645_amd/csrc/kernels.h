@@ -146,13 +146,10 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s);
 hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
                        const float* lse, float* delta, uint16_t* dq, long ld_dqkv,
                        hipStream_t s);
-// Floats of each of the two fp32 partial buffers attn_bwd_dkdv needs
-// ([n_heads / n_kv_heads][T][n_kv * d]).
-size_t attn_bwd_partial_floats(const AttnArgs& a);
-// dk, dv [T, n_kv*d] columns of the dqkv buffer (row stride ld_dqkv), via
-// per-query-head fp32 partials pk, pv summed in a fixed order.
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta, float* pk, float* pv, uint16_t* dk, uint16_t* dv,
-                         long ld_dqkv, hipStream_t s);
+// dk, dv [T, n_kv*d] columns of the dqkv buffer (row stride ld_dqkv), each
+// kv head's sums over its GQA group formed inside one block.
+hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta,
+                         uint16_t* dk, uint16_t* dv, long ld_dqkv, hipStream_t s);
 
 // ----------------------------------------------------------------- MoE ----
 // Routing of fp32 logits [T, E] (E <= 256): idx / gates [T, k], probs [T, E];
