@@ -78,6 +78,9 @@ def parse():
     ap.add_argument("--cpu-seq", type=int, default=4096,
                     help="tokens of the CPU-baseline sample (layer workloads)")
     ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--kernel-rooflines", action="store_true",
+                    help="time every kernel of a dense layer's step alone and print its "
+                         "roofline fraction (markdown table + JSON), then exit")
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the dominant kernel and a 1 GiB device copy (for "
                          "rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE passes), then exit")
@@ -251,6 +254,140 @@ def dominant_kernel(cfg, stream, step, reps):
             "flop_per_launch": flop}
 
 
+def kernel_rooflines(cfg, reps, out=sys.stdout):
+    """Every kernel of a dense layer's step run alone on one stream (HIP
+    events around `reps` launches after 3 warm-up ones), with its algorithmic
+    work per launch and the fraction of its roofline: bf16 MFMA peak for the
+    products, HBM bandwidth for the elementwise kernels and AdamW. The
+    products are the layer's twelve GEMMs with the layouts and epilogues the
+    layer uses; attention backward is the dQ kernel plus the dV and dK passes
+    (a kernel trace of this run splits it)."""
+    import torch
+    from paper_2609_13645_amd import _lib, runtime
+    assert not cfg["n_experts"] and not is_model(cfg), "dense layer workloads only"
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    T, h, f = fi.tokens(cfg), cfg["hidden"], cfg["ffn"]
+    d, nh, nkv = cfg["head_dim"], cfg["n_heads"], cfg["n_kv_heads"]
+    hq, hkv = nh * d, nkv * d
+    qkv_w = hq + 2 * hkv
+    KC, MC = _lib.GEMM_KC, _lib.GEMM_MC
+    bf = lambda *shape: (torch.randn(shape, device="cuda") * 0.5).to(torch.bfloat16)
+    f32 = lambda *shape: torch.zeros(shape, dtype=torch.float32, device="cuda")
+    rows = []
+
+    def timed(label, kernel, launch, work, unit):
+        for _ in range(3):
+            launch()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            launch()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        if unit == "TFLOP/s":
+            achieved, peak = work / us * 1e-6, PEAK_BF16_TFLOPS
+        else:
+            achieved, peak = work / us * 1e-3, 8000.0
+        rows.append({"step": label, "kernel": kernel, "avg_us": round(us, 1),
+                     "work": work, "unit": unit, "achieved": round(achieved, 1),
+                     "peak": peak, "frac": round(achieved / peak, 3)})
+
+    # the twelve products: (label, layouts, epilogue, M, N, K)
+    x_h, x_hq, x_f, x_2f, x_qkv = bf(T, h), bf(T, hq), bf(T, f), bf(T, 2 * f), bf(T, qkv_w)
+    w_qkv, w_o, w_gu, w_d = bf(qkv_w, h), bf(h, hq), bf(2 * f, h), bf(h, f)
+    c_bf = torch.empty(T * max(qkv_w, 2 * f, f, h), dtype=torch.bfloat16, device="cuda")
+    c_f32 = torch.empty(max(qkv_w, 2 * f, h) * max(h, f, hq), dtype=torch.float32, device="cuda")
+    gemms = [
+        ("QKV fwd", KC, KC, _lib.EPI_STORE_BF16, x_h, w_qkv, c_bf, None, T, qkv_w, h, h, h, qkv_w),
+        ("O fwd + residual", KC, KC, _lib.EPI_RESID_BF16, x_hq, w_o, c_bf, x_h, T, h, hq, hq, hq, h),
+        ("gate/up fwd", KC, KC, _lib.EPI_STORE_BF16, x_h, w_gu, c_bf, None, T, 2 * f, h, h, h, 2 * f),
+        ("down fwd + residual", KC, KC, _lib.EPI_RESID_BF16, x_f, w_d, c_bf, x_h, T, h, f, f, f, h),
+        ("down dgrad", KC, MC, _lib.EPI_STORE_BF16, x_h, w_d, c_bf, None, T, f, h, h, f, f),
+        ("gate/up dgrad", KC, MC, _lib.EPI_STORE_BF16, x_2f, w_gu, c_bf, None, T, h, 2 * f, 2 * f, h, h),
+        ("O dgrad", KC, MC, _lib.EPI_STORE_BF16, x_h, w_o, c_bf, None, T, hq, h, h, hq, hq),
+        ("QKV dgrad", KC, MC, _lib.EPI_STORE_BF16, x_qkv, w_qkv, c_bf, None, T, h, qkv_w, qkv_w, h, h),
+        ("down wgrad", MC, MC, _lib.EPI_STORE_F32, x_h, x_f, c_f32, None, h, f, T, h, f, f),
+        ("gate/up wgrad", MC, MC, _lib.EPI_STORE_F32, x_2f, x_h, c_f32, None, 2 * f, h, T, 2 * f, h, h),
+        ("O wgrad", MC, MC, _lib.EPI_STORE_F32, x_h, x_hq, c_f32, None, h, hq, T, h, hq, hq),
+        ("QKV wgrad", MC, MC, _lib.EPI_STORE_F32, x_qkv, x_h, c_f32, None, qkv_w, h, T, qkv_w, h, h),
+    ]
+    lay = {KC: "KC", MC: "MC"}
+    epi = {0: "StoreBF16", 1: "ResidBF16", 2: "AccF32", 3: "StoreF32"}
+    for (label, la, lb, ep, A, B, C, R, M, N, K, lda, ldb, ldc) in gemms:
+        name = (f"{kc_kernel_name(M, N)}" if (la, lb) == (KC, KC) else "ring_kernel<256,256,4,2") + \
+            f",{lay[la]},{lay[lb]},{epi[ep]}>"
+        timed(f"{label} (M={M} N={N} K={K})", name,
+              lambda la=la, lb=lb, ep=ep, A=A, B=B, C=C, R=R, M=M, N=N, K=K, lda=lda, ldb=ldb,
+              ldc=ldc: _lib.forge_gemm(la, lb, ep, A, B, C, R, M, N, K, lda, ldb, ldc,
+                                       ldc if R is not None else 0, stream),
+              2.0 * M * N * K, "TFLOP/s")
+
+    # attention: App. C's count, 4 d FLOP per unmasked (query, key) pair and
+    # head forward, twice that backward
+    S, B = cfg["seq"], cfg["batch"]
+    pairs = B * nh * S * (S + 1) / 2.0
+    ac = _lib.attn_cfg(cfg)
+    o, lse = bf(T, hq), f32(B * nh * S)
+    _lib.forge_attention_fwd(ac, x_qkv, o, lse, stream)
+    dqkv = torch.empty_like(x_qkv)
+    aws = torch.empty(_lib.forge_attention_bwd_workspace_bytes(ac), dtype=torch.uint8, device="cuda")
+    timed("attention fwd", f"attn_fwd_k<{d}>",
+          lambda: _lib.forge_attention_fwd(ac, x_qkv, o, lse, stream), 4.0 * d * pairs, "TFLOP/s")
+    timed("attention bwd (counted: 2x fwd)", f"attn_bwd_dq_k<{d}> + attn_bwd_kv_k<{d},0/1>",
+          lambda: _lib.forge_attention_bwd(ac, x_qkv, o, lse, x_hq, dqkv, aws, stream),
+          8.0 * d * pairs, "TFLOP/s")
+
+    # elementwise kernels: algorithmic HBM bytes (each input read once, each
+    # output written once)
+    g = bf(h)
+    y, rstd = torch.empty_like(x_h), f32(T)
+    timed(f"RMSNorm fwd (T={T} h={h})", "rmsnorm_fwd_k",
+          lambda: _lib.forge_rmsnorm_fwd(x_h, g, y, rstd, T, h, cfg["rms_eps"], stream),
+          4.0 * T * h + 4.0 * T + 2.0 * h, "GB/s")
+    rws = torch.empty(_lib.forge_rmsnorm_bwd_workspace_bytes(T, h), dtype=torch.uint8, device="cuda")
+    dgain, dxn, res = f32(h), torch.empty_like(x_h), bf(T, h)
+    timed(f"RMSNorm bwd + residual (T={T} h={h})", "rmsnorm_bwd_k + dg_reduce_k",
+          lambda: _lib.forge_rmsnorm_bwd(x_h, g, rstd, y, res, dxn, dgain, False, T, h, rws,
+                                         stream),
+          8.0 * T * h + 4.0 * T + 6.0 * h, "GB/s")
+    cos_t, sin_t = f32(S * d // 2), f32(S * d // 2)
+    _lib.forge_rope_table(S, d, cfg["rope_base"], cos_t, sin_t, stream)
+    timed(f"RoPE (q and k heads, T={T})", "rope_apply_k",
+          lambda: _lib.forge_rope_apply(x_qkv, qkv_w, cos_t, sin_t, None, T, S, nh + nkv, d,
+                                        False, stream),
+          4.0 * T * (hq + hkv), "GB/s")
+    a_out, dgu = torch.empty_like(x_f), torch.empty_like(x_2f)
+    timed(f"SwiGLU fwd (T={T} f={f})", "swiglu_fwd_k",
+          lambda: _lib.forge_swiglu_fwd(x_2f, a_out, T, f, stream), 6.0 * T * f, "GB/s")
+    timed(f"SwiGLU bwd (T={T} f={f})", "swiglu_bwd_k",
+          lambda: _lib.forge_swiglu_bwd(x_2f, x_f, dgu, T, f, stream), 10.0 * T * f, "GB/s")
+    flat = runtime.FlatParams(runtime.layer_shapes(cfg))
+    hp = _lib.AdamwHparams(cfg["beta1"], cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"])
+    scal = torch.tensor([1e-4, 0.1, 0.05, 1.0], dtype=torch.float32, device="cuda")
+    n_par = sum(int(np.prod(v)) for v in runtime.layer_shapes(cfg).values())
+    timed(f"AdamW over the layer ({n_par / 1e6:.1f} M params)", "adamw_k",
+          lambda: _lib.forge_adamw_step(flat.master, flat.param, flat.grad, flat.m, flat.v,
+                                        flat.n, hp, scal, stream), 30.0 * n_par, "GB/s")
+
+    # a plain 1 GiB device copy three times: calibrates the FETCH_SIZE /
+    # WRITE_SIZE counters of a --pmc pass over this run (rooflines_traffic)
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"| step | kernel | avg us | algorithmic work | achieved | peak | frac |", file=out)
+    print("|---|---|---|---|---|---|---|", file=out)
+    for r in rows:
+        w = f"{r['work'] / 1e9:.1f} GFLOP" if r["unit"] == "TFLOP/s" else f"{r['work'] / 1e6:.1f} MB"
+        print(f"| {r['step']} | `{r['kernel']}` | {r['avg_us']} | {w} | {r['achieved']} {r['unit']} "
+              f"| {r['peak']:.0f} | {r['frac']:.3f} |", file=out)
+    print(json.dumps({"workload": cfg["name"], "reps": reps, "kernels": rows}), file=out, flush=True)
+
+
 COPY_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dominant_kernel_traffic.json")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_13645_amd", "csrc", "gemm.hip")
@@ -309,6 +446,42 @@ def traffic_from_counters(fetch_csv, write_csv, kernel_grid, out=TRAFFIC_FILE):
     with open(out, "w") as f:
         json.dump(res, f, indent=1)
     print(json.dumps(res, indent=1))
+
+
+def rooflines_traffic(fetch_csv, write_csv, out=sys.stdout):
+    """HBM bytes per dispatch of every kernel in a --kernel-rooflines run,
+    from one FETCH_SIZE and one WRITE_SIZE counter pass: the median over the
+    dispatches of each (kernel, grid), converted to bytes by what the same
+    counter reads for the run's 1 GiB device copy. Products that share a
+    kernel and grid (the dgrad shapes) share a row."""
+    import csv
+    import statistics
+    from collections import defaultdict
+
+    def read(path, counter):
+        vals, copy = defaultdict(list), []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name, grid = r["Kernel_Name"], int(r["Grid_Size"])
+            if "copyBuffer" in name:
+                copy.append(float(r["Counter_Value"]))
+            elif not name.startswith("at::") and "rocclr" not in name:
+                vals[(name, grid)].append(float(r["Counter_Value"]))
+        return vals, max(copy)
+
+    fv, fc = read(fetch_csv, "FETCH_SIZE")
+    wv, wc = read(write_csv, "WRITE_SIZE")
+    print(f"copy calibration: FETCH_SIZE {fc:.0f} KiB, WRITE_SIZE {wc:.0f} KiB for "
+          f"{COPY_BYTES} bytes", file=out)
+    print("| kernel | grid (threads) | dispatches | fetch MB | write MB | HBM MB |", file=out)
+    print("|---|---|---|---|---|---|", file=out)
+    for key in sorted(fv, key=lambda k: -statistics.median(fv[k])):
+        fb = statistics.median(fv[key]) * COPY_BYTES / fc / 1e6
+        wb = statistics.median(wv.get(key, [0.0])) * COPY_BYTES / wc / 1e6
+        name = key[0] if len(key[0]) < 90 else key[0][:87] + "..."
+        print(f"| `{name}` | {key[1]} | {len(fv[key])} | {fb:.1f} | {wb:.1f} | {fb + wb:.1f} |",
+              file=out)
 
 
 def recorded_traffic():
@@ -516,6 +689,9 @@ def main():
     if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
         summarize_profile(sys.argv[2])
         return
+    if len(sys.argv) == 4 and sys.argv[1] == "--rooflines-traffic":
+        rooflines_traffic(sys.argv[2], sys.argv[3])
+        return
     if len(sys.argv) == 5 and sys.argv[1] == "--traffic-summarize":
         traffic_from_counters(sys.argv[2], sys.argv[3], int(sys.argv[4]))
         return
@@ -528,6 +704,9 @@ def main():
     cfg = fi.config(args.workload)
     if args.traffic_run:
         traffic_run(cfg, args.kernel_reps)
+        return
+    if args.kernel_rooflines:
+        kernel_rooflines(cfg, args.kernel_reps)
         return
     T = fi.tokens(cfg)
     step_flop = flops.step_flops(cfg)

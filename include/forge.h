@@ -219,6 +219,67 @@ forge_status forge_layer_saved_item(const forge_layer_cfg* cfg, int32_t item, si
 forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base,
                               float* cos_out, float* sin_out, forge_stream stream);
 
+/* ------------------------------------------------------------------------ */
+/* Elementwise steps of the layer as building blocks (the same kernels the  */
+/* layer calls; for per-kernel measurement and per-step parity tests)       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * RMSNorm forward (App. B pre-normalisation; the layer's two norms): per row
+ * t, rstd[t] = 1 / sqrt(mean_j x[t,j]^2 + eps) in fp32, y[t,j] =
+ * bf16(x[t,j] * rstd[t] * g[j]). x, y [T, h] bf16 (y must not overlap x),
+ * g [h] bf16, rstd [T] fp32. 8 <= h <= 8192, h % 8 == 0.
+ */
+forge_status forge_rmsnorm_fwd(const forge_bf16* x, const forge_bf16* g, forge_bf16* y,
+                               float* rstd, int32_t tokens, int32_t hidden, float eps,
+                               forge_stream stream);
+
+/* Scratch bytes of forge_rmsnorm_bwd (per-block gain-gradient partials).
+ * Host only. */
+forge_status forge_rmsnorm_bwd_workspace_bytes(int32_t tokens, int32_t hidden, size_t* bytes);
+
+/*
+ * RMSNorm backward: with y = RMSNorm(x; g) as above and dy [T, h] bf16,
+ * dx = d<y, dy>/dx (+ resid when resid is non-NULL: a residual stream's
+ * gradient passing the norm), written as bf16 [T, h]; the gain gradient
+ * sum_t dy*x*rstd is added to dg [h] fp32 (accumulate != 0) or stored
+ * (accumulate == 0), summed over fixed row blocks in a fixed order. rstd is
+ * the forward's. dx must not overlap x, dy or resid. Limits as the forward.
+ */
+forge_status forge_rmsnorm_bwd(const forge_bf16* x, const forge_bf16* g, const float* rstd,
+                               const forge_bf16* dy, const forge_bf16* resid, forge_bf16* dx,
+                               float* dg, int32_t accumulate, int32_t tokens, int32_t hidden,
+                               void* workspace, forge_stream stream);
+
+/*
+ * RoPE (App. B), in place on the first n_rot heads of each row of a fused
+ * qkv buffer [T, ld] bf16 (head r at columns r*head_dim ..): rotate-half
+ * pairs (i, i + head_dim/2) of token t rotated by the angle of its position
+ * (positions[t] when non-NULL, clamped to [0, seq); else t mod seq), from the
+ * forge_rope_table tables [seq, head_dim/2]; inverse != 0 rotates back (the
+ * backward). head_dim % 16 == 0, ld % 8 == 0, n_rot * head_dim <= ld.
+ */
+forge_status forge_rope_apply(forge_bf16* qkv, int64_t ld, const float* rope_cos,
+                              const float* rope_sin, const int32_t* positions, int32_t tokens,
+                              int32_t seq, int32_t n_rot, int32_t head_dim, int32_t inverse,
+                              forge_stream stream);
+
+/*
+ * SwiGLU (App. B): gu [T, 2f] bf16 holds the gate G (columns 0..f-1) and up
+ * U (columns f..2f-1) of each row; a [T, f] bf16 = bf16(silu(G) * U) with
+ * silu(z) = z / (1 + exp(-z)) in fp32. f % 8 == 0; a must not overlap gu.
+ */
+forge_status forge_swiglu_fwd(const forge_bf16* gu, forge_bf16* a, int32_t tokens, int32_t ffn,
+                              forge_stream stream);
+
+/*
+ * SwiGLU backward: from da [T, f] bf16, writes dgu [T, 2f] bf16 = [dG | dU]
+ * with dG = da * U * silu'(G), dU = da * silu(G) (fp32 math, one rounding).
+ * dgu must not overlap gu or da.
+ */
+forge_status forge_swiglu_bwd(const forge_bf16* gu, const forge_bf16* da, forge_bf16* dgu,
+                              int32_t tokens, int32_t ffn, forge_stream stream);
+
 /*
  * One decoder layer forward (App. B):
  *   a  = RMSNorm(x; attn_norm)        qkv = a w_qkv^T, RoPE on q and k

@@ -127,6 +127,12 @@ def load():
         "forge_loss_fwd_bwd": (ctypes.c_int, [ctypes.POINTER(HeadCfg), P, P, P, P, P, P,
                                               P, P, P, P]),
         "forge_embed_fwd": (ctypes.c_int, [P, P, P, I32, I32, I32, F32, P]),
+        "forge_rmsnorm_fwd": (ctypes.c_int, [P, P, P, P, I32, I32, F32, P]),
+        "forge_rmsnorm_bwd_workspace_bytes": (ctypes.c_int, [I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
+        "forge_rmsnorm_bwd": (ctypes.c_int, [P, P, P, P, P, P, P, I32, I32, I32, P, P]),
+        "forge_rope_apply": (ctypes.c_int, [P, I64, P, P, P, I32, I32, I32, I32, I32, P]),
+        "forge_swiglu_fwd": (ctypes.c_int, [P, P, I32, I32, P]),
+        "forge_swiglu_bwd": (ctypes.c_int, [P, P, P, I32, I32, P]),
         "forge_embed_bwd": (ctypes.c_int, [P, P, P, I32, I32, I32, F32, P]),
         "forge_adamw_step": (ctypes.c_int, [P, P, P, P, P, I64,
                                             ctypes.POINTER(AdamwHparams), P, P]),
@@ -299,6 +305,39 @@ def forge_loss_fwd_bwd_chunked(cfg, chunk, x_L, final_norm, w_lm, targets, loss_
 def forge_embed_fwd(ids, emb, x0, tokens, hidden, vocab, scale=1.0, stream=None):
     _check(load().forge_embed_fwd(_ptr(ids), _ptr(emb), _ptr(x0), tokens, hidden, vocab,
                                   float(scale), _stream(stream)))
+
+
+def forge_rmsnorm_fwd(x, g, y, rstd, tokens, hidden, eps, stream=None):
+    _check(load().forge_rmsnorm_fwd(_ptr(x), _ptr(g), _ptr(y), _ptr(rstd), tokens, hidden,
+                                    float(eps), _stream(stream)))
+
+
+def forge_rmsnorm_bwd_workspace_bytes(tokens, hidden) -> int:
+    n = ctypes.c_size_t()
+    _check(load().forge_rmsnorm_bwd_workspace_bytes(tokens, hidden, ctypes.byref(n)))
+    return n.value
+
+
+def forge_rmsnorm_bwd(x, g, rstd, dy, resid, dx, dg, accumulate, tokens, hidden, workspace,
+                      stream=None):
+    _check(load().forge_rmsnorm_bwd(_ptr(x), _ptr(g), _ptr(rstd), _ptr(dy), _ptr(resid),
+                                    _ptr(dx), _ptr(dg), int(bool(accumulate)), tokens, hidden,
+                                    _ptr(workspace), _stream(stream)))
+
+
+def forge_rope_apply(qkv, ld, rope_cos, rope_sin, positions, tokens, seq, n_rot, head_dim,
+                     inverse=False, stream=None):
+    _check(load().forge_rope_apply(_ptr(qkv), int(ld), _ptr(rope_cos), _ptr(rope_sin),
+                                   _ptr(positions), tokens, seq, n_rot, head_dim,
+                                   int(bool(inverse)), _stream(stream)))
+
+
+def forge_swiglu_fwd(gu, a, tokens, ffn, stream=None):
+    _check(load().forge_swiglu_fwd(_ptr(gu), _ptr(a), tokens, ffn, _stream(stream)))
+
+
+def forge_swiglu_bwd(gu, da, dgu, tokens, ffn, stream=None):
+    _check(load().forge_swiglu_bwd(_ptr(gu), _ptr(da), _ptr(dgu), tokens, ffn, _stream(stream)))
 
 
 def forge_embed_bwd(ids, dx0, d_emb, tokens, hidden, vocab, scale=1.0, stream=None):

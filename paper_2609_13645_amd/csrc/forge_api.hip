@@ -774,6 +774,120 @@ forge_status forge_rope_table(int32_t seq, int32_t head_dim, float base, float* 
   return ok();
 }
 
+namespace {
+forge_status check_rows(int32_t tokens, int32_t hidden) {
+  FORGE_CHECK(tokens >= 0, FORGE_ERR_INVALID_ARG, "tokens must be >= 0");
+  FORGE_CHECK(hidden >= 8 && hidden <= 8192 && hidden % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "hidden must be a multiple of 8 in [8, 8192]");
+  return ok();
+}
+bool overlap(const void* a, size_t an, const void* b, size_t bn) {
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  return a != nullptr && b != nullptr && x < y + bn && y < x + an;
+}
+}  // namespace
+
+forge_status forge_rmsnorm_fwd(const forge_bf16* x, const forge_bf16* g, forge_bf16* y,
+                               float* rstd, int32_t tokens, int32_t hidden, float eps,
+                               forge_stream stream) {
+  if (forge_status s = check_rows(tokens, hidden)) return s;
+  FORGE_CHECK(eps >= 0.0f && std::isfinite(eps), FORGE_ERR_INVALID_ARG, "eps must be >= 0");
+  if (tokens == 0) return ok();
+  FORGE_PTR(x);
+  FORGE_PTR(g);
+  FORGE_PTR(y);
+  FORGE_PTR(rstd);
+  const size_t n = (size_t)tokens * hidden * 2;
+  FORGE_CHECK(!overlap(x, n, y, n), FORGE_ERR_INVALID_ARG, "y overlaps x");
+  FORGE_HIP(forge::rmsnorm_fwd(x, g, y, rstd, tokens, hidden, eps, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_rmsnorm_bwd_workspace_bytes(int32_t tokens, int32_t hidden, size_t* bytes) {
+  if (forge_status s = check_rows(tokens, hidden)) return s;
+  FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = (size_t)forge::rmsnorm_bwd_blocks(tokens) * hidden * 4;
+  return ok();
+}
+
+forge_status forge_rmsnorm_bwd(const forge_bf16* x, const forge_bf16* g, const float* rstd,
+                               const forge_bf16* dy, const forge_bf16* resid, forge_bf16* dx,
+                               float* dg, int32_t accumulate, int32_t tokens, int32_t hidden,
+                               void* workspace, forge_stream stream) {
+  if (forge_status s = check_rows(tokens, hidden)) return s;
+  FORGE_PTR(g);
+  FORGE_PTR(dg);
+  hipStream_t st = (hipStream_t)stream;
+  if (tokens == 0) {
+    // no rows: the gain gradient is an empty sum (a reduction over zero
+    // partials, which stores zeros; no memset, so the call stays capturable)
+    if (!accumulate) FORGE_HIP(forge::rmsnorm_dg_reduce(nullptr, 0, dg, hidden, false, st));
+    return ok();
+  }
+  FORGE_PTR(x);
+  FORGE_PTR(rstd);
+  FORGE_PTR(dy);
+  FORGE_PTR(dx);
+  FORGE_PTR(workspace);
+  if (resid) FORGE_PTR(resid);
+  const size_t n = (size_t)tokens * hidden * 2;
+  FORGE_CHECK(!overlap(dx, n, x, n) && !overlap(dx, n, dy, n) && !overlap(dx, n, resid, n),
+              FORGE_ERR_INVALID_ARG, "dx overlaps an input");
+  float* part = static_cast<float*>(workspace);
+  FORGE_HIP(forge::rmsnorm_bwd(x, g, rstd, dy, resid, dx, part, tokens, hidden, st));
+  FORGE_HIP(forge::rmsnorm_dg_reduce(part, forge::rmsnorm_bwd_blocks(tokens), dg, hidden,
+                                     accumulate != 0, st));
+  return ok();
+}
+
+forge_status forge_rope_apply(forge_bf16* qkv, int64_t ld, const float* rope_cos,
+                              const float* rope_sin, const int32_t* positions, int32_t tokens,
+                              int32_t seq, int32_t n_rot, int32_t head_dim, int32_t inverse,
+                              forge_stream stream) {
+  FORGE_CHECK(tokens >= 0 && seq >= 1 && n_rot >= 0, FORGE_ERR_INVALID_ARG,
+              "bad tokens / seq / n_rot");
+  FORGE_CHECK(head_dim >= 16 && head_dim % 16 == 0, FORGE_ERR_INVALID_ARG,
+              "head_dim must be a positive multiple of 16");
+  FORGE_CHECK(ld % 8 == 0 && (int64_t)n_rot * head_dim <= ld, FORGE_ERR_INVALID_ARG,
+              "ld must be a multiple of 8 holding n_rot heads");
+  if (tokens == 0 || n_rot == 0) return ok();
+  FORGE_PTR(qkv);
+  FORGE_PTR(rope_cos);
+  FORGE_PTR(rope_sin);
+  FORGE_HIP(forge::rope_apply(qkv, ld, rope_cos, rope_sin, positions, tokens, seq, n_rot,
+                              head_dim, inverse != 0, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_swiglu_fwd(const forge_bf16* gu, forge_bf16* a, int32_t tokens, int32_t ffn,
+                              forge_stream stream) {
+  FORGE_CHECK(tokens >= 0 && ffn >= 8 && ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "ffn must be a positive multiple of 8");
+  if (tokens == 0) return ok();
+  FORGE_PTR(gu);
+  FORGE_PTR(a);
+  FORGE_CHECK(!overlap(a, (size_t)tokens * ffn * 2, gu, (size_t)tokens * ffn * 4),
+              FORGE_ERR_INVALID_ARG, "a overlaps gu");
+  FORGE_HIP(forge::swiglu_fwd(gu, a, tokens, ffn, (hipStream_t)stream));
+  return ok();
+}
+
+forge_status forge_swiglu_bwd(const forge_bf16* gu, const forge_bf16* da, forge_bf16* dgu,
+                              int32_t tokens, int32_t ffn, forge_stream stream) {
+  FORGE_CHECK(tokens >= 0 && ffn >= 8 && ffn % 8 == 0, FORGE_ERR_INVALID_ARG,
+              "ffn must be a positive multiple of 8");
+  if (tokens == 0) return ok();
+  FORGE_PTR(gu);
+  FORGE_PTR(da);
+  FORGE_PTR(dgu);
+  const size_t n2 = (size_t)tokens * ffn * 4;
+  FORGE_CHECK(!overlap(dgu, n2, gu, n2) && !overlap(dgu, n2, da, n2 / 2), FORGE_ERR_INVALID_ARG,
+              "dgu overlaps an input");
+  FORGE_HIP(forge::swiglu_bwd(gu, da, dgu, tokens, ffn, (hipStream_t)stream));
+  return ok();
+}
+
 forge_status forge_layer_fwd(const forge_layer_cfg* cfg, const forge_layer_weights* w,
                              const forge_bf16* x_in, forge_bf16* x_out, void* saved,
                              void* workspace, float* aux_loss, forge_stream stream) {

@@ -241,3 +241,34 @@ def test_binding_structs_match_the_c_header(tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(py), cname
         for f, _ in py._fields_:
             assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def test_elementwise_building_block_argument_rules():
+    E = _lib.ForgeError
+    bad = [
+        lambda: _lib.forge_rmsnorm_fwd(0x1000, 0x2000, 0x3000, 0x4000, 4, 12, 1e-5, 0),   # h % 8
+        lambda: _lib.forge_rmsnorm_fwd(0x1000, 0x2000, 0x3000, 0x4000, 4, 16384, 1e-5, 0),
+        lambda: _lib.forge_rmsnorm_fwd(0x1000, 0x2000, 0x1010, 0x4000, 4, 16, 1e-5, 0),  # y overlaps x
+        lambda: _lib.forge_rmsnorm_fwd(0x1000, 0x2000, 0x3000, 0x4000, 4, 16, -1.0, 0),
+        lambda: _lib.forge_rmsnorm_bwd(0x1000, 0x2000, 0x3000, 0x4000, None, 0x4000, 0x5000, 0,
+                                       4, 16, 0x6000, 0),                                # dx aliases dy
+        lambda: _lib.forge_rope_apply(0x1000, 60, 0x2000, 0x3000, None, 4, 4, 2, 32, 0, 0),  # ld % 8
+        lambda: _lib.forge_rope_apply(0x1000, 64, 0x2000, 0x3000, None, 4, 4, 3, 32, 0, 0),  # heads > ld
+        lambda: _lib.forge_rope_apply(0x1000, 64, 0x2000, 0x3000, None, 4, 4, 2, 24, 0, 0),  # d % 16
+        lambda: _lib.forge_swiglu_fwd(0x1000, 0x1040, 4, 16, 0),                          # a inside gu
+        lambda: _lib.forge_swiglu_bwd(0x1000, 0x9000, 0x1000, 4, 16, 0),                  # dgu is gu
+        lambda: _lib.forge_swiglu_fwd(0x1000, 0x9000, 4, 12, 0),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(E) as e:
+            call()
+        assert e.value.status == _lib.FORGE_ERR_INVALID_ARG, i
+    with pytest.raises(E) as e:                                                    # misaligned
+        _lib.forge_rmsnorm_fwd(0x1008, 0x2000, 0x3000, 0x4000, 4, 16, 1e-5, 0)
+    assert e.value.status == _lib.FORGE_ERR_ALIGNMENT
+    # no rows: OK without a launch
+    _lib.forge_rmsnorm_fwd(None, None, None, None, 0, 16, 1e-5, 0)
+    _lib.forge_rmsnorm_bwd(None, 0x2000, None, None, None, None, 0x5000, 1, 0, 16, None, 0)
+    _lib.forge_swiglu_fwd(None, None, 0, 16, 0)
+    _lib.forge_rope_apply(None, 64, None, None, None, 0, 4, 2, 32, 0, 0)
+    assert _lib.forge_rmsnorm_bwd_workspace_bytes(4096, 4096) % (4096 * 4) == 0
