@@ -85,9 +85,17 @@ __global__ __launch_bounds__(512) void rmsnorm_bwd_k(
        row += (long)gridDim.x * kBwdWaves) {
     const uint4* xr = reinterpret_cast<const uint4*>(x + row * h);
     const uint4* dyr = reinterpret_cast<const uint4*>(dy + row * h);
+    const uint4* rr = resid ? reinterpret_cast<const uint4*>(resid + row * h) : nullptr;
     const float r = rstd[row];
-    uint4 xv[MAXCH], dv[MAXCH];
+    uint4 xv[MAXCH], dv[MAXCH], rv[MAXCH];
     float dot = 0.0f;
+    // the residual rows are loaded with x and dy, so their latency overlaps
+    // the row's reduction
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      const int c = lane + i * 64;
+      if (c < nch && rr) rv[i] = rr[c];
+    }
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i) {
       const int c = lane + i * 64;
@@ -108,7 +116,6 @@ __global__ __launch_bounds__(512) void rmsnorm_bwd_k(
     dot = wave_sum(dot);
     const float coef = r * r * r * dot / (float)h;
     uint4* dxr = reinterpret_cast<uint4*>(dx + row * h);
-    const uint4* rr = resid ? reinterpret_cast<const uint4*>(resid + row * h) : nullptr;
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i) {
       const int c = lane + i * 64;
@@ -121,7 +128,7 @@ __global__ __launch_bounds__(512) void rmsnorm_bwd_k(
         for (int e = 0; e < 8; ++e) o[e] = r * w[e] * df[e] - coef * xf[e];
         if (rr) {
           float rf[8];
-          unpack8(rr[c], rf);
+          unpack8(rv[i], rf);
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] += rf[e];
         }
@@ -148,25 +155,38 @@ __global__ __launch_bounds__(512) void rmsnorm_bwd_k(
   }
 }
 
-// dg[c] += sum_b part[b][c]: a block covers 32 columns; 8 groups of 32
-// threads each sum a fixed stripe of partial rows, then the 8 stripe sums
-// are added in a fixed order (deterministic).
+// dg[c] += sum_b part[b][c]: a block covers 64 columns as 16 groups of four
+// (16-byte loads); 16 stripes of threads each sum every 16th partial row,
+// then the 16 stripe sums of a column are added in stripe order (fixed, so
+// deterministic).
 template <bool ACC>
 __global__ __launch_bounds__(256) void dg_reduce_k(const float* __restrict__ part, int nblk,
                                                    float* __restrict__ dg, int h) {
-  __shared__ float red[8][32];
-  const int col = blockIdx.x * 32 + (threadIdx.x & 31);
-  const int stripe = threadIdx.x >> 5;
-  float s = 0.0f;
-  if (col < h)
-    for (int b = stripe; b < nblk; b += 8) s += part[(long)b * h + col];
-  red[stripe][threadIdx.x & 31] = s;
+  __shared__ float4 red[16][16];
+  const int cg = threadIdx.x & 15, stripe = threadIdx.x >> 4;
+  const int col = blockIdx.x * 64 + cg * 4;
+  float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (col < h) {
+#pragma unroll 8
+    for (int b = stripe; b < nblk; b += 16) {
+      const float4 v = *reinterpret_cast<const float4*>(part + (long)b * h + col);
+      s.x += v.x;
+      s.y += v.y;
+      s.z += v.z;
+      s.w += v.w;
+    }
+  }
+  red[stripe][cg] = s;
   __syncthreads();
-  if (threadIdx.x < 32 && col < h) {
-    float t = 0.0f;
+  if (threadIdx.x < 64) {
+    const int c = blockIdx.x * 64 + threadIdx.x;
+    if (c < h) {
+      const float* rf = reinterpret_cast<const float*>(&red[0][0]);
+      float t = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 8; ++w) t += red[w][threadIdx.x];
-    dg[col] = ACC ? dg[col] + t : t;
+      for (int w = 0; w < 16; ++w) t += rf[w * 64 + threadIdx.x];
+      dg[c] = ACC ? dg[c] + t : t;
+    }
   }
 }
 
@@ -672,9 +692,9 @@ hipError_t rmsnorm_bwd(const uint16_t* x, const uint16_t* g, const float* rstd,
 hipError_t rmsnorm_dg_reduce(const float* dg_partial, int nblk, float* dg, int h, bool accumulate,
                              hipStream_t s) {
   if (accumulate)
-    hipLaunchKernelGGL(dg_reduce_k<true>, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
+    hipLaunchKernelGGL(dg_reduce_k<true>, dim3(blocks_for(h, 64)), dim3(256), 0, s, dg_partial, nblk, dg, h);
   else
-    hipLaunchKernelGGL(dg_reduce_k<false>, dim3(blocks_for(h, 32)), dim3(256), 0, s, dg_partial, nblk, dg, h);
+    hipLaunchKernelGGL(dg_reduce_k<false>, dim3(blocks_for(h, 64)), dim3(256), 0, s, dg_partial, nblk, dg, h);
   return hipGetLastError();
 }
 
