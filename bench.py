@@ -569,8 +569,9 @@ def _phases_and_kernel(cfg, stream, step, steps, kernel_reps):
     return phases, dominant_kernel(cfg, stream, step, kernel_reps)
 
 
-def cpu_baseline(cfg, seq):
-    """The fp64 oracle (as it stands) on a bounded sample of the workload."""
+def cpu_baseline(cfg, seq, reps=3):
+    """The fp64 oracle (as it stands) on a bounded sample of the workload,
+    timed `reps` times (the median is reported)."""
     from oracle import dense, moe, head, adamw as oadam
     try:
         from threadpoolctl import threadpool_info
@@ -586,10 +587,12 @@ def cpu_baseline(cfg, seq):
              "w_lm": None if inp["w_lm"] is None else f64(inp["w_lm"]),
              "layers": [{k: f64(v) for k, v in W.items()} for W in inp["layers"]]}
         n_params = sum(v.size for v in P["layers"][0].values()) + P["embedding"].size
-        t0 = time.perf_counter()
-        _, grads = head.model_fwd_bwd(P, inp["ids"], inp["targets"], c)
-        flat_p = [P["embedding"]] + list(P["layers"][0].values())
-        flat_g = [grads["embedding"]] + [grads["layers"][0][k] for k in P["layers"][0]]
+
+        def fwd_bwd():
+            _, grads = head.model_fwd_bwd(P, inp["ids"], inp["targets"], c)
+            flat_p = [P["embedding"]] + list(P["layers"][0].values())
+            flat_g = [grads["embedding"]] + [grads["layers"][0][k] for k in P["layers"][0]]
+            return flat_p, flat_g
         sample = (f"fp64 oracle: 1 of {cfg['n_layers']} layers, 1 of {cfg['batch']} "
                   f"sequences ({c['seq']} tokens), full LM head and CE, AdamW over that "
                   f"layer and the embedding")
@@ -602,36 +605,45 @@ def cpu_baseline(cfg, seq):
         W = {k: f64(v) for k, v in inp["weights"].items()}
         x, dy = f64(inp["x"]), f64(inp["dy"])
         n_params = sum(w.size for w in W.values())
-        t0 = time.perf_counter()
-        if cfg["n_experts"]:
-            _, _, cache = moe.layer_fwd(x, W, c)
-            _, grads = moe.layer_bwd(cache, W, c, dy)
-        else:
-            _, cache = dense.layer_fwd(x, W, c)
-            _, grads = dense.layer_bwd(cache, W, c, dy)
-        flat_p = list(W.values())
-        flat_g = [grads[k] for k in W]
+
+        def fwd_bwd():
+            if cfg["n_experts"]:
+                _, _, cache = moe.layer_fwd(x, W, c)
+                _, grads = moe.layer_bwd(cache, W, c, dy)
+            else:
+                _, cache = dense.layer_fwd(x, W, c)
+                _, grads = dense.layer_bwd(cache, W, c, dy)
+            return list(W.values()), [grads[k] for k in W]
         sample = (f"fp64 oracle: fwd+bwd of the same layer shapes over {seq} tokens "
                   f"(one sequence; the workload has {cfg['batch']} x {cfg['seq']})")
     # the optimizer over the same fraction of the parameters as the sample's
     # share of the step's tokens
     frac = fi.tokens(c) / fi.tokens(cfg)
-    budget = int(round(frac * n_params))
-    n_opt = 0
-    for p, g in zip(flat_p, flat_g):
-        if budget <= 0:
-            break
-        k = min(budget, g.size)
-        pp, gg = p.reshape(-1)[:k], g.reshape(-1)[:k]
-        oadam.adamw_step(pp, gg, np.zeros_like(pp), np.zeros_like(pp), cfg["lr"],
-                         cfg["beta1"], cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"], 1)
-        budget -= k
-        n_opt += k
-    dt = time.perf_counter() - t0
+
+    def once():
+        t0 = time.perf_counter()
+        flat_p, flat_g = fwd_bwd()
+        budget = int(round(frac * n_params))
+        n_opt = 0
+        for p, g in zip(flat_p, flat_g):
+            if budget <= 0:
+                break
+            k = min(budget, g.size)
+            pp, gg = p.reshape(-1)[:k], g.reshape(-1)[:k]
+            oadam.adamw_step(pp, gg, np.zeros_like(pp), np.zeros_like(pp), cfg["lr"],
+                             cfg["beta1"], cfg["beta2"], cfg["adam_eps"], cfg["weight_decay"], 1)
+            budget -= k
+            n_opt += k
+        return time.perf_counter() - t0, n_opt
+
+    runs = [once() for _ in range(max(1, reps))]
+    times = sorted(t for t, _ in runs)
+    dt, n_opt = times[len(times) // 2], runs[0][1]
     model_flop = flops.step_flops(c)
     return {"value": model_flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": (f"{sample}; AdamW over {n_opt / 1e6:.1f}M params; {dt:.1f} s for "
+            "sample": (f"{sample}; AdamW over {n_opt / 1e6:.1f}M params; median of "
+                       f"{len(times)} runs ({', '.join(f'{t:.2f}' for t in times)} s) for "
                        f"{model_flop / 1e12:.3f} TFLOP of model work"),
             "seconds": dt}
 
