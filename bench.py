@@ -671,6 +671,41 @@ def summarize_profile(db_path, out=sys.stdout):
               f"{max(d):.1f} | {sum(d) / 1e3:.3f} | {100 * sum(d) / total:.1f}% |", file=out)
 
 
+def step_timeline(db_path, which=2, out=sys.stdout):
+    """One layer step of a traced bench run in time order: start and duration
+    (us) from the step's first kernel, the gap to the latest end so far
+    (negative: overlapping earlier work on another stream), the stream and
+    the workgroup count. A step starts with the attention RMSNorm, the QKV
+    product and RoPE; `which` picks the traced step by its index (default 2:
+    the second timed step after one warm-up step)."""
+    import re
+    import sqlite3
+    con = sqlite3.connect(db_path)
+    rows = []
+    for name, gx, start, end, stream, wx in con.execute(
+            "select name, grid_x, start, end, stream_id, workgroup_x from kernels order by start"):
+        short = re.sub(r"\(.*", "", name.replace("void ", "").replace(
+            "forge::(anonymous namespace)::", ""))
+        rows.append((short, gx // max(1, wx), start, end, stream))
+    starts = [i for i in range(len(rows) - 2) if rows[i][0].startswith("rmsnorm_fwd")
+              and rows[i + 1][0].startswith(("gemm_kernel", "ring_kernel"))
+              and rows[i + 2][0].startswith(("rope_apply", "qknorm_rope"))]
+    i0 = starts[which]
+    nxt = [j for j in starts if j > i0]
+    i1 = (nxt[0] if nxt else len(rows)) - 1
+    while i1 > i0 and (rows[i1][0].startswith("at::") or "rocclr" in rows[i1][0]):
+        i1 -= 1   # torch's checks and copies after the step
+    t0 = prev_end = end = rows[i0][2]
+    print("| start us | duration us | gap us | stream | kernel | workgroups |", file=out)
+    print("|---|---|---|---|---|---|", file=out)
+    for name, grid, st, en, stream in rows[i0:i1 + 1]:
+        print(f"| {(st - t0) / 1e3:.1f} | {(en - st) / 1e3:.1f} | {(st - prev_end) / 1e3:.1f} | "
+              f"s{stream} | `{name[:60]}` | {grid} |", file=out)
+        prev_end = max(prev_end, en)
+        end = max(end, en)
+    print(f"\nstep span {(end - t0) / 1e3:.1f} us", file=out)
+
+
 def summarize_counters(csv_paths, out=sys.stdout):
     """Mean per dispatch of every counter, per kernel (libforge's GEMM and
     attention kernels), from rocprofv3 --pmc counter_collection CSV files."""
@@ -697,6 +732,9 @@ def summarize_counters(csv_paths, out=sys.stdout):
 def main():
     if len(sys.argv) >= 3 and sys.argv[1] == "--counters-summarize":
         summarize_counters(sys.argv[2:])
+        return
+    if len(sys.argv) in (3, 4) and sys.argv[1] == "--timeline":
+        step_timeline(sys.argv[2], *(int(a) for a in sys.argv[3:]))
         return
     if len(sys.argv) == 3 and sys.argv[1] == "--summarize":
         summarize_profile(sys.argv[2])
