@@ -561,21 +561,37 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
         }
       }
     }
-    // S and dP: each row fragment feeds both key blocks
+    // S and dP: each row fragment feeds both key blocks. The fragments of
+    // a product are all read at once (inline asm: the compiler would wait
+    // for each read before its MFMAs) and each MFMA pair waits only for its
+    // own fragment.
+    const uint32_t ab = fa::lds_off(base);
+    auto rows_product = [&](auto OFF, const bf16x8_t (&bk)[2][KK], f32x16_t (&c)[2], bool from0)
+        __attribute__((always_inline)) {
+      constexpr int O = decltype(OFF)::value;
+      bf16x8_t f[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8_t fq = row_at<0>(base, ro[kk]);
-      sc[0] = MFMA(fq, kf[0][kk], kk == 0 ? f32x16_t{} : sc[0]);
-      sc[1] = MFMA(fq, kf[1][kk], kk == 0 ? f32x16_t{} : sc[1]);
-    }
-    if constexpr (PASS) {
+      for (int kk = 0; kk < KK; ++kk) f[kk] = fa::rd_b128<O>(ab + ro[kk]);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        const bf16x8_t fo = row_at<SLAB * 16>(base, ro[kk]);
-        dp[0] = MFMA(fo, vf[0][kk], dp[0]);
-        dp[1] = MFMA(fo, vf[1][kk], dp[1]);
+        switch (KK - 1 - kk) {
+          case 7: fa::wait_lds<7>(); break;
+          case 6: fa::wait_lds<6>(); break;
+          case 5: fa::wait_lds<5>(); break;
+          case 4: fa::wait_lds<4>(); break;
+          case 3: fa::wait_lds<3>(); break;
+          case 2: fa::wait_lds<2>(); break;
+          case 1: fa::wait_lds<1>(); break;
+          default: fa::wait_lds<0>(); break;
+        }
+        fa::bind(f[kk]);
+        c[0] = MFMA(f[kk], bk[0][kk], (kk == 0 && from0) ? f32x16_t{} : c[0]);
+        c[1] = MFMA(f[kk], bk[1][kk], (kk == 0 && from0) ? f32x16_t{} : c[1]);
+        __builtin_amdgcn_sched_barrier(0);   // keep each pair at its own wait
       }
-    }
+    };
+    rows_product(fa::ic<0>{}, kf, sc, true);
+    if constexpr (PASS) rows_product(fa::ic<SLAB * 16>{}, vf, dp, false);
     // causal mask and sequence tail (diagonal and last slabs only): -inf
     // scores, so exp2 gives 0
     if (q0 < k0 + BK - 1 || q0 + BQ > S) {
@@ -605,13 +621,25 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
     // time; each transposed fragment feeds both key blocks
     auto quarter = [&](auto SS) __attribute__((always_inline)) {
       constexpr int ss = decltype(SS)::value;
-      constexpr int T0 = PASS ? 0 : SLAB * 16;       // Q slab or dO slab
+      constexpr int T0 = (PASS ? 0 : SLAB * 16) + ss * 16 * D * 2;   // Q or dO rows 16 ss..
+      // all transposed fragments of the quarter in flight (inline asm), each
+      // MFMA pair waiting only for its own two reads
+      bf16x8_t ft[DB];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) ft[db] = fa::rd_tr<T0>(ab + to[db][0], ab + to[db][1]);
       const bf16x8_t p0 = pack_frag(sc[0], ss), p1 = pack_frag(sc[1], ss);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8_t ft = tr_at<T0 + ss * 16 * D * 2>(base, to[db]);
-        acc[db][0] = MFMA(ft, p0, acc[db][0]);
-        acc[db][1] = MFMA(ft, p1, acc[db][1]);
+        switch (DB - 1 - db) {
+          case 3: fa::wait_lds<6>(); break;
+          case 2: fa::wait_lds<4>(); break;
+          case 1: fa::wait_lds<2>(); break;
+          default: fa::wait_lds<0>(); break;
+        }
+        fa::bind(ft[db]);
+        acc[db][0] = MFMA(ft[db], p0, acc[db][0]);
+        acc[db][1] = MFMA(ft[db], p1, acc[db][1]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     };
     quarter(std::integral_constant<int, 0>());
