@@ -257,7 +257,8 @@ forge_status forge_rmsnorm_bwd(const forge_bf16* x, const forge_bf16* g, const f
  * pairs (i, i + head_dim/2) of token t rotated by the angle of its position
  * (positions[t] when non-NULL, clamped to [0, seq); else t mod seq), from the
  * forge_rope_table tables [seq, head_dim/2]; inverse != 0 rotates back (the
- * backward). head_dim % 16 == 0, ld % 8 == 0, n_rot * head_dim <= ld.
+ * backward). head_dim % 16 == 0, ld % 8 == 0, n_rot * head_dim <= ld;
+ * positions (int32 [T]) 4-byte aligned.
  */
 forge_status forge_rope_apply(forge_bf16* qkv, int64_t ld, const float* rope_cos,
                               const float* rope_sin, const int32_t* positions, int32_t tokens,

@@ -855,6 +855,8 @@ forge_status forge_rope_apply(forge_bf16* qkv, int64_t ld, const float* rope_cos
   FORGE_PTR(qkv);
   FORGE_PTR(rope_cos);
   FORGE_PTR(rope_sin);
+  FORGE_CHECK((reinterpret_cast<uintptr_t>(positions) & 3u) == 0, FORGE_ERR_ALIGNMENT,
+              "positions is not 4-byte aligned");
   FORGE_HIP(forge::rope_apply(qkv, ld, rope_cos, rope_sin, positions, tokens, seq, n_rot,
                               head_dim, inverse != 0, (hipStream_t)stream));
   return ok();

@@ -266,6 +266,9 @@ def test_elementwise_building_block_argument_rules():
     with pytest.raises(E) as e:                                                    # misaligned
         _lib.forge_rmsnorm_fwd(0x1008, 0x2000, 0x3000, 0x4000, 4, 16, 1e-5, 0)
     assert e.value.status == _lib.FORGE_ERR_ALIGNMENT
+    with pytest.raises(E) as e:                                                    # positions
+        _lib.forge_rope_apply(0x1000, 64, 0x2000, 0x3000, 0x4002, 4, 4, 2, 32, 0, 0)
+    assert e.value.status == _lib.FORGE_ERR_ALIGNMENT
     # no rows: OK without a launch
     _lib.forge_rmsnorm_fwd(None, None, None, None, 0, 16, 1e-5, 0)
     _lib.forge_rmsnorm_bwd(None, 0x2000, None, None, None, None, 0x5000, 1, 0, 16, None, 0)
