@@ -867,7 +867,13 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
     }
   }
   // 8 waves of 64 x 128 (two per SIMD)
-  if (big >= 256) return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
+  if (big >= 256) {
+    // data gradients (B M/N-contiguous, read with the slower transposing
+    // reads): 128 x 64 wave tiles put the transposing reads on the narrow
+    // side of the wave tile (half as many of them per stage as with 64 x 128)
+    if constexpr (LA == kKC && LB == kMC) return launch<256, 256, 2, 4, LA, LB, EPI>(a, s);
+    return launch<256, 256, 4, 2, LA, LB, EPI>(a, s);
+  }
   if (mid >= 256) return launch<256, 128, 2, 2, LA, LB, EPI>(a, s);
   return launch<128, 128, 2, 2, LA, LB, EPI>(a, s);
 }
@@ -877,7 +883,7 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
 hipError_t gemm_grouped_m(GemmLayout lb, GemmEpilogue epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.groups <= 0) return hipSuccess;
   if (lb == kKC && epi == kStoreBF16) return launch_grouped_m<256, 256, 4, 2, kKC, kStoreBF16>(a, s);
-  if (lb == kMC && epi == kStoreBF16) return launch_grouped_m<256, 256, 4, 2, kMC, kStoreBF16>(a, s);
+  if (lb == kMC && epi == kStoreBF16) return launch_grouped_m<256, 256, 2, 4, kMC, kStoreBF16>(a, s);
   return hipErrorInvalidValue;
 }
 
