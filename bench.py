@@ -336,7 +336,8 @@ def kernel_rooflines(cfg, reps, out=sys.stdout):
     aws = torch.empty(_lib.forge_attention_bwd_workspace_bytes(ac), dtype=torch.uint8, device="cuda")
     timed("attention fwd", f"attn_fwd_k<{d}>",
           lambda: _lib.forge_attention_fwd(ac, x_qkv, o, lse, stream), 4.0 * d * pairs, "TFLOP/s")
-    timed("attention bwd (counted: 2x fwd)", f"attn_bwd_dq_k<{d}> + attn_bwd_kv_k<{d},0/1>",
+    timed("attention bwd (counted: 2x fwd)",
+          f"attn_bwd_prep_k<{d}> + attn_bwd_dv_k<{d}> + attn_bwd_dk_k<{d}> + attn_bwd_dq_k<{d}>",
           lambda: _lib.forge_attention_bwd(ac, x_qkv, o, lse, x_hq, dqkv, aws, stream),
           8.0 * d * pairs, "TFLOP/s")
 

@@ -189,7 +189,10 @@ typedef struct {
 forge_status forge_layer_saved_bytes(const forge_layer_cfg* cfg, size_t* bytes);
 
 /* Bytes of the scratch `workspace` of forge_layer_fwd / forge_layer_bwd.
- * Host only. The contents need not be preserved between calls. */
+ * Host only. The contents need not be preserved between calls. Includes the
+ * attention backward's dS scratch: batch * n_heads * 4096 * t (t + 1) / 2
+ * bf16 for t = ceil(seq / 64) 64-key tiles (the causal half of each head's
+ * seq x seq score gradient; 545 MB at 32 heads and seq 4096). */
 forge_status forge_layer_workspace_bytes(const forge_layer_cfg* cfg, size_t* bytes);
 
 /* Items of a MoE layer's saved buffer that forge_layer_saved_item locates:
@@ -582,13 +585,17 @@ typedef struct {
 forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qkv,
                                  forge_bf16* o, float* lse, forge_stream stream);
 
-/* Scratch bytes of forge_attention_bwd. Host only. */
+/* Scratch bytes of forge_attention_bwd: 2 * batch * n_heads * seq fp32
+ * (per-query -rowsum(dO o) and -lse log2 e) and the dS scratch described at
+ * forge_layer_workspace_bytes, each rounded up to 256 bytes. Host only. */
 forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes);
 
 /*
  * Attention backward: from d_o [T, hq] bf16 and the forward's qkv, o, lse,
  * writes d_qkv [T, hq+2hkv] bf16 (=): dq for every query head, dk and dv
- * summed over each kv head's query group.
+ * summed over each kv head's query group. dS = P (dP - rowsum(dO o)) is
+ * formed once, rounded to bf16 into the workspace, and dq and dk are
+ * products over it (no atomics: bitwise deterministic).
  */
 forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qkv,
                                  const forge_bf16* o, const float* lse,

@@ -1,10 +1,10 @@
 // Causal grouped-query flash attention on gfx950 MFMA: forward, and the
-// backward as a query-owned kernel that accumulates dQ (and on the way forms
-// delta = rowsum(dO * O) for the rest), and a key-owned kernel that
-// accumulates dV and dK of a kv head over every query head of its GQA group.
-// The paper's H100 kernel accumulates dQ through a flat global buffer
-// (App. D, "Anatomy of a Forged Kernel"); here the dQ kernel recomputes two
-// products instead, with no fp32 atomics, so every output is deterministic.
+// backward as a key-owned kernel that forms S, P, dP and dS once per (key,
+// query) block, accumulates dV of a kv head over every query head of its GQA
+// group and stores dS, then one key-owned and one query-owned product over
+// the stored dS for dK and dQ. The paper's H100 kernel accumulates dQ
+// through a flat global buffer (App. D, "Anatomy of a Forged Kernel"); here
+// no output takes fp32 atomics, so every output is deterministic.
 //
 // Operand layout. The 32x32x16 MFMA gives each lane one column of its 32x32
 // result and sixteen rows. Scores are formed with the lane-owned index on the
@@ -414,35 +414,101 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   }
 }
 
-// ------------------------------------------------------ backward dK, dV ----
-// Block: 64 keys [k0, k0 + 64) of one (batch, kv head), four waves, one wave
-// per SIMD. The block's work is every (query head of the GQA group, 32-query
-// slab at or after k0) pair; wave w takes pairs w, w + 4, w + 8, ... and
-// accumulates over them, for all 64 keys,
-//   PASS 0: S = Q K^T, P = exp2(S c - LSE log2 e), dV^T += dO^T P
-//   PASS 1: S, P, dP = dO V^T - delta (accumulators start at -delta),
-//           dS = P dP, dK^T += Q^T dS.
-// The wave keeps K (and V) of its 64 keys in registers as two 32-key column
-// blocks, so every Q / dO fragment read from LDS feeds two MFMAs (a 32-key
-// wave reads twice the LDS bytes per FLOP, which at the MFMA rate is the
-// LDS bandwidth of the whole CU). S is formed in both passes (5 products
-// instead of 4): one pass holding both d x 64 accumulators, K and V does
-// not fit the register file.
-// Each wave streams its own pairs' Q / dO slabs (with their LSE and delta)
-// through a private double buffer in LDS, so the waves never wait for each
-// other inside the loop. At the end the four waves' accumulators are summed
-// through LDS in wave order, so the result does not depend on timing, and
-// written as bf16: no partials leave the block, and K / V are read once per
-// GQA group.
+// ------------------------------------------------------------ backward ----
+// Four launches and five MFMA products in all (S recomputed once), with no
+// atomics, so every output is deterministic:
+//  1. attn_bwd_prep_k: per query, -delta = -rowsum(dO * O) and
+//     -LSE log2(e) (the exponent offset of P = exp(S - LSE) in base 2).
+//  2. attn_bwd_dv_k, key-owned (64 keys of a kv head per block):
+//     S = Q K^T, P, dP = dO V^T, dS = P (dP - delta); dV = sum P^T dO over
+//     the GQA group; dS goes to a scratch buffer in bf16, the precision the
+//     dK and dQ products take it in.
+//  3. attn_bwd_dk_k, key-owned: dK = scale * sum dS^T Q from the stored dS.
+//  4. attn_bwd_dq_k, query-owned: dQ = scale * dS K from the stored dS.
+// The paper's H100 kernel accumulates dQ through fp32 atomics in a flat
+// buffer (App. D); here dQ is a product of its own over the stored dS, and
+// dK no longer needs S and dP formed a second time.
+//
+// dS layout, per (batch, head): for 64-key tile kt, one 4 KB block per
+// 32-query slab j = 2 kt .. NS - 1 (NS = ceil(seq / 32)) in slab order, so
+// only the causal half is stored. A block holds its 64 x 32 values in the
+// dV pass's accumulator order: value 4 g + e of lane hh * 32 + l32 of key
+// block kb, (key 32 kb + l32, query 8 g + 4 hh + e), is element
+// 4 (g & 1) + e of the 16-byte piece at
+//   kb * 2 KB + u * 1 KB + (((2 l32 + hh) * 16) ^ (u * 128)),  u = g / 2.
+// (A key's two lane halves sit side by side and the second query half is
+// shifted by 128 bytes, so the dQ pass's transposed reads cover all banks.)
+// Every
+// visited block is written whole (zeros where the mask or the sequence end
+// removes a score). That order is also the dK pass's B-fragment order
+// (loaded straight into registers, 1 KB per wave instruction); the dQ pass
+// reads its transpose with ds_read_b64_tr_b16.
+struct DsLayout {
+  int ns;      // 32-query slabs of the sequence
+  long head;   // elements per (batch, head)
+  __host__ __device__ explicit DsLayout(int S) {
+    ns = (S + 31) / 32;
+    const long nkt = (S + 63) / 64;
+    head = 2048L * (nkt * ns - nkt * (nkt - 1));
+  }
+  __host__ __device__ long tile(int kt) const { return 2048L * ((long)kt * ns - (long)kt * (kt - 1)); }
+  __host__ __device__ long block(int kt, int j) const { return tile(kt) + 2048L * (j - 2 * kt); }
+};
+
+// 1. -delta and -LSE log2(e) of every (batch, head, query): D / 8 lanes per
+// (token, head) row of dO and O, 16-byte loads (the heads of a token are
+// adjacent rows).
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_prep_k(const bf16_t* __restrict__ o,
+                                                       const bf16_t* __restrict__ dout,
+                                                       const float* __restrict__ lse,
+                                                       float* __restrict__ delta, long rows,
+                                                       int n_heads, int S) {
+  constexpr int TPR = D / 8;
+  const long r = (long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  const int c = threadIdx.x % TPR;
+  float s = 0.0f;
+  if (r < rows) {
+    float x[8], y[8];
+    unpack8(*reinterpret_cast<const uint4*>(dout + r * D + c * 8), x);
+    unpack8(*reinterpret_cast<const uint4*>(o + r * D + c * 8), y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s = __builtin_fmaf(x[e], y[e], s);
+  }
+#pragma unroll
+  for (int w = TPR / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+  if (c == 0 && r < rows) {
+    const long t = r / n_heads;
+    const int n = (int)(r % n_heads);
+    const long li = ((t / S) * n_heads + n) * S + t % S;
+    delta[li] = -s;
+    delta[rows + li] = -lse[li] * kLog2e;
+  }
+}
+
+// 2-3. Key-owned blocks: 64 keys [k0, k0 + 64) of one (batch, kv head), four
+// waves, one per SIMD. The block's work is every (query head of the GQA
+// group, 32-query slab at or after k0) pair; wave w takes pairs w, w + 4,
+// ... and accumulates over them for all 64 keys, streaming each pair's
+// operands through a private LDS double buffer (no block barrier in the
+// loop). At the end the four waves' sums are added through LDS in wave
+// order, so the result does not depend on timing, and written as bf16: no
+// partials leave the block, and K / V are read once per GQA group.
 template <int D>
 struct KvPlan {
   static constexpr int BK = 64, BQ = 32;
   static constexpr int SLAB = BQ * D / 8;         // 16-byte chunks of a 32-row tile
-  static constexpr int WBUF = 2 * SLAB + 16;      // Q, dO slabs, LSE[32] | delta[32]
   static constexpr int RED = BK * (D + 4) / 4;    // one wave's [64][D + 4] fp32 sums
-  static constexpr int ARR = 4 * WBUF > 2 * RED ? 4 * WBUF : 2 * RED;
   static constexpr int LPR = D / 8, RPI = 64 / LPR, PER = BQ / RPI;  // DMA of a slab
-  static constexpr int DMA = 2 * PER + 1;         // DMA instructions per pair
+};
+// dV pass: per-wave buffer (Q, dO slabs, -LSE log2 e | -delta) and its DMA
+// instructions per pair
+template <int D>
+struct KvBuf {
+  using P = KvPlan<D>;
+  static constexpr int WBUF = 2 * P::SLAB + 16;
+  static constexpr int DMA = 2 * P::PER + 1;
+  static constexpr int ARR = 4 * WBUF > 2 * P::RED ? 4 * WBUF : 2 * P::RED;
 };
 // s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding: vmcnt
 // bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 at their maxima)
@@ -470,15 +536,64 @@ __device__ __forceinline__ void dma_slab(const bf16_t* base, long ld, int row0, 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(lds + i * 64), 16, off[i], 0, 0, 0);
 }
 
-template <int D, int PASS>
-__global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
-                                                        const bf16_t* __restrict__ dout,
-                                                        const float* __restrict__ delta,
-                                                        bf16_t* __restrict__ out, long ld_d) {
+// The four waves' [64 keys][D] accumulators (acc[db][kb]: rows d, columns
+// keys) summed in wave order through sm0 / sm1, times scale, stored as bf16
+// rows out[key][D] (key-major, row stride ld).
+template <int D>
+__device__ __forceinline__ void kv_reduce_store(const f32x16_t (&acc)[D / 32][2], uint4* sm0,
+                                                uint4* sm1, int wave, int lane, float scale,
+                                                bf16_t* out, long ld, int nkeys) {
   using P = KvPlan<D>;
+  constexpr int DB = D / 32;
+  const int hh = lane >> 5, l32 = lane & 31;
+  float* red = reinterpret_cast<float*>((wave < 2 ? sm0 : sm1) + (wave & 1) * P::RED);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the unused last reload
+  __syncthreads();
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(red + (kb * 32 + l32) * (D + 4) + db * 32 + g * 8 + hh * 4) =
+            make_float4(acc[db][kb][g * 4], acc[db][kb][g * 4 + 1], acc[db][kb][g * 4 + 2],
+                        acc[db][kb][g * 4 + 3]);
+  __syncthreads();
+  const int key = threadIdx.x >> 2;
+  const int d0 = (threadIdx.x & 3) * (D / 4);
+  if (key < nkeys) {
+    const float* w0 = reinterpret_cast<const float*>(sm0);
+    const float* w1 = reinterpret_cast<const float*>(sm0 + P::RED);
+    const float* w2 = reinterpret_cast<const float*>(sm1);
+    const float* w3 = reinterpret_cast<const float*>(sm1 + P::RED);
+    bf16_t* orow = out + (long)key * ld + d0;
+#pragma unroll
+    for (int e = 0; e < D / 4; e += 8) {
+      const int o = key * (D + 4) + d0 + e;
+      float f[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) f[u] = (((w0[o + u] + w1[o + u]) + w2[o + u]) + w3[o + u]) * scale;
+      *reinterpret_cast<uint4*>(orow + e) = pack8(f);
+    }
+  }
+}
+
+// 2. dV pass. Per pair: S and dP (accumulators starting at -delta, so they
+// hold dP - delta), P = exp2(S c - LSE log2 e), dS = P (dP - delta) stored,
+// dV^T += dO^T P. The wave keeps K and V of its 64 keys in registers as two
+// 32-key column blocks, so every Q / dO fragment read from LDS feeds two
+// MFMAs.
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dv_k(AttnArgs a,
+                                                       const bf16_t* __restrict__ dout,
+                                                       const float* __restrict__ delta,
+                                                       bf16_t* __restrict__ ds,
+                                                       bf16_t* __restrict__ dv, long ld_d) {
+  using P = KvPlan<D>;
+  using B = KvBuf<D>;
   constexpr int BK = P::BK, BQ = P::BQ, SLAB = P::SLAB, KK = D / 16, DB = D / 32;
-  __shared__ uint4 sm0[P::ARR];
-  __shared__ uint4 sm1[P::ARR];
+  __shared__ uint4 sm0[B::ARR];
+  __shared__ uint4 sm1[B::ARR];
 
   const int S = a.seq;
   const int grp = a.n_heads / a.n_kv_heads;
@@ -498,10 +613,11 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
   const long rb = (long)b * S;
   const long ldo = (long)a.n_heads * D;
   const long nrows = (long)a.batch * a.n_heads * S;
+  const DsLayout L(S);
 
-  // K (and V) rows of the lane's two keys k0 + l32 and k0 + 32 + l32: the
+  // K and V rows of the lane's two keys k0 + l32 and k0 + 32 + l32: the
   // B operands of S and dP
-  bf16x8_t kf[2][KK], vf[2][PASS ? KK : 1];
+  bf16x8_t kf[2][KK], vf[2][KK];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int key = k0 + kb * 32 + l32;
@@ -509,7 +625,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       kf[kb][kk] = gload_frag(a.k + r + kk * 16, key < S);
-      if constexpr (PASS) vf[kb][kk] = gload_frag(a.v + r + kk * 16, key < S);
+      vf[kb][kk] = gload_frag(a.v + r + kk * 16, key < S);
     }
   }
   f32x16_t acc[DB][2];
@@ -525,11 +641,16 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
   uint32_t ro[KK], to[DB][2];
   frag_offsets<D>(lane, ro, to);
   const __amdgpu_buffer_rsrc_t drs = rsrc(delta);
+  const int pc0 = (2 * l32 + hh) * 8;   // the lane's dS piece (elements) in a 1 KB half
 
-  // pair p: query head m * grp + p / ns, slab j0 + p % ns
+  // pair p: query head m * grp + p % grp, slab j0 + ns - 1 - p / grp. Every
+  // block of the kv group walks the slabs from the sequence end, head-minor,
+  // so the blocks running at once read the same Q / dO slabs (one XCD's L2
+  // serves them; block ids cycle through the kv heads, which the dispatcher
+  // spreads over the XCDs)
   auto load = [&](int p, uint4* base) __attribute__((always_inline)) {
-    const int n = m * grp + p / ns;
-    const int q0 = (j0 + p % ns) * BQ;
+    const int n = m * grp + p % grp;
+    const int q0 = (j0 + ns - 1 - p / grp) * BQ;
     dma_slab<D>(a.q + rb * a.ld_qkv + (long)n * D, a.ld_qkv, q0, S, base, qoff);
     dma_slab<D>(dout + rb * ldo + (long)n * D, ldo, q0, S, base + SLAB, ooff);
     // lanes 0-31: -LSE log2(e) of the slab's queries; lanes 32-63: -delta
@@ -542,23 +663,22 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
     // this buffer's DMA has landed once only the other buffer's (issued
     // after it) can still be in flight
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(P::DMA));
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(B::DMA));
     __builtin_amdgcn_sched_barrier(0);
-    const int q0 = (j0 + p % ns) * BQ;
-    const float* L = reinterpret_cast<const float*>(base + 2 * SLAB);
-    const float* Dl = L + BQ;
-    f32x16_t sc[2], dp[PASS ? 2 : 1];
-    if constexpr (PASS) {
+    const int n = m * grp + p % grp;
+    const int q0 = (j0 + ns - 1 - p / grp) * BQ;
+    const float* Lp = reinterpret_cast<const float*>(base + 2 * SLAB);
+    const float* Dl = Lp + BQ;
+    f32x16_t sc[2], dp[2];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 dd = *reinterpret_cast<const float4*>(Dl + g * 8 + hh * 4);
+    for (int g = 0; g < 4; ++g) {
+      const float4 dd = *reinterpret_cast<const float4*>(Dl + g * 8 + hh * 4);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          dp[kb][g * 4 + 0] = dd.x;
-          dp[kb][g * 4 + 1] = dd.y;
-          dp[kb][g * 4 + 2] = dd.z;
-          dp[kb][g * 4 + 3] = dd.w;
-        }
+      for (int kb = 0; kb < 2; ++kb) {
+        dp[kb][g * 4 + 0] = dd.x;
+        dp[kb][g * 4 + 1] = dd.y;
+        dp[kb][g * 4 + 2] = dd.z;
+        dp[kb][g * 4 + 3] = dd.w;
       }
     }
     // S and dP: each row fragment feeds both key blocks. The fragments of
@@ -566,7 +686,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
     // for each read before its MFMAs) and each MFMA pair waits only for its
     // own fragment.
     const uint32_t ab = fa::lds_off(base);
-    auto rows_product = [&](auto OFF, const bf16x8_t (&bk)[2][KK], f32x16_t (&c)[2], bool from0)
+    auto rows_product = [&](auto OFF, const bf16x8_t (&bk)[2][KK], f32x16_t (&cc)[2], bool from0)
         __attribute__((always_inline)) {
       constexpr int O = decltype(OFF)::value;
       bf16x8_t f[KK];
@@ -585,13 +705,13 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
           default: fa::wait_lds<0>(); break;
         }
         fa::bind(f[kk]);
-        c[0] = MFMA(f[kk], bk[0][kk], (kk == 0 && from0) ? f32x16_t{} : c[0]);
-        c[1] = MFMA(f[kk], bk[1][kk], (kk == 0 && from0) ? f32x16_t{} : c[1]);
+        cc[0] = MFMA(f[kk], bk[0][kk], (kk == 0 && from0) ? f32x16_t{} : cc[0]);
+        cc[1] = MFMA(f[kk], bk[1][kk], (kk == 0 && from0) ? f32x16_t{} : cc[1]);
         __builtin_amdgcn_sched_barrier(0);   // keep each pair at its own wait
       }
     };
     rows_product(fa::ic<0>{}, kf, sc, true);
-    if constexpr (PASS) rows_product(fa::ic<SLAB * 16>{}, vf, dp, false);
+    rows_product(fa::ic<SLAB * 16>{}, vf, dp, false);
     // causal mask and sequence tail (diagonal and last slabs only): -inf
     // scores, so exp2 gives 0
     if (q0 < k0 + BK - 1 || q0 + BQ > S) {
@@ -603,9 +723,10 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
           if (k0 + kb * 32 + l32 > q || q >= S) sc[kb][i] = -INFINITY;
         }
     }
+    // P into sc, dS into dp
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const float4 ll = *reinterpret_cast<const float4*>(L + g * 8 + hh * 4);
+      const float4 ll = *reinterpret_cast<const float4*>(Lp + g * 8 + hh * 4);
       const float lv[4] = {ll.x, ll.y, ll.z, ll.w};
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -613,15 +734,24 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
         for (int e = 0; e < 4; ++e) {
           const int i = g * 4 + e;
           const float pr = fast_exp2(__builtin_fmaf(sc[kb][i], c, lv[e]));
-          if constexpr (PASS) sc[kb][i] = pr * dp[kb][i];
-          else sc[kb][i] = pr;
+          dp[kb][i] = pr * dp[kb][i];
+          sc[kb][i] = pr;
         }
     }
-    // dV^T += dO^T P (PASS 0) or dK^T += Q^T dS (PASS 1), 16 queries at a
-    // time; each transposed fragment feeds both key blocks
+    // the pair's dS block, in accumulator order: 16-byte stores, 1 KB per
+    // wave instruction
+    bf16_t* blk = ds + ((long)b * a.n_heads + n) * L.head + L.block(kt, q0 / BQ);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        *reinterpret_cast<bf16x8_t*>(blk + kb * 1024 + u * 512 + (pc0 ^ (u * 64))) =
+            pack_frag(dp[kb], u);
+    // dV^T += dO^T P, 16 queries at a time; each transposed fragment feeds
+    // both key blocks
     auto quarter = [&](auto SS) __attribute__((always_inline)) {
       constexpr int ss = decltype(SS)::value;
-      constexpr int T0 = (PASS ? 0 : SLAB * 16) + ss * 16 * D * 2;   // Q or dO rows 16 ss..
+      constexpr int T0 = SLAB * 16 + ss * 16 * D * 2;   // dO rows 16 ss ..
       // all transposed fragments of the quarter in flight (inline asm), each
       // MFMA pair waiting only for its own two reads
       bf16x8_t ft[DB];
@@ -649,10 +779,10 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
   // the wave's pairs through its two buffers (two arrays, so the compiler
   // waits only for the DMA of the buffer being read)
   // Every step issues the same DMA count (past the last pair it reloads the
-  // last pair, which is not used), so the compiler's wait before reading a
-  // buffer can leave the other buffer's DMA in flight.
-  uint4* my0 = sm0 + wave * P::WBUF;
-  uint4* my1 = sm1 + wave * P::WBUF;
+  // last pair, which is not used), so the wait before reading a buffer can
+  // leave the other buffer's DMA in flight.
+  uint4* my0 = sm0 + wave * B::WBUF;
+  uint4* my1 = sm1 + wave * B::WBUF;
   load(min(wave, total - 1), my0);
   for (int p = wave; p < total; p += 8) {
     load(min(p + 4, total - 1), my1);
@@ -661,185 +791,295 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_kv_k(AttnArgs a,
     load(min(p + 8, total - 1), my0);
     pair(my1, p + 4);
   }
+  kv_reduce_store<D>(acc, sm0, sm1, wave, lane, 1.0f, dv + (rb + k0) * ld_d + (long)m * D,
+                             ld_d, S - k0);
+}
 
-  // sum the four waves' accumulators in wave order: each wave stores its
-  // [64 keys][D] fp32 sums (rows padded to D + 4), then thread t adds key
-  // t / 4, columns (t % 4) * D / 4 .. + D / 4, and stores bf16
-  float* red = reinterpret_cast<float*>((wave < 2 ? sm0 : sm1) + (wave & 1) * P::RED);
-  {
-    const float scale = PASS ? a.scale : 1.0f;
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // the unused last reload
-    __syncthreads();
+// 3. dK pass: dK^T += Q^T dS over the block's pairs. Each pair's Q slab and
+// dS block go through the wave's LDS ring by DMA; the A operand is the Q
+// slab's transposed fragments (as the dV pass reads dO^T), and the dS block
+// is already in B-fragment order, so each B fragment is one 16-byte read
+// (1 KB per wave instruction, contiguous). Each wave keeps KR pairs in
+// flight: the pass streams dS from HBM with little arithmetic per byte.
+template <int D>
+struct DkPlan {
+  using P = KvPlan<D>;
+  static constexpr int KR = 3;                      // ring depth (pairs per wave)
+  static constexpr int SLOT = P::SLAB + 256;        // Q slab + 4 KB dS block
+  static constexpr int MEM = P::PER + 4;            // DMA instructions per pair
+  static constexpr int RING = 4 * KR * SLOT;        // chunks of the four waves' rings
+  static constexpr int ARR = RING > 4 * P::RED ? RING : 4 * P::RED;
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 1) void attn_bwd_dk_k(AttnArgs a, const bf16_t* __restrict__ ds,
+                                                       bf16_t* __restrict__ dk, long ld_d) {
+  using P = KvPlan<D>;
+  using R = DkPlan<D>;
+  constexpr int BK = P::BK, BQ = P::BQ, KK = D / 16, DB = D / 32, KR = R::KR;
+  constexpr int NR = 2 * DB + 2;   // LDS reads of one 16-query step
+  __shared__ uint4 sm[R::ARR];
+
+  const int S = a.seq;
+  const int grp = a.n_heads / a.n_kv_heads;
+  const int per_kt = a.n_kv_heads * a.batch;
+  const int kt = (int)blockIdx.x / per_kt;
+  const int m = (int)blockIdx.x % per_kt % a.n_kv_heads;
+  const int b = (int)blockIdx.x % per_kt / a.n_kv_heads;
+  const int k0 = kt * BK;
+  const int j0 = k0 / BQ;
+  const int ns = (S + BQ - 1) / BQ - j0;
+  const int total = grp * ns;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const long rb = (long)b * S;
+  const DsLayout L(S);
+
+  f32x16_t acc[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) zero(acc[db][kb]);
+
+  uint32_t qoff[P::PER];
+  slab_offsets<D>(a.ld_qkv, lane, qoff);
+  uint32_t ro[KK], to[DB][2];
+  frag_offsets<D>(lane, ro, to);
+  // the (batch, key tile kt) dS blocks of query head n are consecutive:
+  // pair p's block is ns - 1 - p / grp blocks after the tile's first
+  const bf16_t* dsk = ds + L.tile(kt);
+  uint4* ring = sm + wave * KR * R::SLOT;
+  const uint32_t lb = lane * 16;   // the lane's 16 bytes of each 1 KB of a dS block (DMA)
+  // the lane's B fragments in a dS block: half ss at ss * 1 KB + (pc ^ ss * 128)
+  const uint32_t pc = (uint32_t)((2 * (lane & 31) + (lane >> 5)) * 16);
+
+  // pair p into ring slot u: the Q slab, then the dS block (four 1 KB DMA)
+  auto load = [&](int p, int u) __attribute__((always_inline)) {
+    const int n = m * grp + p % grp;
+    const int q0 = (j0 + ns - 1 - p / grp) * BQ;
+    uint4* slot = ring + u * R::SLOT;
+    dma_slab<D>(a.q + rb * a.ld_qkv + (long)n * D, a.ld_qkv, q0, S, slot, qoff);
+    const __amdgpu_buffer_rsrc_t r =
+        rsrc(dsk + ((long)b * a.n_heads + n) * L.head + 2048L * (ns - 1 - p / grp));
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(slot + P::SLAB + i * 64), 16,
+                                               lb + i * 1024, 0, 0, 0);
+  };
+
+  auto pair = [&](int u) __attribute__((always_inline)) {
+    // this pair's DMA has landed once only the KR - 1 pairs issued after it
+    // can still be in flight
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((KR - 1) * R::MEM));
+    __builtin_amdgcn_sched_barrier(0);
+    const uint32_t ab = fa::lds_off(ring + u * R::SLOT);
+    // both 16-query steps' fragments in flight; each step's MFMAs wait for
+    // its own reads.
+    bf16x8_t ft[2][DB], fb[2][2];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) ft[0][db] = fa::rd_tr<0>(ab + to[db][0], ab + to[db][1]);
+    fb[0][0] = fa::rd_b128<P::SLAB * 16>(ab + pc);
+    fb[0][1] = fa::rd_b128<P::SLAB * 16 + 2048>(ab + pc);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
+      ft[1][db] = fa::rd_tr<16 * D * 2>(ab + to[db][0], ab + to[db][1]);
+    fb[1][0] = fa::rd_b128<P::SLAB * 16 + 1024>(ab + (pc ^ 128));
+    fb[1][1] = fa::rd_b128<P::SLAB * 16 + 2048 + 1024>(ab + (pc ^ 128));
+    fa::wait_lds<NR>();
+    fa::bind(fb[0][0]);
+    fa::bind(fb[0][1]);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int db = 0; db < DB; ++db) fa::bind(ft[0][db]);
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-          *reinterpret_cast<float4*>(red + (kb * 32 + l32) * (D + 4) + db * 32 + g * 8 + hh * 4) =
-              make_float4(acc[db][kb][g * 4], acc[db][kb][g * 4 + 1], acc[db][kb][g * 4 + 2],
-                          acc[db][kb][g * 4 + 3]);
-    __syncthreads();
-    const int key = threadIdx.x >> 2;
-    const int d0 = (threadIdx.x & 3) * (D / 4);
-    if (k0 + key < S) {
-      const float* w0 = reinterpret_cast<const float*>(sm0);
-      const float* w1 = reinterpret_cast<const float*>(sm0 + P::RED);
-      const float* w2 = reinterpret_cast<const float*>(sm1);
-      const float* w3 = reinterpret_cast<const float*>(sm1 + P::RED);
-      bf16_t* orow = out + (rb + k0 + key) * ld_d + (long)m * D + d0;
+    for (int db = 0; db < DB; ++db) {
+      acc[db][0] = MFMA(ft[0][db], fb[0][0], acc[db][0]);
+      acc[db][1] = MFMA(ft[0][db], fb[0][1], acc[db][1]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    fa::wait_lds<0>();
+    fa::bind(fb[1][0]);
+    fa::bind(fb[1][1]);
 #pragma unroll
-      for (int e = 0; e < D / 4; e += 8) {
-        const int o = key * (D + 4) + d0 + e;
-        float f[8];
+    for (int db = 0; db < DB; ++db) fa::bind(ft[1][db]);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) f[u] = (((w0[o + u] + w1[o + u]) + w2[o + u]) + w3[o + u]) * scale;
-        *reinterpret_cast<uint4*>(orow + e) = pack8(f);
+    for (int db = 0; db < DB; ++db) {
+      acc[db][0] = MFMA(ft[1][db], fb[1][0], acc[db][0]);
+      acc[db][1] = MFMA(ft[1][db], fb[1][1], acc[db][1]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // The wave's pairs p = wave + 4 i; pair i sits in slot i % KR. Every step
+  // issues the same number of DMA instructions (past the last pair it
+  // reloads the last pair, unused), so the wait count above is exact.
+#pragma unroll
+  for (int u = 0; u < KR - 1; ++u) load(min(wave + 4 * u, total - 1), u);
+  bool done = false;
+  for (int p = wave; !done; p += 4 * KR) {
+#pragma unroll
+    for (int u = 0; u < KR; ++u) {
+      if (!done) {
+        const int pp = p + 4 * u;
+        if (pp >= total) {
+          done = true;
+        } else {
+          load(min(pp + 4 * (KR - 1), total - 1), (u + KR - 1) % KR);
+          pair(u);
+        }
       }
     }
   }
+  kv_reduce_store<D>(acc, sm, sm + 2 * P::RED, wave, lane, a.scale,
+                     dk + (rb + k0) * ld_d + (long)m * D, ld_d, S - k0);
 }
 
-// ---------------------------------------------------------- backward dQ ----
-// Block: 128 queries (32 per wave) of one (batch, head); key tiles of 64.
-// Runs first in the backward: each lane forms its query's
-// delta = rowsum(dO * O) from the dO row it holds anyway and the O row (the
-// two halves of d meet through one lane exchange), and stores, for the
-// key-owned kernels, -delta (it initialises their dP accumulators, which
-// then hold dP - delta) and, in the second half of the buffer,
-// -LSE * log2(e) (the exponent offset of P = exp(S - LSE) in base 2).
-// P is recomputed from the saved LSE (exponent argument as one FMA), then
-// dS = P (dP - delta) and dQ^T += K^T dS^T, one 32-key half of a tile at a
-// time (the whole tile's scores, dP and K^T fragments do not fit in the
-// registers of two waves per SIMD). LDS double buffering, batched fragment
-// reads and explicit waits.
+// 4. dQ: block of 256 queries (32 per wave, eight waves) of one (batch,
+// head), 64-key tiles up to the diagonal: dQ^T += K^T dS^T, both operands
+// transposed reads from LDS: K^T from the natural K tile [64 keys][D], dS^T
+// from the tile's eight dS blocks (wave w's 32 queries are block w), whose
+// accumulator order holds four consecutive queries of one key in 8 bytes,
+// the row piece ds_read_b64_tr_b16 transposes. Three stages in a ring, each
+// tile's DMA issued two tiles ahead, and each wave waits only for the
+// oldest stage's DMA. A wave whose queries all precede a tile skips it;
+// blocks of a tile that do not exist (queries before the keys) are fetched
+// as zeros.
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ o,
-                                                const bf16_t* __restrict__ dout,
-                                                const float* __restrict__ lse,
-                                                float* __restrict__ delta,
-                                                bf16_t* __restrict__ dq, long ld_d) {
-  constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
-  __shared__ uint4 sm0[2 * NAT];
-  __shared__ uint4 sm1[2 * NAT];
+struct DqPlan {
+  static constexpr int BQ = 256, BKV = 64, NW = 8, NST = 3;
+  static constexpr int NAT = BKV * D / 8;      // K tile chunks
+  static constexpr int NDS = BKV * BQ / 8;     // dS tile chunks (eight 4 KB blocks)
+  static constexpr int STAGE = NAT + NDS;
+  static constexpr int MEM = DmaPlan<D, NW>::PER + NDS / 64 / NW;   // DMA per wave per tile
+};
+
+template <int D>
+__global__ __launch_bounds__(512, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t* __restrict__ ds,
+                                                       bf16_t* __restrict__ dq, long ld_d) {
+  using Q = DqPlan<D>;
+  constexpr int BQ = Q::BQ, BKV = Q::BKV, NAT = Q::NAT, NW = Q::NW, NST = Q::NST, DB = D / 32;
+  __shared__ uint4 sm[NST * Q::STAGE];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
-  const int qt = nqt - 1 - (int)blockIdx.x;
-  const int n = blockIdx.y, b = blockIdx.z;
-  const int m = n / (a.n_heads / a.n_kv_heads);
+  // block id: kv head fastest (the dispatcher spreads consecutive ids over
+  // the XCDs, so each XCD's L2 holds the K of few kv heads), then the query
+  // head within its group, batch, and query tile, largest first
+  const int grp = a.n_heads / a.n_kv_heads;
+  const int id = (int)blockIdx.x;
+  const int m = id % a.n_kv_heads;
+  const int n = m * grp + id / a.n_kv_heads % grp;
+  const int b = id / a.n_kv_heads / grp % a.batch;
+  const int qt = nqt - 1 - id / (a.n_kv_heads * grp * a.batch);
   const long rb = (long)b * S;
-  const long ldo = (long)a.n_heads * D;
-  const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
+  const DsLayout L(S);
   const bf16_t* Kg = a.k + rb * a.ld_qkv + (long)m * D;
-  const bf16_t* Vg = a.v + rb * a.ld_qkv + (long)m * D;
-  const bf16_t* dOg = dout + rb * ldo + (long)n * D;
+  const bf16_t* dsh = ds + ((long)b * a.n_heads + n) * L.head;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hh = lane >> 5, l32 = lane & 31;
-  const int q0w = qt * BQ + wave * 32;
+  const int qb0 = qt * BQ;
+  const int q0w = qb0 + wave * 32;
   const int q = q0w + l32;
-  bf16x8_t qf[KK], of[KK];
-  float dsum = 0.0f;
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    qf[kk] = gload_frag(Qg + (long)q * a.ld_qkv + kk * 16 + hh * 8, q < S);
-    of[kk] = gload_frag(dOg + (long)q * ldo + kk * 16 + hh * 8, q < S);
-    const bf16x8_t ov = gload_frag(o + (rb + q) * ldo + (long)n * D + kk * 16 + hh * 8, q < S);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dsum += (float)of[kk][e] * (float)ov[e];
-  }
-  dsum += __shfl_xor(dsum, 32, 64);
-  const long li = ((long)b * a.n_heads + n) * S + q;
-  const float nl2 = q < S ? -lse[li] * kLog2e : -INFINITY;
-  const float ndl = -dsum;   // -rowsum(dO O)
-  if (q < S && hh == 0) {
-    delta[li] = ndl;
-    delta[(long)a.batch * a.n_heads * S + li] = nl2;
-  }
   f32x16_t dqa[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) zero(dqa[db]);
-  const float c = a.scale * kLog2e;
-  const int q_last = min(qt * BQ + BQ, S) - 1;
+  const int q_last = min(qb0 + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
-  uint32_t doff[DmaPlan<D, 4>::PER];
-  dma_offsets<D, 4>(a.ld_qkv, wave, lane, doff);
-  auto dma = [&](int kt, uint4* sm) __attribute__((always_inline)) {
-    dma_tile_at<D, 4>(Kg, a.ld_qkv, kt * BKV, S, sm, wave, doff);
-    dma_tile_at<D, 4>(Vg, a.ld_qkv, kt * BKV, S, sm + NAT, wave, doff);
+  uint32_t koff[DmaPlan<D, NW>::PER];
+  dma_offsets<D, NW>(a.ld_qkv, wave, lane, koff);
+  // dS: instruction t of wave w copies KB c = 8 t + w of the tile, the
+  // (c % 4)-th KB of block c / 4 (slab qb0 / 32 + c / 4); blocks past the
+  // sequence end lie past the tile's extent and read as zeros
+  auto dma = [&](int kt, int st) __attribute__((always_inline)) {
+    uint4* stg = sm + st * Q::STAGE;
+    dma_tile_at<D, NW>(Kg, a.ld_qkv, kt * BKV, S, stg, wave, koff);
+    const int jb = qb0 / 32 - 2 * kt;   // block of slab qb0 / 32 in the tile (>= -6)
+    const __amdgpu_buffer_rsrc_t r = rsrc_n(dsh + L.tile(kt), 4096L * (L.ns - 2 * kt));
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int c = t * NW + wave;
+      const int blk = jb + c / 4;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          r, (lds_ptr_t)(stg + NAT + c * 64), 16,
+          blk < 0 ? kOOB : (uint32_t)((2048 * blk + ((c & 3) * 64 + lane) * 8) * 2), 0, 0, 0);
+    }
   };
-  // per-lane offsets of the K / V fragments within a tile
-  uint32_t ro[KK], to[DB][2];
+  // per-lane offsets: K^T fragments of column block db; the wave's dS^T
+  // fragment of key step s: lane i of 16-lane group G supplies key
+  // kr = 16 s + 4 (G >> 1) + (i >> 2) (+ 8 for the second read) and the four
+  // queries 16 (G & 1) + 4 (i & 3) .. + 3, i.e. value quad g = 2 (G & 1) +
+  // (i & 3) / 2 of lane half hh = i & 1: half u = G & 1, piece
+  // ((2 kr + hh) * 16) ^ (u * 128), 8 bytes in at (g & 1) * 8; key step s adds
+  // (s / 2) * 2 KB + (s % 2) * 512 B (the XOR touches bit 7 only)
+  uint32_t ro[D / 16], to[DB][2];
   frag_offsets<D>(lane, ro, to);
-  auto tile = [&](const uint4* Ks, int kt) __attribute__((always_inline)) {
-    const int k0 = kt * BKV;
-    if (k0 > q0w + 31) return;
-    // the two 32-key halves one after the other: scores, dP, dS and the dQ
-    // products of a half need only that half's registers
-    auto half = [&](auto KB) __attribute__((always_inline)) {
-      constexpr int kb = decltype(KB)::value;
-      constexpr int RK = kb * 32 * D * 2;            // byte offset of row 32 kb
-      f32x16_t sc, dp;
+  uint32_t ts[2];
+  {
+    const int G = lane >> 4, i = lane & 15;
+    const int kr = 4 * (G >> 1) + (i >> 2);
+    ts[0] = NAT * 16 + wave * 4096 + (G & 1) * 1024 + (((2 * kr + (i & 1)) * 16) ^ ((G & 1) * 128)) +
+            ((i & 3) >> 1) * 8;
+    ts[1] = ts[0] + 8 * 32;
+  }
+  const uint32_t smb = fa::lds_off(sm);
+  // one key step's fragments: the dS^T fragment, then the DB K^T fragments
+  // (2 (DB + 1) LDS reads, inline asm: a C++ read would make the compiler
+  // wait for every DMA in flight first)
+  auto rd_step = [&](auto SV, uint32_t sb, bf16x8_t& bt, bf16x8_t (&at)[DB])
+      __attribute__((always_inline)) {
+    constexpr int s = decltype(SV)::value;
+    constexpr int SO = (s >> 1) * 2048 + (s & 1) * 512, KO = s * 16 * D * 2;
+    bt = fa::rd_tr<SO>(sb + ts[0], sb + ts[1]);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) dp[i] = ndl;       // dP - delta, formed by the MFMAs
-      // scores and dP: K and V fragments read four 16-deep slices at a time
-      bf16x8_t fk[KK], fv[KK];
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        if (kk % 4 == 0) {
-#pragma unroll
-          for (int u = kk; u < kk + 4; ++u) {
-            fk[u] = row_at<RK>(Ks, ro[u]);
-            fv[u] = row_at<NAT * 16 + RK>(Ks, ro[u]);
-          }
-        }
-        sc = MFMA(fk[kk], qf[kk], kk == 0 ? f32x16_t{} : sc);
-        dp = MFMA(fv[kk], of[kk], dp);
-      }
-      // K^T fragments for dQ^T = K^T dS^T: read before the elementwise part
-      bf16x8_t ft[2][DB];
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        ft[0][db] = tr_at<RK>(Ks, to[db]);
-        ft[1][db] = tr_at<RK + 16 * D * 2>(Ks, to[db]);
-      }
-      // the causal mask (diagonal tiles only) as -inf scores: exp2 gives 0
-      if (k0 + kb * 32 + 31 > q0w) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = k0 + kb * 32 + (i >> 2) * 8 + hh * 4 + (i & 3);
-          if (key > q) sc[i] = -INFINITY;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) dp[i] = fast_exp2(__builtin_fmaf(sc[i], c, nl2)) * dp[i];
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
-        const bf16x8_t df = pack_frag(dp, ss);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) dqa[db] = MFMA(ft[ss][db], df, dqa[db]);
-      }
-    };
-    half(std::integral_constant<int, 0>());
-    half(std::integral_constant<int, 1>());
+    for (int db = 0; db < DB; ++db) at[db] = fa::rd_tr<KO>(sb + to[db][0], sb + to[db][1]);
   };
-  auto sync = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);
+  auto mfma_step = [&](bf16x8_t& bt, bf16x8_t (&at)[DB]) __attribute__((always_inline)) {
+    fa::bind(bt);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) fa::bind(at[db]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dqa[db] = MFMA(at[db], bt, dqa[db]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto tile = [&](int kt, int st) __attribute__((always_inline)) {
+    if (kt * BKV > q0w + 31) return;   // every query of this wave precedes the tile
+    const uint32_t sb = smb + st * Q::STAGE * 16;
+    constexpr int NRS = 2 * (DB + 1);   // reads of one key step
+    bf16x8_t bt[4], at[4][DB];
+    // each step's reads go out before the previous step's MFMAs
+    rd_step(fa::ic<0>{}, sb, bt[0], at[0]);
+    rd_step(fa::ic<1>{}, sb, bt[1], at[1]);
+    fa::wait_lds<NRS>();
+    mfma_step(bt[0], at[0]);
+    rd_step(fa::ic<2>{}, sb, bt[2], at[2]);
+    fa::wait_lds<NRS>();
+    mfma_step(bt[1], at[1]);
+    rd_step(fa::ic<3>{}, sb, bt[3], at[3]);
+    fa::wait_lds<NRS>();
+    mfma_step(bt[2], at[2]);
+    fa::wait_lds<0>();
+    mfma_step(bt[3], at[3]);
+  };
+  // after the wait, every wave's DMA of the tile about to be read has landed
+  // and every wave is done with the stage the next DMA overwrites
+  auto sync = [&](bool ahead) __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_barrier(0);
+    if (ahead) __builtin_amdgcn_s_waitcnt(vmcnt_imm(Q::MEM));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  dma(0, sm0);
-  sync();
-  for (int kt = 0; kt < nkt; kt += 2) {
-    if (kt + 1 < nkt) dma(kt + 1, sm1);
-    tile(sm0, kt);
-    sync();
-    if (kt + 1 < nkt) {
-      if (kt + 2 < nkt) dma(kt + 2, sm0);
-      tile(sm1, kt + 1);
-      sync();
-    }
+  dma(0, 0);
+  if (nkt > 1) dma(1, 1);
+  sync(nkt > 1);
+  int st = 0;
+  for (int kt = 0; kt < nkt; ++kt) {
+    if (kt + 2 < nkt) dma(kt + 2, st == 0 ? 2 : st - 1);
+    tile(kt, st);
+    if (kt + 1 < nkt) sync(kt + 2 < nkt);
+    st = st == NST - 1 ? 0 : st + 1;
   }
   if (q < S) {
     bf16_t* dqr = dq + (rb + q) * ld_d + (long)n * D;
@@ -865,29 +1105,34 @@ hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta,
-                         uint16_t* dk, uint16_t* dv, long ld_d, hipStream_t s) {
-  const dim3 grid((unsigned)((a.seq + 63) / 64 * a.n_kv_heads * a.batch)), block(256);
+size_t attn_bwd_ds_bytes(const AttnArgs& a) {
+  return (size_t)a.batch * a.n_heads * DsLayout(a.seq).head * 2;
+}
+
+hipError_t attn_bwd(const AttnArgs& a, const uint16_t* o, const uint16_t* dout, const float* lse,
+                    float* delta, uint16_t* ds, uint16_t* dq, uint16_t* dk, uint16_t* dv,
+                    long ld_d, hipStream_t s) {
+  const long rows = (long)a.batch * a.seq * a.n_heads;
+  const dim3 block(256);
+  const dim3 kgrid((unsigned)((a.seq + 63) / 64 * a.n_kv_heads * a.batch));
+  const dim3 qgrid((unsigned)((a.seq + 255) / 256 * a.n_heads * a.batch));
   if (a.d == 128) {
-    hipLaunchKernelGGL((attn_bwd_kv_k<128, 0>), grid, block, 0, s, a, dout, delta, dv, ld_d);
-    hipLaunchKernelGGL((attn_bwd_kv_k<128, 1>), grid, block, 0, s, a, dout, delta, dk, ld_d);
+    const dim3 pgrid((unsigned)((rows + 15) / 16));
+    hipLaunchKernelGGL(attn_bwd_prep_k<128>, pgrid, block, 0, s, o, dout, lse, delta, rows,
+                       a.n_heads, a.seq);
+    hipLaunchKernelGGL(attn_bwd_dv_k<128>, kgrid, block, 0, s, a, dout, delta, ds, dv, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dk_k<128>, kgrid, block, 0, s, a, ds, dk, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<128>, qgrid, dim3(512), 0, s, a, ds, dq, ld_d);
   } else if (a.d == 64) {
-    hipLaunchKernelGGL((attn_bwd_kv_k<64, 0>), grid, block, 0, s, a, dout, delta, dv, ld_d);
-    hipLaunchKernelGGL((attn_bwd_kv_k<64, 1>), grid, block, 0, s, a, dout, delta, dk, ld_d);
+    const dim3 pgrid((unsigned)((rows + 31) / 32));
+    hipLaunchKernelGGL(attn_bwd_prep_k<64>, pgrid, block, 0, s, o, dout, lse, delta, rows,
+                       a.n_heads, a.seq);
+    hipLaunchKernelGGL(attn_bwd_dv_k<64>, kgrid, block, 0, s, a, dout, delta, ds, dv, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dk_k<64>, kgrid, block, 0, s, a, ds, dk, ld_d);
+    hipLaunchKernelGGL(attn_bwd_dq_k<64>, qgrid, dim3(512), 0, s, a, ds, dq, ld_d);
   } else {
     return hipErrorInvalidValue;
   }
-  return hipGetLastError();
-}
-
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
-                       const float* lse, float* delta, uint16_t* dq, long ld_d, hipStream_t s) {
-  const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
-  if (a.d == 128)
-    hipLaunchKernelGGL(attn_bwd_dq_k<128>, grid, block, 0, s, a, o, dout, lse, delta, dq, ld_d);
-  else if (a.d == 64)
-    hipLaunchKernelGGL(attn_bwd_dq_k<64>, grid, block, 0, s, a, o, dout, lse, delta, dq, ld_d);
-  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

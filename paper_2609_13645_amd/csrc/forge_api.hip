@@ -194,11 +194,13 @@ Saved saved_layout(const forge_layer_cfg& c) {
 
 // ---- workspace -------------------------------------------------------------
 struct Work {
-  size_t dA, dgu, db, dh1, dO, delta, dqkv, da, dg, o, lse;
+  size_t dA, dgu, db, dh1, dO, delta, ds, dqkv, da, dg, o, lse;
   size_t logits, blk, colsum, dys, dxs, dgate, dl, dbs, wpart;  // MoE
   size_t qk_dg, h1s, dA_s, dgu_s, db1;  // QK-Norm; shared expert
   size_t total;
 };
+
+forge::AttnArgs attn_args(const Dims& d, const uint16_t* qkv);
 
 Work work_layout(const forge_layer_cfg& c) {
   const Dims d = dims(c);
@@ -235,6 +237,7 @@ Work work_layout(const forge_layer_cfg& c) {
   w.dh1 = take(d.T * d.h * 2);
   w.dO = take(d.T * d.hq * 2);
   w.delta = take(2 * d.B * d.nh * d.S * 4);   // delta, then -lse log2(e)
+  w.ds = take(forge::attn_bwd_ds_bytes(attn_args(d, nullptr)));   // dS, causal half
   w.dqkv = take(d.T * d.qkv * 2);
   w.da = take(d.T * d.h * 2);
   w.dg = take((size_t)forge::rmsnorm_bwd_blocks((int)d.T) * d.h * 4);
@@ -527,9 +530,8 @@ forge_status attn_block_bwd(const forge_layer_cfg& c, const Dims& d,
   FORGE_HIP(forge::gemm(forge::kKC, forge::kMC, forge::kStoreBF16,
                         scaled(gargs(dh1, d.h, w->w_o, d.hq, dO, d.hq, d.T, d.hq, d.h), d.bs), s));
   if (opt) FORGE_HIP(opt_update(opt, s, ws, opt->o->w_o, g->d_w_o, d.h * d.hq));
-  FORGE_HIP(forge::attn_bwd_dq(aa, o, dO, lse, delta, dqkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, dO, delta, dqkv + d.hq, dqkv + d.hq + d.hkv,
-                                 d.qkv, s));
+  FORGE_HIP(forge::attn_bwd(aa, o, dO, lse, delta, at<uint16_t>(workspace, wk.ds), dqkv,
+                             dqkv + d.hq, dqkv + d.hq + d.hkv, d.qkv, s));
   if (d.qkn) {
     // inverse RoPE and the QK-Norm backward in place; gain gradients
     float* qdg = at<float>(workspace, wk.qk_dg);
@@ -1592,7 +1594,9 @@ forge_status forge_attention_fwd(const forge_attn_cfg* cfg, const forge_bf16* qk
 forge_status forge_attention_bwd_workspace_bytes(const forge_attn_cfg* cfg, size_t* bytes) {
   if (forge_status s = check_attn(cfg)) return s;
   FORGE_CHECK(bytes != nullptr, FORGE_ERR_INVALID_ARG, "bytes is NULL");
-  *bytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4);
+  const Dims d = attn_dims(*cfg);
+  *bytes = up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4) +
+           up(forge::attn_bwd_ds_bytes(attn_args(d, nullptr)));
   return ok();
 }
 
@@ -1610,9 +1614,9 @@ forge_status forge_attention_bwd(const forge_attn_cfg* cfg, const forge_bf16* qk
   const forge::AttnArgs aa = attn_args(d, qkv);
   hipStream_t s = (hipStream_t)stream;
   float* delta = static_cast<float*>(workspace);
-  FORGE_HIP(forge::attn_bwd_dq(aa, o, d_o, lse, delta, d_qkv, d.qkv, s));
-  FORGE_HIP(forge::attn_bwd_dkdv(aa, d_o, delta, d_qkv + d.hq, d_qkv + d.hq + d.hkv, d.qkv,
-                                 s));
+  uint16_t* ds = at<uint16_t>(workspace, up(2 * (size_t)cfg->batch * cfg->n_heads * cfg->seq * 4));
+  FORGE_HIP(forge::attn_bwd(aa, o, d_o, lse, delta, ds, d_qkv, d_qkv + d.hq,
+                            d_qkv + d.hq + d.hkv, d.qkv, s));
   return ok();
 }
 

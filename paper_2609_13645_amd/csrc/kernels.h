@@ -138,18 +138,15 @@ struct AttnArgs {
 };
 // o [T, n_heads*d] bf16; lse [batch, n_heads, seq] fp32 (natural log).
 hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s);
-// Backward, in this order: attn_bwd_dq, then attn_bwd_dkdv.
-// attn_bwd_dq: dq [T, n_heads*d] columns of the dqkv buffer (row stride
-// ld_dqkv); also fills delta (2 * batch * n_heads * seq fp32): [b,n,i] =
-// -sum_d dO*O, then the second half [b,n,i] = -lse * log2(e), which
-// attn_bwd_dkdv reads.
-hipError_t attn_bwd_dq(const AttnArgs& a, const uint16_t* o, const uint16_t* dout,
-                       const float* lse, float* delta, uint16_t* dq, long ld_dqkv,
-                       hipStream_t s);
-// dk, dv [T, n_kv*d] columns of the dqkv buffer (row stride ld_dqkv), each
-// kv head's sums over its GQA group formed inside one block.
-hipError_t attn_bwd_dkdv(const AttnArgs& a, const uint16_t* dout, const float* delta,
-                         uint16_t* dk, uint16_t* dv, long ld_dqkv, hipStream_t s);
+// Backward. delta: 2 * batch * n_heads * seq fp32 scratch ([b,n,i] =
+// -sum_d dO*O, then [b,n,i] = -lse * log2(e)); ds: attn_bwd_ds_bytes scratch
+// (dS in bf16, the causal half per (batch, head)). dq [T, n_heads*d] and
+// dk, dv [T, n_kv*d] are column blocks of the dqkv buffer (row stride
+// ld_dqkv); dk and dv hold each kv head's sums over its GQA group.
+size_t attn_bwd_ds_bytes(const AttnArgs& a);
+hipError_t attn_bwd(const AttnArgs& a, const uint16_t* o, const uint16_t* dout, const float* lse,
+                    float* delta, uint16_t* ds, uint16_t* dq, uint16_t* dk, uint16_t* dv,
+                    long ld_dqkv, hipStream_t s);
 
 // ----------------------------------------------------------------- MoE ----
 // Routing of fp32 logits [T, E] (E <= 256): idx / gates [T, k], probs [T, E];
