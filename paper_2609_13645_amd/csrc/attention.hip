@@ -50,6 +50,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_n(const void* base, long 
 }
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
 
 // Natural [64 rows][D] bf16 tile in LDS, 16-byte chunk c of row r at slot
@@ -739,14 +740,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dv_k(AttnArgs a,
         }
     }
     // the pair's dS block, in accumulator order: 16-byte stores, 1 KB per
-    // wave instruction
+    // wave instruction; nontemporal, since the block is read back only after
+    // the pass (as ordinary stores, the dirty lines the memory-side cache
+    // holds at the end are written back while the dK pass reads dS: dK
+    // +7 %)
     bf16_t* blk = ds + ((long)b * a.n_heads + n) * L.head + L.block(kt, q0 / BQ);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int u = 0; u < 2; ++u)
-        *reinterpret_cast<bf16x8_t*>(blk + kb * 1024 + u * 512 + (pc0 ^ (u * 64))) =
-            pack_frag(dp[kb], u);
+        __builtin_nontemporal_store(
+            __builtin_bit_cast(u32x4_t, pack_frag(dp[kb], u)),
+            reinterpret_cast<u32x4_t*>(blk + kb * 1024 + u * 512 + (pc0 ^ (u * 64))));
     // dV^T += dO^T P, 16 queries at a time; each transposed fragment feeds
     // both key blocks
     auto quarter = [&](auto SS) __attribute__((always_inline)) {

@@ -858,11 +858,13 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   if constexpr (LA == kKC && LB == kKC) {
     if (big >= kCUs) {
       // 256 x 192 tiles when 256 x 256 ones leave the last wave of workgroups
-      // partly empty: cost ~ waves x tile area, the narrower tile being ~11 %
-      // less efficient per FLOP
+      // partly empty: cost ~ waves x tile area, the narrower (double-buffered)
+      // tile being ~26 % less efficient per FLOP than the ring's 256 x 256
+      // (measured on the 4096 x 6144 x 4096 product: two rounds of each,
+      // 200 us on the ring against 208-212 us)
       const long t192 = (long)((a.M + 255) / 256) * ((a.N + 191) / 192);
       const double c256 = (double)((big + kCUs - 1) / kCUs) * 256.0;
-      const double c192 = (double)((t192 + kCUs - 1) / kCUs) * 192.0 / 0.89;
+      const double c192 = (double)((t192 + kCUs - 1) / kCUs) * 192.0 / 0.74;
       if (c192 < c256) return launch<256, 192, 4, 2, LA, LB, EPI>(a, s);
     }
   }
