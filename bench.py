@@ -101,8 +101,8 @@ def kc_kernel_name(M, N):
     if big >= 256:
         t192 = -(-M // 256) * -(-N // 192)
         c256 = -(-big // 256) * 256.0
-        c192 = -(-t192 // 256) * 192.0 / 0.89
-        return "gemm_kernel<256,192,4,2" if c192 < c256 else "ring_kernel<256,256,4,2"
+        c192 = -(-t192 // 256) * 192.0 / 0.74
+        return "gemm_kernel<256,192,4,2" if c192 < c256 else "ring_kernel<256,256,2,4"
     return "gemm_kernel<256,128,2,2" if mid >= 256 else "gemm_kernel<128,128,2,2"
 
 
@@ -317,7 +317,7 @@ def kernel_rooflines(cfg, reps, out=sys.stdout):
     lay = {KC: "KC", MC: "MC"}
     epi = {0: "StoreBF16", 1: "ResidBF16", 2: "AccF32", 3: "StoreF32"}
     for (label, la, lb, ep, A, B, C, R, M, N, K, lda, ldb, ldc) in gemms:
-        name = (f"{kc_kernel_name(M, N)}" if (la, lb) == (KC, KC) else "ring_kernel<256,256,4,2") + \
+        name = (f"{kc_kernel_name(M, N)}" if (la, lb) == (KC, KC) else "ring_kernel<256,256,2,4") + \
             f",{lay[la]},{lay[lb]},{epi[ep]}>"
         timed(f"{label} (M={M} N={N} K={K})", name,
               lambda la=la, lb=lb, ep=ep, A=A, B=B, C=C, R=R, M=M, N=N, K=K, lda=lda, ldb=ldb,

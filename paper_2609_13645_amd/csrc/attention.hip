@@ -436,9 +436,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
 // dV pass's accumulator order: value 4 g + e of lane hh * 32 + l32 of key
 // block kb, (key 32 kb + l32, query 8 g + 4 hh + e), is element
 // 4 (g & 1) + e of the 16-byte piece at
-//   kb * 2 KB + u * 1 KB + (((2 l32 + hh) * 16) ^ (u * 128)),  u = g / 2.
-// (A key's two lane halves sit side by side and the second query half is
-// shifted by 128 bytes, so the dQ pass's transposed reads cover all banks.)
+//   kb * 2 KB + u * 1 KB + 512 hh + ((16 l32) ^ (128 hh) ^ (64 u)),  u = g / 2.
+// (The LDS serves a 16-byte read 16 lanes at a time from 64 banks: the dK
+// pass's B-fragment reads take 16 consecutive keys' pieces, a contiguous
+// 256 bytes; the XORs put a key's two lane halves 128 bytes apart and the
+// two query halves 64 bytes apart, so the dQ pass's transposed reads cover
+// all banks too.)
 // Every
 // visited block is written whole (zeros where the mask or the sequence end
 // removes a score). That order is also the dK pass's B-fragment order
@@ -539,7 +542,7 @@ __device__ __forceinline__ void dma_slab(const bf16_t* base, long ld, int row0, 
 
 // The four waves' [64 keys][D] accumulators (acc[db][kb]: rows d, columns
 // keys) summed in wave order through sm0 / sm1, times scale, stored as bf16
-// rows out[key][D] (key-major, row stride ld).
+// rows out[key][D] (key-major, row stride ld) for the first nkeys keys.
 template <int D>
 __device__ __forceinline__ void kv_reduce_store(const f32x16_t (&acc)[D / 32][2], uint4* sm0,
                                                 uint4* sm1, int wave, int lane, float scale,
@@ -560,21 +563,23 @@ __device__ __forceinline__ void kv_reduce_store(const f32x16_t (&acc)[D / 32][2]
             make_float4(acc[db][kb][g * 4], acc[db][kb][g * 4 + 1], acc[db][kb][g * 4 + 2],
                         acc[db][kb][g * 4 + 3]);
   __syncthreads();
+  // the four threads of a key take interleaved 8-column pieces (columns
+  // 32 j + 8 part ..), so eight lanes of a 16-byte read cover all banks
   const int key = threadIdx.x >> 2;
-  const int d0 = (threadIdx.x & 3) * (D / 4);
+  const int part = threadIdx.x & 3;
   if (key < nkeys) {
     const float* w0 = reinterpret_cast<const float*>(sm0);
     const float* w1 = reinterpret_cast<const float*>(sm0 + P::RED);
     const float* w2 = reinterpret_cast<const float*>(sm1);
     const float* w3 = reinterpret_cast<const float*>(sm1 + P::RED);
-    bf16_t* orow = out + (long)key * ld + d0;
+    bf16_t* orow = out + (long)key * ld + part * 8;
 #pragma unroll
-    for (int e = 0; e < D / 4; e += 8) {
-      const int o = key * (D + 4) + d0 + e;
+    for (int j = 0; j < D / 32; ++j) {
+      const int o = key * (D + 4) + j * 32 + part * 8;
       float f[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) f[u] = (((w0[o + u] + w1[o + u]) + w2[o + u]) + w3[o + u]) * scale;
-      *reinterpret_cast<uint4*>(orow + e) = pack8(f);
+      *reinterpret_cast<uint4*>(orow + j * 32) = pack8(f);
     }
   }
 }
@@ -642,7 +647,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dv_k(AttnArgs a,
   uint32_t ro[KK], to[DB][2];
   frag_offsets<D>(lane, ro, to);
   const __amdgpu_buffer_rsrc_t drs = rsrc(delta);
-  const int pc0 = (2 * l32 + hh) * 8;   // the lane's dS piece (elements) in a 1 KB half
+  // the lane's dS piece (elements) in a 1 KB half; half u adds the XOR u * 32
+  const int pc0 = 256 * hh + ((8 * l32) ^ (64 * hh));
 
   // pair p: query head m * grp + p % grp, slab j0 + ns - 1 - p / grp. Every
   // block of the kv group walks the slabs from the sequence end, head-minor,
@@ -751,7 +757,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dv_k(AttnArgs a,
       for (int u = 0; u < 2; ++u)
         __builtin_nontemporal_store(
             __builtin_bit_cast(u32x4_t, pack_frag(dp[kb], u)),
-            reinterpret_cast<u32x4_t*>(blk + kb * 1024 + u * 512 + (pc0 ^ (u * 64))));
+            reinterpret_cast<u32x4_t*>(blk + kb * 1024 + u * 512 + (pc0 ^ (u * 32))));
     // dV^T += dO^T P, 16 queries at a time; each transposed fragment feeds
     // both key blocks
     auto quarter = [&](auto SS) __attribute__((always_inline)) {
@@ -855,8 +861,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dk_k(AttnArgs a, const bf16_t
   const bf16_t* dsk = ds + L.tile(kt);
   uint4* ring = sm + wave * KR * R::SLOT;
   const uint32_t lb = lane * 16;   // the lane's 16 bytes of each 1 KB of a dS block (DMA)
-  // the lane's B fragments in a dS block: half ss at ss * 1 KB + (pc ^ ss * 128)
-  const uint32_t pc = (uint32_t)((2 * (lane & 31) + (lane >> 5)) * 16);
+  // the lane's B fragments in a dS block: half ss at ss * 1 KB + (pc ^ ss * 64)
+  const uint32_t pc = (uint32_t)(512 * (lane >> 5) + ((16 * (lane & 31)) ^ (128 * (lane >> 5))));
 
   // pair p into ring slot u: the Q slab, then the dS block (four 1 KB DMA)
   auto load = [&](int p, int u) __attribute__((always_inline)) {
@@ -889,8 +895,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dk_k(AttnArgs a, const bf16_t
 #pragma unroll
     for (int db = 0; db < DB; ++db)
       ft[1][db] = fa::rd_tr<16 * D * 2>(ab + to[db][0], ab + to[db][1]);
-    fb[1][0] = fa::rd_b128<P::SLAB * 16 + 1024>(ab + (pc ^ 128));
-    fb[1][1] = fa::rd_b128<P::SLAB * 16 + 2048 + 1024>(ab + (pc ^ 128));
+    fb[1][0] = fa::rd_b128<P::SLAB * 16 + 1024>(ab + (pc ^ 64));
+    fb[1][1] = fa::rd_b128<P::SLAB * 16 + 2048 + 1024>(ab + (pc ^ 64));
     fa::wait_lds<NR>();
     fa::bind(fb[0][0]);
     fa::bind(fb[0][1]);
@@ -1014,17 +1020,20 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   // kr = 16 s + 4 (G >> 1) + (i >> 2) (+ 8 for the second read) and the four
   // queries 16 (G & 1) + 4 (i & 3) .. + 3, i.e. value quad g = 2 (G & 1) +
   // (i & 3) / 2 of lane half hh = i & 1: half u = G & 1, piece
-  // ((2 kr + hh) * 16) ^ (u * 128), 8 bytes in at (g & 1) * 8; key step s adds
-  // (s / 2) * 2 KB + (s % 2) * 512 B (the XOR touches bit 7 only)
+  // 512 hh + ((16 kr) ^ (128 hh) ^ (64 u)), 8 bytes in at (g & 1) * 8; key step
+  // s adds (s / 2) * 2 KB + (s % 2) * 256 B (bit 8: no XOR touches it), the
+  // second read's + 8 keys sets bit 7 and so has offsets of its own
   uint32_t ro[D / 16], to[DB][2];
   frag_offsets<D>(lane, ro, to);
   uint32_t ts[2];
   {
     const int G = lane >> 4, i = lane & 15;
     const int kr = 4 * (G >> 1) + (i >> 2);
-    ts[0] = NAT * 16 + wave * 4096 + (G & 1) * 1024 + (((2 * kr + (i & 1)) * 16) ^ ((G & 1) * 128)) +
-            ((i & 3) >> 1) * 8;
-    ts[1] = ts[0] + 8 * 32;
+    const int hh = i & 1, u = G & 1;
+#pragma unroll
+    for (int hi = 0; hi < 2; ++hi)
+      ts[hi] = NAT * 16 + wave * 4096 + u * 1024 + 512 * hh +
+               ((16 * (kr + 8 * hi)) ^ (128 * hh) ^ (64 * u)) + ((i & 3) >> 1) * 8;
   }
   const uint32_t smb = fa::lds_off(sm);
   // one key step's fragments: the dS^T fragment, then the DB K^T fragments
@@ -1033,7 +1042,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
   auto rd_step = [&](auto SV, uint32_t sb, bf16x8_t& bt, bf16x8_t (&at)[DB])
       __attribute__((always_inline)) {
     constexpr int s = decltype(SV)::value;
-    constexpr int SO = (s >> 1) * 2048 + (s & 1) * 512, KO = s * 16 * D * 2;
+    constexpr int SO = (s >> 1) * 2048 + (s & 1) * 256, KO = s * 16 * D * 2;
     bt = fa::rd_tr<SO>(sb + ts[0], sb + ts[1]);
 #pragma unroll
     for (int db = 0; db < DB; ++db) at[db] = fa::rd_tr<KO>(sb + to[db][0], sb + to[db][1]);
