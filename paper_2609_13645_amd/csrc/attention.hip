@@ -159,8 +159,10 @@ __device__ __forceinline__ void zero(f32x16_t& a) {
 //    wait + barrier.
 //  * All K fragments of a tile are in flight before its 16 score MFMAs, and
 //    each MFMA pair waits only for its own fragments; the V^T fragments are
-//    read after the row max (whose lane exchange is an LDS operation that
-//    would otherwise wait for them) and land under the exp / row sums.
+//    read after the row max and land under the exp / row sums. The row
+//    max's exchange between the two lane halves is v_permlane32_swap, a
+//    VALU operation: as an LDS lane exchange it waited on the lgkm counter,
+//    which (saturating at 15) then also waited for every V^T read in flight.
 //  * The softmax, not the MFMAs, bounds this kernel on this chip (a wave64
 //    VALU op takes 4 cycles, exp more), so the per-tile VALU work is cut to
 //    the softmax itself: the scale is folded into the exponent's FMA; the
@@ -213,6 +215,27 @@ __device__ __forceinline__ void sync_block() {
 }
 template <int I>
 using ic = std::integral_constant<int, I>;
+// max / sum of the values of lanes l and l ^ 32, on the VALU
+// (v_permlane32_swap): no LDS operation, so no lgkmcnt wait that would also
+// cover the fragment reads in flight
+// (a = lanes 0..31 in both halves, b = lanes 32..63). Inline asm: through
+// the compiler builtin, the second result of the swap was replaced by the
+// first in the code generated for a sum of the two (a miscompile seen with
+// this toolchain). The leading and trailing s_nop give the wait states
+// around a VALU write of the operands and a VALU read of the results.
+__device__ __forceinline__ f32x2_t halves(float v) {
+  uint32_t a = __builtin_bit_cast(uint32_t, v), b = a;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  return f32x2_t{__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)};
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const f32x2_t h = halves(v);
+  return fmaxf(h[0], h[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const f32x2_t h = halves(v);
+  return h[0] + h[1];
+}
 }  // namespace fa
 
 template <int D>
@@ -220,9 +243,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
                                                          float* __restrict__ lse) {
   constexpr int BQ = 128, BKV = 64, NAT = BKV * D / 8, KK = D / 16, DB = D / 32;
   constexpr int TILE_B = NAT * 16;       // bytes of one K or V tile
-  constexpr int STAGE_B = 2 * TILE_B;    // K tile then V tile
   constexpr int HALF_B = TILE_B / 2;     // rows 32..63 of a tile
   constexpr int ROW16_B = 16 * D * 2;    // 16 rows of a tile
+  constexpr int V0_B = 2 * TILE_B;       // V slots after the two K slots
+  constexpr int KW = 4;                  // K fragment steps (kk) in flight
+  // K slots 0, 1 then V slots 0, 1: tile t's K in K slot t & 1, its V in V
+  // slot t & 1. K runs one tile ahead of V (S of tile j + 1 is formed while
+  // tile j's softmax and P V run), so each slot pair is a double buffer.
   __shared__ uint4 smem[4 * NAT];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
@@ -249,9 +276,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   const float c = a.scale * kLog2e;
   const int q_last = min(qt * BQ + BQ, S) - 1;
   const int nkt = q_last / BKV + 1;
+  // the wave's last key tile (its queries end at q0w + 31)
+  const int lw = min(q0w + 31, S - 1) / BKV;
 
-  // per-lane byte addresses in stage 0: K row fragment of slice kk (rows
-  // 0..31), V^T fragment of column block db (rows 0..15, both row quads)
+  // per-lane byte addresses in K slot 0 / V slot 0: K row fragment of slice
+  // kk (rows 0..31), V^T fragment of column block db (rows 0..15, both row
+  // quads)
   const uint32_t base = fa::lds_off(smem);
   uint32_t ka[KK], va[DB][2];
 #pragma unroll
@@ -261,40 +291,38 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
     const int r = (g4 >> 1) * 4 + (i >> 2);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const int d = db * 32 + (g4 & 1) * 16 + 4 * (i & 3);
-      va[db][0] = base + TILE_B + (slot<D>(r, d >> 3) * 8 + (d & 7)) * 2;
-      va[db][1] = base + TILE_B + (slot<D>(r + 8, d >> 3) * 8 + (d & 7)) * 2;
+      const int dd = db * 32 + (g4 & 1) * 16 + 4 * (i & 3);
+      va[db][0] = base + V0_B + (slot<D>(r, dd >> 3) * 8 + (dd & 7)) * 2;
+      va[db][1] = base + V0_B + (slot<D>(r + 8, dd >> 3) * 8 + (dd & 7)) * 2;
     }
   }
 
   uint32_t doff[DmaPlan<D, 4>::PER];
   dma_offsets<D, 4>(a.ld_qkv, wave, lane, doff);
-  auto dma = [&](int kt) __attribute__((always_inline)) {
-    uint4* st = smem + (kt & 1) * 2 * NAT;
-    dma_tile_at<D, 4>(Kg, a.ld_qkv, kt * BKV, S, st, wave, doff);
-    dma_tile_at<D, 4>(Vg, a.ld_qkv, kt * BKV, S, st + NAT, wave, doff);
+  auto dma_k = [&](int kt) __attribute__((always_inline)) {
+    dma_tile_at<D, 4>(Kg, a.ld_qkv, kt * BKV, S, smem + (kt & 1) * NAT, wave, doff);
   };
-  auto tile = [&](auto STG, int kt) __attribute__((always_inline)) {
-    constexpr int SO = decltype(STG)::value * STAGE_B;
-    const int k0 = kt * BKV;
-    if (k0 > q0w + 31) return;   // every query of this wave is before the tile
-    // scores: all K fragments in flight, each MFMA pair waits for its own
+  auto dma_v = [&](int kt) __attribute__((always_inline)) {
+    dma_tile_at<D, 4>(Vg, a.ld_qkv, kt * BKV, S, smem + (2 + (kt & 1)) * NAT, wave, doff);
+  };
+
+  // S^T of a tile (K slot KS) into sc: K fragments KW steps ahead, each MFMA
+  // pair waiting for its own two reads; after MFMA step kk, the hook runs
+  // (the softmax work of the previous tile, interleaved with these MFMAs)
+  auto scores = [&](auto KS, f32x16_t (&sc)[2], auto&& hook) __attribute__((always_inline)) {
+    constexpr int KO = decltype(KS)::value * TILE_B;
     bf16x8_t f[KK][2];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      f[kk][0] = fa::rd_b128<SO>(ka[kk]);
-      f[kk][1] = fa::rd_b128<SO + HALF_B>(ka[kk]);
+    for (int kk = 0; kk < KW; ++kk) {
+      f[kk][0] = fa::rd_b128<KO>(ka[kk]);
+      f[kk][1] = fa::rd_b128<KO + HALF_B>(ka[kk]);
     }
-    f32x16_t s[2];
-    zero(s[0]);
-    zero(s[1]);
+    zero(sc[0]);
+    zero(sc[1]);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      switch (KK - 1 - kk) {
-        case 7: fa::wait_lds<14>(); break;
-        case 6: fa::wait_lds<12>(); break;
-        case 5: fa::wait_lds<10>(); break;
-        case 4: fa::wait_lds<8>(); break;
+      // reads issued after step kk's: min(KW - 1, KK - 1 - kk) steps of two
+      switch (KK - 1 - kk < KW - 1 ? KK - 1 - kk : KW - 1) {
         case 3: fa::wait_lds<6>(); break;
         case 2: fa::wait_lds<4>(); break;
         case 1: fa::wait_lds<2>(); break;
@@ -303,11 +331,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
       fa::bind(f[kk][0]);
       fa::bind(f[kk][1]);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) s[kb] = MFMA(f[kk][kb], qf[kk], s[kb]);
+      for (int kb = 0; kb < 2; ++kb) sc[kb] = MFMA(f[kk][kb], qf[kk], sc[kb]);
+      if (kk + KW < KK) {
+        f[kk + KW][0] = fa::rd_b128<KO>(ka[kk + KW]);
+        f[kk + KW][1] = fa::rd_b128<KO + HALF_B>(ka[kk + KW]);
+      }
+      hook(kk);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // causal mask on the tile that straddles this wave's diagonal
+  };
+  auto no_hook = [](int) {};
+
+  // causal mask of a tile that straddles the wave's diagonal, then the row
+  // max, the lazy rescale; returns -running max (log2 units)
+  auto softmax_head = [&](f32x16_t (&s)[2], int kt) __attribute__((always_inline)) {
+    const int k0 = kt * BKV;
     if (k0 + BKV - 1 > q0w) {
-      asm volatile("" ::: "memory");
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -316,9 +355,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
           if (key > q) s[kb][i] = -INFINITY;
         }
     }
-    // row max: two running-max chains over the 32 scores of the lane (a
-    // running chain lets the compiler use v_max3 without first quieting
-    // every operand; a tree would quiet each leaf)
+    // two running-max chains over the lane's 32 scores (the compiler forms
+    // v_max3 without quieting every operand first)
     float mk[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -327,27 +365,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
       for (int i = 2; i < 16; ++i) t = fmaxf(t, s[kb][i]);
       mk[kb] = t;
     }
-    float mt = fmaxf(mk[0], mk[1]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * c;
-    // the lane exchange above waits for all LDS traffic of the wave: issue
-    // the V^T fragment reads only after it
-    __builtin_amdgcn_sched_barrier(0);
-    // V^T fragments for the P V products, in flight under the softmax
-    bf16x8_t v[2][2][DB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          if (kb == 0 && ss == 0) v[0][0][db] = fa::rd_tr<SO>(va[db][0], va[db][1]);
-          if (kb == 0 && ss == 1) v[0][1][db] = fa::rd_tr<SO + ROW16_B>(va[db][0], va[db][1]);
-          if (kb == 1 && ss == 0) v[1][0][db] = fa::rd_tr<SO + 2 * ROW16_B>(va[db][0], va[db][1]);
-          if (kb == 1 && ss == 1) v[1][1][db] = fa::rd_tr<SO + 3 * ROW16_B>(va[db][0], va[db][1]);
-        }
+    const float mt = fa::max_xor32(fmaxf(mk[0], mk[1])) * c;
     const bool grow = mt > mrow + 8.0f;
     if (__ballot(grow)) {
-      asm volatile("" ::: "memory");
       const float mnew = grow ? mt : mrow;
       const float alpha = fast_exp2(mrow - mnew);
       lrow *= alpha;
@@ -357,48 +377,93 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
         for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
       mrow = mnew;
     }
-    const float nm = -mrow;
+    return -mrow;
+  };
+  // probabilities of scores 4 step .. 4 step + 3 (of 32), in place, and
+  // their share of the row sum
+  auto exp_step = [&](f32x16_t (&s)[2], float nm, int step) __attribute__((always_inline)) {
+    const int kb = step >> 2, i0 = (step & 3) * 4;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int e = 0; e < 4; ++e) {
+      const float pp = fast_exp2(__builtin_fmaf(s[kb][i0 + e], c, nm));
+      s[kb][i0 + e] = pp;
+      lrow += pp;
+    }
+  };
+  // O^T += V^T P^T over the tile in V slot VS (va addresses V slot 0)
+  auto pv = [&](auto VS, const f32x16_t (&p)[2]) __attribute__((always_inline)) {
+    constexpr int VO = decltype(VS)::value * TILE_B;
+    bf16x8_t v[2][2][DB];
+    // two (kb, ss) steps of DB fragments in flight
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pp = fast_exp2(__builtin_fmaf(s[kb][i], c, nm));
-        s[kb][i] = pp;
-        lrow += pp;
-      }
-    // 4 DB fragments (2 reads each) per (kb, ss) step, in issue order
+    for (int db = 0; db < DB; ++db) v[0][0][db] = fa::rd_tr<VO>(va[db][0], va[db][1]);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int db = 0; db < DB; ++db) v[0][1][db] = fa::rd_tr<VO + ROW16_B>(va[db][0], va[db][1]);
 #pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
-        const bf16x8_t pf = pack_frag(s[kb], ss);
-        const int step = kb * 2 + ss;
-        switch (step) {
-          case 0: fa::wait_lds<6 * DB>(); break;
-          case 1: fa::wait_lds<4 * DB>(); break;
-          case 2: fa::wait_lds<2 * DB>(); break;
-          default: fa::wait_lds<0>(); break;
+    for (int st = 0; st < 4; ++st) {
+      const int kb = st >> 1, ss = st & 1;
+      const bf16x8_t pf = pack_frag(p[kb], ss);
+      if (st < 3) fa::wait_lds<2 * DB>();
+      else fa::wait_lds<0>();
+#pragma unroll
+      for (int db = 0; db < DB; ++db) fa::bind(v[kb][ss][db]);
+      if (st + 2 < 4) {
+        const int s2 = st + 2;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          if (s2 == 2) v[1][0][db] = fa::rd_tr<VO + 2 * ROW16_B>(va[db][0], va[db][1]);
+          if (s2 == 3) v[1][1][db] = fa::rd_tr<VO + 3 * ROW16_B>(va[db][0], va[db][1]);
         }
-#pragma unroll
-        for (int db = 0; db < DB; ++db) fa::bind(v[kb][ss][db]);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = MFMA(v[kb][ss][db], pf, oacc[db]);
       }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) oacc[db] = MFMA(v[kb][ss][db], pf, oacc[db]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
-  dma(0);
-  fa::sync_block();
-  for (int kt = 0; kt < nkt; kt += 2) {
-    if (kt + 1 < nkt) dma(kt + 1);
-    tile(fa::ic<0>{}, kt);
+  // iteration j: tile j's softmax, interleaved with the scores of tile
+  // j + 1, then tile j's P V. K of tile j + 1 and V of tile j are resident
+  // (and fenced by the barrier that opens the iteration); the DMA of K of
+  // tile j + 2 and V of tile j + 1 refills the slots that tiles j and j - 1
+  // used.
+  f32x16_t sa[2], sb[2];
+  auto iteration = [&](auto PAR, f32x16_t (&scur)[2], f32x16_t (&snext)[2], int j)
+      __attribute__((always_inline)) {
+    constexpr int P = decltype(PAR)::value;   // j & 1
     fa::sync_block();
-    if (kt + 1 < nkt) {
-      if (kt + 2 < nkt) dma(kt + 2);
-      tile(fa::ic<1>{}, kt + 1);
-      fa::sync_block();
+    if (j + 2 < nkt) dma_k(j + 2);
+    if (j + 1 < nkt) dma_v(j + 1);
+    if (j > lw) return;   // every query of this wave is before the tile
+    const float nm = softmax_head(scur, j);
+    if (j < lw) {
+      // the 8 exp steps of 4 spread over the KK MFMA steps of the next
+      // tile's scores
+      static_assert(8 % KK == 0, "exp steps per MFMA step");
+      scores(fa::ic<P ^ 1>{}, snext, [&](int kk) __attribute__((always_inline)) {
+#pragma unroll
+        for (int st = kk * (8 / KK); st < (kk + 1) * (8 / KK); ++st) exp_step(scur, nm, st);
+      });
+    } else {
+      // (the binds keep the compiler from hoisting the exp steps of both
+      // branches above the branch, which would undo the interleaving)
+      fa::bind(scur[0]);
+      fa::bind(scur[1]);
+#pragma unroll
+      for (int st = 0; st < 8; ++st) exp_step(scur, nm, st);
     }
+    pv(fa::ic<P>{}, scur);
+  };
+
+  dma_k(0);
+  dma_v(0);
+  if (nkt > 1) dma_k(1);
+  fa::sync_block();
+  scores(fa::ic<0>{}, sa, no_hook);
+  for (int j = 0; j < nkt; j += 2) {
+    iteration(fa::ic<0>{}, sa, sb, j);
+    if (j + 1 < nkt) iteration(fa::ic<1>{}, sb, sa, j + 1);
   }
-  lrow += __shfl_xor(lrow, 32, 64);
+  lrow = fa::sum_xor32(lrow);
   if (q < S) {
     const float inv = 1.0f / lrow;
     bf16_t* orow = o + (rb + q) * (long)(a.n_heads * D) + (long)n * D;
@@ -406,8 +471,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = db * 32 + g * 8 + hh * 4;
-        *reinterpret_cast<uint2*>(orow + d) =
+        const int dd = db * 32 + g * 8 + hh * 4;
+        *reinterpret_cast<uint2*>(orow + dd) =
             make_uint2(pack2(oacc[db][g * 4 + 0] * inv, oacc[db][g * 4 + 1] * inv),
                        pack2(oacc[db][g * 4 + 2] * inv, oacc[db][g * 4 + 3] * inv));
       }
