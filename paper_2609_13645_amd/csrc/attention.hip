@@ -253,8 +253,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_k(AttnArgs a, bf16_t* __restr
   __shared__ uint4 smem[4 * NAT];
   const int S = a.seq;
   const int nqt = (S + BQ - 1) / BQ;
-  const int qt = nqt - 1 - (int)blockIdx.x;
-  const int n = blockIdx.y, b = blockIdx.z;
+  // Block order: the query tiles with the most keys (the last ones) first,
+  // one tile level at a time across every (batch, head), so that the long
+  // blocks do not end up in the last round of the grid. Within a level,
+  // consecutive blocks go to the 8 XCDs in turn; when the level's count is
+  // a multiple of 8, XCD x takes a contiguous range of heads at every level,
+  // so the heads that share a kv head keep its K / V in one L2.
+  const int W = a.n_heads * a.batch;
+  const int id = (int)blockIdx.x;
+  const int level = id / W, r = id % W;
+  const int L = (W % 8 == 0) ? (r % 8) * (W / 8) + r / 8 : r;
+  const int qt = nqt - 1 - level;
+  const int n = L % a.n_heads, b = L / a.n_heads;
   const int m = n / (a.n_heads / a.n_kv_heads);
   const long rb = (long)b * S;
   const bf16_t* Qg = a.q + rb * a.ld_qkv + (long)n * D;
@@ -1177,7 +1187,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
 }  // namespace
 
 hipError_t attn_fwd(const AttnArgs& a, uint16_t* o, float* lse, hipStream_t s) {
-  const dim3 grid((a.seq + 127) / 128, a.n_heads, a.batch), block(256);
+  const dim3 grid((unsigned)((a.seq + 127) / 128 * a.n_heads * a.batch)), block(256);
   if (a.d == 128) hipLaunchKernelGGL(attn_fwd_k<128>, grid, block, 0, s, a, o, lse);
   else if (a.d == 64) hipLaunchKernelGGL(attn_fwd_k<64>, grid, block, 0, s, a, o, lse);
   else return hipErrorInvalidValue;
