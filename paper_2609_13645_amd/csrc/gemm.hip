@@ -242,6 +242,22 @@ __device__ __forceinline__ bool tile_setup(GemmArgs& p, int& tm, int& tn) {
     p.B += (long)e * p.strideB;
     p.C = (char*)p.C + r0 * p.ldc * (EPI == kStoreBF16 || EPI == kResidBF16 ? 2 : 4);
     if (EPI == kResidBF16) p.R += r0 * p.ldr;
+  } else if (GROUP == 4) {
+    // the last, partial round of a product of 2BN-wide tiles: full tile
+    // p.tile_base + i of the band order above runs as two BN-wide halves
+    // (workgroups 2i and 2i + 1 after the same XCD remapping), so the round
+    // fills twice as many CUs with half as much work each
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + 2 * BN - 1) / (2 * BN);
+    const int nb = gridDim.x, bid = blockIdx.x;
+    const int nb8 = nb - nb % NUM_XCD;
+    const int ph = bid < nb8 ? (bid % NUM_XCD) * (nb8 / NUM_XCD) + bid / NUM_XCD : bid;
+    const int pid = p.tile_base + ph / 2;
+    const int in_group = GROUP_M * tiles_n;
+    const int first_m = (pid / in_group) * GROUP_M;
+    const int gsize = min(tiles_m - first_m, GROUP_M);
+    tm = first_m + (pid % in_group) % gsize;
+    tn = 2 * ((pid % in_group) / gsize) + (ph & 1);
   } else if (GROUP == 3) {
     // uniform split of the reduction: split e covers k rows [e * ks, e * ks + ks)
     // (ks = p.strideB) and stores its partial product to C + e * strideC
@@ -792,7 +808,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void ring_kernel(GemmArgs
 // on the double-buffered one.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int LA, int LB, int EPI, int GROUP>
 void launch_kernel(const GemmArgs& a, long grid, hipStream_t s) {
-  if constexpr (LA == kMC || LB == kMC || (BM == 256 && BN == 256))
+  if constexpr (LA == kMC || LB == kMC || (BM == 256 && BN == 256) || GROUP == 4)
     hipLaunchKernelGGL((ring_kernel<BM, BN, WAVES_M, WAVES_N, LA, LB, EPI, GROUP>),
                        dim3((unsigned)grid), dim3(WAVES_M * WAVES_N * 64), 0, s, a);
   else
@@ -856,6 +872,19 @@ hipError_t dispatch_tiles(const GemmArgs& a, hipStream_t s) {
   const long big = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
   const long mid = (long)((a.M + 255) / 256) * ((a.N + 127) / 128);
   if constexpr (LA == kKC && LB == kKC) {
+    const long tail = big % kCUs;
+    if (big > kCUs && tail <= kCUs / 2 && tail > 0) {
+      // whole rounds of 256 x 256 tiles, then the last half-empty round's
+      // tiles as 256 x 128 halves, twice as many workgroups; only products
+      // with both operands K-contiguous (the forward ones, which run alone
+      // on the chip; a product that shares the chip with a side stream
+      // leaves its partial round to that stream's work)
+      launch_kernel<256, 256, 2, 4, LA, LB, EPI, 0>(a, big - tail, s);
+      GemmArgs b = a;
+      b.tile_base = (int)(big - tail);
+      launch_kernel<256, 128, 2, 4, LA, LB, EPI, 4>(b, 2 * tail, s);
+      return hipGetLastError();
+    }
     if (big >= kCUs) {
       // 256 x 192 tiles when 256 x 256 ones leave the last wave of workgroups
       // partly empty: cost ~ waves x tile area, the narrower (double-buffered)

@@ -40,6 +40,9 @@ struct GemmArgs {
   const int* g_off = nullptr;
   int groups = 0;
   long strideB = 0, strideC = 0;
+  // split last round (GEMM tile order 4): the full 256-wide tiles from this
+  // one on in the band order, each run as two BN-wide halves
+  int tile_base = 0;
   // AdamW epilogues: fp32 master, moments m and v and the bf16 parameter,
   // laid out like C (leading dimension ldc; grouped: strideC apart), device
   // step scalars {lr, 1 - b1^t, 1 - b2^t, clip} and the hyper-parameters
