@@ -91,19 +91,26 @@ def is_model(cfg):
     return cfg["vocab"] > 0
 
 
-def kc_kernel_name(M, N):
-    """Kernel and tile the library's dispatch picks for a plain GEMM with both
-    operands K-contiguous (for labelling the roofline kernel only): full
-    256 x 256 tiles on the ring pipeline, 256 x 192 when that fills the last
-    wave of workgroups better, smaller tiles for small problems."""
+def kc_kernel_name(M, N, suffix):
+    """Kernel(s) and tile the library's dispatch picks for a plain GEMM with
+    both operands K-contiguous (for labelling the roofline kernel only): full
+    256 x 256 tiles on the ring pipeline, with a last round at most half full
+    run as 256 x 128 halves in a second launch; 256 x 192 when that fills the
+    last wave of workgroups better; smaller tiles for small problems.
+    `suffix` closes each template argument list."""
     big = -(-M // 256) * -(-N // 256)
     mid = -(-M // 256) * -(-N // 128)
     if big >= 256:
+        tail = big % 256
+        if big > 256 and 0 < tail <= 128:
+            return f"ring_kernel<256,256,2,4{suffix} + ring_kernel<256,128,2,4{suffix}"
         t192 = -(-M // 256) * -(-N // 192)
         c256 = -(-big // 256) * 256.0
         c192 = -(-t192 // 256) * 192.0 / 0.74
-        return "gemm_kernel<256,192,4,2" if c192 < c256 else "ring_kernel<256,256,2,4"
-    return "gemm_kernel<256,128,2,2" if mid >= 256 else "gemm_kernel<128,128,2,2"
+        head = "gemm_kernel<256,192,4,2" if c192 < c256 else "ring_kernel<256,256,2,4"
+    else:
+        head = "gemm_kernel<256,128,2,2" if mid >= 256 else "gemm_kernel<128,128,2,2"
+    return head + suffix
 
 
 class Step:
@@ -227,7 +234,7 @@ def dominant_kernel(cfg, stream, step, reps):
             _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
                             T, V, h, h, h, V, 0, stream)
         flop = 2.0 * T * V * h
-        name = f"{kc_kernel_name(T, V)},KC,KC,StoreBF16> (LM-head logits)"
+        name = f"{kc_kernel_name(T, V, ',KC,KC,StoreBF16>')} (LM-head logits)"
         shape = f"M={T} N={V} K={h}"
     else:
         f = cfg["ffn"]
@@ -239,7 +246,7 @@ def dominant_kernel(cfg, stream, step, reps):
             _lib.forge_gemm(_lib.GEMM_KC, _lib.GEMM_KC, _lib.EPI_STORE_BF16, A, W, C, None,
                             T, 2 * f, h, h, h, 2 * f, 0, stream)
         flop = 2.0 * T * 2 * f * h
-        name = f"{kc_kernel_name(T, 2 * f)},KC,KC,StoreBF16> (gate/up fwd)"
+        name = f"{kc_kernel_name(T, 2 * f, ',KC,KC,StoreBF16>')} (gate/up fwd)"
         shape = f"M={T} N={2 * f} K={h}"
     for _ in range(3):
         launch()
@@ -317,8 +324,9 @@ def kernel_rooflines(cfg, reps, out=sys.stdout):
     lay = {KC: "KC", MC: "MC"}
     epi = {0: "StoreBF16", 1: "ResidBF16", 2: "AccF32", 3: "StoreF32"}
     for (label, la, lb, ep, A, B, C, R, M, N, K, lda, ldb, ldc) in gemms:
-        name = (f"{kc_kernel_name(M, N)}" if (la, lb) == (KC, KC) else "ring_kernel<256,256,2,4") + \
-            f",{lay[la]},{lay[lb]},{epi[ep]}>"
+        suffix = f",{lay[la]},{lay[lb]},{epi[ep]}>"
+        name = (kc_kernel_name(M, N, suffix) if (la, lb) == (KC, KC)
+                else "ring_kernel<256,256,2,4" + suffix)
         timed(f"{label} (M={M} N={N} K={K})", name,
               lambda la=la, lb=lb, ep=ep, A=A, B=B, C=C, R=R, M=M, N=N, K=K, lda=lda, ldb=ldb,
               ldc=ldc: _lib.forge_gemm(la, lb, ep, A, B, C, R, M, N, K, lda, ldb, ldc,
@@ -677,8 +685,8 @@ def step_timeline(db_path, which=2, out=sys.stdout):
     (us) from the step's first kernel, the gap to the latest end so far
     (negative: overlapping earlier work on another stream), the stream and
     the workgroup count. A step starts with the attention RMSNorm, the QKV
-    product and RoPE; `which` picks the traced step by its index (default 2:
-    the second timed step after one warm-up step)."""
+    product (one or two launches) and RoPE; `which` picks the traced step by
+    its index (default 2: the second timed step after one warm-up step)."""
     import re
     import sqlite3
     con = sqlite3.connect(db_path)
@@ -688,9 +696,12 @@ def step_timeline(db_path, which=2, out=sys.stdout):
         short = re.sub(r"\(.*", "", name.replace("void ", "").replace(
             "forge::(anonymous namespace)::", ""))
         rows.append((short, gx // max(1, wx), start, end, stream))
-    starts = [i for i in range(len(rows) - 2) if rows[i][0].startswith("rmsnorm_fwd")
-              and rows[i + 1][0].startswith(("gemm_kernel", "ring_kernel"))
-              and rows[i + 2][0].startswith(("rope_apply", "qknorm_rope"))]
+    gemm, rope = ("gemm_kernel", "ring_kernel"), ("rope_apply", "qknorm_rope")
+    # the QKV product is one launch, or two when its last round runs as halves
+    starts = [i for i in range(len(rows) - 3) if rows[i][0].startswith("rmsnorm_fwd")
+              and rows[i + 1][0].startswith(gemm)
+              and (rows[i + 2][0].startswith(rope)
+                   or (rows[i + 2][0].startswith(gemm) and rows[i + 3][0].startswith(rope)))]
     i0 = starts[which]
     nxt = [j for j in starts if j > i0]
     i1 = (nxt[0] if nxt else len(rows)) - 1
