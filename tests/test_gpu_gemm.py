@@ -129,14 +129,16 @@ def test_gemm_single_round_long_k_integer_exact(la, lb, epi):
 
 
 @pytest.mark.parametrize("M,N,K", [(4096, 6144, 264), (4000, 6136, 200), (1280, 13312, 72),
-                                   (4864, 6912, 40)])
+                                   (4864, 6912, 40), (4096, 5896, 40)])
 @pytest.mark.parametrize("epi", [STORE_BF16, RESID_BF16, ACC_F32, STORE_F32])
 def test_gemm_split_last_round_integer_exact(M, N, K, epi):
     """Forward-layout products whose 256 x 256 tiles leave a last round at
     most half full (384 = 256 + 128, 260 = 256 + 4 and 513 = 2 * 256 + 1
     tiles): the whole rounds run as 256 x 256 tiles and the rest as 256 x 128
     halves in a second launch. Ragged M, N and K on the second shape (the
-    last column of halves ends inside a 16-wide block), exact in fp32."""
+    last column of halves ends inside a 16-wide block); on the last shape the
+    last half of the last column of tiles lies wholly past N (N % 256 = 8)
+    and must store nothing. Exact in fp32."""
     banner(f"gemm int split last round M={M} N={N} K={K} epi={epi}")
     got, ref = run_gemm(KC, KC, epi, M, N, K, seed=M + N + K + epi)
     want = (fi.bf16_bits_to_f64(fi.to_bf16_bits(ref.astype(np.float32)))
