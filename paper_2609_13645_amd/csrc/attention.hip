@@ -947,10 +947,12 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dk_k(AttnArgs a, const bf16_t
     dma_slab<D>(a.q + rb * a.ld_qkv + (long)n * D, a.ld_qkv, q0, S, slot, qoff);
     const __amdgpu_buffer_rsrc_t r =
         rsrc(dsk + ((long)b * a.n_heads + n) * L.head + 2048L * (ns - 1 - p / grp));
+    // (cache policy 2 = non-temporal: each dS block is read once by this
+    // pass, so it need not displace the Q slabs every block re-reads from L2)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)(slot + P::SLAB + i * 64), 16,
-                                               lb + i * 1024, 0, 0, 0);
+                                               lb + i * 1024, 0, 0, 2);
   };
 
   auto pair = [&](int u) __attribute__((always_inline)) {
@@ -1085,9 +1087,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_k(AttnArgs a, const bf16_t
     for (int t = 0; t < 4; ++t) {
       const int c = t * NW + wave;
       const int blk = jb + c / 4;
+      // non-temporal (cache policy 2): dS is read once here; K stays in L2
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           r, (lds_ptr_t)(stg + NAT + c * 64), 16,
-          blk < 0 ? kOOB : (uint32_t)((2048 * blk + ((c & 3) * 64 + lane) * 8) * 2), 0, 0, 0);
+          blk < 0 ? kOOB : (uint32_t)((2048 * blk + ((c & 3) * 64 + lane) * 8) * 2), 0, 0, 2);
     }
   };
   // per-lane offsets: K^T fragments of column block db; the wave's dS^T
